@@ -1,0 +1,274 @@
+"""ctypes wrapper over the plain C oracle (``sfs_oracle.c``).
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the CPU-baseline leg
+of the benchmark use it.  The product path never imports this module.
+
+``build()`` compiles the oracle with gcc (-O2 -ffp-contract=off: binary64
+round-to-nearest-even, no fused multiply-add); ``lib()`` loads it, building it
+first if it is missing.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "sfs_oracle.c")
+_LIB = os.path.join(_HERE, "libsfs_oracle.so")
+
+OK, E_ARG, E_STATE, E_CAPACITY, E_ITER = 0, -1, -2, -3, -4
+READING_DECODE_BATCH = 0      # first token = first batch in which the query decodes
+READING_PREFILL_BATCH = 1     # first token = batch completing the query's prefill
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code, where=""):
+        super().__init__(f"oracle error {code} {where}")
+        self.code = code
+
+
+class Params(C.Structure):
+    _fields_ = [("a", C.c_double), ("b", C.c_double), ("c", C.c_double), ("d", C.c_double),
+                ("e", C.c_double), ("budget", C.c_int32), ("max_seqs", C.c_int32)]
+
+
+def build(force: bool = True) -> str:
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.run(["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math",
+                        "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, _SRC], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+_i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
+_f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
+_i64p = np.ctypeslib.ndpointer(np.int64, flags="C_CONTIGUOUS")
+
+
+def _opt(ptr_type):
+    """ndpointer that also accepts None."""
+    class _Opt(ptr_type):
+        @classmethod
+        def from_param(cls, obj):
+            if obj is None:
+                return None
+            return super().from_param(obj)
+    return _Opt
+
+
+def lib():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        build(force=True)
+    L = C.CDLL(_LIB)
+    L.orc_queue_new.restype = C.c_void_p
+    L.orc_queue_new.argtypes = [C.POINTER(Params), C.c_int64, _i32p, _i32p, _i32p, C.c_double,
+                                C.POINTER(C.c_int)]
+    L.orc_queue_free.argtypes = [C.c_void_p]
+    L.orc_queue_size.restype = C.c_int64
+    L.orc_queue_size.argtypes = [C.c_void_p]
+    L.orc_queue_waiting.restype = C.c_int64
+    L.orc_queue_waiting.argtypes = [C.c_void_p]
+    L.orc_queue_get.argtypes = [C.c_void_p, _i32p, _i32p, _i32p, C.POINTER(C.c_double),
+                                C.POINTER(C.c_int64)]
+    L.orc_queue_step.restype = C.c_double
+    L.orc_queue_step.argtypes = [C.c_void_p, _i64p]
+    L.orc_queue_advance.restype = C.c_int
+    L.orc_queue_advance.argtypes = [C.c_void_p, C.c_double, C.c_int64]
+    L.orc_queue_append.restype = C.c_int
+    L.orc_queue_append.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_int64]
+    L.orc_queue_estimate.restype = C.c_int
+    L.orc_queue_estimate.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_double, C.c_int32,
+                                     C.c_int64, C.POINTER(C.c_double), C.POINTER(C.c_int32)]
+    L.orc_route_row.restype = C.c_int32
+    L.orc_route_row.argtypes = [C.c_int32, _f64p, _f64p, _f64p, _i32p, C.c_double, C.c_double,
+                                C.POINTER(C.c_double)]
+    L.orc_trace.restype = C.c_int
+    L.orc_trace.argtypes = [C.c_int32, C.POINTER(Params), _i32p, _i32p, _i32p, _i32p, _i32p,
+                            _f64p, C.c_int32, _i32p, _i32p, _f64p, _f64p, _f64p, C.c_int32,
+                            C.c_double, C.c_double, C.c_int32, C.c_int64, C.c_int64,
+                            _i32p, _opt(_f64p), _opt(_f64p), _opt(_f64p), _opt(_i32p),
+                            _opt(_i32p), _opt(_i32p), _opt(_i32p), _opt(_i32p), _opt(_f64p),
+                            _opt(_i64p), C.c_int64, C.POINTER(C.c_int32)]
+    L.orc_stats.restype = C.c_int
+    L.orc_stats.argtypes = [C.c_int32, _i32p, _f64p, _f64p, _f64p, C.c_int32, _i32p, C.c_double,
+                            _f64p]
+    _lib = L
+    return L
+
+
+def make_params(a, b, c, d, e, budget, max_seqs) -> Params:
+    return Params(float(a), float(b), float(c), float(d), float(e), int(budget), int(max_seqs))
+
+
+def params_of(wl, j) -> Params:
+    return make_params(wl.a[j], wl.b[j], wl.c[j], wl.d[j], wl.e[j], wl.budget[j], wl.max_seqs[j])
+
+
+def _i32(x):
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+
+
+class Queue:
+    """One instance's resident list with its clock (the oracle's state)."""
+
+    def __init__(self, params: Params, rp, rd, cx, clock=0.0):
+        self._L = lib()
+        st = C.c_int(0)
+        rp, rd, cx = _i32(rp), _i32(rd), _i32(cx)
+        self._p = params
+        self._q = self._L.orc_queue_new(C.byref(params), len(rp), rp, rd, cx, float(clock),
+                                        C.byref(st))
+        if st.value != OK:
+            raise OracleError(st.value, "queue_new")
+
+    def __del__(self):
+        q = getattr(self, "_q", None)
+        if q:
+            self._L.orc_queue_free(q)
+            self._q = None
+
+    def size(self) -> int:
+        return int(self._L.orc_queue_size(self._q))
+
+    def waiting(self) -> int:
+        return int(self._L.orc_queue_waiting(self._q))
+
+    def state(self):
+        n = self.size()
+        rp, rd, cx = (np.zeros(n, np.int32) for _ in range(3))
+        clk, it = C.c_double(0), C.c_int64(0)
+        self._L.orc_queue_get(self._q, rp, rd, cx, C.byref(clk), C.byref(it))
+        return rp, rd, cx, clk.value, it.value
+
+    def step(self):
+        f = np.zeros(4, np.int64)
+        T = self._L.orc_queue_step(self._q, f)
+        return T, tuple(int(x) for x in f)
+
+    def advance(self, t, max_iters=10_000_000):
+        st = self._L.orc_queue_advance(self._q, float(t), int(max_iters))
+        if st != OK:
+            raise OracleError(st, "advance")
+
+    def append(self, p, d, queue_cap=1 << 40):
+        st = self._L.orc_queue_append(self._q, int(p), int(d), int(queue_cap))
+        if st != OK:
+            raise OracleError(st, "append")
+
+    def estimate(self, p, d, t, reading=READING_DECODE_BATCH, max_iters=10_000_000):
+        tt, it = C.c_double(0), C.c_int32(0)
+        st = self._L.orc_queue_estimate(self._q, int(p), int(d), float(t), int(reading),
+                                        int(max_iters), C.byref(tt), C.byref(it))
+        if st != OK:
+            raise OracleError(st, "estimate")
+        return tt.value, it.value
+
+
+def route_row(ttft, acc_row, cost_row, col, w_cost, w_lat):
+    ttft = np.ascontiguousarray(ttft, np.float64)
+    bu = C.c_double(0)
+    m = lib().orc_route_row(len(ttft), ttft, np.ascontiguousarray(acc_row, np.float64),
+                            np.ascontiguousarray(cost_row, np.float64), _i32(col),
+                            float(w_cost), float(w_lat), C.byref(bu))
+    return int(m), bu.value
+
+
+@dataclass
+class TraceResult:
+    choice: np.ndarray
+    ttft_chosen: np.ndarray
+    util_chosen: np.ndarray
+    ttft_all: np.ndarray | None
+    iters_all: np.ndarray | None
+    offsets: np.ndarray | None
+    rem_prefill: np.ndarray | None
+    rem_decode: np.ndarray | None
+    context: np.ndarray | None
+    clock_ms: np.ndarray | None
+    iterations: np.ndarray | None
+
+
+def trace(wl, scenario: int = 0, *, n_q: int | None = None, reading=READING_DECODE_BATCH,
+          max_iters=10_000_000, full_rows=False, final_state=True, queue_cap=None) -> TraceResult:
+    """Sequential routing trace of one scenario of workload ``wl`` (first n_q queries)."""
+    L = lib()
+    I = wl.n_inst
+    N = wl.n_q if n_q is None else int(n_q)
+    params = (Params * I)(*[params_of(wl, j) for j in range(I)])
+    choice = np.zeros(N, np.int32)
+    ttft_c = np.zeros(N)
+    util_c = np.zeros(N)
+    ttft_all = np.zeros((N, I)) if full_rows else None
+    iters_all = np.zeros((N, I), np.int32) if full_rows else None
+    cap = int(wl.queue_cap if queue_cap is None else queue_cap)
+    if final_state:
+        out_cap = int(wl.offsets[-1]) + N
+        out_off = np.zeros(I + 1, np.int32)
+        out_rp, out_rd, out_cx = (np.zeros(out_cap, np.int32) for _ in range(3))
+        out_clock = np.zeros(I)
+        out_iters = np.zeros(I, np.int64)
+    else:
+        out_cap = 0
+        out_off = out_rp = out_rd = out_cx = out_clock = out_iters = None
+    failed = C.c_int32(-1)
+    st = L.orc_trace(I, params, _i32(wl.col), _i32(wl.offsets), _i32(wl.rem_prefill),
+                     _i32(wl.rem_decode), _i32(wl.context),
+                     np.ascontiguousarray(wl.clock_ms, np.float64), N,
+                     _i32(wl.q_prefill[:N]), _i32(wl.q_decode[:N]),
+                     np.ascontiguousarray(wl.q_t_ms[:N], np.float64),
+                     np.ascontiguousarray(wl.acc[:N], np.float64),
+                     np.ascontiguousarray(wl.cost[:N], np.float64), wl.n_cols,
+                     float(wl.w_cost[scenario]), float(wl.w_lat_ms[scenario]), int(reading),
+                     int(max_iters), cap, choice, ttft_c, util_c, ttft_all, iters_all,
+                     out_off, out_rp, out_rd, out_cx, out_clock, out_iters, out_cap,
+                     C.byref(failed))
+    if st != OK:
+        raise OracleError(st, f"trace (query {failed.value})")
+    if final_state:
+        n = int(out_off[-1])
+        out_rp, out_rd, out_cx = out_rp[:n], out_rd[:n], out_cx[:n]
+    return TraceResult(choice, ttft_c, util_c, ttft_all, iters_all, out_off, out_rp, out_rd,
+                       out_cx, out_clock, out_iters)
+
+
+def stats(choice, ttft_chosen, acc, cost, col, w_cost):
+    """Mean accuracy, mean cost, mean utility, p50 and p99 TTFT of a routed trace."""
+    n = len(choice)
+    out = np.zeros(5)
+    st = lib().orc_stats(n, _i32(choice), np.ascontiguousarray(ttft_chosen, np.float64),
+                         np.ascontiguousarray(acc[:n], np.float64),
+                         np.ascontiguousarray(cost[:n], np.float64), acc.shape[1], _i32(col),
+                         float(w_cost), out)
+    if st != OK:
+        raise OracleError(st, "stats")
+    return out
+
+
+def instance_queue(wl, j) -> Queue:
+    rp, rd, cx = wl.instance_requests(j)
+    return Queue(params_of(wl, j), rp, rd, cx, wl.clock_ms[j])
+
+
+def estimate_matrix(wl, queries, instances, t_ms=0.0, reading=READING_DECODE_BATCH,
+                    max_iters=10_000_000):
+    """Literal per-pair SFS estimates for the given query and instance indices."""
+    qs = {j: instance_queue(wl, j) for j in sorted(set(int(j) for j in instances))}
+    out = np.zeros((len(queries), len(instances)))
+    its = np.zeros((len(queries), len(instances)), np.int32)
+    for a, i in enumerate(queries):
+        for b, j in enumerate(instances):
+            out[a, b], its[a, b] = qs[int(j)].estimate(int(wl.q_prefill[i]),
+                                                       int(wl.q_decode[i]), t_ms, reading,
+                                                       max_iters)
+    return out, its

@@ -1,0 +1,437 @@
+/*
+ * sfs_oracle.c -- plain, slow CPU oracle of the SFS TTFT estimator and the
+ * latency-aware router.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the CPU
+ * baseline leg of the benchmark may load this file's library.  It shares no code,
+ * header, table or helper with the HIP path; it is compiled with gcc and
+ * -ffp-contract=off so every binary64 operation is a single round-to-nearest-even
+ * operation, with no fused multiply-add.
+ *
+ * What it computes (Sec. 4 "Estimating query latencies across model instances"):
+ *
+ *   * Resident set of an instance (Sec. 4, Setup): an ordered list, in arrival
+ *     (FCFS) order, of requests r with remaining prefill tokens rp, predicted
+ *     remaining decode tokens rd, and context length cx (tokens already in the KV
+ *     cache).  A request is active ("running") iff cx > 0, otherwise it is queued
+ *     ("waiting").  Running requests precede waiting ones; at most M run.
+ *
+ *   * Token batch (Sec. 4.1, paragraph on SFS): at most one decode token per
+ *     decoding sequence plus prefill chunks of one or more sequences; decode of a
+ *     sequence starts only after its whole prefill.  The simulated scheduler
+ *     (App. E, latency estimation paragraph: queue order, admission limit,
+ *     token-budget constraint) is: every running request with rp == 0 decodes one
+ *     token; the remaining budget goes to prefill chunks in FCFS order, a waiting
+ *     request being admitted only while fewer than M requests run; the scan stops
+ *     at the first request it cannot serve (head-of-line blocking).
+ *
+ *   * Batch time (Eq. for the token-batch processing time, Sec. 4.1):
+ *       T = a + b*P + c*D + d*C + e*A,
+ *     P = sum of prefill tokens, D = number of decode tokens,
+ *     C = sum over decoding sequences of their context (KV reads),
+ *     A = sum over chunks of chunk*cx + chunk*(chunk+1)/2 (prefill attention).
+ *     The paper's coefficients are a = beta_0, b = c = beta_1, d = beta_2,
+ *     e = beta_3.  Evaluated as ((((a + b*P) + c*D) + d*C) + e*A).
+ *
+ *   * SFS estimate (Eqs. for the first-output-token batch and the SFS TTFT sum):
+ *     append the new query to the tail of a copy of the resident list, simulate
+ *     batches from the instance clock s, and stop at the first batch in which the
+ *     query produces a decode token; TTFT = (s + T_1 + ... + T_l) - t, the sum a
+ *     left fold in batch order.  Reading A (flag 1) stops instead at the batch in
+ *     which the query's prefill completes.
+ *
+ *   * Route (Eq. for the Lagrangian routing objective with the utility of Eq. 2):
+ *       u_j = (acc_j - w_cost*cost_j) - w_lat*TTFT_j,
+ *     choice = the lowest j attaining the maximum.
+ *
+ *   * Commit / advance (replay of the instances between snapshots, App. E on
+ *     workload snapshots): append the routed query as a waiting request of the
+ *     chosen instance, then on every instance run each batch that starts before
+ *     the next arrival time; an idle instance's clock jumps to that time.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_OK 0
+#define ORC_E_ARG (-1)
+#define ORC_E_STATE (-2)
+#define ORC_E_CAPACITY (-3)
+#define ORC_E_ITER (-4)
+
+typedef struct {
+  double a, b, c, d, e;
+  int32_t budget;
+  int32_t max_seqs;
+} orc_params;
+
+typedef struct {
+  orc_params pr;
+  int64_t n;        /* resident requests */
+  int64_t alloc;    /* allocated entries */
+  int32_t *rp, *rd, *cx;
+  int32_t *dec, *chunk; /* tokens of the batch being built, per request */
+  double clock;
+  int64_t iters;    /* batches run by advance() since creation */
+} orc_queue;
+
+typedef struct {
+  int64_t P, D, C, A;
+} orc_feat;
+
+/* ---------------------------------------------------------------- storage */
+
+static int q_reserve(orc_queue *q, int64_t need) {
+  if (need <= q->alloc) return ORC_OK;
+  int64_t cap = q->alloc ? q->alloc : 16;
+  while (cap < need) cap *= 2;
+  int32_t **arrs[5] = {&q->rp, &q->rd, &q->cx, &q->dec, &q->chunk};
+  for (int k = 0; k < 5; ++k) {
+    int32_t *p = (int32_t *)realloc(*arrs[k], (size_t)cap * sizeof(int32_t));
+    if (!p) return ORC_E_ARG;
+    *arrs[k] = p;
+  }
+  q->alloc = cap;
+  return ORC_OK;
+}
+
+static int params_ok(const orc_params *pr) {
+  return pr->max_seqs >= 1 && pr->budget >= pr->max_seqs;
+}
+
+/* Resident-list invariants: rp >= 0, rd >= 1, cx >= 0, rp == 0 implies cx > 0,
+   running (cx > 0) before waiting (cx == 0), at most M running. */
+static int state_ok(const orc_params *pr, int64_t n, const int32_t *rp, const int32_t *rd,
+                    const int32_t *cx) {
+  int64_t running = 0;
+  int seen_waiting = 0;
+  for (int64_t r = 0; r < n; ++r) {
+    if (rp[r] < 0 || rd[r] < 1 || cx[r] < 0) return 0;
+    if (rp[r] == 0 && cx[r] == 0) return 0;
+    if (cx[r] > 0) {
+      if (seen_waiting) return 0;
+      ++running;
+    } else {
+      seen_waiting = 1;
+    }
+  }
+  return running <= pr->max_seqs;
+}
+
+orc_queue *orc_queue_new(const orc_params *pr, int64_t n, const int32_t *rp,
+                         const int32_t *rd, const int32_t *cx, double clock, int *status) {
+  *status = ORC_OK;
+  if (!params_ok(pr) || n < 0) { *status = ORC_E_ARG; return NULL; }
+  if (!state_ok(pr, n, rp, rd, cx)) { *status = ORC_E_STATE; return NULL; }
+  orc_queue *q = (orc_queue *)calloc(1, sizeof(orc_queue));
+  if (!q) { *status = ORC_E_ARG; return NULL; }
+  q->pr = *pr;
+  if (q_reserve(q, n + 1) != ORC_OK) { free(q); *status = ORC_E_ARG; return NULL; }
+  for (int64_t r = 0; r < n; ++r) { q->rp[r] = rp[r]; q->rd[r] = rd[r]; q->cx[r] = cx[r]; }
+  q->n = n;
+  q->clock = clock;
+  q->iters = 0;
+  return q;
+}
+
+void orc_queue_free(orc_queue *q) {
+  if (!q) return;
+  free(q->rp); free(q->rd); free(q->cx); free(q->dec); free(q->chunk);
+  free(q);
+}
+
+static orc_queue *q_clone(const orc_queue *src) {
+  int st;
+  orc_queue *q = orc_queue_new(&src->pr, src->n, src->rp, src->rd, src->cx, src->clock, &st);
+  if (q) q->iters = src->iters;
+  return q;
+}
+
+int64_t orc_queue_size(const orc_queue *q) { return q->n; }
+
+int64_t orc_queue_waiting(const orc_queue *q) {
+  int64_t w = 0;
+  for (int64_t r = 0; r < q->n; ++r) w += (q->cx[r] == 0);
+  return w;
+}
+
+/* Copy the resident list out (FCFS order); arrays must hold orc_queue_size(). */
+void orc_queue_get(const orc_queue *q, int32_t *rp, int32_t *rd, int32_t *cx, double *clock,
+                   int64_t *iters) {
+  for (int64_t r = 0; r < q->n; ++r) { rp[r] = q->rp[r]; rd[r] = q->rd[r]; cx[r] = q->cx[r]; }
+  *clock = q->clock;
+  *iters = q->iters;
+}
+
+/* ---------------------------------------------------------------- one batch */
+
+/* Build the next token batch: dec[r] in {0,1}, chunk[r] >= 0; return its features. */
+static orc_feat compose(orc_queue *q) {
+  const int64_t n = q->n;
+  int64_t left = q->pr.budget;
+  int64_t running = 0;
+  for (int64_t r = 0; r < n; ++r) {
+    q->dec[r] = 0;
+    q->chunk[r] = 0;
+    if (q->cx[r] > 0) ++running;
+  }
+  /* decodes first: one token per running request whose prefill is complete */
+  for (int64_t r = 0; r < n; ++r) {
+    if (q->cx[r] > 0 && q->rp[r] == 0) {
+      q->dec[r] = 1;
+      left -= 1;
+    }
+  }
+  /* then prefill chunks in FCFS order */
+  for (int64_t r = 0; r < n; ++r) {
+    if (q->rp[r] == 0) continue;
+    if (left == 0) break;
+    if (q->cx[r] == 0) {            /* waiting: needs a free sequence slot */
+      if (running == q->pr.max_seqs) break;
+      running += 1;
+    }
+    int64_t ch = q->rp[r] < left ? q->rp[r] : left;
+    q->chunk[r] = (int32_t)ch;
+    left -= ch;
+  }
+  orc_feat f = {0, 0, 0, 0};
+  for (int64_t r = 0; r < n; ++r) {
+    int64_t ch = q->chunk[r];
+    f.P += ch;
+    f.D += q->dec[r];
+    f.C += (int64_t)q->dec[r] * q->cx[r];
+    f.A += ch * (int64_t)q->cx[r] + ch * (ch + 1) / 2;
+  }
+  return f;
+}
+
+static double batch_time(const orc_params *pr, orc_feat f) {
+  double t = pr->a;
+  t = t + pr->b * (double)f.P;
+  t = t + pr->c * (double)f.D;
+  t = t + pr->d * (double)f.C;
+  t = t + pr->e * (double)f.A;
+  return t;
+}
+
+/* Apply the batch built by compose(): decode tokens extend the context and consume
+   predicted decode; chunks extend the context and consume prefill; requests with
+   no decode left leave, the others keep their order. */
+static void apply(orc_queue *q) {
+  int64_t w = 0;
+  for (int64_t r = 0; r < q->n; ++r) {
+    if (q->dec[r]) { q->cx[r] += 1; q->rd[r] -= 1; }
+    if (q->chunk[r]) { q->cx[r] += q->chunk[r]; q->rp[r] -= q->chunk[r]; }
+    if (q->rd[r] > 0) {
+      q->rp[w] = q->rp[r]; q->rd[w] = q->rd[r]; q->cx[w] = q->cx[r];
+      ++w;
+    }
+  }
+  q->n = w;
+}
+
+/* One batch of the replayed instance; returns its time and features. */
+double orc_queue_step(orc_queue *q, int64_t *feat4) {
+  orc_feat f = compose(q);
+  double T = batch_time(&q->pr, f);
+  q->clock = q->clock + T;
+  apply(q);
+  q->iters += 1;
+  if (feat4) { feat4[0] = f.P; feat4[1] = f.D; feat4[2] = f.C; feat4[3] = f.A; }
+  return T;
+}
+
+/* Run every batch that starts before t; an empty instance idles until t. */
+int orc_queue_advance(orc_queue *q, double t, int64_t max_iters) {
+  int64_t k = 0;
+  while (q->n > 0 && q->clock < t) {
+    if (k == max_iters) return ORC_E_ITER;
+    orc_queue_step(q, NULL);
+    ++k;
+  }
+  if (q->n == 0 && q->clock < t) q->clock = t;
+  return ORC_OK;
+}
+
+/* Append a routed query as a waiting request. */
+int orc_queue_append(orc_queue *q, int32_t p, int32_t dhat, int64_t queue_cap) {
+  if (p < 1) return ORC_E_ARG;
+  if (orc_queue_waiting(q) + 1 > queue_cap) return ORC_E_CAPACITY;
+  if (q_reserve(q, q->n + 2) != ORC_OK) return ORC_E_ARG;
+  q->rp[q->n] = p;
+  q->rd[q->n] = dhat < 1 ? 1 : dhat;
+  q->cx[q->n] = 0;
+  q->n += 1;
+  return ORC_OK;
+}
+
+/* SFS estimate for a query of p prompt tokens arriving at t (the instance must
+   already be advanced to t).  Pure: the queue is not modified. */
+int orc_queue_estimate(const orc_queue *q, int32_t p, int32_t dhat, double t, int32_t reading,
+                       int64_t max_iters, double *ttft, int32_t *iters) {
+  if (p < 1) return ORC_E_ARG;
+  if (q->clock < t) return ORC_E_STATE;
+  orc_queue *w = q_clone(q);
+  if (!w) return ORC_E_ARG;
+  w->rp[w->n] = p;
+  w->rd[w->n] = dhat < 1 ? 1 : dhat;
+  w->cx[w->n] = 0;
+  w->n += 1;
+  double E = w->clock;
+  int64_t l = 0;
+  int done = 0;
+  while (!done) {
+    if (l == max_iters) { orc_queue_free(w); return ORC_E_ITER; }
+    orc_feat f = compose(w);
+    const int64_t me = w->n - 1;             /* the query stays last in the list */
+    if (reading == 1)
+      done = w->chunk[me] > 0 && w->chunk[me] == w->rp[me];
+    else
+      done = w->dec[me] == 1;
+    E = E + batch_time(&w->pr, f);
+    ++l;
+    apply(w);
+  }
+  orc_queue_free(w);
+  *ttft = E - t;
+  *iters = (int32_t)l;
+  return ORC_OK;
+}
+
+/* ---------------------------------------------------------------- routing */
+
+/* Lagrangian objective over one row; ties go to the lowest instance index. */
+int32_t orc_route_row(int32_t n_inst, const double *ttft, const double *acc_row,
+                      const double *cost_row, const int32_t *col, double w_cost, double w_lat,
+                      double *best_u) {
+  int32_t best = -1;
+  double bu = 0.0;
+  for (int32_t j = 0; j < n_inst; ++j) {
+    double pen = w_cost * cost_row[col[j]];
+    double u = acc_row[col[j]] - pen;
+    double lat = w_lat * ttft[j];
+    u = u - lat;
+    if (best < 0 || u > bu) { best = j; bu = u; }
+  }
+  if (best_u) *best_u = bu;
+  return best;
+}
+
+/* ---------------------------------------------------------------- trace */
+
+/*
+ * Sequential routing trace of one scenario:
+ *   advance every instance to t_0;
+ *   for each query i: estimate every instance at t_i, route, append the query to
+ *   the chosen instance, advance every instance to t_{i+1} (t_N := t_{N-1}).
+ * Outputs per query: choice, TTFT at the choice, utility of Eq. 2 at the choice
+ * (acc - w_cost*cost), and optionally the whole TTFT / iteration rows.
+ * The final state is written to the out_* arrays when out_offsets != NULL (each
+ * out array must hold out_cap entries).
+ */
+int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
+              const int32_t *offsets, const int32_t *rp, const int32_t *rd, const int32_t *cx,
+              const double *clock, int32_t n_q, const int32_t *q_p, const int32_t *q_d,
+              const double *q_t, const double *acc, const double *cost, int32_t n_cols,
+              double w_cost, double w_lat, int32_t reading, int64_t max_iters,
+              int64_t queue_cap, int32_t *choice, double *ttft_chosen, double *util_chosen,
+              double *ttft_all, int32_t *iters_all, int32_t *out_offsets, int32_t *out_rp,
+              int32_t *out_rd, int32_t *out_cx, double *out_clock, int64_t *out_iters,
+              int64_t out_cap, int32_t *failed_query) {
+  int st = ORC_OK;
+  *failed_query = -1;
+  if (n_inst < 1 || n_q < 0 || n_cols < 1) return ORC_E_ARG;
+  for (int32_t j = 0; j < n_inst; ++j)
+    if (col[j] < 0 || col[j] >= n_cols) return ORC_E_ARG;
+  orc_queue **qs = (orc_queue **)calloc((size_t)n_inst, sizeof(orc_queue *));
+  double *row = (double *)malloc((size_t)n_inst * sizeof(double));
+  if (!qs || !row) { free(qs); free(row); return ORC_E_ARG; }
+  for (int32_t j = 0; j < n_inst && st == ORC_OK; ++j) {
+    int64_t lo = offsets[j], hi = offsets[j + 1];
+    qs[j] = orc_queue_new(&params[j], hi - lo, rp + lo, rd + lo, cx + lo, clock[j], &st);
+    if (st == ORC_OK && orc_queue_waiting(qs[j]) > queue_cap) st = ORC_E_CAPACITY;
+  }
+  if (st == ORC_OK && n_q > 0)
+    for (int32_t j = 0; j < n_inst && st == ORC_OK; ++j)
+      st = orc_queue_advance(qs[j], q_t[0], max_iters);
+  for (int32_t i = 0; i < n_q && st == ORC_OK; ++i) {
+    int32_t it = 0;
+    for (int32_t j = 0; j < n_inst && st == ORC_OK; ++j) {
+      st = orc_queue_estimate(qs[j], q_p[i], q_d[i], q_t[i], reading, max_iters, &row[j], &it);
+      if (ttft_all) ttft_all[(int64_t)i * n_inst + j] = row[j];
+      if (iters_all) iters_all[(int64_t)i * n_inst + j] = it;
+    }
+    if (st != ORC_OK) { *failed_query = i; break; }
+    const double *arow = acc + (int64_t)i * n_cols;
+    const double *crow = cost + (int64_t)i * n_cols;
+    int32_t m = orc_route_row(n_inst, row, arow, crow, col, w_cost, w_lat, NULL);
+    choice[i] = m;
+    if (ttft_chosen) ttft_chosen[i] = row[m];
+    if (util_chosen) {
+      double pen = w_cost * crow[col[m]];
+      util_chosen[i] = arow[col[m]] - pen;
+    }
+    st = orc_queue_append(qs[m], q_p[i], q_d[i], queue_cap);
+    double t_next = (i + 1 < n_q) ? q_t[i + 1] : q_t[i];
+    for (int32_t j = 0; j < n_inst && st == ORC_OK; ++j)
+      st = orc_queue_advance(qs[j], t_next, max_iters);
+    if (st != ORC_OK) *failed_query = i;
+  }
+  if (st == ORC_OK && out_offsets) {
+    int64_t pos = 0;
+    out_offsets[0] = 0;
+    for (int32_t j = 0; j < n_inst; ++j) {
+      if (pos + qs[j]->n > out_cap) { st = ORC_E_CAPACITY; break; }
+      orc_queue_get(qs[j], out_rp + pos, out_rd + pos, out_cx + pos, &out_clock[j],
+                    &out_iters[j]);
+      pos += qs[j]->n;
+      out_offsets[j + 1] = (int32_t)pos;
+    }
+  }
+  for (int32_t j = 0; j < n_inst; ++j) orc_queue_free(qs[j]);
+  free(qs);
+  free(row);
+  return st;
+}
+
+/* ---------------------------------------------------------------- stats */
+
+static int cmp_double(const void *x, const void *y) {
+  double a = *(const double *)x, b = *(const double *)y;
+  return (a > b) - (a < b);
+}
+
+/*
+ * Per-scenario summary of a routed trace (the two axes of the utility-latency
+ * trade-off, E[U] and E[L], of Sec. 3): mean accuracy, mean cost and mean utility
+ * (Eq. 2) at the chosen instances, each a left fold in query order divided by N,
+ * and the nearest-rank 50th and 99th percentiles of the chosen TTFTs.
+ */
+int orc_stats(int32_t n_q, const int32_t *choice, const double *ttft_chosen, const double *acc,
+              const double *cost, int32_t n_cols, const int32_t *col, double w_cost,
+              double *out5) {
+  if (n_q < 1) return ORC_E_ARG;
+  double sa = 0.0, sc = 0.0, su = 0.0;
+  for (int32_t i = 0; i < n_q; ++i) {
+    double ac = acc[(int64_t)i * n_cols + col[choice[i]]];
+    double co = cost[(int64_t)i * n_cols + col[choice[i]]];
+    double pen = w_cost * co;
+    double u = ac - pen;
+    sa = sa + ac;
+    sc = sc + co;
+    su = su + u;
+  }
+  double *s = (double *)malloc((size_t)n_q * sizeof(double));
+  if (!s) return ORC_E_ARG;
+  memcpy(s, ttft_chosen, (size_t)n_q * sizeof(double));
+  qsort(s, (size_t)n_q, sizeof(double), cmp_double);
+  int64_t k50 = ((int64_t)50 * n_q + 99) / 100 - 1;
+  int64_t k99 = ((int64_t)99 * n_q + 99) / 100 - 1;
+  out5[0] = sa / (double)n_q;
+  out5[1] = sc / (double)n_q;
+  out5[2] = su / (double)n_q;
+  out5[3] = s[k50];
+  out5[4] = s[k99];
+  free(s);
+  return ORC_OK;
+}

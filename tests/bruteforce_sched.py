@@ -1,0 +1,163 @@
+"""Token-at-a-time reference scheduler, used only to pin the C oracle.
+
+It builds each token batch by handing out the token budget ONE TOKEN AT A TIME
+(not in chunks), and accumulates the batch-time features per token from their
+descriptions in Sec. 4.1 (token-batch processing time):
+  * each decode token reads the KV cache of its sequence: C gets the sequence's
+    context length c before the batch;
+  * the k-th prefill token of a chunk attends to the context already present plus
+    the chunk's preceding tokens and itself: A gets c + k.
+Python floats are binary64 with round-to-nearest-even and no fused
+multiply-add.  The logic is written independently of ``oracle/sfs_oracle.c``.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+
+class Req:
+    __slots__ = ("rp", "rd", "cx")
+
+    def __init__(self, rp, rd, cx):
+        self.rp, self.rd, self.cx = int(rp), int(rd), int(cx)
+
+    def tup(self):
+        return (self.rp, self.rd, self.cx)
+
+
+class BFInstance:
+    def __init__(self, a, b, c, d, e, budget, max_seqs, rp=(), rd=(), cx=(), clock=0.0):
+        self.coef = (float(a), float(b), float(c), float(d), float(e))
+        self.B, self.M = int(budget), int(max_seqs)
+        self.reqs = [Req(x, y, z) for x, y, z in zip(rp, rd, cx)]
+        self.clock = float(clock)
+
+    def copy(self):
+        o = BFInstance(*self.coef, self.B, self.M, clock=self.clock)
+        o.reqs = [Req(*r.tup()) for r in self.reqs]
+        return o
+
+    # -- one batch, token by token ---------------------------------------------------
+    def batch(self):
+        """Return (T, features, per-request tokens) of the next batch; do not apply it."""
+        budget = self.B
+        given_pre = [0] * len(self.reqs)
+        given_dec = [0] * len(self.reqs)
+        in_service = [r.cx > 0 for r in self.reqs]
+        slots = sum(in_service)
+        P = D = Cf = A = 0
+        for i, r in enumerate(self.reqs):           # one decode token per decoding sequence
+            if r.cx > 0 and r.rp == 0 and budget > 0:
+                given_dec[i] = 1
+                budget -= 1
+                D += 1
+                Cf += r.cx
+        while budget > 0:                            # then prefill, one token at a time
+            nxt = None
+            for i, r in enumerate(self.reqs):
+                if r.rp - given_pre[i] > 0:
+                    nxt = i
+                    break
+            if nxt is None:
+                break
+            if not in_service[nxt]:
+                if slots >= self.M:
+                    break                            # head of line cannot get a slot
+                in_service[nxt] = True
+                slots += 1
+            given_pre[nxt] += 1
+            budget -= 1
+            P += 1
+            A += self.reqs[nxt].cx + given_pre[nxt]
+        a, b, c, d, e = self.coef
+        T = a
+        T = T + b * float(P)
+        T = T + c * float(D)
+        T = T + d * float(Cf)
+        T = T + e * float(A)
+        return T, (P, D, Cf, A), given_pre, given_dec
+
+    def apply(self, given_pre, given_dec):
+        keep = []
+        for i, r in enumerate(self.reqs):
+            r.cx += given_pre[i] + given_dec[i]
+            r.rp -= given_pre[i]
+            r.rd -= given_dec[i]
+            if r.rd > 0:
+                keep.append(r)
+        self.reqs = keep
+
+    def step(self):
+        T, f, gp, gd = self.batch()
+        self.clock = self.clock + T
+        self.apply(gp, gd)
+        return T, f
+
+    def advance(self, t):
+        while self.reqs and self.clock < t:
+            self.step()
+        if not self.reqs and self.clock < t:
+            self.clock = float(t)
+
+    def append(self, p, d):
+        self.reqs.append(Req(p, max(int(d), 1), 0))
+
+    def estimate(self, p, d, t, reading=0):
+        w = self.copy()
+        w.append(p, d)
+        q = w.reqs[-1]
+        E = w.clock
+        n = 0
+        feats = []
+        while True:
+            T, f, gp, gd = w.batch()
+            me = len(w.reqs) - 1
+            if reading == 1:
+                done = gp[me] > 0 and gp[me] == q.rp
+            else:
+                done = gd[me] == 1
+            E = E + T
+            n += 1
+            feats.append(f)
+            w.apply(gp, gd)
+            if done:
+                return E - t, n, feats
+
+    def state(self):
+        return [r.tup() for r in self.reqs]
+
+
+def instances_of(wl):
+    out = []
+    for j in range(wl.n_inst):
+        rp, rd, cx = wl.instance_requests(j)
+        out.append(BFInstance(wl.a[j], wl.b[j], wl.c[j], wl.d[j], wl.e[j], wl.budget[j],
+                              wl.max_seqs[j], rp, rd, cx, wl.clock_ms[j]))
+    return out
+
+
+def trace(wl, scenario=0, n_q=None, reading=0):
+    """Sequential trace with the route computed by numpy (first maximum wins)."""
+    insts = instances_of(wl)
+    N = wl.n_q if n_q is None else n_q
+    col = np.asarray(wl.col)
+    wc, wlat = float(wl.w_cost[scenario]), float(wl.w_lat_ms[scenario])
+    choices, rows = [], []
+    if N:
+        for x in insts:
+            x.advance(wl.q_t_ms[0])
+    for i in range(N):
+        p, d, t = int(wl.q_prefill[i]), int(wl.q_decode[i]), float(wl.q_t_ms[i])
+        row = np.array([x.estimate(p, d, t, reading)[0] for x in insts])
+        acc = wl.acc[i][col]
+        cost = wl.cost[i][col]
+        u = (acc - wc * cost) - wlat * row
+        m = int(np.argmax(u))
+        choices.append(m)
+        rows.append(row)
+        insts[m].append(p, d)
+        t_next = float(wl.q_t_ms[i + 1]) if i + 1 < N else t
+        for x in insts:
+            x.advance(t_next)
+    return np.array(choices, np.int32), np.array(rows), insts
