@@ -1,0 +1,217 @@
+/*
+ * lar.h -- C ABI of the MI355X SFS TTFT estimator and latency-aware router.
+ *
+ * The library estimates, for every (scenario z, query q, model instance j), the
+ * time-to-first-token of q at j by Serving Framework Simulation (SFS, Sec. 4.1):
+ * the instance's resident requests plus the new query are replayed through the
+ * serving scheduler's token batches -- one decode token per decoding sequence,
+ * then prefill chunks in arrival (FCFS) order under a per-batch token budget B
+ * and a cap M on running sequences -- and the modelled batch times
+ *     T = a + b*P + c*D + d*C + e*A                  (batch-time model, Sec. 4.1)
+ * are summed up to and including the batch in which q produces its first decode
+ * token (the first-output-token batch and the SFS TTFT sum, Sec. 4.1).
+ * P = prefill tokens, D = decode tokens, C = context of the decoding sequences,
+ * A = sum over chunks of chunk*context + chunk*(chunk+1)/2.  In the paper's
+ * notation a = beta_0, b = c = beta_1, d = beta_2, e = beta_3.  Every binary64
+ * operation is one round-to-nearest-even operation in the order written, with no
+ * fused multiply-add; sums over batches are left folds in batch order.
+ *
+ * Routing follows the Lagrangian objective of Sec. 3 with the utility of Eq. 2:
+ *     u_j = (acc_j - w_cost*cost_j) - w_lat*TTFT_j,   choice = lowest j with max u.
+ *
+ * Conventions
+ *  - Every call returns lar_status (LAR_OK == 0, errors < 0).
+ *  - Pointers marked "dev" are device (HBM) pointers; "host" are host pointers.
+ *    The caller owns all array arguments (contiguous, int32 / int64 / float64 as
+ *    declared).  The context owns its device state, allocated by lar_create and
+ *    lar_load_state; the estimate / route / commit / trace / stats calls allocate
+ *    nothing.
+ *  - Calls enqueue work on the context's HIP stream and return without waiting;
+ *    outputs are valid once the caller synchronises the stream (or lar_sync).
+ *  - Errors found on the host (bad arguments) return at once with nothing
+ *    enqueued; lar_error_string() gives the detail.  Errors found by kernels
+ *    (queue overflow, iteration cap, instance not advanced, prompt too long) set a
+ *    sticky device flag, reported by lar_sync / lar_read_state; once observed it is
+ *    returned by every later call until lar_load_state resets it.
+ *  - A context is not thread-safe.
+ *
+ * Time unit: milliseconds.  Layouts are row-major.
+ */
+#ifndef LAR_H
+#define LAR_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct lar_ctx lar_ctx;
+typedef int32_t lar_status;
+
+enum {
+  LAR_OK = 0,
+  LAR_E_ARG = -1,      /* invalid argument                                      */
+  LAR_E_STATE = -2,    /* invalid snapshot, or an instance clock behind t       */
+  LAR_E_CAPACITY = -3, /* waiting queue of an instance would exceed queue_cap   */
+  LAR_E_ITER = -4,     /* a simulation needed more than max_iters batches       */
+  LAR_E_HIP = -5       /* HIP runtime failure                                   */
+};
+
+/* Which batch yields the first token (the first-output-token batch, Sec. 4.1). */
+enum {
+  LAR_FIRST_TOKEN_DECODE_BATCH = 0,  /* default: first batch in which q decodes     */
+  LAR_FIRST_TOKEN_PREFILL_BATCH = 1  /* alternate reading: batch completing q's prefill */
+};
+
+/* Per-instance batch-time coefficients (ms) and scheduler limits (Sec. 4.1). */
+typedef struct {
+  double a, b, c, d, e;   /* T = a + b*P + c*D + d*C + e*A, all finite             */
+  int32_t token_budget;   /* B: tokens per batch, max_seqs <= B <= 2^30            */
+  int32_t max_seqs;       /* M: running sequences, 1 <= M <= lar_config.max_seqs_cap */
+  int32_t col;            /* column of this instance in the acc / cost arrays, >= 0 */
+  int32_t reserved;       /* must be 0                                              */
+} lar_instance_params;
+
+typedef struct {
+  int32_t n_scen;         /* Z >= 1 routing scenarios (independent state copies)    */
+  int32_t n_inst;         /* I >= 1 model instances                                 */
+  int32_t max_seqs_cap;   /* upper bound on every instance's M, 1..1024             */
+  int32_t queue_cap;      /* waiting requests per (scenario, instance), >= 1        */
+  int32_t max_prompt;     /* largest query prompt accepted (tokens), >= 1           */
+  int32_t flags;          /* LAR_FIRST_TOKEN_*                                      */
+  int64_t max_iters;      /* batch cap of one estimate or one advance, >= 1         */
+  void *stream;           /* hipStream_t to enqueue on; NULL = null stream          */
+} lar_config;
+
+/* Create a context and allocate its device state.  *out is NULL on failure. */
+lar_status lar_create(lar_ctx **out, const lar_config *cfg);
+
+/* Free the context (synchronises its stream first).  NULL is accepted. */
+lar_status lar_destroy(lar_ctx *ctx);
+
+/* Detail of the last error on this context; owned by the context. */
+const char *lar_error_string(const lar_ctx *ctx);
+
+/*
+ * Load an instance snapshot (Sec. 4 setup; App. E, workload snapshots): for every
+ * instance j, its resident requests in FCFS order, requests offsets[j] ..
+ * offsets[j+1]-1 of the host arrays, each with remaining prefill rem_prefill,
+ * predicted remaining decode rem_decode and context length context (0 = waiting).
+ * The snapshot is copied into every scenario.  Validates: offsets non-decreasing
+ * from 0; rem_prefill >= 0; rem_decode >= 1; context >= 0; rem_prefill == 0
+ * implies context > 0; running (context > 0) before waiting; at most max_seqs
+ * running (LAR_E_STATE), at most queue_cap waiting (LAR_E_CAPACITY); finite
+ * clocks.  Resets the sticky device error.  Synchronises the stream.
+ *   params   host [I]
+ *   offsets  host [I+1]
+ *   rem_prefill, rem_decode, context  host [offsets[I]]
+ *   clock_ms host [I]  instance clocks
+ */
+lar_status lar_load_state(lar_ctx *ctx, const lar_instance_params *params,
+                          const int32_t *offsets, const int32_t *rem_prefill,
+                          const int32_t *rem_decode, const int32_t *context,
+                          const double *clock_ms);
+
+/*
+ * Re-install the snapshot of the last lar_load_state (kept in device memory) into
+ * every scenario, with device-to-device copies enqueued on the stream: no host
+ * traffic, no synchronisation.  Clears the sticky device error.  Use it to replay
+ * a trace again from the same snapshot.
+ */
+lar_status lar_reload_state(lar_ctx *ctx);
+
+/*
+ * SFS what-if estimate (Sec. 4.1): TTFT of each query q (prompt q_prefill[q]
+ * tokens, 1..max_prompt) arriving at time t_ms at every instance of every
+ * scenario.  Pure: the state is not modified.  Every instance clock must be
+ * >= t_ms (advance with lar_commit first), else the sticky LAR_E_STATE is set.
+ *   q_prefill dev [Q]
+ *   ttft_ms   dev [Z][Q][I]  float64, TTFT = (clock + T_1 + ... + T_l) - t_ms
+ *   iters     dev [Z][Q][I]  int32, l = number of batches simulated; may be NULL
+ */
+lar_status lar_estimate_ttft(lar_ctx *ctx, int32_t n_q, const int32_t *q_prefill, double t_ms,
+                             double *ttft_ms, int32_t *iters);
+
+/*
+ * Route (Lagrangian objective, Sec. 3, with the utility of Eq. 2):
+ *   choice[z][q] = lowest j maximising (acc[q][col_j] - w_cost[z]*cost[q][col_j])
+ *                                        - w_lat[z]*ttft_ms[z][q][j].
+ *   ttft_ms     dev [Z][Q][I]
+ *   acc, cost   dev [Q][n_cols]; col_j = params[j].col must be < n_cols
+ *   w_cost      dev [Z]   (lambda of Eq. 2)
+ *   w_lat       dev [Z]   latency weight per ms (delta of the objective, per ms)
+ *   choice      dev [Z][Q] int32
+ *   chosen_ttft dev [Z][Q] TTFT at the choice; may be NULL
+ *   utility     dev [Z][Q] acc - w_cost*cost at the choice (Eq. 2); may be NULL
+ * NaN utilities are not supported.
+ */
+lar_status lar_route(lar_ctx *ctx, int32_t n_q, const double *ttft_ms, const double *acc,
+                     const double *cost, int32_t n_cols, const double *w_cost,
+                     const double *w_lat, int32_t *choice, double *chosen_ttft,
+                     double *utility);
+
+/*
+ * Commit one routed query and replay the instances to t_next_ms: in scenario z,
+ * the query (q_prefill >= 1 prompt tokens, q_decode predicted decode tokens,
+ * raised to 1) joins the FCFS tail of instance choice[z] as a waiting request
+ * (choice == NULL or choice[z] < 0: nothing is appended); then on every instance
+ * every batch that starts before t_next_ms runs, and an idle instance's clock
+ * jumps to t_next_ms.  A full waiting queue sets the sticky LAR_E_CAPACITY.
+ *   choice dev [Z] or NULL
+ */
+lar_status lar_commit(lar_ctx *ctx, const int32_t *choice, int32_t q_prefill, int32_t q_decode,
+                      double t_next_ms);
+
+/*
+ * Sequential routing of N queries, exactly the call sequence
+ *   for i in 0..N-1:
+ *     lar_estimate_ttft(1 query q_prefill[i], t = q_t_ms[i])
+ *     lar_route(row i of acc / cost)            -> choice[z][i]
+ *     lar_commit(choice[.][i], q_prefill[i], q_decode[i], t_next)
+ *   with t_next = q_t_ms[i+1], and t_after_ms for the last query.
+ * The instances must already be advanced to q_t_ms[0].
+ *   q_prefill, q_decode dev [N] int32;  q_t_ms dev [N] non-decreasing
+ *   acc, cost dev [N][n_cols];  w_cost, w_lat dev [Z]
+ *   choice dev [Z][N];  chosen_ttft, utility dev [Z][N] (may be NULL)
+ */
+lar_status lar_route_trace(lar_ctx *ctx, int32_t n_q, const int32_t *q_prefill,
+                           const int32_t *q_decode, const double *q_t_ms, double t_after_ms,
+                           const double *acc, const double *cost, int32_t n_cols,
+                           const double *w_cost, const double *w_lat, int32_t *choice,
+                           double *chosen_ttft, double *utility);
+
+/*
+ * Per-scenario summary of a routed trace -- the two axes of the utility-latency
+ * trade-off of Sec. 3, E[U] and E[L]:
+ *   stats[z] = { mean acc, mean cost, mean (acc - w_cost[z]*cost) (Eq. 2),
+ *                p50 TTFT, p99 TTFT }
+ * at the chosen instances; means are left folds in query order divided by N,
+ * percentiles nearest-rank (sorted[ceil(p*N/100) - 1]).
+ *   choice, chosen_ttft dev [Z][N];  acc, cost dev [N][n_cols];  w_cost dev [Z]
+ *   stats dev [Z][5] float64
+ */
+lar_status lar_stats(lar_ctx *ctx, int32_t n_q, const int32_t *choice, const double *chosen_ttft,
+                     const double *acc, const double *cost, int32_t n_cols,
+                     const double *w_cost, double *stats);
+
+/*
+ * Copy scenario `scen`'s state out (synchronises): resident requests of every
+ * instance in FCFS order as in lar_load_state, the clocks and the number of
+ * batches replayed per instance since the load.  out_cap = capacity of the
+ * request arrays; LAR_E_CAPACITY if they are too small (*n_total still set).
+ *   offsets host [I+1]; rem_prefill, rem_decode, context host [out_cap]
+ *   clock_ms host [I]; iterations_run host [I]
+ */
+lar_status lar_read_state(lar_ctx *ctx, int32_t scen, int32_t *offsets, int32_t *rem_prefill,
+                          int32_t *rem_decode, int32_t *context, double *clock_ms,
+                          int64_t *iterations_run, int64_t out_cap, int64_t *n_total);
+
+/* Synchronise the stream; return the sticky device error, if any. */
+lar_status lar_sync(lar_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LAR_H */

@@ -1,0 +1,494 @@
+// lar_api.cpp -- host implementation of the C ABI declared in include/lar.h.
+//
+// Owns the device state of a context (structure-of-arrays in HBM, one slice per
+// (scenario, instance) queue), validates snapshots on the host, and enqueues the
+// kernels of sfs_kernels.hip on the caller's stream.  Hot calls (estimate, route,
+// commit, trace, stats) allocate nothing and never synchronise.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/lar.h"
+#include "sfs_launch.h"
+
+using lar::LaunchEnv;
+
+struct lar_ctx {
+  lar_config cfg{};
+  int Z = 0, I = 0, mcap = 0, qcap = 0, ks = 0;
+  hipStream_t stream = nullptr;
+  lar::DevState S{};
+  lar::DevTraj T{};
+  // parameters on device
+  double* pa = nullptr;   // [5][I]: a, b, c, d, e
+  int32_t* pi = nullptr;  // [3][I]: B, M, col
+  double* row_ttft = nullptr;  // [Z][I] scratch of the sequential trace
+  lar::DevState snap{};        // one scenario's copy of the last loaded snapshot
+  int32_t* err = nullptr;
+  size_t tail_elems = 0;  // allocated K * Z * I
+  bool loaded = false;
+  int max_col = 0;
+  lar_status sticky = LAR_OK;
+  std::string msg;
+  std::vector<void*> allocs;
+};
+
+namespace {
+
+lar_status fail(lar_ctx* ctx, lar_status code, const char* fmt, ...) {
+  if (ctx) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    ctx->msg = buf;
+  }
+  return code;
+}
+
+#define HIP_TRY(ctx, expr)                                                             \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail(ctx, LAR_E_HIP, "%s: %s", #expr, hipGetErrorString(e_));             \
+  } while (0)
+
+template <class T>
+lar_status dev_alloc(lar_ctx* ctx, T** p, size_t n) {
+  void* q = nullptr;
+  hipError_t e = hipMalloc(&q, n ? n * sizeof(T) : 16);
+  if (e != hipSuccess) return fail(ctx, LAR_E_HIP, "hipMalloc(%zu): %s", n * sizeof(T),
+                                   hipGetErrorString(e));
+  ctx->allocs.push_back(q);
+  *p = static_cast<T*>(q);
+  return LAR_OK;
+}
+
+void dev_free(lar_ctx* ctx, void* p) {
+  if (!p) return;
+  for (auto& a : ctx->allocs)
+    if (a == p) { (void)hipFree(p); a = nullptr; }
+}
+
+LaunchEnv env_of(const lar_ctx* ctx) {
+  LaunchEnv e;
+  e.S = ctx->S;
+  e.P.a = ctx->pa;
+  e.P.b = ctx->pa + ctx->I;
+  e.P.c = ctx->pa + 2 * ctx->I;
+  e.P.d = ctx->pa + 3 * ctx->I;
+  e.P.e = ctx->pa + 4 * ctx->I;
+  e.P.B = ctx->pi;
+  e.P.M = ctx->pi + ctx->I;
+  e.P.col = ctx->pi + 2 * ctx->I;
+  e.T = ctx->T;
+  e.Z = ctx->Z;
+  e.I = ctx->I;
+  e.ks = ctx->ks;
+  e.max_iters = ctx->cfg.max_iters;
+  e.max_prompt = ctx->cfg.max_prompt;
+  e.reading = ctx->cfg.flags & 1;
+  e.err = ctx->err;
+  e.stream = ctx->stream;
+  return e;
+}
+
+lar_status ready(lar_ctx* ctx) {
+  if (!ctx) return LAR_E_ARG;
+  if (ctx->sticky != LAR_OK) return ctx->sticky;
+  if (!ctx->loaded) return fail(ctx, LAR_E_STATE, "no state loaded (call lar_load_state)");
+  return LAR_OK;
+}
+
+const int64_t kMaxBudget = int64_t(1) << 30;
+
+}  // namespace
+
+extern "C" {
+
+lar_status lar_create(lar_ctx** out, const lar_config* cfg) {
+  if (!out) return LAR_E_ARG;
+  *out = nullptr;
+  if (!cfg) return LAR_E_ARG;
+  if (cfg->n_scen < 1 || cfg->n_inst < 1 || cfg->max_seqs_cap < 1 || cfg->max_seqs_cap > 1024 ||
+      cfg->queue_cap < 1 || cfg->max_prompt < 1 || cfg->max_iters < 1 ||
+      (cfg->flags & ~1) != 0)
+    return LAR_E_ARG;
+  if ((int64_t)cfg->n_scen * cfg->n_inst > (int64_t)1 << 24) return LAR_E_ARG;
+  lar_ctx* ctx = new lar_ctx;
+  ctx->cfg = *cfg;
+  ctx->Z = cfg->n_scen;
+  ctx->I = cfg->n_inst;
+  ctx->mcap = cfg->max_seqs_cap;
+  ctx->qcap = cfg->queue_cap;
+  ctx->ks = 1;
+  while (ctx->ks * 64 < ctx->mcap) ctx->ks *= 2;
+  ctx->stream = static_cast<hipStream_t>(cfg->stream);
+  const size_t ZI = (size_t)ctx->Z * ctx->I;
+  lar_status st = LAR_OK;
+  auto chk = [&](lar_status s) { if (st == LAR_OK) st = s; };
+  chk(dev_alloc(ctx, &ctx->S.run_rp, ZI * ctx->mcap));
+  chk(dev_alloc(ctx, &ctx->S.run_rd, ZI * ctx->mcap));
+  chk(dev_alloc(ctx, &ctx->S.run_cx, ZI * ctx->mcap));
+  chk(dev_alloc(ctx, &ctx->S.wait_p, ZI * ctx->qcap));
+  chk(dev_alloc(ctx, &ctx->S.wait_rd, ZI * ctx->qcap));
+  chk(dev_alloc(ctx, &ctx->S.n_run, ZI));
+  chk(dev_alloc(ctx, &ctx->S.w_head, ZI));
+  chk(dev_alloc(ctx, &ctx->S.n_wait, ZI));
+  chk(dev_alloc(ctx, &ctx->S.clock, ZI));
+  chk(dev_alloc(ctx, &ctx->S.iters, ZI));
+  chk(dev_alloc(ctx, &ctx->pa, 5 * (size_t)ctx->I));
+  chk(dev_alloc(ctx, &ctx->pi, 3 * (size_t)ctx->I));
+  chk(dev_alloc(ctx, &ctx->T.E, ZI));
+  chk(dev_alloc(ctx, &ctx->T.pre, ZI));
+  chk(dev_alloc(ctx, &ctx->T.P, ZI));
+  chk(dev_alloc(ctx, &ctx->T.D, ZI));
+  chk(dev_alloc(ctx, &ctx->T.C, ZI));
+  chk(dev_alloc(ctx, &ctx->T.A, ZI));
+  chk(dev_alloc(ctx, &ctx->T.left, ZI));
+  chk(dev_alloc(ctx, &ctx->T.ok, ZI));
+  chk(dev_alloc(ctx, &ctx->row_ttft, ZI));
+  chk(dev_alloc(ctx, &ctx->err, 1));
+  chk(dev_alloc(ctx, &ctx->snap.run_rp, (size_t)ctx->I * ctx->mcap));
+  chk(dev_alloc(ctx, &ctx->snap.run_rd, (size_t)ctx->I * ctx->mcap));
+  chk(dev_alloc(ctx, &ctx->snap.run_cx, (size_t)ctx->I * ctx->mcap));
+  chk(dev_alloc(ctx, &ctx->snap.wait_p, (size_t)ctx->I * ctx->qcap));
+  chk(dev_alloc(ctx, &ctx->snap.wait_rd, (size_t)ctx->I * ctx->qcap));
+  chk(dev_alloc(ctx, &ctx->snap.n_run, ctx->I));
+  chk(dev_alloc(ctx, &ctx->snap.w_head, ctx->I));
+  chk(dev_alloc(ctx, &ctx->snap.n_wait, ctx->I));
+  chk(dev_alloc(ctx, &ctx->snap.clock, ctx->I));
+  chk(dev_alloc(ctx, &ctx->snap.iters, ctx->I));
+  if (st != LAR_OK) {
+    lar_destroy(ctx);
+    return st;
+  }
+  ctx->S.mcap = ctx->mcap;
+  ctx->S.qcap = ctx->qcap;
+  ctx->T.K = 0;
+  *out = ctx;
+  return LAR_OK;
+}
+
+lar_status lar_destroy(lar_ctx* ctx) {
+  if (!ctx) return LAR_OK;
+  (void)hipStreamSynchronize(ctx->stream);
+  for (void* p : ctx->allocs)
+    if (p) (void)hipFree(p);
+  delete ctx;
+  return LAR_OK;
+}
+
+const char* lar_error_string(const lar_ctx* ctx) {
+  if (!ctx) return "null context";
+  return ctx->msg.c_str();
+}
+
+lar_status lar_load_state(lar_ctx* ctx, const lar_instance_params* params, const int32_t* offsets,
+                          const int32_t* rem_prefill, const int32_t* rem_decode,
+                          const int32_t* context, const double* clock_ms) {
+  if (!ctx) return LAR_E_ARG;
+  if (!params || !offsets || !clock_ms) return fail(ctx, LAR_E_ARG, "null argument");
+  const int I = ctx->I, Z = ctx->Z, mcap = ctx->mcap, qcap = ctx->qcap;
+  if (offsets[0] != 0) return fail(ctx, LAR_E_ARG, "offsets[0] must be 0");
+  for (int j = 0; j < I; ++j)
+    if (offsets[j + 1] < offsets[j]) return fail(ctx, LAR_E_ARG, "offsets decrease at %d", j);
+  if (offsets[I] > 0 && (!rem_prefill || !rem_decode || !context))
+    return fail(ctx, LAR_E_ARG, "null request arrays");
+  int max_col = 0;
+  int64_t K = 1;
+  for (int j = 0; j < I; ++j) {
+    const lar_instance_params& p = params[j];
+    const double co[5] = {p.a, p.b, p.c, p.d, p.e};
+    for (double v : co)
+      if (!std::isfinite(v)) return fail(ctx, LAR_E_ARG, "instance %d: non-finite coefficient", j);
+    if (p.max_seqs < 1 || p.max_seqs > mcap)
+      return fail(ctx, LAR_E_ARG, "instance %d: max_seqs %d outside [1, %d]", j, p.max_seqs, mcap);
+    if (p.token_budget < p.max_seqs || p.token_budget > kMaxBudget)
+      return fail(ctx, LAR_E_ARG, "instance %d: token_budget %d outside [max_seqs, 2^30]", j,
+                  p.token_budget);
+    if (p.col < 0 || p.reserved != 0)
+      return fail(ctx, LAR_E_ARG, "instance %d: bad col/reserved", j);
+    if (!std::isfinite(clock_ms[j])) return fail(ctx, LAR_E_ARG, "instance %d: bad clock", j);
+    if (p.col > max_col) max_col = p.col;
+    // decode-only batches the longest query can need after its admission batch:
+    // it gets >= 1 token there and >= B - M + 1 per later batch, then one decode batch
+    const int64_t room = (int64_t)p.token_budget - p.max_seqs + 1;
+    const int64_t k = ((int64_t)ctx->cfg.max_prompt - 1 + room - 1) / room + 1;
+    if (k > K) K = k;
+  }
+  // validate the snapshot and lay it out as the device SoA of one scenario
+  std::vector<int32_t> run_rp((size_t)I * mcap, 0), run_rd((size_t)I * mcap, 0),
+      run_cx((size_t)I * mcap, 0), wait_p((size_t)I * qcap, 0), wait_rd((size_t)I * qcap, 0),
+      n_run(I), head(I, 0), n_wait(I);
+  std::vector<double> clock(clock_ms, clock_ms + I);
+  std::vector<int64_t> iters(I, 0);
+  for (int j = 0; j < I; ++j) {
+    int nr = 0, nw = 0;
+    for (int r = offsets[j]; r < offsets[j + 1]; ++r) {
+      const int32_t rp = rem_prefill[r], rd = rem_decode[r], cx = context[r];
+      if (rp < 0 || rd < 1 || cx < 0 || (rp == 0 && cx == 0))
+        return fail(ctx, LAR_E_STATE, "instance %d request %d: invalid (rp %d, rd %d, cx %d)", j,
+                    r - offsets[j], rp, rd, cx);
+      if (cx > 0) {
+        if (nw > 0)
+          return fail(ctx, LAR_E_STATE, "instance %d: running request after a waiting one", j);
+        if (nr >= params[j].max_seqs)
+          return fail(ctx, LAR_E_STATE, "instance %d: more than max_seqs running", j);
+        run_rp[(size_t)j * mcap + nr] = rp;
+        run_rd[(size_t)j * mcap + nr] = rd;
+        run_cx[(size_t)j * mcap + nr] = cx;
+        ++nr;
+      } else {
+        if (nw >= qcap)
+          return fail(ctx, LAR_E_CAPACITY, "instance %d: more than queue_cap waiting", j);
+        wait_p[(size_t)j * qcap + nw] = rp;
+        wait_rd[(size_t)j * qcap + nw] = rd;
+        ++nw;
+      }
+    }
+    n_run[j] = nr;
+    n_wait[j] = nw;
+  }
+  // trajectory tail buffers (grow only)
+  const size_t ZI = (size_t)Z * I;
+  if ((size_t)K * ZI > ctx->tail_elems) {
+    dev_free(ctx, ctx->T.tailD);
+    dev_free(ctx, ctx->T.tailC);
+    ctx->T.tailD = nullptr;
+    ctx->T.tailC = nullptr;
+    ctx->tail_elems = 0;
+    lar_status s = dev_alloc(ctx, &ctx->T.tailD, (size_t)K * ZI);
+    if (s == LAR_OK) s = dev_alloc(ctx, &ctx->T.tailC, (size_t)K * ZI);
+    if (s != LAR_OK) return s;
+    ctx->tail_elems = (size_t)K * ZI;
+  }
+  ctx->T.K = (int32_t)K;
+  // parameters
+  std::vector<double> pa(5 * (size_t)I);
+  std::vector<int32_t> pi(3 * (size_t)I);
+  for (int j = 0; j < I; ++j) {
+    pa[j] = params[j].a;
+    pa[I + j] = params[j].b;
+    pa[2 * I + j] = params[j].c;
+    pa[3 * I + j] = params[j].d;
+    pa[4 * I + j] = params[j].e;
+    pi[j] = params[j].token_budget;
+    pi[I + j] = params[j].max_seqs;
+    pi[2 * I + j] = params[j].col;
+  }
+  hipStream_t s = ctx->stream;
+  HIP_TRY(ctx, hipStreamSynchronize(s));
+  HIP_TRY(ctx, hipMemcpy(ctx->pa, pa.data(), pa.size() * sizeof(double), hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(ctx->pi, pi.data(), pi.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+  lar::DevState& sn = ctx->snap;
+  HIP_TRY(ctx, hipMemcpy(sn.run_rp, run_rp.data(), run_rp.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.run_rd, run_rd.data(), run_rd.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.run_cx, run_cx.data(), run_cx.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.wait_p, wait_p.data(), wait_p.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.wait_rd, wait_rd.data(), wait_rd.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.n_run, n_run.data(), I * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.w_head, head.data(), I * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.n_wait, n_wait.data(), I * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.clock, clock.data(), I * 8, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.iters, iters.data(), I * 8, hipMemcpyHostToDevice));
+  ctx->loaded = true;
+  ctx->sticky = LAR_OK;
+  {
+    lar_status rs = lar_reload_state(ctx);
+    if (rs != LAR_OK) { ctx->loaded = false; return rs; }
+  }
+  HIP_TRY(ctx, hipStreamSynchronize(s));
+  ctx->max_col = max_col;
+  ctx->msg.clear();
+  return LAR_OK;
+}
+
+lar_status lar_reload_state(lar_ctx* ctx) {
+  if (!ctx) return LAR_E_ARG;
+  if (!ctx->loaded) return fail(ctx, LAR_E_STATE, "no state loaded (call lar_load_state)");
+  const int I = ctx->I, mcap = ctx->mcap, qcap = ctx->qcap;
+  const lar::DevState& sn = ctx->snap;
+  const lar::DevState& S = ctx->S;
+  hipStream_t s = ctx->stream;
+  const hipMemcpyKind k = hipMemcpyDeviceToDevice;
+  for (int z = 0; z < ctx->Z; ++z) {
+    const size_t o = (size_t)z * I;
+    HIP_TRY(ctx, hipMemcpyAsync(S.run_rp + o * mcap, sn.run_rp, (size_t)I * mcap * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.run_rd + o * mcap, sn.run_rd, (size_t)I * mcap * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.run_cx + o * mcap, sn.run_cx, (size_t)I * mcap * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.wait_p + o * qcap, sn.wait_p, (size_t)I * qcap * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.wait_rd + o * qcap, sn.wait_rd, (size_t)I * qcap * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.n_run + o, sn.n_run, (size_t)I * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.w_head + o, sn.w_head, (size_t)I * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.n_wait + o, sn.n_wait, (size_t)I * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.clock + o, sn.clock, (size_t)I * 8, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.iters + o, sn.iters, (size_t)I * 8, k, s));
+  }
+  HIP_TRY(ctx, lar::launch_clear_error(env_of(ctx)));
+  ctx->sticky = LAR_OK;
+  return LAR_OK;
+}
+
+lar_status lar_estimate_ttft(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill, double t_ms,
+                             double* ttft_ms, int32_t* iters) {
+  lar_status st = ready(ctx);
+  if (st != LAR_OK) return st;
+  if (n_q < 0) return fail(ctx, LAR_E_ARG, "n_q < 0");
+  if (n_q == 0) return LAR_OK;
+  if (!q_prefill || !ttft_ms) return fail(ctx, LAR_E_ARG, "null argument");
+  if (!std::isfinite(t_ms)) return fail(ctx, LAR_E_ARG, "t_ms not finite");
+  if ((int64_t)ctx->Z * n_q * ctx->I > ((int64_t)1 << 40))
+    return fail(ctx, LAR_E_ARG, "output too large");
+  const LaunchEnv env = env_of(ctx);
+  HIP_TRY(ctx, lar::launch_traj(env, nullptr, t_ms));
+  HIP_TRY(ctx, lar::launch_est(env, n_q, q_prefill, nullptr, t_ms, ttft_ms, iters));
+  return LAR_OK;
+}
+
+lar_status lar_route(lar_ctx* ctx, int32_t n_q, const double* ttft_ms, const double* acc,
+                     const double* cost, int32_t n_cols, const double* w_cost,
+                     const double* w_lat, int32_t* choice, double* chosen_ttft,
+                     double* utility) {
+  lar_status st = ready(ctx);
+  if (st != LAR_OK) return st;
+  if (n_q < 0) return fail(ctx, LAR_E_ARG, "n_q < 0");
+  if (n_q == 0) return LAR_OK;
+  if (!ttft_ms || !acc || !cost || !w_cost || !w_lat || !choice)
+    return fail(ctx, LAR_E_ARG, "null argument");
+  if (n_cols <= ctx->max_col)
+    return fail(ctx, LAR_E_ARG, "n_cols %d does not cover instance column %d", n_cols, ctx->max_col);
+  if ((int64_t)ctx->Z * n_q > INT32_MAX) return fail(ctx, LAR_E_ARG, "too many rows");
+  const LaunchEnv env = env_of(ctx);
+  HIP_TRY(ctx, lar::launch_route(env, n_q, ttft_ms, (int64_t)n_q * ctx->I, acc, cost, n_cols,
+                                 w_cost, w_lat, choice, chosen_ttft, utility, n_q, 0));
+  return LAR_OK;
+}
+
+lar_status lar_commit(lar_ctx* ctx, const int32_t* choice, int32_t q_prefill, int32_t q_decode,
+                      double t_next_ms) {
+  lar_status st = ready(ctx);
+  if (st != LAR_OK) return st;
+  if (choice && q_prefill < 1) return fail(ctx, LAR_E_ARG, "q_prefill < 1");
+  if (!std::isfinite(t_next_ms)) return fail(ctx, LAR_E_ARG, "t_next_ms not finite");
+  const LaunchEnv env = env_of(ctx);
+  HIP_TRY(ctx, lar::launch_commit(env, choice, 1, nullptr, nullptr, q_prefill, q_decode, nullptr,
+                                  t_next_ms));
+  return LAR_OK;
+}
+
+lar_status lar_route_trace(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill,
+                           const int32_t* q_decode, const double* q_t_ms, double t_after_ms,
+                           const double* acc, const double* cost, int32_t n_cols,
+                           const double* w_cost, const double* w_lat, int32_t* choice,
+                           double* chosen_ttft, double* utility) {
+  lar_status st = ready(ctx);
+  if (st != LAR_OK) return st;
+  if (n_q < 0) return fail(ctx, LAR_E_ARG, "n_q < 0");
+  if (n_q == 0) return LAR_OK;
+  if (!q_prefill || !q_decode || !q_t_ms || !acc || !cost || !w_cost || !w_lat || !choice)
+    return fail(ctx, LAR_E_ARG, "null argument");
+  if (n_cols <= ctx->max_col)
+    return fail(ctx, LAR_E_ARG, "n_cols %d does not cover instance column %d", n_cols, ctx->max_col);
+  if (!std::isfinite(t_after_ms)) return fail(ctx, LAR_E_ARG, "t_after_ms not finite");
+  const LaunchEnv env = env_of(ctx);
+  const int I = ctx->I;
+  for (int32_t i = 0; i < n_q; ++i) {
+    HIP_TRY(ctx, lar::launch_traj(env, q_t_ms + i, 0.0));
+    HIP_TRY(ctx, lar::launch_est(env, 1, q_prefill + i, q_t_ms + i, 0.0, ctx->row_ttft, nullptr));
+    HIP_TRY(ctx, lar::launch_route(env, 1, ctx->row_ttft, I, acc + (int64_t)i * n_cols,
+                                   cost + (int64_t)i * n_cols, n_cols, w_cost, w_lat, choice,
+                                   chosen_ttft, utility, n_q, i));
+    const double* tn = (i + 1 < n_q) ? q_t_ms + i + 1 : nullptr;
+    HIP_TRY(ctx, lar::launch_commit(env, choice + i, n_q, q_prefill + i, q_decode + i, 0, 0, tn,
+                                    t_after_ms));
+  }
+  return LAR_OK;
+}
+
+lar_status lar_stats(lar_ctx* ctx, int32_t n_q, const int32_t* choice, const double* chosen_ttft,
+                     const double* acc, const double* cost, int32_t n_cols,
+                     const double* w_cost, double* stats) {
+  lar_status st = ready(ctx);
+  if (st != LAR_OK) return st;
+  if (n_q < 1) return fail(ctx, LAR_E_ARG, "n_q < 1");
+  if (!choice || !chosen_ttft || !acc || !cost || !w_cost || !stats)
+    return fail(ctx, LAR_E_ARG, "null argument");
+  if (n_cols <= ctx->max_col)
+    return fail(ctx, LAR_E_ARG, "n_cols %d does not cover instance column %d", n_cols, ctx->max_col);
+  const LaunchEnv env = env_of(ctx);
+  HIP_TRY(ctx, lar::launch_stats(env, n_q, choice, chosen_ttft, acc, cost, n_cols, w_cost, stats));
+  return LAR_OK;
+}
+
+lar_status lar_sync(lar_ctx* ctx) {
+  if (!ctx) return LAR_E_ARG;
+  HIP_TRY(ctx, hipStreamSynchronize(ctx->stream));
+  if (ctx->loaded && ctx->sticky == LAR_OK) {
+    int32_t e = 0;
+    HIP_TRY(ctx, hipMemcpy(&e, ctx->err, sizeof e, hipMemcpyDeviceToHost));
+    if (e != 0) {
+      ctx->sticky = e;
+      fail(ctx, e, "device error %d (sticky until lar_load_state)", e);
+    }
+  }
+  return ctx->sticky;
+}
+
+lar_status lar_read_state(lar_ctx* ctx, int32_t scen, int32_t* offsets, int32_t* rem_prefill,
+                          int32_t* rem_decode, int32_t* context, double* clock_ms,
+                          int64_t* iterations_run, int64_t out_cap, int64_t* n_total) {
+  if (!ctx) return LAR_E_ARG;
+  if (!ctx->loaded) return fail(ctx, LAR_E_STATE, "no state loaded");
+  if (scen < 0 || scen >= ctx->Z) return fail(ctx, LAR_E_ARG, "scenario out of range");
+  if (!offsets || !clock_ms || !iterations_run || !n_total || out_cap < 0)
+    return fail(ctx, LAR_E_ARG, "null argument");
+  lar_status st = lar_sync(ctx);
+  if (st == LAR_E_HIP) return st;
+  const int I = ctx->I, mcap = ctx->mcap, qcap = ctx->qcap;
+  const size_t o = (size_t)scen * I;
+  std::vector<int32_t> run_rp((size_t)I * mcap), run_rd((size_t)I * mcap), run_cx((size_t)I * mcap),
+      wait_p((size_t)I * qcap), wait_rd((size_t)I * qcap), n_run(I), head(I), n_wait(I);
+  HIP_TRY(ctx, hipMemcpy(run_rp.data(), ctx->S.run_rp + o * mcap, run_rp.size() * 4, hipMemcpyDeviceToHost));
+  HIP_TRY(ctx, hipMemcpy(run_rd.data(), ctx->S.run_rd + o * mcap, run_rd.size() * 4, hipMemcpyDeviceToHost));
+  HIP_TRY(ctx, hipMemcpy(run_cx.data(), ctx->S.run_cx + o * mcap, run_cx.size() * 4, hipMemcpyDeviceToHost));
+  HIP_TRY(ctx, hipMemcpy(wait_p.data(), ctx->S.wait_p + o * qcap, wait_p.size() * 4, hipMemcpyDeviceToHost));
+  HIP_TRY(ctx, hipMemcpy(wait_rd.data(), ctx->S.wait_rd + o * qcap, wait_rd.size() * 4, hipMemcpyDeviceToHost));
+  HIP_TRY(ctx, hipMemcpy(n_run.data(), ctx->S.n_run + o, I * 4, hipMemcpyDeviceToHost));
+  HIP_TRY(ctx, hipMemcpy(head.data(), ctx->S.w_head + o, I * 4, hipMemcpyDeviceToHost));
+  HIP_TRY(ctx, hipMemcpy(n_wait.data(), ctx->S.n_wait + o, I * 4, hipMemcpyDeviceToHost));
+  HIP_TRY(ctx, hipMemcpy(clock_ms, ctx->S.clock + o, I * 8, hipMemcpyDeviceToHost));
+  HIP_TRY(ctx, hipMemcpy(iterations_run, ctx->S.iters + o, I * 8, hipMemcpyDeviceToHost));
+  int64_t total = 0;
+  for (int j = 0; j < I; ++j) total += n_run[j] + n_wait[j];
+  *n_total = total;
+  if (total > out_cap) return fail(ctx, LAR_E_CAPACITY, "output arrays hold %lld < %lld",
+                                   (long long)out_cap, (long long)total);
+  if (total > 0 && (!rem_prefill || !rem_decode || !context))
+    return fail(ctx, LAR_E_ARG, "null request arrays");
+  int64_t pos = 0;
+  offsets[0] = 0;
+  for (int j = 0; j < I; ++j) {
+    for (int r = 0; r < n_run[j]; ++r, ++pos) {
+      rem_prefill[pos] = run_rp[(size_t)j * mcap + r];
+      rem_decode[pos] = run_rd[(size_t)j * mcap + r];
+      context[pos] = run_cx[(size_t)j * mcap + r];
+    }
+    for (int w = 0; w < n_wait[j]; ++w, ++pos) {
+      const int slot = (head[j] + w) % qcap;
+      rem_prefill[pos] = wait_p[(size_t)j * qcap + slot];
+      rem_decode[pos] = wait_rd[(size_t)j * qcap + slot];
+      context[pos] = 0;
+    }
+    offsets[j + 1] = (int32_t)pos;
+  }
+  return ctx->sticky;
+}
+
+}  // extern "C"

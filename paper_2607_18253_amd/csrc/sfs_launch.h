@@ -1,0 +1,39 @@
+// sfs_launch.h -- host-side launch environment shared by the C ABI and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sfs_device.h"
+
+namespace lar {
+
+struct LaunchEnv {
+  DevState S;
+  DevParams P;
+  DevTraj T;
+  int Z, I;
+  int ks;             // running slots per lane (1, 2, 4, 8, 16)
+  int64_t max_iters;
+  int max_prompt;
+  int reading;        // 0: first decode batch, 1: batch completing the prefill
+  int32_t* err;       // sticky device error
+  hipStream_t stream;
+};
+
+hipError_t launch_traj(const LaunchEnv& env, const double* t_ptr, double t_val);
+hipError_t launch_est(const LaunchEnv& env, int Q, const int32_t* q_prefill, const double* t_ptr,
+                      double t_val, double* ttft, int32_t* iters);
+hipError_t launch_route(const LaunchEnv& env, int Q, const double* ttft, int64_t ttft_zstride,
+                        const double* acc, const double* cost, int n_cols, const double* w_cost,
+                        const double* w_lat, int32_t* choice, double* chosen_ttft,
+                        double* utility, int64_t out_zstride, int out_q0);
+hipError_t launch_commit(const LaunchEnv& env, const int32_t* choice, int64_t choice_zstride,
+                         const int32_t* qp_ptr, const int32_t* qd_ptr, int32_t qp, int32_t qd,
+                         const double* t_ptr, double t_val);
+hipError_t launch_clear_error(const LaunchEnv& env);
+hipError_t launch_stats(const LaunchEnv& env, int N, const int32_t* choice,
+                        const double* chosen_ttft, const double* acc, const double* cost,
+                        int n_cols, const double* w_cost, double* out);
+
+}  // namespace lar

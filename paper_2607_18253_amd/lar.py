@@ -1,0 +1,286 @@
+"""Python binding of ``liblar.so`` (the C ABI in include/lar.h): argument
+marshalling only.  Device arrays are torch tensors on the GPU; snapshots go in and
+out as host numpy arrays.  Every step of the estimator and router runs in the HIP
+kernels behind the C ABI; there is no fallback path -- a missing library raises.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liblar.so")
+
+LAR_OK, LAR_E_ARG, LAR_E_STATE, LAR_E_CAPACITY, LAR_E_ITER, LAR_E_HIP = 0, -1, -2, -3, -4, -5
+FIRST_TOKEN_DECODE_BATCH, FIRST_TOKEN_PREFILL_BATCH = 0, 1
+
+EXPORTED = ("lar_create", "lar_destroy", "lar_error_string", "lar_load_state", "lar_reload_state",
+            "lar_estimate_ttft", "lar_route", "lar_commit", "lar_route_trace", "lar_stats",
+            "lar_read_state", "lar_sync")
+
+
+class LarError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"lar error {code}: {msg}")
+        self.code = code
+
+
+class Config(C.Structure):
+    _fields_ = [("n_scen", C.c_int32), ("n_inst", C.c_int32), ("max_seqs_cap", C.c_int32),
+                ("queue_cap", C.c_int32), ("max_prompt", C.c_int32), ("flags", C.c_int32),
+                ("max_iters", C.c_int64), ("stream", C.c_void_p)]
+
+
+class InstanceParams(C.Structure):
+    _fields_ = [("a", C.c_double), ("b", C.c_double), ("c", C.c_double), ("d", C.c_double),
+                ("e", C.c_double), ("token_budget", C.c_int32), ("max_seqs", C.c_int32),
+                ("col", C.c_int32), ("reserved", C.c_int32)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load liblar.so (after torch, so both share torch's HIP runtime)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run __graft_entry__.build() "
+                           "or python paper_2607_18253_amd/build.py")
+    import torch  # noqa: F401  -- maps torch's HIP runtime before the library's
+    L = C.CDLL(path)
+    vp, i32, i64, dbl = C.c_void_p, C.c_int32, C.c_int64, C.c_double
+    L.lar_create.restype = i32
+    L.lar_create.argtypes = [C.POINTER(vp), C.POINTER(Config)]
+    L.lar_destroy.restype = i32
+    L.lar_destroy.argtypes = [vp]
+    L.lar_error_string.restype = C.c_char_p
+    L.lar_error_string.argtypes = [vp]
+    L.lar_load_state.restype = i32
+    L.lar_load_state.argtypes = [vp, C.POINTER(InstanceParams), vp, vp, vp, vp, vp]
+    L.lar_reload_state.restype = i32
+    L.lar_reload_state.argtypes = [vp]
+    L.lar_estimate_ttft.restype = i32
+    L.lar_estimate_ttft.argtypes = [vp, i32, vp, dbl, vp, vp]
+    L.lar_route.restype = i32
+    L.lar_route.argtypes = [vp, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp]
+    L.lar_commit.restype = i32
+    L.lar_commit.argtypes = [vp, vp, i32, i32, dbl]
+    L.lar_route_trace.restype = i32
+    L.lar_route_trace.argtypes = [vp, i32, vp, vp, vp, dbl, vp, vp, i32, vp, vp, vp, vp, vp]
+    L.lar_stats.restype = i32
+    L.lar_stats.argtypes = [vp, i32, vp, vp, vp, vp, i32, vp, vp]
+    L.lar_read_state.restype = i32
+    L.lar_read_state.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, i64, C.POINTER(i64)]
+    L.lar_sync.restype = i32
+    L.lar_sync.argtypes = [vp]
+    _lib = L
+    return L
+
+
+def _dev(t, dtype, name, numel=None):
+    """Device pointer of a contiguous GPU tensor of the given torch dtype (None -> NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} < {numel} elements")
+    return t.data_ptr()
+
+
+def _host(a, dtype):
+    return np.ascontiguousarray(np.asarray(a, dtype=dtype))
+
+
+class LarContext:
+    """One estimator/router context: Z scenarios x I instances of device state."""
+
+    def __init__(self, n_scen: int, n_inst: int, *, max_seqs_cap: int, queue_cap: int,
+                 max_prompt: int, flags: int = FIRST_TOKEN_DECODE_BATCH,
+                 max_iters: int = 10_000_000, stream=None):
+        import torch
+        self._torch = torch
+        self._L = load_library()
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self.stream = stream
+        cfg = Config(int(n_scen), int(n_inst), int(max_seqs_cap), int(queue_cap),
+                     int(max_prompt), int(flags), int(max_iters), C.c_void_p(stream.cuda_stream))
+        h = C.c_void_p()
+        st = self._L.lar_create(C.byref(h), C.byref(cfg))
+        if st != LAR_OK:
+            raise LarError(st, "lar_create failed")
+        self._h = h
+        self.Z, self.I = int(n_scen), int(n_inst)
+        self.n_cols = None
+
+    # ------------------------------------------------------------------ plumbing
+    def _check(self, st: int):
+        if st != LAR_OK:
+            msg = self._L.lar_error_string(self._h)
+            raise LarError(st, msg.decode() if msg else "")
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._L.lar_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    # ------------------------------------------------------------------ calls
+    def load_state(self, *, a, b, c, d, e, budget, max_seqs, col, offsets, rem_prefill,
+                   rem_decode, context, clock_ms):
+        I = self.I
+        params = (InstanceParams * I)()
+        for j in range(I):
+            params[j] = InstanceParams(float(a[j]), float(b[j]), float(c[j]), float(d[j]),
+                                       float(e[j]), int(budget[j]), int(max_seqs[j]),
+                                       int(col[j]), 0)
+        off = _host(offsets, np.int32)
+        rp, rd, cx = _host(rem_prefill, np.int32), _host(rem_decode, np.int32), _host(context, np.int32)
+        clk = _host(clock_ms, np.float64)
+        if off.shape[0] != I + 1 or clk.shape[0] != I:
+            raise ValueError("offsets must have I+1 entries and clock_ms I entries")
+        n = int(off[-1])
+        if min(rp.shape[0], rd.shape[0], cx.shape[0]) < n:
+            raise ValueError("request arrays shorter than offsets[I]")
+        self._check(self._L.lar_load_state(self._h, params, off.ctypes.data, rp.ctypes.data,
+                                           rd.ctypes.data, cx.ctypes.data, clk.ctypes.data))
+
+    def reload_state(self):
+        self._check(self._L.lar_reload_state(self._h))
+
+    def load_workload(self, wl):
+        self.load_state(a=wl.a, b=wl.b, c=wl.c, d=wl.d, e=wl.e, budget=wl.budget,
+                        max_seqs=wl.max_seqs, col=wl.col, offsets=wl.offsets,
+                        rem_prefill=wl.rem_prefill, rem_decode=wl.rem_decode,
+                        context=wl.context, clock_ms=wl.clock_ms)
+
+    def estimate(self, q_prefill, t_ms: float, ttft=None, iters=None, want_iters=True):
+        torch = self._torch
+        Q = int(q_prefill.numel())
+        dev = q_prefill.device
+        if ttft is None:
+            ttft = torch.empty((self.Z, Q, self.I), dtype=torch.float64, device=dev)
+        if iters is None and want_iters:
+            iters = torch.empty((self.Z, Q, self.I), dtype=torch.int32, device=dev)
+        n = self.Z * Q * self.I
+        self._check(self._L.lar_estimate_ttft(
+            self._h, Q, _dev(q_prefill, torch.int32, "q_prefill"), float(t_ms),
+            _dev(ttft, torch.float64, "ttft", n), _dev(iters, torch.int32, "iters", n)))
+        return ttft, iters
+
+    def route(self, ttft, acc, cost, w_cost, w_lat, choice=None, chosen_ttft=None,
+              utility=None):
+        torch = self._torch
+        Q = int(acc.shape[0])
+        n_cols = int(acc.shape[1])
+        dev = acc.device
+        if choice is None:
+            choice = torch.empty((self.Z, Q), dtype=torch.int32, device=dev)
+        self._check(self._L.lar_route(
+            self._h, Q, _dev(ttft, torch.float64, "ttft", self.Z * Q * self.I),
+            _dev(acc, torch.float64, "acc", Q * n_cols), _dev(cost, torch.float64, "cost", Q * n_cols),
+            n_cols, _dev(w_cost, torch.float64, "w_cost", self.Z),
+            _dev(w_lat, torch.float64, "w_lat", self.Z), _dev(choice, torch.int32, "choice", self.Z * Q),
+            _dev(chosen_ttft, torch.float64, "chosen_ttft", self.Z * Q),
+            _dev(utility, torch.float64, "utility", self.Z * Q)))
+        return choice
+
+    def commit(self, choice, q_prefill: int, q_decode: int, t_next_ms: float):
+        torch = self._torch
+        self._check(self._L.lar_commit(self._h, _dev(choice, torch.int32, "choice", self.Z),
+                                       int(q_prefill), int(q_decode), float(t_next_ms)))
+
+    def advance(self, t_ms: float):
+        self.commit(None, 1, 1, t_ms)
+
+    def route_trace(self, q_prefill, q_decode, q_t_ms, t_after_ms, acc, cost, w_cost, w_lat,
+                    choice=None, chosen_ttft=None, utility=None):
+        torch = self._torch
+        N = int(q_prefill.numel())
+        n_cols = int(acc.shape[1])
+        dev = q_prefill.device
+        if choice is None:
+            choice = torch.empty((self.Z, N), dtype=torch.int32, device=dev)
+        self._check(self._L.lar_route_trace(
+            self._h, N, _dev(q_prefill, torch.int32, "q_prefill"),
+            _dev(q_decode, torch.int32, "q_decode", N), _dev(q_t_ms, torch.float64, "q_t_ms", N),
+            float(t_after_ms), _dev(acc, torch.float64, "acc", N * n_cols),
+            _dev(cost, torch.float64, "cost", N * n_cols), n_cols,
+            _dev(w_cost, torch.float64, "w_cost", self.Z), _dev(w_lat, torch.float64, "w_lat", self.Z),
+            _dev(choice, torch.int32, "choice", self.Z * N),
+            _dev(chosen_ttft, torch.float64, "chosen_ttft", self.Z * N),
+            _dev(utility, torch.float64, "utility", self.Z * N)))
+        return choice
+
+    def stats(self, choice, chosen_ttft, acc, cost, w_cost, out=None):
+        torch = self._torch
+        N = int(choice.shape[-1])
+        n_cols = int(acc.shape[1])
+        if out is None:
+            out = torch.empty((self.Z, 5), dtype=torch.float64, device=choice.device)
+        self._check(self._L.lar_stats(
+            self._h, N, _dev(choice, torch.int32, "choice", self.Z * N),
+            _dev(chosen_ttft, torch.float64, "chosen_ttft", self.Z * N),
+            _dev(acc, torch.float64, "acc", N * n_cols), _dev(cost, torch.float64, "cost", N * n_cols),
+            n_cols, _dev(w_cost, torch.float64, "w_cost", self.Z),
+            _dev(out, torch.float64, "stats", self.Z * 5)))
+        return out
+
+    def sync(self):
+        self._check(self._L.lar_sync(self._h))
+
+    def status(self) -> int:
+        """Synchronise and return the sticky status code without raising."""
+        return int(self._L.lar_sync(self._h))
+
+    def read_state(self, scen: int = 0, cap: int | None = None):
+        I = self.I
+        off = np.zeros(I + 1, np.int32)
+        clk = np.zeros(I)
+        its = np.zeros(I, np.int64)
+        n_total = C.c_int64(0)
+        cap = 0 if cap is None else int(cap)
+        rp = np.zeros(max(cap, 1), np.int32)
+        rd = np.zeros(max(cap, 1), np.int32)
+        cx = np.zeros(max(cap, 1), np.int32)
+        st = self._L.lar_read_state(self._h, int(scen), off.ctypes.data, rp.ctypes.data,
+                                    rd.ctypes.data, cx.ctypes.data, clk.ctypes.data,
+                                    its.ctypes.data, cap, C.byref(n_total))
+        if st == LAR_E_CAPACITY and n_total.value > cap:
+            return self.read_state(scen, int(n_total.value))
+        self._check(st)
+        n = int(n_total.value)
+        return dict(offsets=off, rem_prefill=rp[:n], rem_decode=rd[:n], context=cx[:n],
+                    clock_ms=clk, iterations=its)
+
+
+def context_for(wl, *, flags=FIRST_TOKEN_DECODE_BATCH, max_iters=10_000_000, stream=None,
+                queue_cap=None) -> LarContext:
+    """A context sized for workload ``wl`` with its snapshot loaded."""
+    ctx = LarContext(wl.n_scen, wl.n_inst, max_seqs_cap=int(np.max(wl.max_seqs)),
+                     queue_cap=int(wl.queue_cap if queue_cap is None else queue_cap),
+                     max_prompt=int(wl.max_prompt), flags=flags, max_iters=max_iters,
+                     stream=stream)
+    ctx.load_workload(wl)
+    return ctx

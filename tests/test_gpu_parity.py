@@ -1,0 +1,344 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Integer results (iteration counts, choices, final states) must match exactly;
+fp64 TTFT must match within 1e-9 relative error -- the kernels evaluate every
+batch time in the same operation order with the same roundings as the oracle, so
+the tests demand bit equality, which implies that bound.
+"""
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from gpu_util import DEV, T, assert_state_equal, bits, gpu_trace  # noqa: E402
+from oracle import oracle as O  # noqa: E402
+from paper_2607_18253_amd import LarContext, LarError, context_for  # noqa: E402
+from paper_2607_18253_amd import lar as L  # noqa: E402
+from workloads import make_tiny_workload, make_workload  # noqa: E402
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden", "hand_worked.json")
+REL_TOL = 1e-9
+
+
+def _close(a, b):
+    a, b = np.asarray(a), np.asarray(b)
+    return np.all(np.abs(a - b) <= REL_TOL * np.maximum(np.abs(a), np.abs(b)))
+
+
+def _single(coef, B, M, reqs, clock=0.0, flags=0, max_prompt=64, mcap=None, qcap=64):
+    ctx = LarContext(1, 1, max_seqs_cap=mcap or M, queue_cap=qcap, max_prompt=max_prompt,
+                     flags=flags)
+    ctx.load_state(a=[coef["a"]], b=[coef["b"]], c=[coef["c"]], d=[coef["d"]], e=[coef["e"]],
+                   budget=[B], max_seqs=[M], col=[0], offsets=[0, len(reqs)],
+                   rem_prefill=[r[0] for r in reqs], rem_decode=[r[1] for r in reqs],
+                   context=[r[2] for r in reqs], clock_ms=[clock])
+    return ctx
+
+
+# ------------------------------------------------------------------ hand-worked
+@pytest.mark.parametrize("flags", [0, 1])
+def test_hand_worked_gpu(flags):
+    g = json.load(open(GOLD))
+    for case in g["estimates"]:
+        ctx = _single(g["coef"], case["budget"], case["max_seqs"], case["requests"],
+                      case["clock"], flags=flags)
+        if "advance_to" in case:
+            ctx.advance(case["advance_to"])
+        tt, it = ctx.estimate(T([case["p"]], torch.int32), case["t"])
+        ctx.sync()
+        key = "B" if flags == 0 else "A"
+        assert tt.item() == case["ttft_" + key], case["name"]
+        assert it.item() == case["iters_" + key], case["name"]
+        ctx.close()
+
+
+def test_hand_worked_routes_gpu():
+    g = json.load(open(GOLD))
+    for case in g["routes"]:
+        n = len(case["ttft"])
+        ctx = LarContext(1, n, max_seqs_cap=1, queue_cap=4, max_prompt=4)
+        ctx.load_state(a=[1] * n, b=[1] * n, c=[1] * n, d=[0] * n, e=[0] * n, budget=[1] * n,
+                       max_seqs=[1] * n, col=list(range(n)), offsets=[0] * (n + 1),
+                       rem_prefill=[], rem_decode=[], context=[], clock_ms=[0.0] * n)
+        util = torch.empty((1, 1), dtype=torch.float64, device=DEV)
+        ch = ctx.route(T([[case["ttft"]]], torch.float64), T([case["acc"]], torch.float64),
+                       T([case["cost"]], torch.float64), T([case["w_cost"]], torch.float64),
+                       T([case["w_lat"]], torch.float64), utility=util)
+        ctx.sync()
+        assert ch.item() == case["choice"], case["name"]
+        ctx.close()
+
+
+# ------------------------------------------------------------------ what-if estimates
+@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("flags", [0, 1])
+def test_estimate_tiny_pools(seed, flags):
+    wl = make_tiny_workload(seed, n_inst=7, max_res=6, n_q=9, budget=(1, 9), max_seqs=(1, 5),
+                            prompt=(1, 14), dyadic=(seed % 3 == 0))
+    ref, ref_it = O.estimate_matrix(wl, range(wl.n_q), range(wl.n_inst), 0.0, reading=flags)
+    ctx = context_for(wl, flags=flags)
+    tt, it = ctx.estimate(T(wl.q_prefill, torch.int32), 0.0)
+    ctx.sync()
+    np.testing.assert_array_equal(it.cpu().numpy()[0], ref_it)
+    np.testing.assert_array_equal(bits(tt.cpu().numpy()[0]), bits(ref))
+    ctx.close()
+
+
+def test_estimate_many_slots_and_ragged():
+    """Wide running sets (several 64-slot passes per lane group), a ragged instance
+    count, empty instances, long prompts crossing many budget windows."""
+    rng = np.random.default_rng(11)
+    I = 67
+    M_all = rng.choice([1, 3, 64, 65, 130, 300, 700], size=I)
+    B_all = M_all + rng.integers(0, 2000, size=I)
+    reqs, offs = [], [0]
+    for j in range(I):
+        n = int(rng.integers(0, 900)) if j % 5 else 0
+        n_run = int(min(n, M_all[j], rng.integers(0, n + 1)))
+        rp = np.where(np.arange(n) < n_run, np.where(rng.random(n) < 0.85, 0,
+                      rng.integers(1, 300, n)), rng.integers(1, 3000, n))
+        cx = np.where(np.arange(n) < n_run, rng.integers(1, 5000, n), 0)
+        rd = rng.integers(1, 400, n)
+        reqs.append((rp, rd, cx))
+        offs.append(offs[-1] + n)
+    coef = rng.random((5, I))
+    coef[3] *= 1e-3
+    coef[4] *= 1e-6
+    ctx = LarContext(1, I, max_seqs_cap=int(M_all.max()), queue_cap=1024, max_prompt=20000)
+    ctx.load_state(a=coef[0], b=coef[1], c=coef[2], d=coef[3], e=coef[4], budget=B_all,
+                   max_seqs=M_all, col=np.zeros(I, np.int32), offsets=offs,
+                   rem_prefill=np.concatenate([r[0] for r in reqs]),
+                   rem_decode=np.concatenate([r[1] for r in reqs]),
+                   context=np.concatenate([r[2] for r in reqs]), clock_ms=np.zeros(I))
+    ps = np.array([1, 2, 63, 64, 65, 1000, 4096, 19999], np.int32)
+    tt, it = ctx.estimate(T(ps, torch.int32), 0.0)
+    ctx.sync()
+    tt, it = tt.cpu().numpy()[0], it.cpu().numpy()[0]
+    for j in range(I):
+        q = O.Queue(O.make_params(*coef[:, j], B_all[j], M_all[j]), *reqs[j], 0.0)
+        for a, p in enumerate(ps):
+            want, wit = q.estimate(int(p), 1, 0.0)
+            assert it[a, j] == wit and bits(tt[a, j]) == bits(want), (j, p)
+    ctx.close()
+
+
+def test_estimate_c3_full_matrix_sampled():
+    """Config 3 at full size: 1024 instances x 512 residents, 4096 queries in one
+    call.  Every iteration count and TTFT bit is checked on two whole rows and a
+    random sample of pairs; the row argmax is checked on every row."""
+    wl = make_workload("c3")
+    ctx = context_for(wl)
+    qp = T(wl.q_prefill, torch.int32)
+    tt, it = ctx.estimate(qp, 0.0)
+    acc, cost = T(wl.acc, torch.float64), T(wl.cost, torch.float64)
+    util = torch.empty((1, wl.n_q), dtype=torch.float64, device=DEV)
+    chosen = torch.empty((1, wl.n_q), dtype=torch.float64, device=DEV)
+    ch = ctx.route(tt, acc, cost, T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64),
+                   chosen_ttft=chosen, utility=util)
+    ctx.sync()
+    tt, it, ch = tt.cpu().numpy()[0], it.cpu().numpy()[0], ch.cpu().numpy()[0]
+    rng = np.random.default_rng(0)
+    rows = [0, int(np.argmax(wl.q_prefill))]
+    ref, ref_it = O.estimate_matrix(wl, rows, range(wl.n_inst), 0.0)
+    np.testing.assert_array_equal(it[rows], ref_it)
+    np.testing.assert_array_equal(bits(tt[rows]), bits(ref))
+    for r, i in enumerate(rows):
+        m, _ = O.route_row(ref[r], wl.acc[i], wl.cost[i], wl.col, wl.w_cost[0], wl.w_lat_ms[0])
+        assert ch[i] == m
+    qs = rng.integers(0, wl.n_q, 300)
+    js = rng.integers(0, wl.n_inst, 300)
+    for q, j in zip(qs, js):
+        want, wit = O.instance_queue(wl, int(j)).estimate(int(wl.q_prefill[q]), 1, 0.0)
+        assert it[q, j] == wit and bits(tt[q, j]) == bits(want), (q, j)
+    # every row: choice is the oracle's route of the GPU's (oracle-identical) TTFT row
+    for i in range(wl.n_q):
+        m, _ = O.route_row(tt[i], wl.acc[i], wl.cost[i], wl.col, wl.w_cost[0], wl.w_lat_ms[0])
+        assert ch[i] == m, i
+    assert np.array_equal(bits(chosen.cpu().numpy()[0]), bits(tt[np.arange(wl.n_q), ch]))
+    ctx.close()
+
+
+# ------------------------------------------------------------------ sequential traces
+@pytest.mark.parametrize("seed", range(16))
+@pytest.mark.parametrize("flags", [0, 1])
+def test_trace_tiny_pools(seed, flags):
+    wl = make_tiny_workload(seed, n_inst=5, max_res=6, n_q=40, dyadic=(seed % 2 == 0),
+                            n_scen=3)
+    choice, chosen, util, ctx = gpu_trace(wl, flags=flags, queue_cap=10 ** 4)
+    for z in range(wl.n_scen):
+        ref = O.trace(wl, scenario=z, reading=flags, queue_cap=10 ** 4)
+        np.testing.assert_array_equal(choice[z], ref.choice)
+        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen))
+        np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
+        assert_state_equal(ctx, z, ref)
+    ctx.close()
+
+
+def test_trace_c1_full():
+    wl = make_workload("c1")
+    choice, chosen, util, ctx = gpu_trace(wl)
+    ref = O.trace(wl)
+    np.testing.assert_array_equal(choice[0], ref.choice)
+    np.testing.assert_array_equal(bits(chosen[0]), bits(ref.ttft_chosen))
+    np.testing.assert_array_equal(bits(util[0]), bits(ref.util_chosen))
+    assert_state_equal(ctx, 0, ref)
+    ctx.close()
+
+
+def test_trace_c2_prefix():
+    wl = make_workload("c2", n_q=2000)
+    choice, chosen, util, ctx = gpu_trace(wl)
+    ref = O.trace(wl)
+    np.testing.assert_array_equal(choice[0], ref.choice)
+    np.testing.assert_array_equal(bits(chosen[0]), bits(ref.ttft_chosen))
+    assert_state_equal(ctx, 0, ref)
+    ctx.close()
+
+
+def test_trace_c4_prefix():
+    wl = make_workload("c4", n_q=4)
+    choice, chosen, util, ctx = gpu_trace(wl)
+    ref = O.trace(wl)
+    np.testing.assert_array_equal(choice[0], ref.choice)
+    np.testing.assert_array_equal(bits(chosen[0]), bits(ref.ttft_chosen))
+    assert_state_equal(ctx, 0, ref)
+    ctx.close()
+
+
+def test_trace_c5_all_scenarios_prefix_and_stats():
+    wl = make_workload("c5", n_q=24)
+    choice, chosen, util, ctx = gpu_trace(wl)
+    acc, cost = T(wl.acc, torch.float64), T(wl.cost, torch.float64)
+    st = ctx.stats(T(choice, torch.int32), T(chosen, torch.float64), acc, cost,
+                   T(wl.w_cost, torch.float64))
+    ctx.sync()
+    st = st.cpu().numpy()
+    for z in range(wl.n_scen):
+        ref = O.trace(wl, scenario=z)
+        np.testing.assert_array_equal(choice[z], ref.choice, err_msg=f"scenario {z}")
+        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen))
+        if z in (0, 27, 63):
+            assert_state_equal(ctx, z, ref)
+        want = O.stats(ref.choice, ref.ttft_chosen, wl.acc, wl.cost, wl.col, wl.w_cost[z])
+        np.testing.assert_array_equal(bits(st[z]), bits(want), err_msg=f"stats {z}")
+    ctx.close()
+
+
+def test_checkpoint_resume_identical():
+    """read_state -> load_state into a fresh context, continue: same results."""
+    wl = make_workload("c2", n_q=600, n_inst=8)
+    full_c, full_t, _, ctx = gpu_trace(wl)
+    ctx.close()
+    N1 = 250
+    from paper_2607_18253_amd import context_for as cf
+    ctx1 = cf(wl)
+    ctx1.advance(float(wl.q_t_ms[0]))
+    c1 = ctx1.route_trace(T(wl.q_prefill[:N1], torch.int32), T(wl.q_decode[:N1], torch.int32),
+                          T(wl.q_t_ms[:N1], torch.float64), float(wl.q_t_ms[N1]),
+                          T(wl.acc[:N1], torch.float64), T(wl.cost[:N1], torch.float64),
+                          T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64))
+    ctx1.sync()
+    st = ctx1.read_state(0)
+    ctx2 = LarContext(1, wl.n_inst, max_seqs_cap=int(wl.max_seqs.max()), queue_cap=wl.queue_cap,
+                      max_prompt=wl.max_prompt)
+    ctx2.load_state(a=wl.a, b=wl.b, c=wl.c, d=wl.d, e=wl.e, budget=wl.budget,
+                    max_seqs=wl.max_seqs, col=wl.col, offsets=st["offsets"],
+                    rem_prefill=st["rem_prefill"], rem_decode=st["rem_decode"],
+                    context=st["context"], clock_ms=st["clock_ms"])
+    c2 = ctx2.route_trace(T(wl.q_prefill[N1:], torch.int32), T(wl.q_decode[N1:], torch.int32),
+                          T(wl.q_t_ms[N1:], torch.float64), float(wl.q_t_ms[-1]),
+                          T(wl.acc[N1:], torch.float64), T(wl.cost[N1:], torch.float64),
+                          T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64))
+    ctx2.sync()
+    got = np.concatenate([c1.cpu().numpy()[0], c2.cpu().numpy()[0]])
+    np.testing.assert_array_equal(got, full_c[0])
+    ctx1.close()
+    ctx2.close()
+
+
+# ------------------------------------------------------------------ edge cases / errors
+def test_empty_pool_and_single_slot():
+    """All instances empty; M = 1; prompts equal to, below and above the budget."""
+    coef = dict(a=1.0, b=0.5, c=0.25, d=0.125, e=0.0625)
+    ctx = _single(coef, 1, 1, [], max_prompt=50)
+    tt, it = ctx.estimate(T([1, 2, 50], torch.int32), 0.0)
+    ctx.sync()
+    q = O.Queue(O.make_params(1, .5, .25, .125, .0625, 1, 1), [], [], [])
+    for a, p in enumerate([1, 2, 50]):
+        want, wit = q.estimate(p, 1, 0.0)
+        assert tt.cpu().numpy()[0, a, 0] == want and it.cpu().numpy()[0, a, 0] == wit
+    ctx.close()
+
+
+def test_sticky_errors():
+    coef = dict(a=1.0, b=0.5, c=0.25, d=0.0, e=0.0)
+    # prompt above max_prompt -> LAR_E_ARG from the kernel, sticky until reload
+    ctx = _single(coef, 8, 2, [[0, 3, 4]], max_prompt=10)
+    ctx.estimate(T([11], torch.int32), 0.0)
+    assert ctx.status() == L.LAR_E_ARG
+    with pytest.raises(LarError):
+        ctx.estimate(T([3], torch.int32), 0.0)
+    ctx.load_state(a=[1.0], b=[0.5], c=[0.25], d=[0.0], e=[0.0], budget=[8], max_seqs=[2],
+                   col=[0], offsets=[0, 0], rem_prefill=[], rem_decode=[], context=[],
+                   clock_ms=[0.0])
+    ctx.estimate(T([3], torch.int32), 0.0)
+    assert ctx.status() == L.LAR_OK
+    # estimate at a time the instance has not reached -> LAR_E_STATE
+    ctx.estimate(T([3], torch.int32), 5.0)
+    assert ctx.status() == L.LAR_E_STATE
+    ctx.close()
+    # waiting queue overflow on commit -> LAR_E_CAPACITY
+    ctx = _single(coef, 8, 1, [[0, 50, 4], [5, 1, 0]], qcap=2)
+    ch = T([0], torch.int32)
+    ctx.commit(ch, 4, 1, 0.0)
+    assert ctx.status() == L.LAR_OK
+    ctx.commit(ch, 4, 1, 0.0)
+    assert ctx.status() == L.LAR_E_CAPACITY
+    ctx.close()
+    # iteration cap -> LAR_E_ITER, for estimates and for the replay
+    ctx = LarContext(1, 1, max_seqs_cap=1, queue_cap=4, max_prompt=100, max_iters=5)
+    ctx.load_state(a=[1.0], b=[1.0], c=[1.0], d=[0.0], e=[0.0], budget=[1], max_seqs=[1],
+                   col=[0], offsets=[0, 1], rem_prefill=[0], rem_decode=[20], context=[3],
+                   clock_ms=[0.0])
+    ctx.estimate(T([1], torch.int32), 0.0)
+    assert ctx.status() == L.LAR_E_ITER
+    ctx.close()
+    ctx = LarContext(1, 1, max_seqs_cap=1, queue_cap=4, max_prompt=100, max_iters=5)
+    ctx.load_state(a=[1.0], b=[1.0], c=[1.0], d=[0.0], e=[0.0], budget=[1], max_seqs=[1],
+                   col=[0], offsets=[0, 1], rem_prefill=[0], rem_decode=[20], context=[3],
+                   clock_ms=[0.0])
+    ctx.advance(1000.0)
+    assert ctx.status() == L.LAR_E_ITER
+    ctx.close()
+
+
+def test_host_argument_errors():
+    with pytest.raises(LarError):
+        LarContext(0, 1, max_seqs_cap=1, queue_cap=1, max_prompt=1)
+    ctx = LarContext(1, 2, max_seqs_cap=4, queue_cap=4, max_prompt=8)
+    good = dict(a=[1, 1], b=[1, 1], c=[1, 1], d=[0, 0], e=[0, 0], budget=[8, 8], max_seqs=[4, 4],
+                col=[0, 1], offsets=[0, 1, 2], rem_prefill=[0, 3], rem_decode=[1, 1],
+                context=[2, 0], clock_ms=[0.0, 0.0])
+    ctx.load_state(**good)
+    for k, v, code in [("max_seqs", [5, 4], L.LAR_E_ARG), ("budget", [3, 8], L.LAR_E_ARG),
+                       ("rem_decode", [0, 1], L.LAR_E_STATE),
+                       ("context", [0, 0], L.LAR_E_STATE), ("a", [np.nan, 1], L.LAR_E_ARG)]:
+        bad = dict(good)
+        bad[k] = v
+        with pytest.raises(LarError) as e:
+            ctx.load_state(**bad)
+        assert e.value.code == code, k
+    ctx.load_state(**good)
+    with pytest.raises(LarError):   # n_cols does not cover col 1
+        ctx.route(T(np.zeros((1, 1, 2)), torch.float64), T(np.zeros((1, 1)), torch.float64),
+                  T(np.zeros((1, 1)), torch.float64), T([0.0], torch.float64),
+                  T([0.0], torch.float64))
+    ctx.close()
