@@ -2,15 +2,23 @@
 """Benchmark of the SFS TTFT estimator + latency-aware router on one MI355X.
 
 A step is one pass of the whole hot path over one synthetic workload, all inputs
-resident in HBM before the timed region:
-  re-install the instance snapshot (device-to-device), replay the instances to the
-  first arrival, then route every query of the trace in order -- SFS estimate at
-  every instance, Lagrangian utility + argmax, commit + replay to the next arrival
-  -- and finally the per-scenario summary (mean accuracy / cost / utility, p50 and
-  p99 TTFT).
+resident in HBM before the timed region.  For the sequential-routing workloads
+(default: the 32-instance medium pool, 100k queries):
+  re-install the instance snapshot (device to device), replay the instances to the
+  first arrival, route every query of the trace in order -- SFS estimate at every
+  instance, Lagrangian utility + argmax, commit + replay to the next arrival -- in
+  one persistent kernel, then the per-scenario summary (mean accuracy / cost /
+  utility, p50 and p99 TTFT).
+For the batched what-if workload (c3): one estimate call for 4096 queries x 1024
+instances followed by the row argmax.
 
 Prints ONE JSON line.  ``value`` = TTFT estimates per second (scenarios x queries x
 instances per step / step time); routed queries per second are reported next to it.
+``roofline`` covers the dominant kernel, timed with HIP events on the context's
+stream; its algorithmic work is counted in simulated token batches (each one is a
+batch time -- 4 multiplies, 4 adds -- plus one add folding it into the clock or the
+TTFT sum: 9 fp64 operations), the batch counts coming from the oracle's replay of
+the same trace.
 """
 
 from __future__ import annotations
@@ -26,10 +34,9 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "TTFT estimates/sec (query x instance) and routed queries/sec on 1 MI355X"
-# fp64 operations of one simulated batch: the batch time (4 multiplies, 4 adds)
-# plus the fold into the clock / TTFT sum (1 add).
-FLOPS_PER_BATCH = 9
-PEAK = {"fp64_vector_tflops": 78.6, "hbm_gbs": 8000.0}
+FLOPS_PER_BATCH = 9                 # 4 mul + 4 add (batch time) + 1 add (fold)
+FP64_VECTOR_PEAK_TFLOPS = 78.6      # MI355X dense fp64 vector
+HBM_PEAK_GBS = 8000.0
 
 
 def _parse():
@@ -37,39 +44,66 @@ def _parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c4", "c5"])
+    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--n-q", type=int, default=None, help="shorten the trace (testing only)")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0,
-                    help="budget of the CPU-oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="time budget of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     return ap.parse_args()
 
 
-def cpu_baseline(wl, budget_s):
-    """The plain C oracle, single-threaded, on a prefix of the same trace."""
+def oracle_sample(wl, budget_s):
+    """The plain C oracle, single-threaded, on a prefix of the same trace (scenario 0).
+
+    Returns the CPU baseline record and the oracle's count of simulated batches over
+    that prefix (estimate batches + replayed batches), used for the roofline when the
+    prefix is the whole trace."""
     from oracle import oracle as orc
-    n = 16
+    n = min(wl.n_q, 256)
     while True:
         t0 = time.perf_counter()
-        orc.trace(wl, scenario=0, n_q=n, final_state=False)
+        r = orc.trace(wl, scenario=0, n_q=n, full_rows=True, final_state=True)
         dt = time.perf_counter() - t0
-        if dt >= budget_s / 4 or n >= wl.n_q:
+        if n >= wl.n_q or dt >= budget_s / 3:
             break
-        n = min(wl.n_q, int(n * max(2.0, budget_s / 4 / max(dt, 1e-3))))
+        n = min(wl.n_q, int(n * max(2.0, budget_s / 3 / max(dt, 1e-3))))
     est = n * wl.n_inst
-    return {"value": est / dt, "unit": "TTFT estimates/s", "cores": 1, "kind": "oracle",
-            "sample": f"scenario 0, first {n} queries of the trace ({est} estimates, "
-                      f"{dt:.2f} s single-threaded)",
-            "routed_queries_per_s": n / dt}
+    batches = int(r.iters_all.astype(np.int64).sum() + r.iterations.sum())
+    rec = {"value": est / dt, "unit": "TTFT estimates/s", "cores": 1, "kind": "oracle",
+           "sample": f"scenario 0, first {n} of {wl.n_q} queries ({est} estimates + the "
+                     f"replay; {dt:.2f} s single-threaded)",
+           "routed_queries_per_s": n / dt}
+    return rec, n, batches
+
+
+def whatif_oracle_sample(wl, budget_s):
+    from oracle import oracle as orc
+    rng = np.random.default_rng(1)
+    n, t_used, batches = 0, 0.0, 0
+    qs = {}
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < budget_s:
+        i, j = int(rng.integers(wl.n_q)), int(rng.integers(wl.n_inst))
+        if j not in qs:
+            qs[j] = orc.instance_queue(wl, j)
+        _, it = qs[j].estimate(int(wl.q_prefill[i]), 1, 0.0)
+        batches += it
+        n += 1
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "TTFT estimates/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} random (query, instance) pairs, literal per-pair SFS "
+                      f"({dt:.1f} s single-threaded)"}, batches / max(n, 1)
+
+
+import numpy as np  # noqa: E402
 
 
 def main():
     args = _parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(the sharded design is described, not built)", file=sys.stderr)
+              "(the multi-GPU sharding is a design, not a built path)", file=sys.stderr)
         sys.exit(2)
-    import numpy as np
     import torch
 
     from paper_2607_18253_amd import context_for
@@ -92,33 +126,50 @@ def main():
     stats = torch.empty((Z, 5), dtype=torch.float64, device=dev)
     ctx = context_for(wl)
     stream = ctx.stream
+    whatif = args.workload == "c3"
     t_first, t_last = float(wl.q_t_ms[0]), float(wl.q_t_ms[-1])
+    if whatif:
+        ttft = torch.empty((Z, N, I), dtype=torch.float64, device=dev)
+    kev = []   # (start, end) events around the dominant kernel of each timed step
 
-    def step():
+    def step(record=False):
+        if whatif:
+            if record:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            ctx.estimate(qp, 0.0, ttft=ttft, want_iters=False)
+            if record:
+                e1.record(stream)
+                kev.append((e0, e1))
+            ctx.route(ttft, acc, cost, wc, wlat, choice=choice, chosen_ttft=chosen, utility=util)
+            return
         ctx.reload_state()
         ctx.advance(t_first)
+        if record:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
         ctx.route_trace(qp, qd, qt, t_last, acc, cost, wc, wlat, choice=choice,
                         chosen_ttft=chosen, utility=util)
+        if record:
+            e1.record(stream)
+            kev.append((e0, e1))
         ctx.stats(choice, chosen, acc, cost, wc, out=stats)
 
     for _ in range(args.warmup):
         step()
     ctx.sync()
     torch.cuda.synchronize()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
-    ev0.record(stream)
     for _ in range(args.steps):
-        step()
-    ev1.record(stream)
+        step(record=True)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ctx.sync()
-    gpu_ms = ev0.elapsed_time(ev1)
     ms_per_step = wall * 1000.0 / args.steps
-    est_per_step = Z * N * I
-    value = est_per_step / (ms_per_step / 1000.0)
+    kernel_ms = sum(a.elapsed_time(b) for a, b in kev) / len(kev)
+    value = Z * N * I / (ms_per_step / 1000.0)
 
     line = {
         "metric": METRIC, "value": value, "unit": "TTFT estimates/s", "n_gpus": 1,
@@ -130,11 +181,40 @@ def main():
                    "token_budget": int(wl.budget[0]), "max_seqs": int(wl.max_seqs[0]),
                    "parallelism": "1 GPU"},
         "routed_queries_per_s": Z * N / (ms_per_step / 1000.0),
-        "gpu_event_ms_per_step": gpu_ms / args.steps,
-        "stats_scenario0": stats[0].tolist(),
     }
+    if whatif:
+        line["roofline_kernel"] = "k_traj + k_est (lar_estimate_ttft)"
+    else:
+        line["roofline_kernel"] = "k_trace (lar_route_trace, one launch per step)"
+        line["stats_scenario0"] = stats[0].tolist()
+    line["kernel_ms"] = kernel_ms
+
+    roof = None
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        if whatif:
+            rec, batches_per_pair = whatif_oracle_sample(wl, args.cpu_seconds)
+            line["cpu_baseline"] = rec
+            # HBM-bound output: the fp64 TTFT matrix written once, plus per-query and
+            # per-instance inputs (negligible); algorithmic bytes per estimate = 8
+            achieved = Z * N * I * 8 / (kernel_ms / 1000.0) / 1e9
+            roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                    "note": "algorithmic bytes = 8 B of TTFT output per (query, instance); "
+                            f"a literal per-pair SFS would simulate {batches_per_pair:.0f} "
+                            "batches per pair"}
+        else:
+            rec, n, batches = oracle_sample(wl, args.cpu_seconds)
+            line["cpu_baseline"] = rec
+            if n == N:
+                flops = FLOPS_PER_BATCH * batches * Z
+                achieved = flops / (kernel_ms / 1000.0) / 1e12
+                roof = {"bound": "alu", "achieved": achieved, "peak": FP64_VECTOR_PEAK_TFLOPS,
+                        "unit": "TFLOP/s", "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
+                        "traffic": None,
+                        "note": f"{batches} simulated batches per scenario (oracle count: "
+                                "every estimate's batches + the replay) x 9 fp64 ops; "
+                                "sequential trace, latency-bound"}
+    line["roofline"] = roof
     print(json.dumps(line), flush=True)
     ctx.close()
 

@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -133,16 +134,22 @@ lar_status lar_create(lar_ctx** out, const lar_config* cfg) {
   const size_t ZI = (size_t)ctx->Z * ctx->I;
   lar_status st = LAR_OK;
   auto chk = [&](lar_status s) { if (st == LAR_OK) st = s; };
-  chk(dev_alloc(ctx, &ctx->S.run_rp, ZI * ctx->mcap));
-  chk(dev_alloc(ctx, &ctx->S.run_rd, ZI * ctx->mcap));
-  chk(dev_alloc(ctx, &ctx->S.run_cx, ZI * ctx->mcap));
-  chk(dev_alloc(ctx, &ctx->S.wait_p, ZI * ctx->qcap));
-  chk(dev_alloc(ctx, &ctx->S.wait_rd, ZI * ctx->qcap));
-  chk(dev_alloc(ctx, &ctx->S.n_run, ZI));
-  chk(dev_alloc(ctx, &ctx->S.w_head, ZI));
-  chk(dev_alloc(ctx, &ctx->S.n_wait, ZI));
-  chk(dev_alloc(ctx, &ctx->S.clock, ZI));
-  chk(dev_alloc(ctx, &ctx->S.iters, ZI));
+  const int rcap = ctx->qcap + ctx->mcap;
+  auto alloc_state = [&](lar::DevState& D, size_t nq) {
+    chk(dev_alloc(ctx, &D.sc, nq));
+    chk(dev_alloc(ctx, &D.d_last, nq * ctx->mcap));
+    chk(dev_alloc(ctx, &D.d_cx0, nq * ctx->mcap));
+    chk(dev_alloc(ctx, &D.d_seq, nq * ctx->mcap));
+    chk(dev_alloc(ctx, &D.r_rp, nq * rcap));
+    chk(dev_alloc(ctx, &D.r_rd, nq * rcap));
+    chk(dev_alloc(ctx, &D.r_cx, nq * rcap));
+    chk(dev_alloc(ctx, &D.r_seq, nq * rcap));
+    D.mcap = ctx->mcap;
+    D.rcap = rcap;
+    D.qcap = ctx->qcap;
+  };
+  alloc_state(ctx->S, ZI);
+  alloc_state(ctx->snap, (size_t)ctx->I);
   chk(dev_alloc(ctx, &ctx->pa, 5 * (size_t)ctx->I));
   chk(dev_alloc(ctx, &ctx->pi, 3 * (size_t)ctx->I));
   chk(dev_alloc(ctx, &ctx->T.E, ZI));
@@ -155,22 +162,10 @@ lar_status lar_create(lar_ctx** out, const lar_config* cfg) {
   chk(dev_alloc(ctx, &ctx->T.ok, ZI));
   chk(dev_alloc(ctx, &ctx->row_ttft, ZI));
   chk(dev_alloc(ctx, &ctx->err, 1));
-  chk(dev_alloc(ctx, &ctx->snap.run_rp, (size_t)ctx->I * ctx->mcap));
-  chk(dev_alloc(ctx, &ctx->snap.run_rd, (size_t)ctx->I * ctx->mcap));
-  chk(dev_alloc(ctx, &ctx->snap.run_cx, (size_t)ctx->I * ctx->mcap));
-  chk(dev_alloc(ctx, &ctx->snap.wait_p, (size_t)ctx->I * ctx->qcap));
-  chk(dev_alloc(ctx, &ctx->snap.wait_rd, (size_t)ctx->I * ctx->qcap));
-  chk(dev_alloc(ctx, &ctx->snap.n_run, ctx->I));
-  chk(dev_alloc(ctx, &ctx->snap.w_head, ctx->I));
-  chk(dev_alloc(ctx, &ctx->snap.n_wait, ctx->I));
-  chk(dev_alloc(ctx, &ctx->snap.clock, ctx->I));
-  chk(dev_alloc(ctx, &ctx->snap.iters, ctx->I));
   if (st != LAR_OK) {
     lar_destroy(ctx);
     return st;
   }
-  ctx->S.mcap = ctx->mcap;
-  ctx->S.qcap = ctx->qcap;
   ctx->T.K = 0;
   *out = ctx;
   return LAR_OK;
@@ -223,38 +218,62 @@ lar_status lar_load_state(lar_ctx* ctx, const lar_instance_params* params, const
     const int64_t k = ((int64_t)ctx->cfg.max_prompt - 1 + room - 1) / room + 1;
     if (k > K) K = k;
   }
-  // validate the snapshot and lay it out as the device SoA of one scenario
-  std::vector<int32_t> run_rp((size_t)I * mcap, 0), run_rd((size_t)I * mcap, 0),
-      run_cx((size_t)I * mcap, 0), wait_p((size_t)I * qcap, 0), wait_rd((size_t)I * qcap, 0),
-      n_run(I), head(I, 0), n_wait(I);
-  std::vector<double> clock(clock_ms, clock_ms + I);
-  std::vector<int64_t> iters(I, 0);
+  // validate the snapshot and lay it out as the device state of one scenario:
+  // decoding requests in slots, the rest (partially prefilled, then waiting) in the
+  // prefill ring, every request tagged with its FCFS position
+  const int rcap = qcap + mcap;
+  std::vector<int32_t> d_last((size_t)I * mcap, 0), d_cx0((size_t)I * mcap, 0),
+      d_seq((size_t)I * mcap, 0), r_rp((size_t)I * rcap, 0), r_rd((size_t)I * rcap, 0),
+      r_cx((size_t)I * rcap, 0), r_seq((size_t)I * rcap, 0);
+  std::vector<lar::QScal> sc(I);
   for (int j = 0; j < I; ++j) {
-    int nr = 0, nw = 0;
+    int nr = 0, nw = 0, nd = 0, np = 0, npart = 0;
+    int64_t c0 = 0, ps = 0;
     for (int r = offsets[j]; r < offsets[j + 1]; ++r) {
       const int32_t rp = rem_prefill[r], rd = rem_decode[r], cx = context[r];
+      const int seq = r - offsets[j];
       if (rp < 0 || rd < 1 || cx < 0 || (rp == 0 && cx == 0))
         return fail(ctx, LAR_E_STATE, "instance %d request %d: invalid (rp %d, rd %d, cx %d)", j,
-                    r - offsets[j], rp, rd, cx);
+                    seq, rp, rd, cx);
       if (cx > 0) {
         if (nw > 0)
           return fail(ctx, LAR_E_STATE, "instance %d: running request after a waiting one", j);
         if (nr >= params[j].max_seqs)
           return fail(ctx, LAR_E_STATE, "instance %d: more than max_seqs running", j);
-        run_rp[(size_t)j * mcap + nr] = rp;
-        run_rd[(size_t)j * mcap + nr] = rd;
-        run_cx[(size_t)j * mcap + nr] = cx;
         ++nr;
       } else {
         if (nw >= qcap)
           return fail(ctx, LAR_E_CAPACITY, "instance %d: more than queue_cap waiting", j);
-        wait_p[(size_t)j * qcap + nw] = rp;
-        wait_rd[(size_t)j * qcap + nw] = rd;
         ++nw;
       }
+      if (rp == 0) {   // decoding: last batch = rd (batch counter starts at 0)
+        d_last[(size_t)j * mcap + nd] = rd;
+        d_cx0[(size_t)j * mcap + nd] = cx;
+        d_seq[(size_t)j * mcap + nd] = seq;
+        c0 += cx;
+        ++nd;
+      } else {
+        r_rp[(size_t)j * rcap + np] = rp;
+        r_rd[(size_t)j * rcap + np] = rd;
+        r_cx[(size_t)j * rcap + np] = cx;
+        r_seq[(size_t)j * rcap + np] = seq;
+        ps += rp;
+        if (cx > 0) ++npart;
+        ++np;
+      }
     }
-    n_run[j] = nr;
-    n_wait[j] = nw;
+    lar::QScal q{};
+    q.g = 0;
+    q.n_dec = nd;
+    q.n_part = npart;
+    q.n_pre = np;
+    q.head = 0;
+    q.next_seq = offsets[j + 1] - offsets[j];
+    q.c0sum = c0;
+    q.pre_sum = ps;
+    q.clock = clock_ms[j];
+    q.iters = 0;
+    sc[j] = q;
   }
   // trajectory tail buffers (grow only)
   const size_t ZI = (size_t)Z * I;
@@ -288,16 +307,14 @@ lar_status lar_load_state(lar_ctx* ctx, const lar_instance_params* params, const
   HIP_TRY(ctx, hipMemcpy(ctx->pa, pa.data(), pa.size() * sizeof(double), hipMemcpyHostToDevice));
   HIP_TRY(ctx, hipMemcpy(ctx->pi, pi.data(), pi.size() * sizeof(int32_t), hipMemcpyHostToDevice));
   lar::DevState& sn = ctx->snap;
-  HIP_TRY(ctx, hipMemcpy(sn.run_rp, run_rp.data(), run_rp.size() * 4, hipMemcpyHostToDevice));
-  HIP_TRY(ctx, hipMemcpy(sn.run_rd, run_rd.data(), run_rd.size() * 4, hipMemcpyHostToDevice));
-  HIP_TRY(ctx, hipMemcpy(sn.run_cx, run_cx.data(), run_cx.size() * 4, hipMemcpyHostToDevice));
-  HIP_TRY(ctx, hipMemcpy(sn.wait_p, wait_p.data(), wait_p.size() * 4, hipMemcpyHostToDevice));
-  HIP_TRY(ctx, hipMemcpy(sn.wait_rd, wait_rd.data(), wait_rd.size() * 4, hipMemcpyHostToDevice));
-  HIP_TRY(ctx, hipMemcpy(sn.n_run, n_run.data(), I * 4, hipMemcpyHostToDevice));
-  HIP_TRY(ctx, hipMemcpy(sn.w_head, head.data(), I * 4, hipMemcpyHostToDevice));
-  HIP_TRY(ctx, hipMemcpy(sn.n_wait, n_wait.data(), I * 4, hipMemcpyHostToDevice));
-  HIP_TRY(ctx, hipMemcpy(sn.clock, clock.data(), I * 8, hipMemcpyHostToDevice));
-  HIP_TRY(ctx, hipMemcpy(sn.iters, iters.data(), I * 8, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.sc, sc.data(), sc.size() * sizeof(lar::QScal), hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.d_last, d_last.data(), d_last.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.d_cx0, d_cx0.data(), d_cx0.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.d_seq, d_seq.data(), d_seq.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.r_rp, r_rp.data(), r_rp.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.r_rd, r_rd.data(), r_rd.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.r_cx, r_cx.data(), r_cx.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.r_seq, r_seq.data(), r_seq.size() * 4, hipMemcpyHostToDevice));
   ctx->loaded = true;
   ctx->sticky = LAR_OK;
   {
@@ -313,23 +330,21 @@ lar_status lar_load_state(lar_ctx* ctx, const lar_instance_params* params, const
 lar_status lar_reload_state(lar_ctx* ctx) {
   if (!ctx) return LAR_E_ARG;
   if (!ctx->loaded) return fail(ctx, LAR_E_STATE, "no state loaded (call lar_load_state)");
-  const int I = ctx->I, mcap = ctx->mcap, qcap = ctx->qcap;
+  const size_t I = ctx->I, mcap = ctx->mcap, rcap = ctx->snap.rcap;
   const lar::DevState& sn = ctx->snap;
   const lar::DevState& S = ctx->S;
   hipStream_t s = ctx->stream;
   const hipMemcpyKind k = hipMemcpyDeviceToDevice;
   for (int z = 0; z < ctx->Z; ++z) {
     const size_t o = (size_t)z * I;
-    HIP_TRY(ctx, hipMemcpyAsync(S.run_rp + o * mcap, sn.run_rp, (size_t)I * mcap * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.run_rd + o * mcap, sn.run_rd, (size_t)I * mcap * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.run_cx + o * mcap, sn.run_cx, (size_t)I * mcap * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.wait_p + o * qcap, sn.wait_p, (size_t)I * qcap * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.wait_rd + o * qcap, sn.wait_rd, (size_t)I * qcap * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.n_run + o, sn.n_run, (size_t)I * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.w_head + o, sn.w_head, (size_t)I * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.n_wait + o, sn.n_wait, (size_t)I * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.clock + o, sn.clock, (size_t)I * 8, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.iters + o, sn.iters, (size_t)I * 8, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.sc + o, sn.sc, I * sizeof(lar::QScal), k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.d_last + o * mcap, sn.d_last, I * mcap * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.d_cx0 + o * mcap, sn.d_cx0, I * mcap * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.d_seq + o * mcap, sn.d_seq, I * mcap * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.r_rp + o * rcap, sn.r_rp, I * rcap * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.r_rd + o * rcap, sn.r_rd, I * rcap * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.r_cx + o * rcap, sn.r_cx, I * rcap * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.r_seq + o * rcap, sn.r_seq, I * rcap * 4, k, s));
   }
   HIP_TRY(ctx, lar::launch_clear_error(env_of(ctx)));
   ctx->sticky = LAR_OK;
@@ -398,17 +413,21 @@ lar_status lar_route_trace(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill,
     return fail(ctx, LAR_E_ARG, "n_cols %d does not cover instance column %d", n_cols, ctx->max_col);
   if (!std::isfinite(t_after_ms)) return fail(ctx, LAR_E_ARG, "t_after_ms not finite");
   const LaunchEnv env = env_of(ctx);
-  const int I = ctx->I;
-  for (int32_t i = 0; i < n_q; ++i) {
-    HIP_TRY(ctx, lar::launch_traj(env, q_t_ms + i, 0.0));
-    HIP_TRY(ctx, lar::launch_est(env, 1, q_prefill + i, q_t_ms + i, 0.0, ctx->row_ttft, nullptr));
-    HIP_TRY(ctx, lar::launch_route(env, 1, ctx->row_ttft, I, acc + (int64_t)i * n_cols,
-                                   cost + (int64_t)i * n_cols, n_cols, w_cost, w_lat, choice,
-                                   chosen_ttft, utility, n_q, i));
-    const double* tn = (i + 1 < n_q) ? q_t_ms + i + 1 : nullptr;
-    HIP_TRY(ctx, lar::launch_commit(env, choice + i, n_q, q_prefill + i, q_decode + i, 0, 0, tn,
-                                    t_after_ms));
-  }
+  lar::TraceArgs ta;
+  ta.N = n_q;
+  ta.qp = q_prefill;
+  ta.qd = q_decode;
+  ta.qt = q_t_ms;
+  ta.t_after = t_after_ms;
+  ta.acc = acc;
+  ta.cost = cost;
+  ta.n_cols = n_cols;
+  ta.w_cost = w_cost;
+  ta.w_lat = w_lat;
+  ta.choice = choice;
+  ta.chosen_ttft = chosen_ttft;
+  ta.utility = utility;
+  HIP_TRY(ctx, lar::launch_trace(env, ta));
   return LAR_OK;
 }
 
@@ -451,40 +470,54 @@ lar_status lar_read_state(lar_ctx* ctx, int32_t scen, int32_t* offsets, int32_t*
     return fail(ctx, LAR_E_ARG, "null argument");
   lar_status st = lar_sync(ctx);
   if (st == LAR_E_HIP) return st;
-  const int I = ctx->I, mcap = ctx->mcap, qcap = ctx->qcap;
+  const int I = ctx->I, mcap = ctx->mcap, rcap = ctx->S.rcap;
   const size_t o = (size_t)scen * I;
-  std::vector<int32_t> run_rp((size_t)I * mcap), run_rd((size_t)I * mcap), run_cx((size_t)I * mcap),
-      wait_p((size_t)I * qcap), wait_rd((size_t)I * qcap), n_run(I), head(I), n_wait(I);
-  HIP_TRY(ctx, hipMemcpy(run_rp.data(), ctx->S.run_rp + o * mcap, run_rp.size() * 4, hipMemcpyDeviceToHost));
-  HIP_TRY(ctx, hipMemcpy(run_rd.data(), ctx->S.run_rd + o * mcap, run_rd.size() * 4, hipMemcpyDeviceToHost));
-  HIP_TRY(ctx, hipMemcpy(run_cx.data(), ctx->S.run_cx + o * mcap, run_cx.size() * 4, hipMemcpyDeviceToHost));
-  HIP_TRY(ctx, hipMemcpy(wait_p.data(), ctx->S.wait_p + o * qcap, wait_p.size() * 4, hipMemcpyDeviceToHost));
-  HIP_TRY(ctx, hipMemcpy(wait_rd.data(), ctx->S.wait_rd + o * qcap, wait_rd.size() * 4, hipMemcpyDeviceToHost));
-  HIP_TRY(ctx, hipMemcpy(n_run.data(), ctx->S.n_run + o, I * 4, hipMemcpyDeviceToHost));
-  HIP_TRY(ctx, hipMemcpy(head.data(), ctx->S.w_head + o, I * 4, hipMemcpyDeviceToHost));
-  HIP_TRY(ctx, hipMemcpy(n_wait.data(), ctx->S.n_wait + o, I * 4, hipMemcpyDeviceToHost));
-  HIP_TRY(ctx, hipMemcpy(clock_ms, ctx->S.clock + o, I * 8, hipMemcpyDeviceToHost));
-  HIP_TRY(ctx, hipMemcpy(iterations_run, ctx->S.iters + o, I * 8, hipMemcpyDeviceToHost));
+  std::vector<lar::QScal> sc(I);
+  std::vector<int32_t> d_last((size_t)I * mcap), d_cx0((size_t)I * mcap), d_seq((size_t)I * mcap),
+      r_rp((size_t)I * rcap), r_rd((size_t)I * rcap), r_cx((size_t)I * rcap), r_seq((size_t)I * rcap);
+  const lar::DevState& S = ctx->S;
+  const hipMemcpyKind k = hipMemcpyDeviceToHost;
+  HIP_TRY(ctx, hipMemcpy(sc.data(), S.sc + o, I * sizeof(lar::QScal), k));
+  HIP_TRY(ctx, hipMemcpy(d_last.data(), S.d_last + o * mcap, d_last.size() * 4, k));
+  HIP_TRY(ctx, hipMemcpy(d_cx0.data(), S.d_cx0 + o * mcap, d_cx0.size() * 4, k));
+  HIP_TRY(ctx, hipMemcpy(d_seq.data(), S.d_seq + o * mcap, d_seq.size() * 4, k));
+  HIP_TRY(ctx, hipMemcpy(r_rp.data(), S.r_rp + o * rcap, r_rp.size() * 4, k));
+  HIP_TRY(ctx, hipMemcpy(r_rd.data(), S.r_rd + o * rcap, r_rd.size() * 4, k));
+  HIP_TRY(ctx, hipMemcpy(r_cx.data(), S.r_cx + o * rcap, r_cx.size() * 4, k));
+  HIP_TRY(ctx, hipMemcpy(r_seq.data(), S.r_seq + o * rcap, r_seq.size() * 4, k));
   int64_t total = 0;
-  for (int j = 0; j < I; ++j) total += n_run[j] + n_wait[j];
+  for (int j = 0; j < I; ++j) {
+    clock_ms[j] = sc[j].clock;
+    iterations_run[j] = sc[j].iters;
+    total += sc[j].n_dec + sc[j].n_pre;
+  }
   *n_total = total;
   if (total > out_cap) return fail(ctx, LAR_E_CAPACITY, "output arrays hold %lld < %lld",
                                    (long long)out_cap, (long long)total);
   if (total > 0 && (!rem_prefill || !rem_decode || !context))
     return fail(ctx, LAR_E_ARG, "null request arrays");
+  // merge decoding requests and the prefill list back into arrival order
+  struct Req { int32_t seq, rp, rd, cx; };
+  std::vector<Req> reqs;
   int64_t pos = 0;
   offsets[0] = 0;
   for (int j = 0; j < I; ++j) {
-    for (int r = 0; r < n_run[j]; ++r, ++pos) {
-      rem_prefill[pos] = run_rp[(size_t)j * mcap + r];
-      rem_decode[pos] = run_rd[(size_t)j * mcap + r];
-      context[pos] = run_cx[(size_t)j * mcap + r];
+    const lar::QScal& q = sc[j];
+    reqs.clear();
+    for (int s2 = 0; s2 < q.n_dec; ++s2) {
+      const size_t x = (size_t)j * mcap + s2;
+      reqs.push_back({d_seq[x], 0, d_last[x] - q.g, d_cx0[x] + q.g});
     }
-    for (int w = 0; w < n_wait[j]; ++w, ++pos) {
-      const int slot = (head[j] + w) % qcap;
-      rem_prefill[pos] = wait_p[(size_t)j * qcap + slot];
-      rem_decode[pos] = wait_rd[(size_t)j * qcap + slot];
-      context[pos] = 0;
+    for (int e = 0; e < q.n_pre; ++e) {
+      const size_t x = (size_t)j * rcap + (q.head + e) % rcap;
+      reqs.push_back({r_seq[x], r_rp[x], r_rd[x], r_cx[x]});
+    }
+    std::sort(reqs.begin(), reqs.end(), [](const Req& a, const Req& b) { return a.seq < b.seq; });
+    for (const Req& r : reqs) {
+      rem_prefill[pos] = r.rp;
+      rem_decode[pos] = r.rd;
+      context[pos] = r.cx;
+      ++pos;
     }
     offsets[j + 1] = (int32_t)pos;
   }

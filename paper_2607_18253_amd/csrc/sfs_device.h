@@ -1,12 +1,20 @@
-// sfs_device.h -- device-side layout and the wave-level SFS batch engine (gfx950).
+// sfs_device.h -- device-side state layout and the event-driven wave batch engine
+// for gfx950.
 //
-// One wavefront owns one (scenario, instance) queue.  Its running requests live in
-// VGPRs, slot s = k*64 + lane (k < KS), compacted in FCFS order; the waiting
-// requests stay in an HBM ring that is only read, a window of 64 at a time.  One
-// token batch (Sec. 4.1: one decode token per decoding sequence, then prefill
-// chunks in arrival order under the token budget and the running-sequence cap)
-// costs a few ballots, saturating wave prefix sums and, when requests finish or
-// are admitted, one order-preserving compaction through LDS.
+// One wavefront owns one (scenario, instance) queue.  The resident set (Sec. 4,
+// setup) is split by what a token batch does with each request (Sec. 4.1):
+//   * decoding requests (prefill done): one decode token per batch, nothing else,
+//     so they are kept lazily as (last, cx0) -- `last` = index of the batch that
+//     produces their final predicted token, context = cx0 + g at batch counter g --
+//     in unordered VGPR slots (slot s = k*64 + lane).  A batch only has to find the
+//     slots whose `last` is due; D and the decode-context sum C are running totals.
+//   * the prefill list: running partially prefilled requests, then waiting
+//     requests, in arrival (FCFS) order, in an HBM ring.  Its head sits in a
+//     64-lane register window; one saturating wave prefix sum of the remaining
+//     prefill gives every chunk of the batch.  Fully served entries are always a
+//     prefix of the window and move to the decode slots.
+// Every request carries its arrival sequence number, so the FCFS list can be
+// rebuilt on read-out.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -19,13 +27,29 @@ constexpr int kWave = 64;
 // Error codes shared with the C ABI (lar.h); kept numerically identical.
 constexpr int kErrArg = -1, kErrState = -2, kErrCapacity = -3, kErrIter = -4;
 
+// Per-queue scalars, one 64-byte record per (scenario, instance).
+struct alignas(64) QScal {
+  int32_t g;         // batches completed since the snapshot (batch counter)
+  int32_t n_dec;     // decoding requests
+  int32_t n_part;    // running partially prefilled requests (head of the prefill list)
+  int32_t n_pre;     // prefill list length (partials + waiting)
+  int32_t head;      // ring index of the prefill list head
+  int32_t next_seq;  // arrival number of the next appended request
+  int64_t c0sum;     // sum of cx0 over decoding requests
+  int64_t pre_sum;   // sum of remaining prefill over the prefill list
+  double clock;      // instance clock, ms
+  int64_t iters;     // batches replayed since the load
+  int32_t pad[2];
+};
+static_assert(sizeof(QScal) == 64, "QScal is one 64-byte record");
+
+// Device state of Z*I queues.  Decode slots are compacted (first n_dec valid) in
+// HBM; the prefill list is a ring of rcap entries per queue.
 struct DevState {
-  int32_t *run_rp, *run_rd, *run_cx;  // [ZI][mcap] running requests, FCFS, compacted
-  int32_t *wait_p, *wait_rd;          // [ZI][qcap] ring of waiting requests (FCFS)
-  int32_t *n_run, *w_head, *n_wait;   // [ZI]
-  double *clock;                      // [ZI] instance clock, ms
-  int64_t *iters;                     // [ZI] batches replayed since the load
-  int32_t mcap, qcap;
+  QScal* sc;                          // [ZI]
+  int32_t *d_last, *d_cx0, *d_seq;    // [ZI][mcap]
+  int32_t *r_rp, *r_rd, *r_cx, *r_seq;  // [ZI][rcap]
+  int32_t mcap, rcap, qcap;           // rcap = qcap + mcap
 };
 
 struct DevParams {
@@ -35,25 +59,21 @@ struct DevParams {
 
 // Background trajectory of one queue up to the batch in which a new tail query
 // would first receive prefill tokens (its admission batch), plus the decode-only
-// batches that follow it.  Written by k_traj, read by k_est.
+// batches that follow it.
 struct DevTraj {
-  double *E;            // [ZI] clock folded over the batches before the admission batch
-  int32_t *pre;         // [ZI] number of those batches
+  double* E;            // [ZI] clock folded over the batches before the admission batch
+  int32_t* pre;         // [ZI] number of those batches
   int64_t *P, *D, *C, *A;  // [ZI] background features of the admission batch
-  int32_t *left;        // [ZI] budget the background leaves in that batch (>= 1)
-  int32_t *ok;          // [ZI] 1 = valid; 0 = iteration cap or clock behind t
-  int32_t *tailD;       // [K][ZI] decode tokens of the k-th batch after admission
-  int64_t *tailC;       // [K][ZI] their context sum
+  int32_t* left;        // [ZI] budget the background leaves in that batch (>= 1)
+  int32_t* ok;          // [ZI] 1 = valid; 0 = iteration cap or clock behind t
+  int32_t* tailD;       // [K][ZI] decode tokens of the k-th batch after admission
+  int64_t* tailC;       // [K][ZI] their context sum
   int32_t K;
 };
 
 struct Coef {
   double a, b, c, d, e;
   int B, M;
-};
-
-struct Feat {
-  int64_t P, D, C, A;
 };
 
 __device__ __forceinline__ Coef load_coef(const DevParams& pr, int j) {
@@ -64,19 +84,19 @@ __device__ __forceinline__ Coef load_coef(const DevParams& pr, int j) {
 }
 
 // Batch time (Sec. 4.1): ((((a + b*P) + c*D) + d*C) + e*A), one rounding per op.
-__device__ __forceinline__ double batch_time(const Coef& k, int64_t P, int64_t D, int64_t C,
-                                             int64_t A) {
+// P <= B and D <= M fit in 32 bits.  C and A are converted only when their
+// coefficient is non-zero; otherwise the term is computed as coef * 0.0, which has
+// the same bits as coef * C for every finite C >= 0.
+__device__ __forceinline__ double batch_time(const Coef& k, int P, int D, int64_t C, int64_t A) {
   double t = k.a;
   t = __dadd_rn(t, __dmul_rn(k.b, (double)P));
   t = __dadd_rn(t, __dmul_rn(k.c, (double)D));
-  t = __dadd_rn(t, __dmul_rn(k.d, (double)C));
-  t = __dadd_rn(t, __dmul_rn(k.e, (double)A));
+  t = __dadd_rn(t, __dmul_rn(k.d, k.d != 0.0 ? (double)C : 0.0));
+  t = __dadd_rn(t, __dmul_rn(k.e, k.e != 0.0 ? (double)A : 0.0));
   return t;
 }
 
-__device__ __forceinline__ void set_error(int32_t* err, int code) {
-  atomicCAS(err, 0, code);
-}
+__device__ __forceinline__ void set_error(int32_t* err, int code) { atomicCAS(err, 0, code); }
 
 // ------------------------------------------------------------------ wave primitives
 __device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
@@ -84,16 +104,58 @@ __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
 __device__ __forceinline__ int popc(uint64_t m) { return __popcll(m); }
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 __device__ __forceinline__ int lane_last(int x) { return __builtin_amdgcn_readlane(x, kWave - 1); }
+__device__ __forceinline__ int lane_read(int x, int l) { return __builtin_amdgcn_readlane(x, l); }
 
-// Inclusive prefix sum over the wave, saturating at cap.  Inputs in [0, cap] with
-// cap <= 2^30, so no intermediate overflows; min(sat(x), L) == min(x, L) for L <= cap.
+// Number of set bits of m below this lane.
+__device__ __forceinline__ int mbcnt(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Inclusive prefix sum over the wave, saturating at cap, with DPP lane moves
+// (row_shr within 16-lane rows, then row_bcast:15 / row_bcast:31 across rows).
+// Inputs in [0, cap] with cap <= 2^30, so no intermediate overflows;
+// min(sat(x), L) == min(x, L) for every L <= cap.
 __device__ __forceinline__ int scan_sat(int x, int cap) {
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    int y = __shfl_up(x, o, kWave);
-    if (lane_id() >= o) x = min(x + y, cap);
-  }
+  x = min(x + __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true), cap);  // row_shr:1
+  x = min(x + __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true), cap);  // row_shr:2
+  x = min(x + __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true), cap);  // row_shr:4
+  x = min(x + __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true), cap);  // row_shr:8
+  x = min(x + __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false), cap); // row_bcast:15
+  x = min(x + __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false), cap); // row_bcast:31
   return x;
+}
+
+// Minimum over the wave (DPP row_shr within rows, then row_bcast across rows; lanes
+// without a source keep INT_MAX).
+__device__ __forceinline__ int wave_min(int x) {
+  const int big = 0x7fffffff;
+  x = min(x, __builtin_amdgcn_update_dpp(big, x, 0x111, 0xf, 0xf, false));  // row_shr:1
+  x = min(x, __builtin_amdgcn_update_dpp(big, x, 0x112, 0xf, 0xf, false));  // row_shr:2
+  x = min(x, __builtin_amdgcn_update_dpp(big, x, 0x114, 0xf, 0xf, false));  // row_shr:4
+  x = min(x, __builtin_amdgcn_update_dpp(big, x, 0x118, 0xf, 0xf, false));  // row_shr:8
+  x = min(x, __builtin_amdgcn_update_dpp(big, x, 0x142, 0xa, 0xf, false));  // row_bcast:15
+  x = min(x, __builtin_amdgcn_update_dpp(big, x, 0x143, 0xc, 0xf, false));  // row_bcast:31
+  return uni(__builtin_amdgcn_readlane(x, kWave - 1));
+}
+
+// Value of the previous lane (0 in lane 0): DPP wave_shr:1.
+__device__ __forceinline__ int prev_lane(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, 0x138, 0xf, 0xf, true);
+}
+
+// Sum of a 64-bit per-lane value over the lanes set in m (few lanes expected).
+__device__ __forceinline__ int64_t sum_lanes64(int64_t v, uint64_t m) {
+  int64_t s = 0;
+  const int lo = (int)(uint32_t)(uint64_t)v;
+  const int hi = (int)(uint32_t)((uint64_t)v >> 32);
+  while (m) {
+    const int l = __builtin_ctzll(m);
+    m &= m - 1;
+    s += (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(hi, l) << 32) |
+                   (uint64_t)(uint32_t)__builtin_amdgcn_readlane(lo, l));
+  }
+  return s;
 }
 
 __device__ __forceinline__ int64_t shfl_xor64(int64_t x, int m) {
@@ -123,217 +185,382 @@ __device__ __forceinline__ int wave_sum32(int x) {
 }
 
 // ------------------------------------------------------------------ the batch engine
-struct StepInfo {
-  Feat f;
-  int left;      // budget left after the batch
-  int n_adm;     // waiting requests admitted in the batch
-  int n_wait0;   // waiting requests before the batch
-  int n_run0;    // running requests before the batch
+struct StepOut {
+  int P, D;
+  int64_t C, A;
 };
 
-template <int KS>
-struct WaveQueue {
-  int rp[KS], rd[KS], cx[KS];  // slot s = k*64 + lane
-  int n_run, head, n_wait;     // wave-uniform
-  int qcap;
-  const int32_t* wp;           // waiting ring of this queue
-  const int32_t* wr;
-  int* l_rp;                   // LDS staging, KS*64 ints each
-  int* l_rd;
-  int* l_cx;
+// What a wave needs besides the state to work on one queue: the batch-time
+// coefficients, the queue's prefill ring in HBM, and the wave's LDS staging area
+// (3 x 64 ints).  Rebuilt from the parameters whenever a wave picks the queue up.
+struct QEnv {
   Coef k;
-  bool need_C, need_A;         // d != 0, e != 0: only then are C / A needed
+  bool need_C, need_A;   // d != 0, e != 0: only then are C / A accumulated
+  int32_t *r_rp, *r_rd, *r_cx, *r_seq;
+  int rcap;
+  int* stg;
+};
 
-  __device__ void load(const DevState& S, int qid) {
+__device__ __forceinline__ QEnv make_env(const DevState& S, const DevParams& pr, int qid, int j,
+                                         int* stage) {
+  QEnv e;
+  e.k = load_coef(pr, j);
+  e.need_C = e.k.d != 0.0;
+  e.need_A = e.k.e != 0.0;
+  e.rcap = S.rcap;
+  const int64_t rb = (int64_t)qid * S.rcap;
+  e.r_rp = S.r_rp + rb; e.r_rd = S.r_rd + rb; e.r_cx = S.r_cx + rb; e.r_seq = S.r_seq + rb;
+  e.stg = stage;
+  return e;
+}
+
+template <int KS>
+struct Queue {
+  // decode slots (slot s = k*64 + lane); a slot is free iff dl <= g
+  int dl[KS], dc[KS], ds[KS];
+  // prefill-list window: lane woff + i holds entry i of the list, i < nwin
+  int wrp, wrd, wcx, wseq;
+  int woff, nwin;
+  // scalars (wave-uniform)
+  int g, n_dec, n_part, n_pre, head, next_seq;
+  int64_t c0sum, pre_sum;
+  double clock;
+  int64_t iters;
+  __device__ void load(const DevState& S, const QEnv& e, int qid) {
     const int ln = lane_id();
-    n_run = uni(S.n_run[qid]);
-    head = uni(S.w_head[qid]);
-    n_wait = uni(S.n_wait[qid]);
-    qcap = S.qcap;
-    wp = S.wait_p + (int64_t)qid * S.qcap;
-    wr = S.wait_rd + (int64_t)qid * S.qcap;
-    const int64_t base = (int64_t)qid * S.mcap;
+    const QScal* q = S.sc + qid;
+    g = uni(q->g); n_dec = uni(q->n_dec); n_part = uni(q->n_part); n_pre = uni(q->n_pre);
+    head = uni(q->head); next_seq = uni(q->next_seq);
+    c0sum = uni64(q->c0sum); pre_sum = uni64(q->pre_sum);
+    clock = q->clock;
+    iters = uni64(q->iters);
+    const int64_t db = (int64_t)qid * S.mcap;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const int slot = s * kWave + ln;
-      if (slot < n_run) {
-        rp[s] = S.run_rp[base + slot];
-        rd[s] = S.run_rd[base + slot];
-        cx[s] = S.run_cx[base + slot];
+      if (slot < n_dec) {
+        dl[s] = S.d_last[db + slot]; dc[s] = S.d_cx0[db + slot]; ds[s] = S.d_seq[db + slot];
       } else {
-        rp[s] = 0; rd[s] = 0; cx[s] = 0;
+        dl[s] = 0; dc[s] = 0; ds[s] = 0;
       }
     }
+    woff = 0;
+    nwin = 0;
+    wrp = 0; wrd = 0; wcx = 0; wseq = 0;
+    refill(e);
   }
 
-  __device__ void store(const DevState& S, int qid) const {
+  // Write the queue back: decode slots compacted, window entries into the ring.
+  __device__ void store(const DevState& S, const QEnv& e, int qid) const {
     const int ln = lane_id();
-    const int64_t base = (int64_t)qid * S.mcap;
+    const int64_t db = (int64_t)qid * S.mcap;
+    int base = 0;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      const int slot = s * kWave + ln;
-      if (slot < S.mcap) {
-        S.run_rp[base + slot] = rp[s];
-        S.run_rd[base + slot] = rd[s];
-        S.run_cx[base + slot] = cx[s];
+      const bool live = dl[s] > g;
+      const uint64_t m = ballot(live);
+      if (live) {
+        const int dst = base + mbcnt(m);
+        S.d_last[db + dst] = dl[s]; S.d_cx0[db + dst] = dc[s]; S.d_seq[db + dst] = ds[s];
       }
+      base += popc(m);
+    }
+    const int idx = ln - woff;
+    if (idx >= 0 && idx < nwin) {
+      int pos = head + idx;
+      if (pos >= e.rcap) pos -= e.rcap;
+      e.r_rp[pos] = wrp; e.r_rd[pos] = wrd; e.r_cx[pos] = wcx; e.r_seq[pos] = wseq;
     }
     if (ln == 0) {
-      S.n_run[qid] = n_run;
-      S.w_head[qid] = head;
-      S.n_wait[qid] = n_wait;
+      QScal* q = S.sc + qid;
+      q->g = g; q->n_dec = n_dec; q->n_part = n_part; q->n_pre = n_pre; q->head = head;
+      q->next_seq = next_seq; q->c0sum = c0sum; q->pre_sum = pre_sum; q->clock = clock;
+      q->iters = iters;
     }
+    // the same wave loads this queue again later in a persistent kernel
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
   }
 
-  __device__ int resident() const { return n_run + n_wait; }
+  // Move the window down to lane 0.
+  __device__ void compact() {
+    if (woff == 0) return;
+    const int src = min(lane_id() + woff, kWave - 1);
+    wrp = __shfl(wrp, src, kWave);
+    wrd = __shfl(wrd, src, kWave);
+    wcx = __shfl(wcx, src, kWave);
+    wseq = __shfl(wseq, src, kWave);
+    woff = 0;
+  }
 
-  // Build the next token batch, apply it, and return its features.
-  __device__ StepInfo step() {
+  // Make min(n_pre, 64) list entries visible in the window.
+  __device__ void refill(const QEnv& e) {
+    const int want = min(n_pre, kWave);
+    if (nwin >= want) return;
+    if (woff + want > kWave) compact();
+    const int idx = lane_id() - woff;
+    if (idx >= nwin && idx < want) {
+      int pos = head + idx;
+      if (pos >= e.rcap) pos -= e.rcap;
+      wrp = e.r_rp[pos]; wrd = e.r_rd[pos]; wcx = e.r_cx[pos]; wseq = e.r_seq[pos];
+    }
+    nwin = want;
+  }
+
+  __device__ int resident() const { return n_dec + n_pre; }
+
+  // A new query at the FCFS tail gets prefill tokens in the next batch iff every
+  // request of the prefill list is served in full with budget to spare and a
+  // sequence slot is left for the query.
+  __device__ bool tail_admitted_next(const QEnv& e) const {
+    return n_dec + n_pre < e.k.M && (int64_t)n_dec + pre_sum < (int64_t)e.k.B;
+  }
+
+  // No prefill token can be scheduled in the next batch (empty prefill list, budget
+  // used up by decodes, or no running partial and no free sequence slot).  Nothing
+  // then changes until the next decode finishes: D, P = A = 0 stay fixed and C grows
+  // by D per batch.
+  __device__ bool quiet(const QEnv& e) const {
+    return !(n_pre > 0 && e.k.B - n_dec > 0 && (n_part > 0 || e.k.M - n_dec - n_part > 0));
+  }
+
+  // Index of the next batch in which a decoding request finishes (INT_MAX if none).
+  __device__ int next_finish() const {
+    int m = 0x7fffffff;
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      if (dl[s] > g) m = min(m, dl[s]);
+    return wave_min(m);
+  }
+
+  // Append a waiting request at the FCFS tail (the caller checked the capacity).
+  __device__ void append(const QEnv& e, int p, int d) {
     const int ln = lane_id();
+    const int idx = n_pre;
+    int pos = head + idx;
+    if (pos >= e.rcap) pos -= e.rcap;
+    if (nwin == n_pre && idx < kWave) {     // the window holds the whole list: extend it
+      if (woff + idx >= kWave) compact();
+      if (ln == woff + idx) { wrp = p; wrd = d; wcx = 0; wseq = next_seq; }
+      nwin = idx + 1;
+    } else {                                // beyond the window: the ring, read on refill
+      if (ln == 0) { e.r_rp[pos] = p; e.r_rd[pos] = d; e.r_cx[pos] = 0; e.r_seq[pos] = next_seq; }
+      // other lanes of this wave read the entry back on refill
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    }
+    n_pre += 1;
+    pre_sum += p;
+    next_seq += 1;
+  }
+
+  // Sum over the prefill list of rp*cx + rp*(rp+1)/2: the prefill-attention feature
+  // of a batch that serves the whole list.  Entries beyond the window have not been
+  // served since they were written to the ring, so the ring holds their values.
+  __device__ int64_t pre_attention_all(const QEnv& e) const {
+    const int ln = lane_id();
+    const int idx = ln - woff;
+    int64_t a = 0;
+    if (idx >= 0 && idx < nwin) a = (int64_t)wrp * wcx + (int64_t)wrp * (wrp + 1) / 2;
+    for (int base = nwin; base < n_pre; base += kWave) {
+      const int x = base + ln;
+      if (x < n_pre) {
+        int pos = head + x;
+        if (pos >= e.rcap) pos -= e.rcap;
+        const int64_t r = e.r_rp[pos];
+        a += r * e.r_cx[pos] + r * (r + 1) / 2;
+      }
+    }
+    return wave_sum64(a);
+  }
+
+  // Build the next token batch, apply it, return its features.
+  __device__ StepOut step(const QEnv& e) {
+    const int ln = lane_id();
+    const Coef& k = e.k;
+    const bool need_C = e.need_C, need_A = e.need_A;
+    int* stg = e.stg;
     const int B = k.B;
-    StepInfo info;
-    info.n_wait0 = n_wait;
-    info.n_run0 = n_run;
+    const int gn = g + 1;   // index of this batch
+    StepOut o;
+    o.D = n_dec;
+    o.C = need_C ? c0sum + (int64_t)n_dec * g : 0;
+    int left = B - n_dec;
 
-    // 1. one decode token for every running request whose prefill is complete
-    bool valid[KS], dec[KS];
-    int D = 0;
-    int64_t c_lane = 0;
+    // decoding requests whose last token is in this batch leave after it
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      valid[s] = (s * kWave + ln) < n_run;
-      dec[s] = valid[s] && rp[s] == 0;
-      D += popc(ballot(dec[s]));
-      if (dec[s]) c_lane += cx[s];
-    }
-    int left = B - D;
-
-    // 2a. prefill chunks for running requests with prefill left, in slot (FCFS) order
-    int chunk[KS];
-    int64_t p_lane = 0, a_lane = 0;
-    uint64_t any_part = 0;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      chunk[s] = 0;
-      any_part |= ballot(valid[s] && rp[s] > 0);
-    }
-    if (any_part) {
-      int carry = 0;   // saturating prefix of the earlier passes
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const int x = (valid[s] && rp[s] > 0) ? min(rp[s], B) : 0;
-        int incl = scan_sat(x, B);
-        int excl = __shfl_up(incl, 1, kWave);
-        if (ln == 0) excl = 0;
-        incl = min(incl + carry, B);
-        excl = min(excl + carry, B);
-        chunk[s] = min(incl, left) - min(excl, left);
-        carry = uni(lane_last(incl));
+      const uint64_t fm = ballot(dl[s] == gn);
+      if (fm) {
+        n_dec -= popc(fm);
+        if (need_C) c0sum -= sum_lanes64(dc[s], fm);
       }
-      left -= min(carry, left);
     }
 
-    // apply decode tokens and running chunks; find the requests that stay
-    bool keep[KS];
-    int n_keep = 0;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const int ch = chunk[s];
+    // prefill chunks in FCFS order over the window (and further windows)
+    int64_t P = 0, A = 0;
+    int free_slots = k.M - (int)o.D - n_part;   // slots for waiting admissions
+    while (n_pre > 0 && left > 0 && (n_part > 0 || free_slots > 0)) {
+      if (nwin == 0) refill(e);
+      const int nw0 = nwin;
+      const int idx = ln - woff;
+      const bool valid = idx >= 0 && idx < nw0;
+      const bool part = idx < n_part;
+      const bool elig = valid && (part || (idx - n_part) < free_slots);
+      const int x = elig ? min(wrp, B) : 0;
+      const int incl = scan_sat(x, B);
+      const int excl = prev_lane(incl);
+      const int ch = min(incl, left) - min(excl, left);
+      const int served = min(uni(lane_last(incl)), left);
+      P += served;
+      left -= served;
+      pre_sum -= served;
+      const uint64_t chm = ballot(ch > 0);
+      const uint64_t fullm = ballot(ch > 0 && ch == wrp);
+      const int n_full = popc(fullm);
+      const int n_adm_w = popc(chm & ~ballot(part));
+      // the first entry not served in full was waiting and got a chunk
+      const bool part_waiting = n_full < nw0 && n_full >= n_part &&
+                                ((chm >> (woff + n_full)) & 1ull) != 0;
+      if (need_A && chm) {
+        const int64_t av = (int64_t)ch * wcx + (int64_t)ch * (ch + 1) / 2;
+        A += sum_lanes64(av, chm);
+      }
       if (ch > 0) {
-        p_lane += ch;
-        a_lane += (int64_t)ch * cx[s] + (int64_t)ch * (ch + 1) / 2;
-        cx[s] += ch;
-        rp[s] -= ch;
+        wrp -= ch;
+        wcx += ch;
       }
-      if (dec[s]) {
-        cx[s] += 1;
-        rd[s] -= 1;
-      }
-      keep[s] = valid[s] && rd[s] > 0;
-      n_keep += popc(ballot(keep[s]));
-    }
-
-    // 2b. admit waiting requests in FCFS order while budget and sequence slots last
-    int n_adm = 0;
-    const bool admit = left > 0 && n_run < k.M && n_wait > 0;
-    const bool relayout = admit || n_keep != n_run;
-    if (relayout) {
-      // order-preserving compaction of the running slots into LDS
-      int before = 0;
+      free_slots -= n_adm_w;
+      if (n_full > 0) {
+        // completed prefills start decoding next batch: last = g + 1 + rd
+        const int nl = gn + wrd;
+        const int nc = wcx - gn;
+        if (need_C) c0sum += sum_lanes64(nc, fullm);
+        const bool full = ((fullm >> ln) & 1ull) != 0;
+        if (full) { stg[idx] = nl; stg[kWave + idx] = nc; stg[2 * kWave + idx] = wseq; }
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        int placed = 0;
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const uint64_t m = ballot(keep[s]);
-        if (keep[s]) {
-          const int dst = before + (int)__builtin_amdgcn_mbcnt_hi(
-              (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-          l_rp[dst] = rp[s];
-          l_rd[dst] = rd[s];
-          l_cx[dst] = cx[s];
+        for (int s = 0; s < KS; ++s) {
+          if (placed < n_full) {
+            const bool fr = dl[s] <= gn;
+            const uint64_t fm = ballot(fr);
+            const int r = placed + mbcnt(fm);
+            if (fr && r < n_full) { dl[s] = stg[r]; dc[s] = stg[kWave + r]; ds[s] = stg[2 * kWave + r]; }
+            placed += popc(fm);
+          }
         }
-        before += popc(m);
+        __builtin_amdgcn_wave_barrier();
+        n_dec += n_full;
+        woff += n_full;
+        nwin -= n_full;
+        head += n_full;
+        if (head >= e.rcap) head -= e.rcap;
+        n_pre -= n_full;
       }
+      n_part = n_part - min(n_full, n_part) + (part_waiting ? 1 : 0);
+      // continue only if the whole window was served (more entries may wait in the ring)
+      if (n_full < nw0) break;
+      refill(e);
     }
-    if (admit) {
-      const int lim = min(n_wait, k.M - n_run);
-      for (;;) {
-        const int w = n_adm + ln;
-        const bool v = w < lim;
-        int p = 0, r = 0;
-        if (v) {
-          int pos = head + w;
-          if (pos >= qcap) pos -= qcap;
-          p = wp[pos];
-          r = wr[pos];
-        }
-        const int x = v ? min(p, B) : 0;
-        const int incl = scan_sat(x, B);
-        int excl = __shfl_up(incl, 1, kWave);
-        if (ln == 0) excl = 0;
-        const int ch = min(incl, left) - min(excl, left);
-        const uint64_t am = ballot(ch > 0);
-        if (ch > 0) {
-          const int dst = n_keep + n_adm + ln;
-          l_rp[dst] = p - ch;
-          l_rd[dst] = r;
-          l_cx[dst] = ch;
-          p_lane += ch;
-          a_lane += (int64_t)ch * (ch + 1) / 2;
-        }
-        const int na = popc(am);
-        left -= min(uni(lane_last(incl)), left);
-        n_adm += na;
-        if (na < kWave || left == 0 || n_adm >= lim) break;
-      }
-      head += n_adm;
-      if (head >= qcap) head -= qcap;
-      n_wait -= n_adm;
-    }
-    if (relayout) {
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      n_run = n_keep + n_adm;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const int slot = s * kWave + ln;
-        if (slot < n_run) {
-          rp[s] = l_rp[slot];
-          rd[s] = l_rd[slot];
-          cx[s] = l_cx[slot];
-        } else {
-          rp[s] = 0; rd[s] = 0; cx[s] = 0;
-        }
-      }
-      __builtin_amdgcn_wave_barrier();
-    }
+    if (nwin < n_pre && nwin < kWave / 2) refill(e);
+    o.P = (int)P;
+    o.A = need_A ? A : 0;
+    g = gn;
+    return o;
+  }
 
-    info.f.P = wave_sum64(p_lane);
-    info.f.D = D;
-    info.f.C = need_C ? wave_sum64(c_lane) : 0;
-    info.f.A = need_A ? wave_sum64(a_lane) : 0;
-    info.left = left;
-    info.n_adm = n_adm;
-    return info;
+  // The decode-only batches that follow the admission batch of a tail query, read
+  // from the current state without changing it.  Valid when tail_admitted_next()
+  // holds and the whole prefill list is in the window: the admission batch serves
+  // every list entry in full (entry e then decodes until batch g + 1 + rd_e) and
+  // keeps the decoding requests with last > g + 1.  Batch k after it (k >= 1) has
+  //   D_k = #{dl >= g + 1 + k} + #{list entries: rd >= k},
+  //   C_k = (sum of cx0 over those) + D_k * (g + k).
+  // tail_begin() sets up k = 1; tail_next() moves to k + 1.
+  struct Tail {
+    int k;
+    int64_t D, c0;   // count and cx0 sum of the requests alive in batch k
+  };
+
+  __device__ Tail tail_begin(const QEnv& e) const {
+    const bool need_C = e.need_C;
+    const int ln = lane_id();
+    Tail t;
+    t.k = 1;
+    // decoding requests surviving the admission batch, plus every list entry
+    // (all have rd >= 1); the cx0 sum is c0sum minus the leavers plus the entries
+    int64_t D = 0, c0 = c0sum;
+    const int gn = g + 1;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      D += popc(ballot(dl[s] > gn));
+      if (need_C) {
+        const uint64_t fm = ballot(dl[s] == gn);
+        if (fm) c0 -= sum_lanes64(dc[s], fm);
+      }
+    }
+    const int idx = ln - woff;
+    const bool ent = idx >= 0 && idx < nwin;
+    const uint64_t em = ballot(ent);
+    D += popc(em);
+    if (need_C) c0 += sum_lanes64((int64_t)(wcx + wrp) - gn, em);
+    t.D = D;
+    t.c0 = c0;
+    return t;
+  }
+
+  __device__ void tail_next(const QEnv& e, Tail& t) const {
+    const bool need_C = e.need_C;
+    const int ln = lane_id();
+    // requests whose last decode is batch k leave: old slots with dl == g + 1 + k,
+    // list entries with rd == k
+    const int due = g + 1 + t.k;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const uint64_t m = ballot(dl[s] == due);
+      if (m) {
+        t.D -= popc(m);
+        if (need_C) t.c0 -= sum_lanes64(dc[s], m);
+      }
+    }
+    const int idx = ln - woff;
+    const bool ent = idx >= 0 && idx < nwin;
+    const uint64_t em = ballot(ent && wrd == t.k);
+    if (em) {
+      t.D -= popc(em);
+      if (need_C) t.c0 -= sum_lanes64((int64_t)(wcx + wrp) - (g + 1), em);
+    }
+    t.k += 1;
+  }
+
+  // Fold the quiet batches that precede the next decode finish into clk (one add
+  // per batch, in batch order), stopping early once clk >= t_stop or n reaches
+  // max_iters.  Call only when quiet(e) holds; returns the batches folded.
+  __device__ int64_t quiet_run(const QEnv& e, double& clk, double t_stop, int64_t n,
+                               int64_t max_iters) {
+    const int nf = next_finish();
+    const int D = n_dec;
+    int64_t done = 0;
+    if (!e.need_C) {
+      const double T = batch_time(e.k, 0, D, 0, 0);
+      while (g + 1 < nf && clk < t_stop && n + done < max_iters) {
+        clk = __dadd_rn(clk, T);
+        ++g;
+        ++done;
+      }
+    } else {
+      int64_t C = c0sum + (int64_t)D * g;
+      while (g + 1 < nf && clk < t_stop && n + done < max_iters) {
+        clk = __dadd_rn(clk, batch_time(e.k, 0, D, C, 0));
+        C += D;
+        ++g;
+        ++done;
+      }
+    }
+    return done;
   }
 };
 

@@ -19,76 +19,86 @@
 
 namespace lar {
 
+// Total order for the argmax: larger utility first, then the lower instance index.
+__device__ __forceinline__ bool better(double u1, int j1, double u2, int j2) {
+  if (j2 < 0) return j1 >= 0;
+  if (j1 < 0) return false;
+  return u1 > u2 || (u1 == u2 && j1 < j2);
+}
+
 // ------------------------------------------------------------------ k_traj
 template <int KS>
 __global__ __launch_bounds__(kWave) void k_traj(DevState S, DevParams pr, DevTraj tr, int Z, int I,
                                                const double* t_ptr, double t_val,
                                                int64_t max_iters, int32_t* err) {
-  __shared__ int l_rp[KS * kWave], l_rd[KS * kWave], l_cx[KS * kWave];
   const int qid = blockIdx.x;
   if (qid >= Z * I) return;
   const int j = qid % I;
   const double t = t_ptr ? *t_ptr : t_val;
-  WaveQueue<KS> w;
-  w.k = load_coef(pr, j);
-  w.need_C = w.k.d != 0.0;
-  w.need_A = w.k.e != 0.0;
-  w.l_rp = l_rp; w.l_rd = l_rd; w.l_cx = l_cx;
-  w.load(S, qid);
   const int ln = lane_id();
-  double E = S.clock[qid];
+  __shared__ int stage[3 * kWave];
+  const QEnv e = make_env(S, pr, qid, j, stage);
+  Queue<KS> w;
+  w.load(S, e, qid);
+  double E = w.clock;
   int ok = 1;
   if (E < t) {
     ok = 0;
     if (ln == 0) set_error(err, kErrState);
   }
-  int pre = 0;
-  StepInfo adm;
-  adm.f = Feat{0, 0, 0, 0};
-  adm.left = w.k.B;
-  bool admitted = false;
-  while (ok) {
-    if ((int64_t)pre >= max_iters) {   // admission batch would exceed the cap
+  int64_t pre = 0;
+  while (ok && !w.tail_admitted_next(e)) {
+    if (pre >= max_iters) {   // the admission batch would exceed the cap
       ok = 0;
       break;
     }
-    if (w.resident() == 0) {           // empty: the query is served alone from now on
-      admitted = true;
-      adm.f = Feat{0, 0, 0, 0};
-      adm.left = w.k.B;
-      break;
+    if (w.quiet(e)) {
+      pre += w.quiet_run(e, E, __builtin_inf(), pre, max_iters);
+      if (pre >= max_iters) continue;
     }
-    StepInfo si = w.step();
-    const bool reached = si.n_adm == si.n_wait0 && si.left > 0 && si.n_run0 + si.n_adm < w.k.M;
-    if (reached) {
-      admitted = true;
-      adm = si;
-      break;
-    }
-    E = __dadd_rn(E, batch_time(w.k, si.f.P, si.f.D, si.f.C, si.f.A));
+    const StepOut o = w.step(e);
+    E = __dadd_rn(E, batch_time(e.k, o.P, o.D, o.C, o.A));
     ++pre;
+  }
+  const int64_t aP = w.pre_sum, aD = w.n_dec;
+  const int64_t aC = e.need_C ? w.c0sum + aD * w.g : 0;
+  int64_t aA = 0;
+  if (ok) {
+    w.refill(e);
+    if (e.need_A) aA = w.pre_attention_all(e);
   }
   if (ln == 0) {
     tr.E[qid] = E;
-    tr.pre[qid] = pre;
-    tr.P[qid] = adm.f.P;
-    tr.D[qid] = adm.f.D;
-    tr.C[qid] = adm.f.C;
-    tr.A[qid] = adm.f.A;
-    tr.left[qid] = adm.left;
-    tr.ok[qid] = ok && admitted ? 1 : 0;
+    tr.pre[qid] = (int32_t)pre;
+    tr.P[qid] = aP;
+    tr.D[qid] = aD;
+    tr.C[qid] = aC;
+    tr.A[qid] = aA;
+    tr.left[qid] = (int)((int64_t)e.k.B - aD - aP);
+    tr.ok[qid] = ok;
+  }
+  const bool readonly = w.nwin == w.n_pre;
+  typename Queue<KS>::Tail tl{};
+  if (ok) {
+    if (readonly) tl = w.tail_begin(e);
+    else w.step(e);   // the admission batch itself (background only)
   }
   const int ZI = Z * I;
   for (int kk = 0; kk < tr.K; ++kk) {
-    int D = 0;
-    int64_t C = 0;
-    if (ok && w.n_run > 0) {
-      StepInfo si = w.step();   // decode-only after the admission batch
-      D = (int)si.f.D;
-      C = si.f.C;
+    int64_t D = 0, C = 0;
+    if (ok) {
+      if (readonly) {
+        D = tl.D;
+        C = e.need_C ? tl.c0 + D * (int64_t)(w.g + tl.k) : 0;
+        w.tail_next(e, tl);
+      } else {
+        D = w.n_dec;
+        C = e.need_C ? w.c0sum + D * w.g : 0;
+        if (D > 0) w.step(e);   // decode-only batch
+      }
     }
     if (ln == 0) {
-      tr.tailD[(int64_t)kk * ZI + qid] = D;
+      tr.tailD[(int64_t)kk * ZI + qid] = (int32_t)D;
       tr.tailC[(int64_t)kk * ZI + qid] = C;
     }
   }
@@ -163,17 +173,6 @@ __global__ __launch_bounds__(256) void k_est(DevParams pr, DevTraj tr, int Z, in
 }
 
 // ------------------------------------------------------------------ k_route
-struct Best {
-  double u;
-  int j;   // -1 = none
-};
-
-__device__ __forceinline__ bool better(double u1, int j1, double u2, int j2) {
-  if (j2 < 0) return j1 >= 0;
-  if (j1 < 0) return false;
-  return u1 > u2 || (u1 == u2 && j1 < j2);
-}
-
 __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double* ttft,
                                               int64_t ttft_zstride, const double* acc,
                                               const double* cost, int n_cols, const int32_t* col,
@@ -224,6 +223,43 @@ __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double
 }
 
 // ------------------------------------------------------------------ k_commit
+// Append (p, d) when this queue is the chosen one, then replay every batch that
+// starts before t; an idle queue's clock jumps to t.
+template <int KS>
+__device__ __forceinline__ void commit_advance(Queue<KS>& w, const QEnv& e, bool chosen, int p,
+                                               int d, double t, int qcap, int64_t max_iters,
+                                               int32_t* err) {
+  const int ln = lane_id();
+  if (chosen) {
+    d = d < 1 ? 1 : d;
+    if (p < 1) {
+      if (ln == 0) set_error(err, kErrArg);
+    } else if (w.n_pre - w.n_part + 1 > qcap) {
+      if (ln == 0) set_error(err, kErrCapacity);
+    } else {
+      w.append(e, p, d);
+    }
+  }
+  double clock = w.clock;
+  int64_t n = 0;
+  while (w.resident() > 0 && clock < t) {
+    if (n == max_iters) {
+      if (ln == 0) set_error(err, kErrIter);
+      break;
+    }
+    if (w.quiet(e)) {
+      n += w.quiet_run(e, clock, t, n, max_iters);
+      if (!(clock < t) || n == max_iters) continue;
+    }
+    const StepOut o = w.step(e);
+    clock = __dadd_rn(clock, batch_time(e.k, o.P, o.D, o.C, o.A));
+    ++n;
+  }
+  if (w.resident() == 0 && clock < t) clock = t;
+  w.clock = clock;
+  w.iters += n;
+}
+
 template <int KS>
 __global__ __launch_bounds__(kWave) void k_commit(DevState S, DevParams pr, int Z, int I,
                                                  const int32_t* choice, int64_t choice_zstride,
@@ -231,57 +267,293 @@ __global__ __launch_bounds__(kWave) void k_commit(DevState S, DevParams pr, int 
                                                  int32_t qp_val, int32_t qd_val,
                                                  const double* t_ptr, double t_val,
                                                  int64_t max_iters, int32_t* err) {
-  __shared__ int l_rp[KS * kWave], l_rd[KS * kWave], l_cx[KS * kWave];
   const int qid = blockIdx.x;
   if (qid >= Z * I) return;
   const int z = qid / I;
   const int j = qid % I;
-  const int ln = lane_id();
   const double t = t_ptr ? *t_ptr : t_val;
-  WaveQueue<KS> w;
-  w.k = load_coef(pr, j);
-  w.need_C = w.k.d != 0.0;
-  w.need_A = w.k.e != 0.0;
-  w.l_rp = l_rp; w.l_rd = l_rd; w.l_cx = l_cx;
-  w.load(S, qid);
-  if (choice && choice[(int64_t)z * choice_zstride] == j) {
-    const int p = qp_ptr ? *qp_ptr : qp_val;
-    int d = qd_ptr ? *qd_ptr : qd_val;
-    d = d < 1 ? 1 : d;
-    if (p < 1) {
-      if (ln == 0) set_error(err, kErrArg);
-    } else if (w.n_wait + 1 > w.qcap) {
-      if (ln == 0) set_error(err, kErrCapacity);
-    } else {
-      int pos = w.head + w.n_wait;
-      if (pos >= w.qcap) pos -= w.qcap;
-      if (ln == 0) {
-        S.wait_p[(int64_t)qid * S.qcap + pos] = p;
-        S.wait_rd[(int64_t)qid * S.qcap + pos] = d;
+  __shared__ int stage[3 * kWave];
+  const QEnv e = make_env(S, pr, qid, j, stage);
+  Queue<KS> w;
+  w.load(S, e, qid);
+  const bool chosen = choice && choice[(int64_t)z * choice_zstride] == j;
+  const int p = qp_ptr ? *qp_ptr : qp_val;
+  const int d = qd_ptr ? *qd_ptr : qd_val;
+  commit_advance(w, e, chosen, p, d, t, S.qcap, max_iters, err);
+  w.store(S, e, qid);
+}
+
+// ------------------------------------------------------------------ k_trace
+// From a state whose next batch admits a new tail query (clock folded to E after
+// `it` batches): the admission batch -- the whole prefill list, the decodes, and the
+// query's first chunk at context 0 -- then the query's further chunks and its first
+// decode batch, over the background's decode-only batches.  The background comes
+// from Queue::tail_begin/tail_next (read-only) when the whole prefill list is in the
+// window, else from stepping the (private) state.
+template <int KS>
+__device__ __forceinline__ double finish_estimate(Queue<KS>& w, const QEnv& e, double E,
+                                                  int64_t it, int p, double t, int reading,
+                                                  int64_t max_iters, int32_t* err) {
+  const int ln = lane_id();
+  const int aP = (int)w.pre_sum, aD = w.n_dec;
+  const int64_t aC = e.need_C ? w.c0sum + (int64_t)aD * w.g : 0;
+  const int64_t aA = e.need_A ? w.pre_attention_all(e) : 0;
+  const int left = e.k.B - aD - aP;
+  const int ch = p < left ? p : left;
+  E = __dadd_rn(E, batch_time(e.k, aP + ch, aD, aC, aA + (int64_t)ch * (ch + 1) / 2));
+  ++it;
+  int rem = p - ch;
+  int64_t cxq = ch;
+  bool done = reading == 1 && rem == 0;
+  if (!done) {
+    const bool readonly = w.nwin == w.n_pre;
+    typename Queue<KS>::Tail tl{};
+    if (readonly) tl = w.tail_begin(e); else w.step(e);
+    while (!done) {
+      int Dk;
+      int64_t Ck;
+      if (readonly) {
+        Dk = (int)tl.D;
+        Ck = e.need_C ? tl.c0 + (int64_t)Dk * (w.g + tl.k) : 0;
+      } else {
+        Dk = w.n_dec;
+        Ck = e.need_C ? w.c0sum + (int64_t)Dk * w.g : 0;
       }
-      w.n_wait += 1;
-      // make lane 0's store visible to the loads of the replay below
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-      __syncthreads();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      if (rem > 0) {
+        const int room = e.k.B - Dk;
+        const int c2 = rem < room ? rem : room;
+        E = __dadd_rn(E, batch_time(e.k, c2, Dk, Ck, (int64_t)c2 * cxq + (int64_t)c2 * (c2 + 1) / 2));
+        rem -= c2;
+        cxq += c2;
+        done = reading == 1 && rem == 0;
+      } else {
+        E = __dadd_rn(E, batch_time(e.k, 0, Dk + 1, Ck + cxq, 0));
+        done = true;
+      }
+      ++it;
+      if (!done) {
+        if (readonly) w.tail_next(e, tl);
+        else if (Dk > 0) w.step(e);
+      }
     }
   }
-  double clock = S.clock[qid];
-  int64_t n = 0;
-  while (w.resident() > 0 && clock < t) {
-    if (n == max_iters) {
+  if (it > max_iters && ln == 0) set_error(err, kErrIter);
+  return __dsub_rn(E, t);
+}
+
+// SFS estimate of a query (p prompt tokens, arrival t) at one queue; the queue is
+// not modified.  Returns NaN (and sets the error) when it cannot.
+template <int KS>
+__device__ __forceinline__ double estimate(const Queue<KS>& q, const QEnv& e, int p, double t,
+                                           int reading, int64_t max_iters, int32_t* err) {
+  const int ln = lane_id();
+  if (q.clock < t) {
+    if (ln == 0) set_error(err, kErrState);
+    return __builtin_nan("");
+  }
+  Queue<KS> w = q;
+  double E = w.clock;
+  int64_t it = 0;
+  while (!w.tail_admitted_next(e)) {
+    if (it >= max_iters) {
       if (ln == 0) set_error(err, kErrIter);
-      break;
+      return __builtin_nan("");
     }
-    StepInfo si = w.step();
-    clock = __dadd_rn(clock, batch_time(w.k, si.f.P, si.f.D, si.f.C, si.f.A));
-    ++n;
+    if (w.quiet(e)) {
+      it += w.quiet_run(e, E, __builtin_inf(), it, max_iters);
+      if (it >= max_iters) continue;
+    }
+    const StepOut o = w.step(e);
+    E = __dadd_rn(E, batch_time(e.k, o.P, o.D, o.C, o.A));
+    ++it;
   }
-  if (w.resident() == 0 && clock < t) clock = t;
-  w.store(S, qid);
-  if (ln == 0) {
-    S.clock[qid] = clock;
-    S.iters[qid] += n;
+  w.refill(e);
+  return finish_estimate(w, e, E, it, p, t, reading, max_iters, err);
+}
+
+// Trace inputs of one query, loaded one query ahead so their memory latency hides
+// behind the previous query's work.  Lane l of a wave holds acc / cost of the wave's
+// l-th owned instance.
+struct QueryIn {
+  int p, d;
+  double t, tn;
+  double acc_l, cost_l;   // per lane
+};
+
+__device__ __forceinline__ QueryIn fetch_query(int i, int N, const int32_t* qp, const int32_t* qd,
+                                               const double* qt, double t_after,
+                                               const double* acc, const double* cost,
+                                               int n_cols, int col_l, bool own_l) {
+  QueryIn q;
+  if (i < N) {
+    q.p = qp[i];
+    q.d = qd[i];
+    q.t = qt[i];
+    q.tn = (i + 1 < N) ? qt[i + 1] : t_after;
+    const int64_t o = (int64_t)i * n_cols + col_l;
+    q.acc_l = own_l ? acc[o] : 0.0;
+    q.cost_l = own_l ? cost[o] : 0.0;
+  } else {
+    q.p = 1; q.d = 1; q.t = 0.0; q.tn = 0.0; q.acc_l = 0.0; q.cost_l = 0.0;
+  }
+  return q;
+}
+
+__device__ __forceinline__ double read_lane_f64(double v, int l) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), l);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+__device__ __forceinline__ double utility_lane(const QueryIn& q, int l, double wc, double wl,
+                                               double ttft, double* eq2) {
+  const double a = read_lane_f64(q.acc_l, l);
+  const double c = read_lane_f64(q.cost_l, l);
+  const double u = __dsub_rn(a, __dmul_rn(wc, c));
+  *eq2 = u;
+  return __dsub_rn(u, __dmul_rn(wl, ttft));
+}
+
+// Workgroup argmax over the waves' candidates (double-buffered by query parity, so
+// one barrier per query suffices); thread 0 writes the outputs.
+template <int NW>
+__device__ __forceinline__ int trace_pick(double bu, int bj, double bt, double bq, int i, int z,
+                                          int N, int32_t* choice, double* chosen_ttft,
+                                          double* utility, double (*s_u)[NW], double (*s_t)[NW],
+                                          double (*s_q)[NW], int (*s_j)[NW]) {
+  const int wid = threadIdx.x / kWave;
+  const int nw = blockDim.x / kWave;
+  const int buf = i & 1;
+  if (lane_id() == 0) { s_u[buf][wid] = bu; s_j[buf][wid] = bj; s_t[buf][wid] = bt; s_q[buf][wid] = bq; }
+  __syncthreads();
+  double mu = s_u[buf][0], mt = s_t[buf][0], mq = s_q[buf][0];
+  int m = s_j[buf][0];
+  for (int v = 1; v < nw; ++v)
+    if (better(s_u[buf][v], s_j[buf][v], mu, m)) {
+      mu = s_u[buf][v]; m = s_j[buf][v]; mt = s_t[buf][v]; mq = s_q[buf][v];
+    }
+  if (threadIdx.x == 0) {
+    const int64_t o = (int64_t)z * N + i;
+    choice[o] = m;
+    if (chosen_ttft) chosen_ttft[o] = mt;
+    if (utility && m >= 0) utility[o] = mq;
+  }
+  return m;
+}
+
+#define LAR_TRACE_PARAMS                                                                     \
+  DevState S, DevParams pr, int Z, int I, int N, const int32_t *qp, const int32_t *qd,       \
+      const double *qt, double t_after, const double *acc, const double *cost, int n_cols,   \
+      const double *w_cost, const double *w_lat, int reading, int max_prompt,                \
+      int64_t max_iters, int32_t *choice, double *chosen_ttft, double *utility, int32_t *err
+
+// The whole sequential trace in one launch: one workgroup per scenario, wave w owning
+// instances j = w*IPW + r (r < IPW), their states resident in VGPRs for the whole
+// trace.  Per query: SFS estimate at every owned instance, wave and workgroup argmax
+// of the Lagrangian utility, append to the chosen instance, replay every instance to
+// the next arrival -- identical, operation for operation, to estimate + route +
+// commit per query.
+template <int KS, int NW, int IPW>
+__global__ __launch_bounds__(NW * kWave) void k_trace(LAR_TRACE_PARAMS) {
+  __shared__ double s_u[2][NW], s_t[2][NW], s_q[2][NW];
+  __shared__ int s_j[2][NW];
+  __shared__ int stage[NW][3 * kWave];
+  const int z = blockIdx.x;
+  const int wid = threadIdx.x / kWave;
+  const int ln = lane_id();
+  const double wc = w_cost[z];
+  const double wl = w_lat[z];
+  const int j_l = wid * IPW + ln;            // this lane's owned instance (lane < IPW)
+  const bool own_l = ln < IPW && j_l < I;
+  const int col_l = own_l ? pr.col[j_l] : 0;
+  Queue<KS> qs[IPW];
+#pragma unroll
+  for (int r = 0; r < IPW; ++r) {
+    const int j = wid * IPW + r;
+    if (j < I) qs[r].load(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
+  }
+  QueryIn nx = fetch_query(0, N, qp, qd, qt, t_after, acc, cost, n_cols, col_l, own_l);
+  for (int i = 0; i < N; ++i) {
+    const QueryIn q = nx;
+    nx = fetch_query(i + 1, N, qp, qd, qt, t_after, acc, cost, n_cols, col_l, own_l);
+    const bool p_ok = q.p >= 1 && q.p <= max_prompt;
+    if (!p_ok && threadIdx.x == 0) set_error(err, kErrArg);
+    double bu = 0.0, bt = 0.0, bq = 0.0;
+    int bj = -1;
+#pragma unroll
+    for (int r = 0; r < IPW; ++r) {
+      const int j = wid * IPW + r;
+      if (j < I) {
+        const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
+        const double ttft = p_ok ? estimate(qs[r], e, q.p, q.t, reading, max_iters, err)
+                                 : __builtin_nan("");
+        double eq2;
+        const double u = utility_lane(q, r, wc, wl, ttft, &eq2);
+        if (bj < 0 || u > bu) { bu = u; bj = j; bt = ttft; bq = eq2; }
+      }
+    }
+    const int m = trace_pick<NW>(bu, bj, bt, bq, i, z, N, choice, chosen_ttft, utility, s_u,
+                                 s_t, s_q, s_j);
+#pragma unroll
+    for (int r = 0; r < IPW; ++r) {
+      const int j = wid * IPW + r;
+      if (j < I)
+        commit_advance(qs[r], make_env(S, pr, z * I + j, j, stage[wid]), j == m, q.p, q.d,
+                       q.tn, S.qcap, max_iters, err);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < IPW; ++r) {
+    const int j = wid * IPW + r;
+    if (j < I) qs[r].store(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
+  }
+}
+
+// The same trace for pools too large to keep in registers: each owned instance's
+// state is loaded from HBM (L2) when it is needed and written back after its commit.
+// Wave w owns instances j = w + v*nw; lane v holds the inputs of the v-th one.
+template <int KS, int NW>
+__global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
+  __shared__ double s_u[2][NW], s_t[2][NW], s_q[2][NW];
+  __shared__ int s_j[2][NW];
+  __shared__ int stage[NW][3 * kWave];
+  const int z = blockIdx.x;
+  const int wid = threadIdx.x / kWave;
+  const int nw = blockDim.x / kWave;
+  const int ln = lane_id();
+  const double wc = w_cost[z];
+  const double wl = w_lat[z];
+  const int j_l = wid + ln * nw;
+  const bool own_l = j_l < I;
+  const int col_l = own_l ? pr.col[j_l] : 0;
+  QueryIn nx = fetch_query(0, N, qp, qd, qt, t_after, acc, cost, n_cols, col_l, own_l);
+  for (int i = 0; i < N; ++i) {
+    const QueryIn q = nx;
+    nx = fetch_query(i + 1, N, qp, qd, qt, t_after, acc, cost, n_cols, col_l, own_l);
+    const bool p_ok = q.p >= 1 && q.p <= max_prompt;
+    if (!p_ok && threadIdx.x == 0) set_error(err, kErrArg);
+    double bu = 0.0, bt = 0.0, bq = 0.0;
+    int bj = -1;
+    for (int v = 0, j = wid; j < I; ++v, j += nw) {
+      const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
+      Queue<KS> w;
+      w.load(S, e, z * I + j);
+      const double ttft = p_ok ? estimate(w, e, q.p, q.t, reading, max_iters, err)
+                               : __builtin_nan("");
+      double eq2;
+      const double u = utility_lane(q, v, wc, wl, ttft, &eq2);
+      if (bj < 0 || u > bu) { bu = u; bj = j; bt = ttft; bq = eq2; }
+    }
+    const int m = trace_pick<NW>(bu, bj, bt, bq, i, z, N, choice, chosen_ttft, utility, s_u,
+                                 s_t, s_q, s_j);
+    for (int j = wid; j < I; j += nw) {
+      const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
+      Queue<KS> w;
+      w.load(S, e, z * I + j);
+      commit_advance(w, e, j == m, q.p, q.d, q.tn, S.qcap, max_iters, err);
+      w.store(S, e, z * I + j);
+    }
   }
 }
 
@@ -400,6 +672,47 @@ static hipError_t launch_commit_ks(const LaunchEnv& env, const int32_t* choice,
                      env.P, env.Z, env.I, choice, choice_zstride, qp_ptr, qd_ptr, qp, qd, t_ptr,
                      t_val, env.max_iters, env.err);
   return hipGetLastError();
+}
+
+#define LAR_TRACE_ARGS                                                                   \
+  env.S, env.P, env.Z, env.I, a.N, a.qp, a.qd, a.qt, a.t_after, a.acc, a.cost, a.n_cols,     \
+      a.w_cost, a.w_lat, env.reading, env.max_prompt, env.max_iters, a.choice, a.chosen_ttft, \
+      a.utility, env.err
+
+// Register-resident trace: NW waves x IPW instances per wave must cover I.
+template <int KS, int NW, int IPW>
+static hipError_t launch_trace_res(const LaunchEnv& env, const TraceArgs& a) {
+  const int nw = (env.I + IPW - 1) / IPW;
+  hipLaunchKernelGGL((k_trace<KS, NW, IPW>), dim3(env.Z), dim3(nw * kWave), 0, env.stream,
+                     LAR_TRACE_ARGS);
+  return hipGetLastError();
+}
+
+template <int KS, int NW>
+static hipError_t launch_trace_mem(const LaunchEnv& env, const TraceArgs& a) {
+  const int nw = env.I < NW ? env.I : NW;
+  if ((env.I + nw - 1) / nw > kWave) return hipErrorInvalidValue;   // 64 instances per wave
+  hipLaunchKernelGGL((k_trace_mem<KS, NW>), dim3(env.Z), dim3(nw * kWave), 0, env.stream,
+                     LAR_TRACE_ARGS);
+  return hipGetLastError();
+}
+
+template <int KS>
+static hipError_t launch_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
+  // Register-resident states (k_trace) spill to scratch at the register budget of a
+  // full workgroup and measured slower than L2-resident states; use the latter.
+  return launch_trace_mem<KS, (KS <= 4 ? 8 : (KS == 8 ? 8 : 4))>(env, a);
+}
+
+hipError_t launch_trace(const LaunchEnv& env, const TraceArgs& a) {
+  switch (env.ks) {
+    case 1: return launch_trace_ks<1>(env, a);
+    case 2: return launch_trace_ks<2>(env, a);
+    case 4: return launch_trace_ks<4>(env, a);
+    case 8: return launch_trace_ks<8>(env, a);
+    case 16: return launch_trace_ks<16>(env, a);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_traj(const LaunchEnv& env, const double* t_ptr, double t_val) {

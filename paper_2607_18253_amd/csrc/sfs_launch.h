@@ -21,6 +21,19 @@ struct LaunchEnv {
   hipStream_t stream;
 };
 
+struct TraceArgs {
+  int N;
+  const int32_t *qp, *qd;
+  const double* qt;
+  double t_after;
+  const double *acc, *cost;
+  int n_cols;
+  const double *w_cost, *w_lat;
+  int32_t* choice;
+  double *chosen_ttft, *utility;
+};
+
+hipError_t launch_trace(const LaunchEnv& env, const TraceArgs& a);
 hipError_t launch_traj(const LaunchEnv& env, const double* t_ptr, double t_val);
 hipError_t launch_est(const LaunchEnv& env, int Q, const int32_t* q_prefill, const double* t_ptr,
                       double t_val, double* ttft, int32_t* iters);
