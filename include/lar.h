@@ -55,7 +55,8 @@ enum {
   LAR_E_STATE = -2,    /* invalid snapshot, or an instance clock behind t       */
   LAR_E_CAPACITY = -3, /* waiting queue of an instance would exceed queue_cap   */
   LAR_E_ITER = -4,     /* a simulation needed more than max_iters batches       */
-  LAR_E_HIP = -5       /* HIP runtime failure                                   */
+  LAR_E_HIP = -5,      /* HIP runtime failure                                   */
+  LAR_E_SYNC = -6      /* workgroups of one scenario could not run together     */
 };
 
 /* Which batch yields the first token (the first-output-token batch, Sec. 4.1). */

@@ -25,7 +25,7 @@ namespace lar {
 constexpr int kWave = 64;
 
 // Error codes shared with the C ABI (lar.h); kept numerically identical.
-constexpr int kErrArg = -1, kErrState = -2, kErrCapacity = -3, kErrIter = -4;
+constexpr int kErrArg = -1, kErrState = -2, kErrCapacity = -3, kErrIter = -4, kErrSync = -6;
 
 // Per-queue scalars, one 64-byte record per (scenario, instance).
 struct alignas(64) QScal {
@@ -184,6 +184,18 @@ __device__ __forceinline__ int wave_sum32(int x) {
   return uni(x);
 }
 
+// ------------------------------------------------------------------ LDS-resident queues
+// A queue's state kept in LDS between uses by a persistent kernel: decode slots in
+// the register layout (slot s = k*64 + lane), the prefill window, and the scalars.
+template <int KS>
+struct LdsQueue {
+  int dl[KS * kWave], dc[KS * kWave], ds[KS * kWave];
+  int wrp[kWave], wrd[kWave], wcx[kWave], wseq[kWave];
+  int g, n_dec, n_part, n_pre, head, next_seq, woff, nwin;
+  int64_t c0sum, pre_sum, iters;
+  double clock;
+};
+
 // ------------------------------------------------------------------ the batch engine
 struct StepOut {
   int P, D;
@@ -248,6 +260,34 @@ struct Queue {
     nwin = 0;
     wrp = 0; wrd = 0; wcx = 0; wseq = 0;
     refill(e);
+  }
+
+  // Copy to / from an LDS mirror (same layout as the registers).
+  __device__ void to_lds(LdsQueue<KS>& L) const {
+    const int ln = lane_id();
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      L.dl[s * kWave + ln] = dl[s]; L.dc[s * kWave + ln] = dc[s]; L.ds[s * kWave + ln] = ds[s];
+    }
+    L.wrp[ln] = wrp; L.wrd[ln] = wrd; L.wcx[ln] = wcx; L.wseq[ln] = wseq;
+    if (ln == 0) {
+      L.g = g; L.n_dec = n_dec; L.n_part = n_part; L.n_pre = n_pre; L.head = head;
+      L.next_seq = next_seq; L.woff = woff; L.nwin = nwin; L.c0sum = c0sum;
+      L.pre_sum = pre_sum; L.iters = iters; L.clock = clock;
+    }
+  }
+
+  __device__ void from_lds(const LdsQueue<KS>& L) {
+    const int ln = lane_id();
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      dl[s] = L.dl[s * kWave + ln]; dc[s] = L.dc[s * kWave + ln]; ds[s] = L.ds[s * kWave + ln];
+    }
+    wrp = L.wrp[ln]; wrd = L.wrd[ln]; wcx = L.wcx[ln]; wseq = L.wseq[ln];
+    g = uni(L.g); n_dec = uni(L.n_dec); n_part = uni(L.n_part); n_pre = uni(L.n_pre);
+    head = uni(L.head); next_seq = uni(L.next_seq); woff = uni(L.woff); nwin = uni(L.nwin);
+    c0sum = uni64(L.c0sum); pre_sum = uni64(L.pre_sum); iters = uni64(L.iters);
+    clock = L.clock;
   }
 
   // Write the queue back: decode slots compacted, window entries into the ring.

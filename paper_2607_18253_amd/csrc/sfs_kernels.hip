@@ -557,6 +557,353 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
   }
 }
 
+// Trace inputs of 64 consecutive queries, lane l holding query base + l; the acc /
+// cost values are those of the wave's IPW owned instances.
+template <int IPW>
+struct QueryBlock {
+  int p, d;
+  double t;
+  double acc[IPW], cost[IPW];
+};
+
+template <int IPW>
+__device__ __forceinline__ QueryBlock<IPW> fetch_block(int base, int N, const int32_t* qp,
+                                                       const int32_t* qd, const double* qt,
+                                                       const double* acc, const double* cost,
+                                                       int n_cols, const int* cols) {
+  QueryBlock<IPW> b;
+  const int i = base + lane_id();
+  const bool in = i < N;
+  b.p = in ? qp[i] : 1;
+  b.d = in ? qd[i] : 1;
+  b.t = in ? qt[i] : 0.0;
+#pragma unroll
+  for (int r = 0; r < IPW; ++r) {
+    const int64_t o = (int64_t)i * n_cols + cols[r];
+    b.acc[r] = in && cols[r] >= 0 ? acc[o] : 0.0;
+    b.cost[r] = in && cols[r] >= 0 ? cost[o] : 0.0;
+  }
+  return b;
+}
+
+// Candidate of one wave for one query.
+struct Cand {
+  double u, ttft, eq2;
+  int j;
+};
+
+__device__ __forceinline__ void cand_take(Cand& c, double u, int j, double ttft, double eq2) {
+  if (c.j < 0 || u > c.u) { c.u = u; c.j = j; c.ttft = ttft; c.eq2 = eq2; }
+}
+
+// The whole sequential trace in one launch with every instance state resident in
+// LDS: one workgroup per scenario, wave w owning instances j = w*IPW + r.  Per
+// query and owned instance the state is read from LDS once: the commit of query i
+// (append when chosen, replay to t_{i+1}) and the estimate of query i+1 run on the
+// same registers; one barrier per query publishes the waves' candidates.
+// Identical, operation for operation, to estimate + route + commit per query.
+template <int KS, int NW, int IPW>
+__global__ __launch_bounds__(NW * kWave) void k_trace_lds(LAR_TRACE_PARAMS) {
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  LdsQueue<KS>* lq = reinterpret_cast<LdsQueue<KS>*>(lds_raw);   // [NW * IPW]
+  __shared__ double s_u[2][NW], s_t[2][NW], s_q[2][NW];
+  __shared__ int s_j[2][NW];
+  __shared__ int stage[NW][3 * kWave];
+  const int z = blockIdx.x;
+  const int wid = threadIdx.x / kWave;
+  const int nw = blockDim.x / kWave;
+  const int ln = lane_id();
+  const double wc = w_cost[z];
+  const double wl = w_lat[z];
+  int cols[IPW];
+#pragma unroll
+  for (int r = 0; r < IPW; ++r) {
+    const int j = wid * IPW + r;
+    cols[r] = j < I ? pr.col[j] : -1;
+    if (j < I) {
+      const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
+      Queue<KS> w;
+      w.load(S, e, z * I + j);
+      w.to_lds(lq[wid * IPW + r]);
+    }
+  }
+  QueryBlock<IPW> cur = fetch_block<IPW>(0, N, qp, qd, qt, acc, cost, n_cols, cols);
+  QueryBlock<IPW> nxt = fetch_block<IPW>(kWave, N, qp, qd, qt, acc, cost, n_cols, cols);
+  // candidate of query 0
+  Cand c;
+  c.j = -1; c.u = 0.0; c.ttft = 0.0; c.eq2 = 0.0;
+  {
+    const int p = uni(cur.p);
+    const double t = read_lane_f64(cur.t, 0);
+    const bool p_ok = p >= 1 && p <= max_prompt;
+    if (!p_ok && threadIdx.x == 0) set_error(err, kErrArg);
+#pragma unroll
+    for (int r = 0; r < IPW; ++r) {
+      const int j = wid * IPW + r;
+      if (j < I) {
+        const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
+        Queue<KS> w;
+        w.from_lds(lq[wid * IPW + r]);
+        const double ttft = p_ok ? estimate(w, e, p, t, reading, max_iters, err)
+                                 : __builtin_nan("");
+        const double a = read_lane_f64(cur.acc[r], 0), co = read_lane_f64(cur.cost[r], 0);
+        const double eq2 = __dsub_rn(a, __dmul_rn(wc, co));
+        cand_take(c, __dsub_rn(eq2, __dmul_rn(wl, ttft)), j, ttft, eq2);
+      }
+    }
+  }
+  for (int i = 0; i < N; ++i) {
+    const int l = i & (kWave - 1);
+    // inputs of query i (in cur) and i + 1 (in cur or nxt)
+    const int p = __builtin_amdgcn_readlane(cur.p, l);
+    const int dq = __builtin_amdgcn_readlane(cur.d, l);
+    double tn;
+    const bool last_in_block = l == kWave - 1;
+    if (i + 1 >= N) tn = t_after;
+    else tn = last_in_block ? read_lane_f64(nxt.t, 0) : read_lane_f64(cur.t, l + 1);
+    // publish candidates, pick the winner (one barrier; LDS double-buffered)
+    const int buf = i & 1;
+    if (ln == 0) { s_u[buf][wid] = c.u; s_j[buf][wid] = c.j; s_t[buf][wid] = c.ttft; s_q[buf][wid] = c.eq2; }
+    __syncthreads();
+    double mu = s_u[buf][0], mt = s_t[buf][0], mq = s_q[buf][0];
+    int m = s_j[buf][0];
+    for (int v = 1; v < nw; ++v)
+      if (better(s_u[buf][v], s_j[buf][v], mu, m)) {
+        mu = s_u[buf][v]; m = s_j[buf][v]; mt = s_t[buf][v]; mq = s_q[buf][v];
+      }
+    if (threadIdx.x == 0) {
+      const int64_t o = (int64_t)z * N + i;
+      choice[o] = m;
+      if (chosen_ttft) chosen_ttft[o] = mt;
+      if (utility && m >= 0) utility[o] = mq;
+    }
+    // next query's inputs
+    const bool more = i + 1 < N;
+    int p1 = 1;
+    double t1 = 0.0;
+    if (more) {
+      p1 = last_in_block ? uni(nxt.p) : __builtin_amdgcn_readlane(cur.p, l + 1);
+      t1 = tn;
+    }
+    const bool p1_ok = p1 >= 1 && p1 <= max_prompt;
+    if (more && !p1_ok && threadIdx.x == 0) set_error(err, kErrArg);
+    c.j = -1; c.u = 0.0; c.ttft = 0.0; c.eq2 = 0.0;
+#pragma unroll
+    for (int r = 0; r < IPW; ++r) {
+      const int j = wid * IPW + r;
+      if (j < I) {
+        const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
+        Queue<KS> w;
+        w.from_lds(lq[wid * IPW + r]);
+        commit_advance(w, e, j == m, p, dq, tn, S.qcap, max_iters, err);
+        if (more) {
+          const double ttft = p1_ok ? estimate(w, e, p1, t1, reading, max_iters, err)
+                                    : __builtin_nan("");
+          const int l1 = last_in_block ? 0 : l + 1;
+          const double a = read_lane_f64(last_in_block ? nxt.acc[r] : cur.acc[r], l1);
+          const double co = read_lane_f64(last_in_block ? nxt.cost[r] : cur.cost[r], l1);
+          const double eq2 = __dsub_rn(a, __dmul_rn(wc, co));
+          cand_take(c, __dsub_rn(eq2, __dmul_rn(wl, ttft)), j, ttft, eq2);
+        }
+        w.to_lds(lq[wid * IPW + r]);
+      }
+    }
+    if (last_in_block) {
+      cur = nxt;
+      nxt = fetch_block<IPW>(i + 1 + kWave, N, qp, qd, qt, acc, cost, n_cols, cols);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < IPW; ++r) {
+    const int j = wid * IPW + r;
+    if (j < I) {
+      const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
+      Queue<KS> w;
+      w.from_lds(lq[wid * IPW + r]);
+      w.store(S, e, z * I + j);
+    }
+  }
+}
+
+// Candidate exchange between the workgroups of one scenario: each workgroup posts
+// its best candidate for query i into slot (i & 1) and bumps the scenario's arrival
+// counter (release, agent scope); all wait until the counter reaches G * (i + 1)
+// (acquire) and reduce the G posts in the same total order.  The wait is bounded in
+// wall time (s_memrealtime, 100 MHz): after kSpinTicks it flags kErrSync and gives
+// up, and every other member leaves as soon as it sees that flag, so a cluster whose
+// workgroups cannot all be resident terminates instead of hanging.
+constexpr uint64_t kSpinTicks = 1000000000ull;   // 10 s
+
+__device__ __forceinline__ bool cluster_exchange(Cand& c, int i, int G, int cid,
+                                                 uint32_t* cnt, double* xc, int32_t* err) {
+  double* slot = xc + ((int64_t)(i & 1) * kMaxCluster + cid) * 4;
+  slot[0] = c.u;
+  slot[1] = (double)c.j;
+  slot[2] = c.ttft;
+  slot[3] = c.eq2;
+  __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  const uint32_t target = (uint32_t)G * (uint32_t)(i + 1);
+  const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+  while (__hip_atomic_load(cnt, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target) {
+    if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == kErrSync ||
+        __builtin_amdgcn_s_memrealtime() - t0 > kSpinTicks) {
+      set_error(err, kErrSync);
+      return false;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+  Cand b;
+  b.j = -1; b.u = 0.0; b.ttft = 0.0; b.eq2 = 0.0;
+  for (int v = 0; v < G; ++v) {
+    const double* o = xc + ((int64_t)(i & 1) * kMaxCluster + v) * 4;
+    const double u = __hip_atomic_load(o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int j = (int)__hip_atomic_load(o + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (better(u, j, b.u, b.j)) {
+      b.u = u;
+      b.j = j;
+      b.ttft = __hip_atomic_load(o + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      b.eq2 = __hip_atomic_load(o + 3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  c = b;
+  return true;
+}
+
+__global__ void k_clear_exchange(uint32_t* cnt, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) cnt[i * 16] = 0u;
+}
+
+// The whole sequential trace with each wave owning IPW instances whose states stay
+// in VGPRs for the whole trace.  A scenario spans G workgroups of W waves; block b
+// serves scenario z = (b / 8 / G) * 8 + b % 8 as cluster member (b / 8) % G, so the
+// members of a scenario share one XCD (blocks are dispatched to the 8 XCDs
+// round-robin) and exchange through that XCD's L2.  Per query: the estimate of every
+// owned instance (computed right after the previous commit), the workgroup argmax
+// (LDS, one barrier), the cluster argmax (global exchange, when G > 1), the commit
+// and replay of every owned instance, and the estimate of the next query.
+// Identical, operation for operation, to estimate + route + commit per query.
+template <int KS, int W, int IPW>
+__global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G, uint32_t* xcount,
+                                                        double* xcand) {
+  __shared__ double s_u[2][W], s_t[2][W], s_q[2][W];
+  __shared__ int s_j[2][W];
+  __shared__ double s_m[2][4];
+  __shared__ int stage[W][3 * kWave];
+  const int b = blockIdx.x;
+  const int z = (b / 8 / G) * 8 + b % 8;
+  const int cid = (b / 8) % G;
+  if (z >= Z) return;
+  const int wid = threadIdx.x / kWave;
+  const int nw = blockDim.x / kWave;   // waves launched (<= W)
+  const int ln = lane_id();
+  const double wc = w_cost[z];
+  const double wl = w_lat[z];
+  uint32_t* cnt = xcount + (int64_t)z * 16;
+  double* xc = xcand + (int64_t)z * 2 * kMaxCluster * 4;
+  const int jbase = (cid * W + wid) * IPW;
+  int cols[IPW];
+  Queue<KS> qs[IPW];
+#pragma unroll
+  for (int r = 0; r < IPW; ++r) {
+    const int j = jbase + r;
+    cols[r] = j < I ? pr.col[j] : -1;
+    if (j < I) qs[r].load(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
+  }
+  QueryBlock<IPW> cur = fetch_block<IPW>(0, N, qp, qd, qt, acc, cost, n_cols, cols);
+  QueryBlock<IPW> nxt = fetch_block<IPW>(kWave, N, qp, qd, qt, acc, cost, n_cols, cols);
+  Cand c;
+  c.j = -1; c.u = 0.0; c.ttft = 0.0; c.eq2 = 0.0;
+  {
+    const int p = uni(cur.p);
+    const double t = read_lane_f64(cur.t, 0);
+    const bool p_ok = p >= 1 && p <= max_prompt;
+    if (!p_ok && threadIdx.x == 0 && cid == 0) set_error(err, kErrArg);
+#pragma unroll
+    for (int r = 0; r < IPW; ++r) {
+      const int j = jbase + r;
+      if (j < I) {
+        const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
+        const double ttft = p_ok ? estimate(qs[r], e, p, t, reading, max_iters, err)
+                                 : __builtin_nan("");
+        const double a = read_lane_f64(cur.acc[r], 0), co = read_lane_f64(cur.cost[r], 0);
+        const double eq2 = __dsub_rn(a, __dmul_rn(wc, co));
+        cand_take(c, __dsub_rn(eq2, __dmul_rn(wl, ttft)), j, ttft, eq2);
+      }
+    }
+  }
+  bool alive = true;
+  for (int i = 0; i < N && alive; ++i) {
+    const int l = i & (kWave - 1);
+    const int p = __builtin_amdgcn_readlane(cur.p, l);
+    const int dq = __builtin_amdgcn_readlane(cur.d, l);
+    const bool last_in_block = l == kWave - 1;
+    double tn;
+    if (i + 1 >= N) tn = t_after;
+    else tn = last_in_block ? read_lane_f64(nxt.t, 0) : read_lane_f64(cur.t, l + 1);
+    // workgroup argmax
+    const int buf = i & 1;
+    if (ln == 0) { s_u[buf][wid] = c.u; s_j[buf][wid] = c.j; s_t[buf][wid] = c.ttft; s_q[buf][wid] = c.eq2; }
+    __syncthreads();
+    Cand wb;
+    wb.u = s_u[buf][0]; wb.j = s_j[buf][0]; wb.ttft = s_t[buf][0]; wb.eq2 = s_q[buf][0];
+    for (int v = 1; v < nw; ++v)
+      if (better(s_u[buf][v], s_j[buf][v], wb.u, wb.j)) {
+        wb.u = s_u[buf][v]; wb.j = s_j[buf][v]; wb.ttft = s_t[buf][v]; wb.eq2 = s_q[buf][v];
+      }
+    if (G > 1) {
+      // one thread exchanges with the other workgroups, then broadcasts the winner
+      if (threadIdx.x == 0) {
+        const bool ok = cluster_exchange(wb, i, G, cid, cnt, xc, err);
+        s_m[buf][0] = wb.u; s_m[buf][1] = (double)wb.j; s_m[buf][2] = wb.ttft; s_m[buf][3] = wb.eq2;
+        if (!ok) s_m[buf][1] = -2.0;
+      }
+      __syncthreads();
+      wb.u = s_m[buf][0]; wb.j = (int)s_m[buf][1]; wb.ttft = s_m[buf][2]; wb.eq2 = s_m[buf][3];
+      if (wb.j == -2) { alive = false; break; }
+    }
+    const int m = wb.j;
+    if (threadIdx.x == 0 && cid == 0) {
+      const int64_t o = (int64_t)z * N + i;
+      choice[o] = m;
+      if (chosen_ttft) chosen_ttft[o] = wb.ttft;
+      if (utility && m >= 0) utility[o] = wb.eq2;
+    }
+    const bool more = i + 1 < N;
+    int p1 = 1;
+    if (more) p1 = last_in_block ? uni(nxt.p) : __builtin_amdgcn_readlane(cur.p, l + 1);
+    const bool p1_ok = p1 >= 1 && p1 <= max_prompt;
+    if (more && !p1_ok && threadIdx.x == 0 && cid == 0) set_error(err, kErrArg);
+    c.j = -1; c.u = 0.0; c.ttft = 0.0; c.eq2 = 0.0;
+#pragma unroll
+    for (int r = 0; r < IPW; ++r) {
+      const int j = jbase + r;
+      if (j < I) {
+        const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
+        commit_advance(qs[r], e, j == m, p, dq, tn, S.qcap, max_iters, err);
+        if (more) {
+          const double ttft = p1_ok ? estimate(qs[r], e, p1, tn, reading, max_iters, err)
+                                    : __builtin_nan("");
+          const int l1 = last_in_block ? 0 : l + 1;
+          const double a = read_lane_f64(last_in_block ? nxt.acc[r] : cur.acc[r], l1);
+          const double co = read_lane_f64(last_in_block ? nxt.cost[r] : cur.cost[r], l1);
+          const double eq2 = __dsub_rn(a, __dmul_rn(wc, co));
+          cand_take(c, __dsub_rn(eq2, __dmul_rn(wl, ttft)), j, ttft, eq2);
+        }
+      }
+    }
+    if (last_in_block) {
+      cur = nxt;
+      nxt = fetch_block<IPW>(i + 1 + kWave, N, qp, qd, qt, acc, cost, n_cols, cols);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < IPW; ++r) {
+    const int j = jbase + r;
+    if (j < I) qs[r].store(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
+  }
+}
+
 // ------------------------------------------------------------------ k_stats
 // Orderable key of a binary64 (no NaN): larger key <=> larger value.
 __device__ __forceinline__ uint64_t okey(double v) {
@@ -697,10 +1044,51 @@ static hipError_t launch_trace_mem(const LaunchEnv& env, const TraceArgs& a) {
   return hipGetLastError();
 }
 
+template <int KS, int NW, int IPW>
+static hipError_t launch_trace_lds(const LaunchEnv& env, const TraceArgs& a) {
+  const int nw = (env.I + IPW - 1) / IPW;
+  const size_t lds = sizeof(LdsQueue<KS>) * (size_t)nw * IPW;
+  hipError_t e = hipFuncSetAttribute((const void*)k_trace_lds<KS, NW, IPW>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_trace_lds<KS, NW, IPW>), dim3(env.Z), dim3(nw * kWave), lds,
+                     env.stream, LAR_TRACE_ARGS);
+  return hipGetLastError();
+}
+
+template <int KS, int W, int IPW>
+static hipError_t launch_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
+  const int per_wg = W * IPW;
+  const int G = (env.I + per_wg - 1) / per_wg;
+  if (G > kMaxCluster) return hipErrorInvalidValue;
+  if ((uint64_t)G * (uint64_t)a.N >= (1ull << 32)) return hipErrorInvalidValue;  // counter range
+  const int w_used = G == 1 ? (env.I + IPW - 1) / IPW : W;
+  hipLaunchKernelGGL(k_clear_exchange, dim3((env.Z + 255) / 256), dim3(256), 0, env.stream,
+                     env.xcount, env.Z);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int blocks = 8 * ((env.Z + 7) / 8) * G;
+  hipLaunchKernelGGL((k_trace_cl<KS, W, IPW>), dim3(blocks), dim3(w_used * kWave), 0,
+                     env.stream, LAR_TRACE_ARGS, G, env.xcount, env.xcand);
+  return hipGetLastError();
+}
+
 template <int KS>
 static hipError_t launch_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
-  // Register-resident states (k_trace) spill to scratch at the register budget of a
-  // full workgroup and measured slower than L2-resident states; use the latter.
+  // one or two instances per wave, states in VGPRs, 8 waves per workgroup; the
+  // whole grid must be resident at once (2048 waves: 8 per CU)
+  const int64_t queues = (int64_t)env.Z * env.I;
+  auto fits = [&](int per_wg) {
+    const int64_t G = (env.I + per_wg - 1) / per_wg;
+    return G <= kMaxCluster && (uint64_t)G * (uint64_t)a.N < (1ull << 32);
+  };
+  if (KS <= 4) {
+    if (queues <= 2048 && fits(8)) return launch_trace_cl<KS, 8, 1>(env, a);
+    if (queues <= 4096 && fits(16)) return launch_trace_cl<KS, 8, 2>(env, a);
+  } else if (KS == 8 && queues <= 2048 && fits(8)) {
+    return launch_trace_cl<8, 8, 1>(env, a);
+  }
+  // Otherwise the states stay in HBM (L2) and are loaded per use.
   return launch_trace_mem<KS, (KS <= 4 ? 8 : (KS == 8 ? 8 : 4))>(env, a);
 }
 

@@ -19,7 +19,12 @@ struct LaunchEnv {
   int reading;        // 0: first decode batch, 1: batch completing the prefill
   int32_t* err;       // sticky device error
   hipStream_t stream;
+  // cross-workgroup candidate exchange of the clustered trace kernel
+  uint32_t* xcount;   // [Z] arrival counters (64-byte stride)
+  double* xcand;      // [Z][2][kMaxCluster][4]
 };
+
+constexpr int kMaxCluster = 64;
 
 struct TraceArgs {
   int N;

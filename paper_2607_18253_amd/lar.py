@@ -14,7 +14,8 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "liblar.so")
 
-LAR_OK, LAR_E_ARG, LAR_E_STATE, LAR_E_CAPACITY, LAR_E_ITER, LAR_E_HIP = 0, -1, -2, -3, -4, -5
+LAR_OK, LAR_E_ARG, LAR_E_STATE, LAR_E_CAPACITY, LAR_E_ITER, LAR_E_HIP, LAR_E_SYNC = (
+    0, -1, -2, -3, -4, -5, -6)
 FIRST_TOKEN_DECODE_BATCH, FIRST_TOKEN_PREFILL_BATCH = 0, 1
 
 EXPORTED = ("lar_create", "lar_destroy", "lar_error_string", "lar_load_state", "lar_reload_state",
