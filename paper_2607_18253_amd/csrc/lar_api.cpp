@@ -29,8 +29,7 @@ struct lar_ctx {
   double* pa = nullptr;   // [5][I]: a, b, c, d, e
   int32_t* pi = nullptr;  // [3][I]: B, M, col
   double* row_ttft = nullptr;  // [Z][I] scratch of the sequential trace
-  uint32_t* xcount = nullptr;  // [Z * 16] exchange counters of the clustered trace
-  double* xcand = nullptr;     // [Z][2][kMaxCluster][4] exchanged candidates
+  uint64_t* xslot = nullptr;   // [Z][2][kMaxCluster][4] candidate posts of the clustered trace
   lar::DevState snap{};        // one scenario's copy of the last loaded snapshot
   int32_t* err = nullptr;
   size_t tail_elems = 0;  // allocated K * Z * I
@@ -99,8 +98,7 @@ LaunchEnv env_of(const lar_ctx* ctx) {
   e.reading = ctx->cfg.flags & 1;
   e.err = ctx->err;
   e.stream = ctx->stream;
-  e.xcount = ctx->xcount;
-  e.xcand = ctx->xcand;
+  e.xslot = ctx->xslot;
   return e;
 }
 
@@ -166,8 +164,7 @@ lar_status lar_create(lar_ctx** out, const lar_config* cfg) {
   chk(dev_alloc(ctx, &ctx->T.ok, ZI));
   chk(dev_alloc(ctx, &ctx->row_ttft, ZI));
   chk(dev_alloc(ctx, &ctx->err, 1));
-  chk(dev_alloc(ctx, &ctx->xcount, (size_t)ctx->Z * 16));
-  chk(dev_alloc(ctx, &ctx->xcand, (size_t)ctx->Z * 2 * lar::kMaxCluster * 4));
+  chk(dev_alloc(ctx, &ctx->xslot, (size_t)ctx->Z * 2 * lar::kMaxCluster * 4));
   if (st != LAR_OK) {
     lar_destroy(ctx);
     return st;

@@ -184,9 +184,9 @@ __device__ __forceinline__ int wave_sum32(int x) {
   return uni(x);
 }
 
-// ------------------------------------------------------------------ LDS-resident queues
-// A queue's state kept in LDS between uses by a persistent kernel: decode slots in
-// the register layout (slot s = k*64 + lane), the prefill window, and the scalars.
+// ------------------------------------------------------------------ LDS copies of queues
+// A queue's state kept in LDS by a persistent kernel: decode slots in the register
+// layout (slot s = k*64 + lane), the prefill window, and the scalars.
 template <int KS>
 struct LdsQueue {
   int dl[KS * kWave], dc[KS * kWave], ds[KS * kWave];
@@ -262,7 +262,7 @@ struct Queue {
     refill(e);
   }
 
-  // Copy to / from an LDS mirror (same layout as the registers).
+  // Copy to / from an LDS copy (same layout as the registers).
   __device__ void to_lds(LdsQueue<KS>& L) const {
     const int ln = lane_id();
 #pragma unroll
@@ -275,10 +275,12 @@ struct Queue {
       L.next_seq = next_seq; L.woff = woff; L.nwin = nwin; L.c0sum = c0sum;
       L.pre_sum = pre_sum; L.iters = iters; L.clock = clock;
     }
+    __builtin_amdgcn_wave_barrier();
   }
 
   __device__ void from_lds(const LdsQueue<KS>& L) {
     const int ln = lane_id();
+    __builtin_amdgcn_wave_barrier();
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       dl[s] = L.dl[s * kWave + ln]; dc[s] = L.dc[s * kWave + ln]; ds[s] = L.ds[s * kWave + ln];

@@ -204,7 +204,7 @@ __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double
     const int j2 = __shfl_xor(bj, o, kWave);
     if (better(u2, j2, bu, bj)) { bu = u2; bj = j2; }
   }
-  const int wid = threadIdx.x / kWave;
+  const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
   if (lane_id() == 0) { s_u[wid] = bu; s_j[wid] = bj; }
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -422,7 +422,7 @@ __device__ __forceinline__ int trace_pick(double bu, int bj, double bt, double b
                                           int N, int32_t* choice, double* chosen_ttft,
                                           double* utility, double (*s_u)[NW], double (*s_t)[NW],
                                           double (*s_q)[NW], int (*s_j)[NW]) {
-  const int wid = threadIdx.x / kWave;
+  const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
   const int nw = blockDim.x / kWave;
   const int buf = i & 1;
   if (lane_id() == 0) { s_u[buf][wid] = bu; s_j[buf][wid] = bj; s_t[buf][wid] = bt; s_q[buf][wid] = bq; }
@@ -448,68 +448,6 @@ __device__ __forceinline__ int trace_pick(double bu, int bj, double bt, double b
       const double *w_cost, const double *w_lat, int reading, int max_prompt,                \
       int64_t max_iters, int32_t *choice, double *chosen_ttft, double *utility, int32_t *err
 
-// The whole sequential trace in one launch: one workgroup per scenario, wave w owning
-// instances j = w*IPW + r (r < IPW), their states resident in VGPRs for the whole
-// trace.  Per query: SFS estimate at every owned instance, wave and workgroup argmax
-// of the Lagrangian utility, append to the chosen instance, replay every instance to
-// the next arrival -- identical, operation for operation, to estimate + route +
-// commit per query.
-template <int KS, int NW, int IPW>
-__global__ __launch_bounds__(NW * kWave) void k_trace(LAR_TRACE_PARAMS) {
-  __shared__ double s_u[2][NW], s_t[2][NW], s_q[2][NW];
-  __shared__ int s_j[2][NW];
-  __shared__ int stage[NW][3 * kWave];
-  const int z = blockIdx.x;
-  const int wid = threadIdx.x / kWave;
-  const int ln = lane_id();
-  const double wc = w_cost[z];
-  const double wl = w_lat[z];
-  const int j_l = wid * IPW + ln;            // this lane's owned instance (lane < IPW)
-  const bool own_l = ln < IPW && j_l < I;
-  const int col_l = own_l ? pr.col[j_l] : 0;
-  Queue<KS> qs[IPW];
-#pragma unroll
-  for (int r = 0; r < IPW; ++r) {
-    const int j = wid * IPW + r;
-    if (j < I) qs[r].load(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
-  }
-  QueryIn nx = fetch_query(0, N, qp, qd, qt, t_after, acc, cost, n_cols, col_l, own_l);
-  for (int i = 0; i < N; ++i) {
-    const QueryIn q = nx;
-    nx = fetch_query(i + 1, N, qp, qd, qt, t_after, acc, cost, n_cols, col_l, own_l);
-    const bool p_ok = q.p >= 1 && q.p <= max_prompt;
-    if (!p_ok && threadIdx.x == 0) set_error(err, kErrArg);
-    double bu = 0.0, bt = 0.0, bq = 0.0;
-    int bj = -1;
-#pragma unroll
-    for (int r = 0; r < IPW; ++r) {
-      const int j = wid * IPW + r;
-      if (j < I) {
-        const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
-        const double ttft = p_ok ? estimate(qs[r], e, q.p, q.t, reading, max_iters, err)
-                                 : __builtin_nan("");
-        double eq2;
-        const double u = utility_lane(q, r, wc, wl, ttft, &eq2);
-        if (bj < 0 || u > bu) { bu = u; bj = j; bt = ttft; bq = eq2; }
-      }
-    }
-    const int m = trace_pick<NW>(bu, bj, bt, bq, i, z, N, choice, chosen_ttft, utility, s_u,
-                                 s_t, s_q, s_j);
-#pragma unroll
-    for (int r = 0; r < IPW; ++r) {
-      const int j = wid * IPW + r;
-      if (j < I)
-        commit_advance(qs[r], make_env(S, pr, z * I + j, j, stage[wid]), j == m, q.p, q.d,
-                       q.tn, S.qcap, max_iters, err);
-    }
-  }
-#pragma unroll
-  for (int r = 0; r < IPW; ++r) {
-    const int j = wid * IPW + r;
-    if (j < I) qs[r].store(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
-  }
-}
-
 // The same trace for pools too large to keep in registers: each owned instance's
 // state is loaded from HBM (L2) when it is needed and written back after its commit.
 // Wave w owns instances j = w + v*nw; lane v holds the inputs of the v-th one.
@@ -519,7 +457,7 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
   __shared__ int s_j[2][NW];
   __shared__ int stage[NW][3 * kWave];
   const int z = blockIdx.x;
-  const int wid = threadIdx.x / kWave;
+  const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
   const int nw = blockDim.x / kWave;
   const int ln = lane_id();
   const double wc = w_cost[z];
@@ -596,282 +534,402 @@ __device__ __forceinline__ void cand_take(Cand& c, double u, int j, double ttft,
   if (c.j < 0 || u > c.u) { c.u = u; c.j = j; c.ttft = ttft; c.eq2 = eq2; }
 }
 
-// The whole sequential trace in one launch with every instance state resident in
-// LDS: one workgroup per scenario, wave w owning instances j = w*IPW + r.  Per
-// query and owned instance the state is read from LDS once: the commit of query i
-// (append when chosen, replay to t_{i+1}) and the estimate of query i+1 run on the
-// same registers; one barrier per query publishes the waves' candidates.
-// Identical, operation for operation, to estimate + route + commit per query.
-template <int KS, int NW, int IPW>
-__global__ __launch_bounds__(NW * kWave) void k_trace_lds(LAR_TRACE_PARAMS) {
-  extern __shared__ __align__(16) unsigned char lds_raw[];
-  LdsQueue<KS>* lq = reinterpret_cast<LdsQueue<KS>*>(lds_raw);   // [NW * IPW]
-  __shared__ double s_u[2][NW], s_t[2][NW], s_q[2][NW];
-  __shared__ int s_j[2][NW];
-  __shared__ int stage[NW][3 * kWave];
-  const int z = blockIdx.x;
-  const int wid = threadIdx.x / kWave;
-  const int nw = blockDim.x / kWave;
-  const int ln = lane_id();
-  const double wc = w_cost[z];
-  const double wl = w_lat[z];
-  int cols[IPW];
-#pragma unroll
-  for (int r = 0; r < IPW; ++r) {
-    const int j = wid * IPW + r;
-    cols[r] = j < I ? pr.col[j] : -1;
-    if (j < I) {
-      const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
-      Queue<KS> w;
-      w.load(S, e, z * I + j);
-      w.to_lds(lq[wid * IPW + r]);
-    }
-  }
-  QueryBlock<IPW> cur = fetch_block<IPW>(0, N, qp, qd, qt, acc, cost, n_cols, cols);
-  QueryBlock<IPW> nxt = fetch_block<IPW>(kWave, N, qp, qd, qt, acc, cost, n_cols, cols);
-  // candidate of query 0
-  Cand c;
-  c.j = -1; c.u = 0.0; c.ttft = 0.0; c.eq2 = 0.0;
-  {
-    const int p = uni(cur.p);
-    const double t = read_lane_f64(cur.t, 0);
-    const bool p_ok = p >= 1 && p <= max_prompt;
-    if (!p_ok && threadIdx.x == 0) set_error(err, kErrArg);
-#pragma unroll
-    for (int r = 0; r < IPW; ++r) {
-      const int j = wid * IPW + r;
-      if (j < I) {
-        const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
-        Queue<KS> w;
-        w.from_lds(lq[wid * IPW + r]);
-        const double ttft = p_ok ? estimate(w, e, p, t, reading, max_iters, err)
-                                 : __builtin_nan("");
-        const double a = read_lane_f64(cur.acc[r], 0), co = read_lane_f64(cur.cost[r], 0);
-        const double eq2 = __dsub_rn(a, __dmul_rn(wc, co));
-        cand_take(c, __dsub_rn(eq2, __dmul_rn(wl, ttft)), j, ttft, eq2);
-      }
-    }
-  }
-  for (int i = 0; i < N; ++i) {
-    const int l = i & (kWave - 1);
-    // inputs of query i (in cur) and i + 1 (in cur or nxt)
-    const int p = __builtin_amdgcn_readlane(cur.p, l);
-    const int dq = __builtin_amdgcn_readlane(cur.d, l);
-    double tn;
-    const bool last_in_block = l == kWave - 1;
-    if (i + 1 >= N) tn = t_after;
-    else tn = last_in_block ? read_lane_f64(nxt.t, 0) : read_lane_f64(cur.t, l + 1);
-    // publish candidates, pick the winner (one barrier; LDS double-buffered)
-    const int buf = i & 1;
-    if (ln == 0) { s_u[buf][wid] = c.u; s_j[buf][wid] = c.j; s_t[buf][wid] = c.ttft; s_q[buf][wid] = c.eq2; }
-    __syncthreads();
-    double mu = s_u[buf][0], mt = s_t[buf][0], mq = s_q[buf][0];
-    int m = s_j[buf][0];
-    for (int v = 1; v < nw; ++v)
-      if (better(s_u[buf][v], s_j[buf][v], mu, m)) {
-        mu = s_u[buf][v]; m = s_j[buf][v]; mt = s_t[buf][v]; mq = s_q[buf][v];
-      }
-    if (threadIdx.x == 0) {
-      const int64_t o = (int64_t)z * N + i;
-      choice[o] = m;
-      if (chosen_ttft) chosen_ttft[o] = mt;
-      if (utility && m >= 0) utility[o] = mq;
-    }
-    // next query's inputs
-    const bool more = i + 1 < N;
-    int p1 = 1;
-    double t1 = 0.0;
-    if (more) {
-      p1 = last_in_block ? uni(nxt.p) : __builtin_amdgcn_readlane(cur.p, l + 1);
-      t1 = tn;
-    }
-    const bool p1_ok = p1 >= 1 && p1 <= max_prompt;
-    if (more && !p1_ok && threadIdx.x == 0) set_error(err, kErrArg);
-    c.j = -1; c.u = 0.0; c.ttft = 0.0; c.eq2 = 0.0;
-#pragma unroll
-    for (int r = 0; r < IPW; ++r) {
-      const int j = wid * IPW + r;
-      if (j < I) {
-        const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
-        Queue<KS> w;
-        w.from_lds(lq[wid * IPW + r]);
-        commit_advance(w, e, j == m, p, dq, tn, S.qcap, max_iters, err);
-        if (more) {
-          const double ttft = p1_ok ? estimate(w, e, p1, t1, reading, max_iters, err)
-                                    : __builtin_nan("");
-          const int l1 = last_in_block ? 0 : l + 1;
-          const double a = read_lane_f64(last_in_block ? nxt.acc[r] : cur.acc[r], l1);
-          const double co = read_lane_f64(last_in_block ? nxt.cost[r] : cur.cost[r], l1);
-          const double eq2 = __dsub_rn(a, __dmul_rn(wc, co));
-          cand_take(c, __dsub_rn(eq2, __dmul_rn(wl, ttft)), j, ttft, eq2);
-        }
-        w.to_lds(lq[wid * IPW + r]);
-      }
-    }
-    if (last_in_block) {
-      cur = nxt;
-      nxt = fetch_block<IPW>(i + 1 + kWave, N, qp, qd, qt, acc, cost, n_cols, cols);
-    }
-  }
-#pragma unroll
-  for (int r = 0; r < IPW; ++r) {
-    const int j = wid * IPW + r;
-    if (j < I) {
-      const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
-      Queue<KS> w;
-      w.from_lds(lq[wid * IPW + r]);
-      w.store(S, e, z * I + j);
-    }
-  }
-}
-
-// Candidate exchange between the workgroups of one scenario: each workgroup posts
-// its best candidate for query i into slot (i & 1) and bumps the scenario's arrival
-// counter (release, agent scope); all wait until the counter reaches G * (i + 1)
-// (acquire) and reduce the G posts in the same total order.  The wait is bounded in
-// wall time (s_memrealtime, 100 MHz): after kSpinTicks it flags kErrSync and gives
-// up, and every other member leaves as soon as it sees that flag, so a cluster whose
-// workgroups cannot all be resident terminates instead of hanging.
+// Candidate exchange between the workgroups of one scenario, run by one wave of
+// each.  Lane 0 posts the workgroup's best (utility, instance) for query i as three
+// 64-bit words -- low and high half of the utility's bits, and the instance index --
+// each carrying the tag i + 1 in its upper 32 bits, into slot set (i & 1).  Lane v
+// polls post v until all three of its words carry the tag, so a post is taken only
+// when it is whole, and the G posts arrive together with the poll: no counter, no
+// fence, one round trip after the last member posts.  All accesses are relaxed
+// agent-scope atomics on the same words, which the memory model keeps coherent.
+// The wait is bounded in wall-clock time (s_memrealtime runs at 100 MHz): a member
+// that never posts, or an error raised by another member, ends the trace with
+// kErrSync instead of a hang.  Two slot sets suffice: a member posts query i + 2
+// only after every member has posted i + 1, i.e. has finished reading the posts of i.
 constexpr uint64_t kSpinTicks = 1000000000ull;   // 10 s
 
-__device__ __forceinline__ bool cluster_exchange(Cand& c, int i, int G, int cid,
-                                                 uint32_t* cnt, double* xc, int32_t* err) {
-  double* slot = xc + ((int64_t)(i & 1) * kMaxCluster + cid) * 4;
-  slot[0] = c.u;
-  slot[1] = (double)c.j;
-  slot[2] = c.ttft;
-  slot[3] = c.eq2;
-  __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-  const uint32_t target = (uint32_t)G * (uint32_t)(i + 1);
+__device__ __forceinline__ bool cluster_exchange(double& u, int& j, int i, int G, int cid,
+                                                 uint64_t* xs, int32_t* err) {
+  const int ln = lane_id();
+  uint64_t* base = xs + (int64_t)(i & 1) * kMaxCluster * 4;
+  const uint32_t tag = (uint32_t)(i + 1);
+  if (ln == 0) {
+    const uint64_t ub = (uint64_t)__double_as_longlong(u);
+    const uint64_t hi = (uint64_t)tag << 32;
+    uint64_t* sl = base + cid * 4;
+    __hip_atomic_store(sl + 0, hi | (ub & 0xffffffffull), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(sl + 1, hi | (ub >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(sl + 2, hi | (uint32_t)j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  uint64_t w0 = 0, w1 = 0, w2 = 0;
+  bool ready = ln >= G;
   const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-  while (__hip_atomic_load(cnt, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target) {
-    if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == kErrSync ||
-        __builtin_amdgcn_s_memrealtime() - t0 > kSpinTicks) {
-      set_error(err, kErrSync);
+  for (;;) {
+    if (!ready) {
+      const uint64_t* o = base + ln * 4;
+      w0 = __hip_atomic_load(o + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      w1 = __hip_atomic_load(o + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      w2 = __hip_atomic_load(o + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      ready = (uint32_t)(w0 >> 32) == tag && (uint32_t)(w1 >> 32) == tag &&
+              (uint32_t)(w2 >> 32) == tag;
+    }
+    if (ballot(!ready) == 0) break;
+    int bad = 0;
+    if (ln == 0)
+      bad = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == kErrSync ||
+            __builtin_amdgcn_s_memrealtime() - t0 > kSpinTicks;
+    if (__builtin_amdgcn_readlane(bad, 0)) {
+      if (ln == 0) set_error(err, kErrSync);
       return false;
     }
     __builtin_amdgcn_s_sleep(1);
   }
-  Cand b;
-  b.j = -1; b.u = 0.0; b.ttft = 0.0; b.eq2 = 0.0;
-  for (int v = 0; v < G; ++v) {
-    const double* o = xc + ((int64_t)(i & 1) * kMaxCluster + v) * 4;
-    const double u = __hip_atomic_load(o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int j = (int)__hip_atomic_load(o + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (better(u, j, b.u, b.j)) {
-      b.u = u;
-      b.j = j;
-      b.ttft = __hip_atomic_load(o + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      b.eq2 = __hip_atomic_load(o + 3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+  double bu = 0.0;
+  int bj = -1;
+  if (ln < G) {
+    bu = __longlong_as_double((long long)((w0 & 0xffffffffull) | (w1 << 32)));
+    bj = (int)(uint32_t)w2;
   }
-  c = b;
+  for (int m = 1; m < G; m <<= 1) {   // lanes [G, 2^ceil(log2 G)) hold no candidate
+    const double xu = __shfl_xor(bu, m, kWave);
+    const int xj = __shfl_xor(bj, m, kWave);
+    if (better(xu, xj, bu, bj)) { bu = xu; bj = xj; }
+  }
+  u = read_lane_f64(bu, 0);
+  j = __builtin_amdgcn_readlane(bj, 0);
   return true;
 }
 
-__global__ void k_clear_exchange(uint32_t* cnt, int n) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) cnt[i * 16] = 0u;
+// Clears the exchange posts (tags included) of every scenario before a trace.
+__global__ void k_clear_exchange(uint64_t* xs, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) xs[i] = 0;
+}
+
+// ------------------------------------------------------------------ frontier cache
+// For a queue whose next batch would not admit a new tail query (a backlog), the
+// state F at the admission point of such a query does not depend on the query (the
+// query is last in FCFS order), and neither do the clock folded up to F, the
+// background features of the admission batch, or the decode-only batches after it.
+// The cache keeps F in LDS and those values in registers (tail batch k in lane
+// k - 1), so an estimate is a short fold over them.  F stays valid while the world
+// has not run past it; when the queue receives a query, F + query is walked to its
+// next admission point (again exact by the FCFS argument).
+struct FCache {
+  bool valid;
+  int g;           // batch counter of F
+  double E;        // clock folded up to F
+  int aP, aD, left;
+  int64_t aC, aA;  // admission-batch background features
+  int tD;          // lane k: decode tokens of tail batch k + 1
+  int64_t tC;      // lane k: their context sum
+};
+
+__device__ __forceinline__ int64_t read_lane_i64(int64_t v, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(uint64_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), l);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Summary of the admission batch of w (which must satisfy tail_admitted_next).
+template <int KS>
+__device__ __forceinline__ void admission_summary(FCache& fc, const Queue<KS>& w, const QEnv& e,
+                                                  double E) {
+  fc.g = w.g;
+  fc.E = E;
+  fc.aP = (int)w.pre_sum;
+  fc.aD = w.n_dec;
+  fc.aC = e.need_C ? w.c0sum + (int64_t)w.n_dec * w.g : 0;
+  fc.aA = e.need_A ? w.pre_attention_all(e) : 0;
+  fc.left = e.k.B - fc.aD - fc.aP;
+}
+
+// Record the decode-only tail read-only from w (whole prefill list in the window).
+template <int KS>
+__device__ __forceinline__ void tail_readonly(FCache& fc, const Queue<KS>& w, const QEnv& e,
+                                              int kmax) {
+  const int ln = lane_id();
+  typename Queue<KS>::Tail tl = w.tail_begin(e);
+  for (int k = 0; k < kmax; ++k) {
+    const int64_t C = e.need_C ? tl.c0 + tl.D * (int64_t)(w.g + tl.k) : 0;
+    if (ln == k) { fc.tD = (int)tl.D; fc.tC = C; }
+    w.tail_next(e, tl);
+  }
+}
+
+// One visit of a wave to one owned queue for one query: append the query if it was
+// routed here, replay to tn, and keep the frontier cache in step.  Every batch --
+// replayed, walked to a new admission point, or recorded as tail -- runs through the
+// single Queue::step / quiet_run below, on the working copy wk.
+template <int KS>
+__device__ __forceinline__ void visit(Queue<KS>& S, FCache& fc, Queue<KS>& wk, const QEnv& e,
+                                      bool chosen, int p, int d, double tn, int qcap, int kmax,
+                                      int64_t max_iters, int32_t* err, LdsQueue<KS>& F) {
+  const int ln = lane_id();
+  bool joined = false;
+  if (chosen) {
+    d = d < 1 ? 1 : d;
+    if (p < 1) {
+      if (ln == 0) set_error(err, kErrArg);
+    } else if (S.n_pre - S.n_part + 1 > qcap) {
+      if (ln == 0) set_error(err, kErrCapacity);
+    } else {
+      S.append(e, p, d);
+      joined = true;
+    }
+  }
+  enum { kReplay, kWalk, kTail };
+  int phase = kReplay;
+  wk = S;
+  double clk = wk.clock;
+  double stop_t = tn;
+  int64_t n = 0;
+  int kk = -1;
+  for (;;) {
+    bool stop;
+    if (phase == kReplay) {
+      stop = !(wk.resident() > 0 && clk < stop_t);
+      if (!stop && n == max_iters) {
+        if (ln == 0) set_error(err, kErrIter);
+        stop = true;
+      }
+    } else if (phase == kWalk) {
+      stop = wk.tail_admitted_next(e) || n == max_iters;
+    } else {
+      stop = kk == kmax;
+    }
+    if (stop) {
+      if (phase == kReplay) {
+        if (wk.resident() == 0 && clk < stop_t) clk = stop_t;
+        wk.clock = clk;
+        wk.iters += n;
+        S = wk;
+        // the world ran the admission batch, or sat idle at F and its clock jumped
+        if (fc.valid && (S.g > fc.g || (S.g == fc.g && S.clock != fc.E))) fc.valid = false;
+        if (joined && fc.valid) {
+          wk.from_lds(F);
+          wk.append(e, p, d);
+          clk = fc.E;
+        } else if (!fc.valid) {
+          S.refill(e);
+          wk.refill(e);
+          if (S.tail_admitted_next(e) && S.nwin == S.n_pre) break;   // estimate from S directly
+          clk = S.clock;
+        } else {
+          break;
+        }
+        phase = kWalk;
+        stop_t = __builtin_inf();
+        n = 0;
+        continue;
+      }
+      if (phase == kWalk) {
+        if (!wk.tail_admitted_next(e)) {   // the cap ran out
+          fc.valid = false;
+          if (ln == 0) set_error(err, kErrIter);
+          break;
+        }
+        wk.refill(e);
+        admission_summary(fc, wk, e, clk);
+        fc.valid = true;
+        wk.to_lds(F);
+        if (wk.nwin == wk.n_pre) {
+          tail_readonly(fc, wk, e, kmax);
+          break;
+        }
+        phase = kTail;   // step the admission batch, then record kmax decode-only batches
+        kk = -1;
+        continue;
+      }
+      break;
+    }
+    if (phase != kTail && wk.quiet(e)) {
+      // a quiet run ends before the batch in which a decode finishes (or at the stop
+      // time or the cap); that batch is then stepped below
+      n += wk.quiet_run(e, clk, stop_t, n, max_iters);
+      if (!(clk < stop_t) || n == max_iters) continue;
+    }
+    const StepOut o = wk.step(e);
+    if (phase != kTail) {
+      clk = __dadd_rn(clk, batch_time(e.k, o.P, o.D, o.C, o.A));
+      ++n;
+    } else {
+      if (kk >= 0 && ln == kk) { fc.tD = o.D; fc.tC = o.C; }
+      ++kk;
+    }
+  }
+}
+
+// SFS estimate of a query (p tokens, arrival t) from the admission batch summary and
+// the decode-only tail: from the cache (tail in lanes) or, when S admits the query
+// in its very next batch, read-only from S.
+template <int KS>
+__device__ __forceinline__ double estimate_visit(const FCache& fc, const Queue<KS>& S,
+                                                 const QEnv& e, int p, double t, int reading,
+                                                 int kmax, int64_t max_iters, int32_t* err) {
+  const int ln = lane_id();
+  if (S.clock < t) {
+    if (ln == 0) set_error(err, kErrState);
+    return __builtin_nan("");
+  }
+  const Coef& k = e.k;
+  double E;
+  int64_t it;
+  int aP, aD, left;
+  int64_t aC, aA;
+  const bool cached = fc.valid;
+  if (!cached && !S.tail_admitted_next(e)) return __builtin_nan("");   // error already set
+  if (cached) {
+    E = fc.E; it = (int64_t)(fc.g - S.g) + 1;
+    aP = fc.aP; aD = fc.aD; left = fc.left; aC = fc.aC; aA = fc.aA;
+  } else {
+    E = S.clock; it = 1;
+    aP = (int)S.pre_sum; aD = S.n_dec; left = k.B - aD - aP;
+    aC = e.need_C ? S.c0sum + (int64_t)aD * S.g : 0;
+    aA = e.need_A ? S.pre_attention_all(e) : 0;
+  }
+  const int ch = p < left ? p : left;
+  E = __dadd_rn(E, batch_time(k, aP + ch, aD, aC, aA + (int64_t)ch * (ch + 1) / 2));
+  int rem = p - ch;
+  int64_t cxq = ch;
+  bool done = reading == 1 && rem == 0;
+  typename Queue<KS>::Tail tl{};
+  if (!cached && !done) tl = S.tail_begin(e);
+  int kk = 0;
+  while (!done) {
+    int Dk;
+    int64_t Ck;
+    if (cached) {
+      if (kk >= kmax) {   // more tail batches than recorded (kmax bounds every prompt)
+        if (ln == 0) set_error(err, kErrIter);
+        return __builtin_nan("");
+      }
+      Dk = __builtin_amdgcn_readlane(fc.tD, kk);
+      Ck = read_lane_i64(fc.tC, kk);
+    } else {
+      Dk = (int)tl.D;
+      Ck = e.need_C ? tl.c0 + (int64_t)Dk * (S.g + tl.k) : 0;
+    }
+    if (rem > 0) {
+      const int room = k.B - Dk;
+      const int c2 = rem < room ? rem : room;
+      E = __dadd_rn(E, batch_time(k, c2, Dk, Ck, (int64_t)c2 * cxq + (int64_t)c2 * (c2 + 1) / 2));
+      rem -= c2;
+      cxq += c2;
+      done = reading == 1 && rem == 0;
+    } else {
+      E = __dadd_rn(E, batch_time(k, 0, Dk + 1, Ck + cxq, 0));
+      done = true;
+    }
+    ++kk;
+    ++it;
+    if (!done && !cached) S.tail_next(e, tl);
+  }
+  if (it > max_iters && ln == 0) set_error(err, kErrIter);
+  return __dsub_rn(E, t);
 }
 
 // The whole sequential trace with each wave owning IPW instances whose states stay
 // in VGPRs for the whole trace.  A scenario spans G workgroups of W waves; block b
 // serves scenario z = (b / 8 / G) * 8 + b % 8 as cluster member (b / 8) % G, so the
 // members of a scenario share one XCD (blocks are dispatched to the 8 XCDs
-// round-robin) and exchange through that XCD's L2.  Per query: the estimate of every
-// owned instance (computed right after the previous commit), the workgroup argmax
-// (LDS, one barrier), the cluster argmax (global exchange, when G > 1), the commit
-// and replay of every owned instance, and the estimate of the next query.
+// round-robin) and exchange through that XCD's L2.  Iteration i (from -1): the
+// workgroup argmax (LDS, one barrier) and the cluster argmax (global exchange, when
+// G > 1) of query i, then per owned instance one visit (commit of query i, replay,
+// frontier cache) and the estimate of query i + 1.
 // Identical, operation for operation, to estimate + route + commit per query.
 template <int KS, int W, int IPW>
-__global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G, uint32_t* xcount,
-                                                        double* xcand) {
-  __shared__ double s_u[2][W], s_t[2][W], s_q[2][W];
+__global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G, uint64_t* xslot,
+                                                        int tail_k) {
+  __shared__ double s_u[2][W];
   __shared__ int s_j[2][W];
-  __shared__ double s_m[2][4];
+  __shared__ double s_mu[2];
+  __shared__ int s_mj[2];
   __shared__ int stage[W][3 * kWave];
+  __shared__ LdsQueue<KS> fst[W][IPW];   // frontier states
   const int b = blockIdx.x;
   const int z = (b / 8 / G) * 8 + b % 8;
   const int cid = (b / 8) % G;
   if (z >= Z) return;
-  const int wid = threadIdx.x / kWave;
+  const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
   const int nw = blockDim.x / kWave;   // waves launched (<= W)
   const int ln = lane_id();
   const double wc = w_cost[z];
   const double wl = w_lat[z];
-  uint32_t* cnt = xcount + (int64_t)z * 16;
-  double* xc = xcand + (int64_t)z * 2 * kMaxCluster * 4;
+  uint64_t* xs = xslot + (int64_t)z * 2 * kMaxCluster * 4;
   const int jbase = (cid * W + wid) * IPW;
+  const int kmax = tail_k;   // <= 64, checked at launch
   int cols[IPW];
   Queue<KS> qs[IPW];
+  FCache fc[IPW];
+  Queue<KS> wk;   // working copy
 #pragma unroll
   for (int r = 0; r < IPW; ++r) {
     const int j = jbase + r;
     cols[r] = j < I ? pr.col[j] : -1;
+    fc[r].valid = false;
+    fc[r].tD = 0;
+    fc[r].tC = 0;
     if (j < I) qs[r].load(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
   }
   QueryBlock<IPW> cur = fetch_block<IPW>(0, N, qp, qd, qt, acc, cost, n_cols, cols);
   QueryBlock<IPW> nxt = fetch_block<IPW>(kWave, N, qp, qd, qt, acc, cost, n_cols, cols);
   Cand c;
   c.j = -1; c.u = 0.0; c.ttft = 0.0; c.eq2 = 0.0;
-  {
-    const int p = uni(cur.p);
-    const double t = read_lane_f64(cur.t, 0);
-    const bool p_ok = p >= 1 && p <= max_prompt;
-    if (!p_ok && threadIdx.x == 0 && cid == 0) set_error(err, kErrArg);
-#pragma unroll
-    for (int r = 0; r < IPW; ++r) {
-      const int j = jbase + r;
-      if (j < I) {
-        const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
-        const double ttft = p_ok ? estimate(qs[r], e, p, t, reading, max_iters, err)
-                                 : __builtin_nan("");
-        const double a = read_lane_f64(cur.acc[r], 0), co = read_lane_f64(cur.cost[r], 0);
-        const double eq2 = __dsub_rn(a, __dmul_rn(wc, co));
-        cand_take(c, __dsub_rn(eq2, __dmul_rn(wl, ttft)), j, ttft, eq2);
-      }
-    }
-  }
-  bool alive = true;
-  for (int i = 0; i < N && alive; ++i) {
+  for (int i = -1; i < N; ++i) {
+    // inputs of query i (if any) and of query i + 1
     const int l = i & (kWave - 1);
-    const int p = __builtin_amdgcn_readlane(cur.p, l);
-    const int dq = __builtin_amdgcn_readlane(cur.d, l);
-    const bool last_in_block = l == kWave - 1;
-    double tn;
-    if (i + 1 >= N) tn = t_after;
-    else tn = last_in_block ? read_lane_f64(nxt.t, 0) : read_lane_f64(cur.t, l + 1);
-    // workgroup argmax
-    const int buf = i & 1;
-    if (ln == 0) { s_u[buf][wid] = c.u; s_j[buf][wid] = c.j; s_t[buf][wid] = c.ttft; s_q[buf][wid] = c.eq2; }
-    __syncthreads();
-    Cand wb;
-    wb.u = s_u[buf][0]; wb.j = s_j[buf][0]; wb.ttft = s_t[buf][0]; wb.eq2 = s_q[buf][0];
-    for (int v = 1; v < nw; ++v)
-      if (better(s_u[buf][v], s_j[buf][v], wb.u, wb.j)) {
-        wb.u = s_u[buf][v]; wb.j = s_j[buf][v]; wb.ttft = s_t[buf][v]; wb.eq2 = s_q[buf][v];
-      }
-    if (G > 1) {
-      // one thread exchanges with the other workgroups, then broadcasts the winner
-      if (threadIdx.x == 0) {
-        const bool ok = cluster_exchange(wb, i, G, cid, cnt, xc, err);
-        s_m[buf][0] = wb.u; s_m[buf][1] = (double)wb.j; s_m[buf][2] = wb.ttft; s_m[buf][3] = wb.eq2;
-        if (!ok) s_m[buf][1] = -2.0;
-      }
+    const bool last_in_block = i >= 0 && l == kWave - 1;
+    int p = 1, dq = 1, m = -1;
+    double tn = -__builtin_inf();
+    if (i >= 0) {
+      p = __builtin_amdgcn_readlane(cur.p, l);
+      dq = __builtin_amdgcn_readlane(cur.d, l);
+      if (i + 1 >= N) tn = t_after;
+      else tn = last_in_block ? read_lane_f64(nxt.t, 0) : read_lane_f64(cur.t, l + 1);
+      // workgroup argmax
+      const int buf = i & 1;
+      if (ln == 0) { s_u[buf][wid] = c.u; s_j[buf][wid] = c.j; }
       __syncthreads();
-      wb.u = s_m[buf][0]; wb.j = (int)s_m[buf][1]; wb.ttft = s_m[buf][2]; wb.eq2 = s_m[buf][3];
-      if (wb.j == -2) { alive = false; break; }
-    }
-    const int m = wb.j;
-    if (threadIdx.x == 0 && cid == 0) {
-      const int64_t o = (int64_t)z * N + i;
-      choice[o] = m;
-      if (chosen_ttft) chosen_ttft[o] = wb.ttft;
-      if (utility && m >= 0) utility[o] = wb.eq2;
+      double bu = s_u[buf][0];
+      int bj = s_j[buf][0];
+      for (int v = 1; v < nw; ++v)
+        if (better(s_u[buf][v], s_j[buf][v], bu, bj)) { bu = s_u[buf][v]; bj = s_j[buf][v]; }
+      if (G > 1) {
+        // wave 0 exchanges with the other workgroups, then broadcasts the winner
+        if (wid == 0) {
+          const bool ok = cluster_exchange(bu, bj, i, G, cid, xs, err);
+          if (ln == 0) { s_mu[buf] = bu; s_mj[buf] = ok ? bj : -2; }
+        }
+        __syncthreads();
+        bu = s_mu[buf];
+        bj = s_mj[buf];
+        if (bj == -2) break;
+      }
+      m = bj;
+      // the wave holding the winner (its own best) writes the outputs
+      const bool mine = m >= 0 ? c.j == m : (cid == 0 && wid == 0);
+      if (mine && ln == 0) {
+        const int64_t o = (int64_t)z * N + i;
+        choice[o] = m;
+        if (chosen_ttft) chosen_ttft[o] = c.ttft;
+        if (utility && m >= 0) utility[o] = c.eq2;
+      }
     }
     const bool more = i + 1 < N;
     int p1 = 1;
-    if (more) p1 = last_in_block ? uni(nxt.p) : __builtin_amdgcn_readlane(cur.p, l + 1);
+    double t1 = 0.0;
+    int l1 = 0;
+    bool in_nxt = false;
+    if (more) {
+      if (i < 0) { p1 = uni(cur.p); t1 = read_lane_f64(cur.t, 0); }
+      else {
+        in_nxt = last_in_block;
+        l1 = last_in_block ? 0 : l + 1;
+        p1 = last_in_block ? uni(nxt.p) : __builtin_amdgcn_readlane(cur.p, l + 1);
+        t1 = tn;
+      }
+    }
     const bool p1_ok = p1 >= 1 && p1 <= max_prompt;
     if (more && !p1_ok && threadIdx.x == 0 && cid == 0) set_error(err, kErrArg);
     c.j = -1; c.u = 0.0; c.ttft = 0.0; c.eq2 = 0.0;
@@ -880,13 +938,14 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
       const int j = jbase + r;
       if (j < I) {
         const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
-        commit_advance(qs[r], e, j == m, p, dq, tn, S.qcap, max_iters, err);
+        visit(qs[r], fc[r], wk, e, i >= 0 && j == m, p, dq, tn, S.qcap, kmax, max_iters, err,
+              fst[wid][r]);
         if (more) {
-          const double ttft = p1_ok ? estimate(qs[r], e, p1, tn, reading, max_iters, err)
+          const double ttft = p1_ok ? estimate_visit(fc[r], qs[r], e, p1, t1, reading, kmax,
+                                                     max_iters, err)
                                     : __builtin_nan("");
-          const int l1 = last_in_block ? 0 : l + 1;
-          const double a = read_lane_f64(last_in_block ? nxt.acc[r] : cur.acc[r], l1);
-          const double co = read_lane_f64(last_in_block ? nxt.cost[r] : cur.cost[r], l1);
+          const double a = read_lane_f64(in_nxt ? nxt.acc[r] : cur.acc[r], l1);
+          const double co = read_lane_f64(in_nxt ? nxt.cost[r] : cur.cost[r], l1);
           const double eq2 = __dsub_rn(a, __dmul_rn(wc, co));
           cand_take(c, __dsub_rn(eq2, __dmul_rn(wl, ttft)), j, ttft, eq2);
         }
@@ -1026,15 +1085,6 @@ static hipError_t launch_commit_ks(const LaunchEnv& env, const int32_t* choice,
       a.w_cost, a.w_lat, env.reading, env.max_prompt, env.max_iters, a.choice, a.chosen_ttft, \
       a.utility, env.err
 
-// Register-resident trace: NW waves x IPW instances per wave must cover I.
-template <int KS, int NW, int IPW>
-static hipError_t launch_trace_res(const LaunchEnv& env, const TraceArgs& a) {
-  const int nw = (env.I + IPW - 1) / IPW;
-  hipLaunchKernelGGL((k_trace<KS, NW, IPW>), dim3(env.Z), dim3(nw * kWave), 0, env.stream,
-                     LAR_TRACE_ARGS);
-  return hipGetLastError();
-}
-
 template <int KS, int NW>
 static hipError_t launch_trace_mem(const LaunchEnv& env, const TraceArgs& a) {
   const int nw = env.I < NW ? env.I : NW;
@@ -1044,49 +1094,43 @@ static hipError_t launch_trace_mem(const LaunchEnv& env, const TraceArgs& a) {
   return hipGetLastError();
 }
 
-template <int KS, int NW, int IPW>
-static hipError_t launch_trace_lds(const LaunchEnv& env, const TraceArgs& a) {
-  const int nw = (env.I + IPW - 1) / IPW;
-  const size_t lds = sizeof(LdsQueue<KS>) * (size_t)nw * IPW;
-  hipError_t e = hipFuncSetAttribute((const void*)k_trace_lds<KS, NW, IPW>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_trace_lds<KS, NW, IPW>), dim3(env.Z), dim3(nw * kWave), lds,
-                     env.stream, LAR_TRACE_ARGS);
-  return hipGetLastError();
-}
-
 template <int KS, int W, int IPW>
 static hipError_t launch_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
   const int per_wg = W * IPW;
   const int G = (env.I + per_wg - 1) / per_wg;
   if (G > kMaxCluster) return hipErrorInvalidValue;
-  if ((uint64_t)G * (uint64_t)a.N >= (1ull << 32)) return hipErrorInvalidValue;  // counter range
+  if ((uint64_t)a.N >= (1ull << 31)) return hipErrorInvalidValue;  // 32-bit post tags
   const int w_used = G == 1 ? (env.I + IPW - 1) / IPW : W;
-  hipLaunchKernelGGL(k_clear_exchange, dim3((env.Z + 255) / 256), dim3(256), 0, env.stream,
-                     env.xcount, env.Z);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (G > 1) {
+    const int64_t n = (int64_t)env.Z * 2 * kMaxCluster * 4;
+    hipLaunchKernelGGL(k_clear_exchange, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                       env.stream, env.xslot, n);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   const int blocks = 8 * ((env.Z + 7) / 8) * G;
   hipLaunchKernelGGL((k_trace_cl<KS, W, IPW>), dim3(blocks), dim3(w_used * kWave), 0,
-                     env.stream, LAR_TRACE_ARGS, G, env.xcount, env.xcand);
+                     env.stream, LAR_TRACE_ARGS, G, env.xslot, env.T.K);
   return hipGetLastError();
 }
 
 template <int KS>
 static hipError_t launch_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
-  // one or two instances per wave, states in VGPRs, 8 waves per workgroup; the
-  // whole grid must be resident at once (2048 waves: 8 per CU)
+  // one or two instances per wave with their states in VGPRs, 8 waves per
+  // workgroup; the whole grid must be resident at once (at most 2048 waves: 8 per
+  // CU), N must fit the 31-bit post tags and the decode-only tail of an estimate
+  // (at most K batches) must fit one lane per batch
   const int64_t queues = (int64_t)env.Z * env.I;
   auto fits = [&](int per_wg) {
     const int64_t G = (env.I + per_wg - 1) / per_wg;
-    return G <= kMaxCluster && (uint64_t)G * (uint64_t)a.N < (1ull << 32);
+    return G <= kMaxCluster && (uint64_t)a.N < (1ull << 31) && env.T.K >= 1 &&
+           env.T.K <= kWave;
   };
-  if (KS <= 4) {
+  if constexpr (KS <= 4) {
     if (queues <= 2048 && fits(8)) return launch_trace_cl<KS, 8, 1>(env, a);
     if (queues <= 4096 && fits(16)) return launch_trace_cl<KS, 8, 2>(env, a);
-  } else if (KS == 8 && queues <= 2048 && fits(8)) {
-    return launch_trace_cl<8, 8, 1>(env, a);
+  } else if constexpr (KS == 8) {
+    if (queues <= 2048 && fits(8)) return launch_trace_cl<8, 8, 1>(env, a);
   }
   // Otherwise the states stay in HBM (L2) and are loaded per use.
   return launch_trace_mem<KS, (KS <= 4 ? 8 : (KS == 8 ? 8 : 4))>(env, a);

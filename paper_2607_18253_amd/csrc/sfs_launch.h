@@ -20,8 +20,7 @@ struct LaunchEnv {
   int32_t* err;       // sticky device error
   hipStream_t stream;
   // cross-workgroup candidate exchange of the clustered trace kernel
-  uint32_t* xcount;   // [Z] arrival counters (64-byte stride)
-  double* xcand;      // [Z][2][kMaxCluster][4]
+  uint64_t* xslot;    // [Z][2][kMaxCluster][4] tagged candidate posts
 };
 
 constexpr int kMaxCluster = 64;
