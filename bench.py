@@ -24,6 +24,8 @@ the same trace.
 from __future__ import annotations
 
 import argparse
+import csv
+import hashlib
 import json
 import os
 import sys
@@ -49,7 +51,77 @@ def _parse():
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="time budget of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run one plain 256 MiB device copy first (counter calibration)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of "
+                         "'bench.py --copy-probe --steps 1 --warmup 0' into the traffic record")
     return ap.parse_args()
+
+
+COPY_PROBE_BYTES = 256 << 20
+KERNEL_SOURCES = ("paper_2607_18253_amd/csrc/sfs_kernels.hip",
+                  "paper_2607_18253_amd/csrc/sfs_device.h")
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_path(workload):
+    return os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+
+
+def summarize_pmc(fetch_csv, write_csv, workload):
+    """HBM bytes per launch of the dominant kernel from two counter runs, each scaled
+    by what the same counter reads for the plain device copy of known size."""
+    def per_kernel(path, counter):
+        vals = {}
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] != counter:
+                    continue
+                key = (r["Kernel_Name"], r.get("Dispatch_Id", r.get("Correlation_Id", "")))
+                vals[key] = vals.get(key, 0.0) + float(r["Counter_Value"])
+        return vals
+
+    out = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        v = per_kernel(path, counter)
+        copy = [x for (k, _), x in v.items() if "copy" in k.lower() or "elementwise" in k.lower()]
+        dom = [x for (k, _), x in v.items() if dominant_kernel(workload) in k]
+        if not copy or not dom:
+            raise SystemExit(f"{path}: no copy-probe or {dominant_kernel(workload)} dispatch")
+        factor = max(copy) * 1024.0 / COPY_PROBE_BYTES   # KiB counted per true byte
+        out[counter] = {"kib_per_launch": sum(dom) / len(dom), "copy_probe_kib": max(copy),
+                        "scale": factor, "bytes_per_launch": sum(dom) / len(dom) * 1024.0 / factor}
+    rec = {"workload": workload, "kernel": dominant_kernel(workload), "source_hash": kernel_source_hash(),
+           "fetch": out["FETCH_SIZE"], "write": out["WRITE_SIZE"],
+           "bytes_per_launch": out["FETCH_SIZE"]["bytes_per_launch"]
+           + out["WRITE_SIZE"]["bytes_per_launch"]}
+    with open(traffic_path(workload), "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec))
+
+
+def load_traffic(workload):
+    """Measured HBM bytes per launch, or None when absent or taken on other sources."""
+    try:
+        with open(traffic_path(workload)) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    return rec["bytes_per_launch"]
+
+
+def dominant_kernel(workload):
+    return "k_traj" if workload == "c3" else "k_trace_cl"
 
 
 def oracle_sample(wl, budget_s):
@@ -100,6 +172,9 @@ import numpy as np  # noqa: E402
 
 def main():
     args = _parse()
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, args.workload)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
               "(the multi-GPU sharding is a design, not a built path)", file=sys.stderr)
@@ -131,6 +206,12 @@ def main():
     if whatif:
         ttft = torch.empty((Z, N, I), dtype=torch.float64, device=dev)
     kev = []   # (start, end) events around the dominant kernel of each timed step
+    if args.copy_probe:
+        src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step(record=False):
         if whatif:
@@ -185,7 +266,7 @@ def main():
     if whatif:
         line["roofline_kernel"] = "k_traj + k_est (lar_estimate_ttft)"
     else:
-        line["roofline_kernel"] = "k_trace (lar_route_trace, one launch per step)"
+        line["roofline_kernel"] = "k_trace_cl (lar_route_trace, one launch per step)"
         line["stats_scenario0"] = stats[0].tolist()
     line["kernel_ms"] = kernel_ms
 
@@ -210,7 +291,7 @@ def main():
                 achieved = flops / (kernel_ms / 1000.0) / 1e12
                 roof = {"bound": "alu", "achieved": achieved, "peak": FP64_VECTOR_PEAK_TFLOPS,
                         "unit": "TFLOP/s", "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
-                        "traffic": None,
+                        "traffic": load_traffic(args.workload),
                         "note": f"{batches} simulated batches per scenario (oracle count: "
                                 "every estimate's batches + the replay) x 9 fp64 ops; "
                                 "sequential trace, latency-bound"}
