@@ -657,31 +657,45 @@ __device__ __forceinline__ void tail_readonly(FCache& fc, const Queue<KS>& w, co
   }
 }
 
-// One visit of a wave to one owned queue for one query: append the query if it was
-// routed here, replay to tn, and keep the frontier cache in step.  Every batch --
-// replayed, walked to a new admission point, or recorded as tail -- runs through the
-// single Queue::step / quiet_run below, on the working copy wk.
+// What the estimate needs of the instance after a visit: its batch counter and
+// clock, and whether the working copy still equals it with the whole prefill list in
+// the window and the query admitted in the very next batch (then the estimate reads
+// the tail straight from it).
+struct VisitOut {
+  int g;
+  double clock;
+  bool direct;
+};
+
+// One visit of a wave to one owned queue for one query.  wk enters as the instance
+// state (loaded from SL); the query is appended if it was routed here, the instance
+// is replayed to tn and written back to SL, and the frontier cache is kept in step.
+// Every batch -- replayed, walked to a new admission point, or recorded as tail --
+// runs through the single Queue::step / quiet_run below, on wk.
 template <int KS>
-__device__ __forceinline__ void visit(Queue<KS>& S, FCache& fc, Queue<KS>& wk, const QEnv& e,
-                                      bool chosen, int p, int d, double tn, int qcap, int kmax,
-                                      int64_t max_iters, int32_t* err, LdsQueue<KS>& F) {
+__device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv& e, bool chosen,
+                                          int p, int d, double tn, int qcap, int kmax,
+                                          int64_t max_iters, int32_t* err, LdsQueue<KS>& SL,
+                                          LdsQueue<KS>& F) {
   const int ln = lane_id();
+  VisitOut vo;
+  vo.direct = false;
   bool joined = false;
   if (chosen) {
     d = d < 1 ? 1 : d;
     if (p < 1) {
       if (ln == 0) set_error(err, kErrArg);
-    } else if (S.n_pre - S.n_part + 1 > qcap) {
+    } else if (wk.n_pre - wk.n_part + 1 > qcap) {
       if (ln == 0) set_error(err, kErrCapacity);
     } else {
-      S.append(e, p, d);
+      wk.append(e, p, d);
       joined = true;
     }
   }
   enum { kReplay, kWalk, kTail };
   int phase = kReplay;
-  wk = S;
-  double clk = wk.clock;
+  const double clk0 = wk.clock;
+  double clk = clk0;
   double stop_t = tn;
   int64_t n = 0;
   int kk = -1;
@@ -703,18 +717,21 @@ __device__ __forceinline__ void visit(Queue<KS>& S, FCache& fc, Queue<KS>& wk, c
         if (wk.resident() == 0 && clk < stop_t) clk = stop_t;
         wk.clock = clk;
         wk.iters += n;
-        S = wk;
-        // the world ran the admission batch, or sat idle at F and its clock jumped
-        if (fc.valid && (S.g > fc.g || (S.g == fc.g && S.clock != fc.E))) fc.valid = false;
+        if (joined || n > 0 || clk != clk0) wk.to_lds(SL);   // the instance moved on
+        vo.g = wk.g;
+        vo.clock = clk;
+        // the instance ran the admission batch, or sat idle at F and its clock jumped
+        if (fc.valid && (wk.g > fc.g || (wk.g == fc.g && clk != fc.E))) fc.valid = false;
         if (joined && fc.valid) {
           wk.from_lds(F);
           wk.append(e, p, d);
           clk = fc.E;
         } else if (!fc.valid) {
-          S.refill(e);
           wk.refill(e);
-          if (S.tail_admitted_next(e) && S.nwin == S.n_pre) break;   // estimate from S directly
-          clk = S.clock;
+          if (wk.tail_admitted_next(e) && wk.nwin == wk.n_pre) {
+            vo.direct = true;   // estimate straight from the instance state
+            break;
+          }
         } else {
           break;
         }
@@ -758,17 +775,20 @@ __device__ __forceinline__ void visit(Queue<KS>& S, FCache& fc, Queue<KS>& wk, c
       ++kk;
     }
   }
+  return vo;
 }
 
 // SFS estimate of a query (p tokens, arrival t) from the admission batch summary and
-// the decode-only tail: from the cache (tail in lanes) or, when S admits the query
-// in its very next batch, read-only from S.
+// the decode-only tail: from the cache (tail in lanes) or, when the visit left the
+// instance state in S with the query admitted in its very next batch, read-only
+// from S.
 template <int KS>
 __device__ __forceinline__ double estimate_visit(const FCache& fc, const Queue<KS>& S,
-                                                 const QEnv& e, int p, double t, int reading,
-                                                 int kmax, int64_t max_iters, int32_t* err) {
+                                                 const VisitOut& vo, const QEnv& e, int p,
+                                                 double t, int reading, int kmax,
+                                                 int64_t max_iters, int32_t* err) {
   const int ln = lane_id();
-  if (S.clock < t) {
+  if (vo.clock < t) {
     if (ln == 0) set_error(err, kErrState);
     return __builtin_nan("");
   }
@@ -778,9 +798,9 @@ __device__ __forceinline__ double estimate_visit(const FCache& fc, const Queue<K
   int aP, aD, left;
   int64_t aC, aA;
   const bool cached = fc.valid;
-  if (!cached && !S.tail_admitted_next(e)) return __builtin_nan("");   // error already set
+  if (!cached && !vo.direct) return __builtin_nan("");   // the walk's cap ran out: error set
   if (cached) {
-    E = fc.E; it = (int64_t)(fc.g - S.g) + 1;
+    E = fc.E; it = (int64_t)(fc.g - vo.g) + 1;
     aP = fc.aP; aD = fc.aD; left = fc.left; aC = fc.aC; aA = fc.aA;
   } else {
     E = S.clock; it = 1;
@@ -830,7 +850,7 @@ __device__ __forceinline__ double estimate_visit(const FCache& fc, const Queue<K
 }
 
 // The whole sequential trace with each wave owning IPW instances whose states stay
-// in VGPRs for the whole trace.  A scenario spans G workgroups of W waves; block b
+// in LDS for the whole trace (one working copy in VGPRs per visit).  A scenario spans G workgroups of W waves; block b
 // serves scenario z = (b / 8 / G) * 8 + b % 8 as cluster member (b / 8) % G, so the
 // members of a scenario share one XCD (blocks are dispatched to the 8 XCDs
 // round-robin) and exchange through that XCD's L2.  Iteration i (from -1): the
@@ -846,6 +866,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
   __shared__ double s_mu[2];
   __shared__ int s_mj[2];
   __shared__ int stage[W][3 * kWave];
+  __shared__ LdsQueue<KS> sst[W][IPW];   // instance states
   __shared__ LdsQueue<KS> fst[W][IPW];   // frontier states
   const int b = blockIdx.x;
   const int z = (b / 8 / G) * 8 + b % 8;
@@ -860,9 +881,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
   const int jbase = (cid * W + wid) * IPW;
   const int kmax = tail_k;   // <= 64, checked at launch
   int cols[IPW];
-  Queue<KS> qs[IPW];
   FCache fc[IPW];
-  Queue<KS> wk;   // working copy
 #pragma unroll
   for (int r = 0; r < IPW; ++r) {
     const int j = jbase + r;
@@ -870,7 +889,11 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
     fc[r].valid = false;
     fc[r].tD = 0;
     fc[r].tC = 0;
-    if (j < I) qs[r].load(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
+    if (j < I) {
+      Queue<KS> q;
+      q.load(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
+      q.to_lds(sst[wid][r]);
+    }
   }
   QueryBlock<IPW> cur = fetch_block<IPW>(0, N, qp, qd, qt, acc, cost, n_cols, cols);
   QueryBlock<IPW> nxt = fetch_block<IPW>(kWave, N, qp, qd, qt, acc, cost, n_cols, cols);
@@ -938,10 +961,12 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
       const int j = jbase + r;
       if (j < I) {
         const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
-        visit(qs[r], fc[r], wk, e, i >= 0 && j == m, p, dq, tn, S.qcap, kmax, max_iters, err,
-              fst[wid][r]);
+        Queue<KS> wk;
+        wk.from_lds(sst[wid][r]);
+        const VisitOut vo = visit(wk, fc[r], e, i >= 0 && j == m, p, dq, tn, S.qcap, kmax,
+                                  max_iters, err, sst[wid][r], fst[wid][r]);
         if (more) {
-          const double ttft = p1_ok ? estimate_visit(fc[r], qs[r], e, p1, t1, reading, kmax,
+          const double ttft = p1_ok ? estimate_visit(fc[r], wk, vo, e, p1, t1, reading, kmax,
                                                      max_iters, err)
                                     : __builtin_nan("");
           const double a = read_lane_f64(in_nxt ? nxt.acc[r] : cur.acc[r], l1);
@@ -959,7 +984,11 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
 #pragma unroll
   for (int r = 0; r < IPW; ++r) {
     const int j = jbase + r;
-    if (j < I) qs[r].store(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
+    if (j < I) {
+      Queue<KS> q;
+      q.from_lds(sst[wid][r]);
+      q.store(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
+    }
   }
 }
 

@@ -182,6 +182,33 @@ def test_trace_tiny_pools(seed, flags):
     ctx.close()
 
 
+def _tail_k(wl):
+    """Bound on the decode-only batches after an admission batch (one lane each in the
+    clustered trace kernel, which needs it <= 64; larger bounds take the HBM-state
+    trace kernel)."""
+    return int(max(-(-(wl.max_prompt - 1) // (int(b) - int(m) + 1)) + 1
+                   for b, m in zip(wl.budget, wl.max_seqs)))
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("prompt_max,path", [(60, "clustered"), (300, "hbm-state")])
+def test_trace_tiny_pools_long_prompts(seed, prompt_max, path):
+    """Prompts many batches long: deep frontier tails (clustered kernel) and, past 64
+    tail batches, the HBM-state trace kernel."""
+    wl = make_tiny_workload(100 + seed, n_inst=6, max_res=8, n_q=30, prompt=(1, prompt_max),
+                            budget=(1, 6), max_seqs=(1, 3), n_scen=2)
+    k = _tail_k(wl)
+    assert (k <= 64) == (path == "clustered"), k
+    choice, chosen, util, ctx = gpu_trace(wl, queue_cap=10 ** 4)
+    for z in range(wl.n_scen):
+        ref = O.trace(wl, scenario=z, queue_cap=10 ** 4)
+        np.testing.assert_array_equal(choice[z], ref.choice)
+        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen))
+        np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
+        assert_state_equal(ctx, z, ref)
+    ctx.close()
+
+
 def test_trace_c1_full():
     wl = make_workload("c1")
     choice, chosen, util, ctx = gpu_trace(wl)
