@@ -1145,10 +1145,11 @@ static hipError_t launch_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
 
 template <int KS>
 static hipError_t launch_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
-  // one or two instances per wave with their states in VGPRs, 8 waves per
-  // workgroup; the whole grid must be resident at once (at most 2048 waves: 8 per
-  // CU), N must fit the 31-bit post tags and the decode-only tail of an estimate
-  // (at most K batches) must fit one lane per batch
+  // One instance per wave.  The whole grid must be resident at once: up to 1024
+  // queues get one wave per SIMD (4 per workgroup; the per-query chain is issue
+  // latency bound, so a wave runs fastest alone on its SIMD), up to 4096 get 16-wave
+  // workgroups (4 waves per SIMD, 128 VGPRs each).  N must fit the 31-bit post tags
+  // and the decode-only tail of an estimate (at most K batches) one lane per batch.
   const int64_t queues = (int64_t)env.Z * env.I;
   auto fits = [&](int per_wg) {
     const int64_t G = (env.I + per_wg - 1) / per_wg;
@@ -1156,9 +1157,10 @@ static hipError_t launch_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
            env.T.K <= kWave;
   };
   if constexpr (KS <= 4) {
-    if (queues <= 2048 && fits(8)) return launch_trace_cl<KS, 8, 1>(env, a);
-    if (queues <= 4096 && fits(16)) return launch_trace_cl<KS, 8, 2>(env, a);
+    if (queues <= 1024 && fits(4)) return launch_trace_cl<KS, 4, 1>(env, a);
+    if (queues <= 4096 && fits(16)) return launch_trace_cl<KS, 16, 1>(env, a);
   } else if constexpr (KS == 8) {
+    if (queues <= 1024 && fits(4)) return launch_trace_cl<8, 4, 1>(env, a);
     if (queues <= 2048 && fits(8)) return launch_trace_cl<8, 8, 1>(env, a);
   }
   // Otherwise the states stay in HBM (L2) and are loaded per use.
