@@ -564,7 +564,7 @@ __device__ __forceinline__ bool cluster_exchange(double& u, int& j, int i, int G
   uint64_t w0 = 0, w1 = 0, w2 = 0;
   bool ready = ln >= G;
   const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-  for (;;) {
+  for (uint32_t polls = 1;; ++polls) {
     if (!ready) {
       const uint64_t* o = base + ln * 4;
       w0 = __hip_atomic_load(o + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -574,15 +574,17 @@ __device__ __forceinline__ bool cluster_exchange(double& u, int& j, int i, int G
               (uint32_t)(w2 >> 32) == tag;
     }
     if (ballot(!ready) == 0) break;
-    int bad = 0;
-    if (ln == 0)
-      bad = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == kErrSync ||
-            __builtin_amdgcn_s_memrealtime() - t0 > kSpinTicks;
-    if (__builtin_amdgcn_readlane(bad, 0)) {
-      if (ln == 0) set_error(err, kErrSync);
-      return false;
+    // the escape checks cost a round trip of their own: every 256th poll only
+    if ((polls & 255u) == 0) {
+      int bad = 0;
+      if (ln == 0)
+        bad = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == kErrSync ||
+              __builtin_amdgcn_s_memrealtime() - t0 > kSpinTicks;
+      if (__builtin_amdgcn_readlane(bad, 0)) {
+        if (ln == 0) set_error(err, kErrSync);
+        return false;
+      }
     }
-    __builtin_amdgcn_s_sleep(1);
   }
   double bu = 0.0;
   int bj = -1;
@@ -882,6 +884,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
   const int kmax = tail_k;   // <= 64, checked at launch
   int cols[IPW];
   FCache fc[IPW];
+  QEnv env[IPW];   // per owned instance: coefficients, ring, staging (loop invariant)
 #pragma unroll
   for (int r = 0; r < IPW; ++r) {
     const int j = jbase + r;
@@ -890,8 +893,9 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
     fc[r].tD = 0;
     fc[r].tC = 0;
     if (j < I) {
+      env[r] = make_env(S, pr, z * I + j, j, stage[wid]);
       Queue<KS> q;
-      q.load(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
+      q.load(S, env[r], z * I + j);
       q.to_lds(sst[wid][r]);
     }
   }
@@ -914,10 +918,17 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
       const int buf = i & 1;
       if (ln == 0) { s_u[buf][wid] = c.u; s_j[buf][wid] = c.j; }
       __syncthreads();
-      double bu = s_u[buf][0];
-      int bj = s_j[buf][0];
-      for (int v = 1; v < nw; ++v)
-        if (better(s_u[buf][v], s_j[buf][v], bu, bj)) { bu = s_u[buf][v]; bj = s_j[buf][v]; }
+      // lane v reads wave v's candidate; log2(nw) shuffle steps apply the total order
+      double bu = 0.0;
+      int bj = -1;
+      if (ln < nw) { bu = s_u[buf][ln]; bj = s_j[buf][ln]; }
+      for (int mk = 1; mk < nw; mk <<= 1) {
+        const double xu = __shfl_xor(bu, mk, kWave);
+        const int xj = __shfl_xor(bj, mk, kWave);
+        if (better(xu, xj, bu, bj)) { bu = xu; bj = xj; }
+      }
+      bu = read_lane_f64(bu, 0);
+      bj = __builtin_amdgcn_readlane(bj, 0);
       if (G > 1) {
         // wave 0 exchanges with the other workgroups, then broadcasts the winner
         if (wid == 0) {
@@ -960,7 +971,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
     for (int r = 0; r < IPW; ++r) {
       const int j = jbase + r;
       if (j < I) {
-        const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
+        const QEnv& e = env[r];
         Queue<KS> wk;
         wk.from_lds(sst[wid][r]);
         const VisitOut vo = visit(wk, fc[r], e, i >= 0 && j == m, p, dq, tn, S.qcap, kmax,
