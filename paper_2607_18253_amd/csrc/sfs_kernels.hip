@@ -19,11 +19,50 @@
 
 namespace lar {
 
-// Total order for the argmax: larger utility first, then the lower instance index.
+// Total order for the argmax: larger utility first, then the lower instance index;
+// j < 0 marks "no candidate".  Written without branches so a lane-wise use stays a
+// few selects.
 __device__ __forceinline__ bool better(double u1, int j1, double u2, int j2) {
-  if (j2 < 0) return j1 >= 0;
-  if (j1 < 0) return false;
-  return u1 > u2 || (u1 == u2 && j1 < j2);
+  return (j1 >= 0) & ((j2 < 0) | (u1 > u2) | ((u1 == u2) & (j1 < j2)));
+}
+
+// One butterfly step of the lane argmax: take the partner lane's candidate (DPP
+// pattern CTRL) when it is better.
+template <int CTRL>
+__device__ __forceinline__ void best_step_dpp(double& u, int& j) {
+  const long long b = __double_as_longlong(u);
+  const int lo = __builtin_amdgcn_mov_dpp((int)b, CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_mov_dpp((int)(b >> 32), CTRL, 0xf, 0xf, false);
+  const double xu = __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+  const int xj = __builtin_amdgcn_mov_dpp(j, CTRL, 0xf, 0xf, false);
+  const bool t = better(xu, xj, u, j);
+  u = t ? xu : u;
+  j = t ? xj : j;
+}
+
+__device__ __forceinline__ void best_step_xor(double& u, int& j, int m) {
+  const double xu = __shfl_xor(u, m, kWave);
+  const int xj = __shfl_xor(j, m, kWave);
+  const bool t = better(xu, xj, u, j);
+  u = t ? xu : u;
+  j = t ? xj : j;
+}
+
+// Argmax of the candidates in lanes [0, n) (lanes from n up to the next power of two
+// must hold j = -1); the result is returned wave-uniform.  Quad permutations and the
+// row mirrors combine 2, 4, 8 and 16 lanes; larger n continue with lane shuffles.
+__device__ __forceinline__ void lane_best(double& u, int& j, int n) {
+  if (n > 1) best_step_dpp<0xB1>(u, j);    // quad_perm [1,0,3,2]
+  if (n > 2) best_step_dpp<0x4E>(u, j);    // quad_perm [2,3,0,1]
+  if (n > 4) best_step_dpp<0x141>(u, j);   // row_half_mirror
+  if (n > 8) best_step_dpp<0x140>(u, j);   // row_mirror
+  if (n > 16) best_step_xor(u, j, 16);
+  if (n > 32) best_step_xor(u, j, 32);
+  const long long b = __double_as_longlong(u);
+  const unsigned lo = (unsigned)__builtin_amdgcn_readfirstlane((int)b);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((int)(b >> 32));
+  u = __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+  j = __builtin_amdgcn_readfirstlane(j);
 }
 
 // ------------------------------------------------------------------ k_traj
@@ -592,13 +631,9 @@ __device__ __forceinline__ bool cluster_exchange(double& u, int& j, int i, int G
     bu = __longlong_as_double((long long)((w0 & 0xffffffffull) | (w1 << 32)));
     bj = (int)(uint32_t)w2;
   }
-  for (int m = 1; m < G; m <<= 1) {   // lanes [G, 2^ceil(log2 G)) hold no candidate
-    const double xu = __shfl_xor(bu, m, kWave);
-    const int xj = __shfl_xor(bj, m, kWave);
-    if (better(xu, xj, bu, bj)) { bu = xu; bj = xj; }
-  }
-  u = read_lane_f64(bu, 0);
-  j = __builtin_amdgcn_readlane(bj, 0);
+  lane_best(bu, bj, G);
+  u = bu;
+  j = bj;
   return true;
 }
 
@@ -922,13 +957,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
       double bu = 0.0;
       int bj = -1;
       if (ln < nw) { bu = s_u[buf][ln]; bj = s_j[buf][ln]; }
-      for (int mk = 1; mk < nw; mk <<= 1) {
-        const double xu = __shfl_xor(bu, mk, kWave);
-        const int xj = __shfl_xor(bj, mk, kWave);
-        if (better(xu, xj, bu, bj)) { bu = xu; bj = xj; }
-      }
-      bu = read_lane_f64(bu, 0);
-      bj = __builtin_amdgcn_readlane(bj, 0);
+      lane_best(bu, bj, nw);
       if (G > 1) {
         // wave 0 exchanges with the other workgroups, then broadcasts the winner
         if (wid == 0) {
