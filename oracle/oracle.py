@@ -96,10 +96,20 @@ def lib():
     L.orc_trace.restype = C.c_int
     L.orc_trace.argtypes = [C.c_int32, C.POINTER(Params), _i32p, _i32p, _i32p, _i32p, _i32p,
                             _f64p, C.c_int32, _i32p, _i32p, _f64p, _f64p, _f64p, C.c_int32,
-                            C.c_double, C.c_double, C.c_int32, C.c_int64, C.c_int64,
+                            C.c_double, C.c_double, _opt(_f64p), C.c_int32, C.c_int64, C.c_int64,
                             _i32p, _opt(_f64p), _opt(_f64p), _opt(_f64p), _opt(_i32p),
                             _opt(_i32p), _opt(_i32p), _opt(_i32p), _opt(_i32p), _opt(_f64p),
                             _opt(_i64p), C.c_int64, C.POINTER(C.c_int32)]
+    L.orc_route_row_constrained.restype = C.c_int32
+    L.orc_route_row_constrained.argtypes = [C.c_int32, _f64p, C.c_double, _f64p, _f64p, _i32p,
+                                            C.c_double]
+    L.orc_ttft_target.restype = C.c_double
+    L.orc_ttft_target.argtypes = [C.c_int32, C.c_double, C.c_double]
+    L.orc_ttft_targets.restype = None
+    L.orc_ttft_targets.argtypes = [C.c_int32, _i32p, _f64p, _f64p, _f64p]
+    L.orc_ontime_utility.restype = C.c_int
+    L.orc_ontime_utility.argtypes = [C.c_int32, _i32p, _f64p, _f64p, _f64p, _f64p, C.c_int32,
+                                     _i32p, C.c_double, C.POINTER(C.c_double)]
     L.orc_stats.restype = C.c_int
     L.orc_stats.argtypes = [C.c_int32, _i32p, _f64p, _f64p, _f64p, C.c_int32, _i32p, C.c_double,
                             _f64p]
@@ -184,6 +194,42 @@ def route_row(ttft, acc_row, cost_row, col, w_cost, w_lat):
     return int(m), bu.value
 
 
+def route_row_constrained(ttft, tau, acc_row, cost_row, col, w_cost):
+    """Eq. 3: best utility within the TTFT target, else the least estimated TTFT."""
+    ttft = np.ascontiguousarray(ttft, np.float64)
+    return int(lib().orc_route_row_constrained(len(ttft), ttft, float(tau),
+                                               np.ascontiguousarray(acc_row, np.float64),
+                                               np.ascontiguousarray(cost_row, np.float64),
+                                               _i32(col), float(w_cost)))
+
+
+def ttft_target(p, u_ms, v):
+    return float(lib().orc_ttft_target(int(p), float(u_ms), float(v)))
+
+
+def ttft_targets(p, u_ms, v):
+    """Per-query TTFT targets (ms) from the prompt lengths and the drawn u, v."""
+    p = _i32(p)
+    out = np.zeros(len(p))
+    lib().orc_ttft_targets(len(p), p, np.ascontiguousarray(u_ms, np.float64),
+                           np.ascontiguousarray(v, np.float64), out)
+    return out
+
+
+def ontime_utility(choice, ttft_chosen, tau, acc, cost, col, w_cost):
+    """Eq. 4 over a routed trace (estimated TTFT at the choice taken as realised)."""
+    n = len(choice)
+    out = C.c_double(0)
+    st = lib().orc_ontime_utility(n, _i32(choice), np.ascontiguousarray(ttft_chosen, np.float64),
+                                  np.ascontiguousarray(tau[:n], np.float64),
+                                  np.ascontiguousarray(acc[:n], np.float64),
+                                  np.ascontiguousarray(cost[:n], np.float64), acc.shape[1],
+                                  _i32(col), float(w_cost), C.byref(out))
+    if st != OK:
+        raise OracleError(st, "ontime_utility")
+    return out.value
+
+
 @dataclass
 class TraceResult:
     choice: np.ndarray
@@ -200,8 +246,11 @@ class TraceResult:
 
 
 def trace(wl, scenario: int = 0, *, n_q: int | None = None, reading=READING_DECODE_BATCH,
-          max_iters=10_000_000, full_rows=False, final_state=True, queue_cap=None) -> TraceResult:
-    """Sequential routing trace of one scenario of workload ``wl`` (first n_q queries)."""
+          max_iters=10_000_000, full_rows=False, final_state=True, queue_cap=None,
+          tau=None) -> TraceResult:
+    """Sequential routing trace of one scenario of workload ``wl`` (first n_q queries);
+    Lagrangian route, or the constrained route of Eq. 3 when per-query targets
+    ``tau`` (ms) are given."""
     L = lib()
     I = wl.n_inst
     N = wl.n_q if n_q is None else int(n_q)
@@ -229,7 +278,9 @@ def trace(wl, scenario: int = 0, *, n_q: int | None = None, reading=READING_DECO
                      np.ascontiguousarray(wl.q_t_ms[:N], np.float64),
                      np.ascontiguousarray(wl.acc[:N], np.float64),
                      np.ascontiguousarray(wl.cost[:N], np.float64), wl.n_cols,
-                     float(wl.w_cost[scenario]), float(wl.w_lat_ms[scenario]), int(reading),
+                     float(wl.w_cost[scenario]), float(wl.w_lat_ms[scenario]),
+                     None if tau is None else np.ascontiguousarray(tau[:N], np.float64),
+                     int(reading),
                      int(max_iters), cap, choice, ttft_c, util_c, ttft_all, iters_all,
                      out_off, out_rp, out_rd, out_cx, out_clock, out_iters, out_cap,
                      C.byref(failed))

@@ -48,6 +48,18 @@
  *     workload snapshots): append the routed query as a waiting request of the
  *     chosen instance, then on every instance run each batch that starts before
  *     the next arrival time; an idle instance's clock jumps to that time.
+ *
+ *   * Constrained route (Eq. 3, the primary objective of Sec. 3): among the
+ *     instances whose estimated TTFT is within the query's target tau, the lowest
+ *     j of maximal utility acc_j - w_cost*cost_j (Eq. 2); when none is within the
+ *     target, the lowest j of minimal estimated TTFT.
+ *
+ *   * TTFT target of a query (appendix on TTFT latency assignment):
+ *       tau = min{1120, max{150, u + (155 + 3.5e-3*p)*v}}  (ms),
+ *     u ~ U(1, 5) ms and v ~ U(0.98, 1.02) drawn by the caller.
+ *
+ *   * OnTimeUtility (Eq. 4): (1/N) * sum over queries, in query order, of the
+ *     utility at the chosen instance when its TTFT is within the target, else 0.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -317,6 +329,40 @@ int32_t orc_route_row(int32_t n_inst, const double *ttft, const double *acc_row,
   return best;
 }
 
+/* Eq. 3: argmax of the utility over the feasible set {j : ttft_j <= tau}; if that
+ * set is empty, argmin of the estimated TTFT.  Lowest index on ties. */
+int32_t orc_route_row_constrained(int32_t n_inst, const double *ttft, double tau,
+                                  const double *acc_row, const double *cost_row,
+                                  const int32_t *col, double w_cost) {
+  int32_t best = -1;
+  double bu = 0.0;
+  for (int32_t j = 0; j < n_inst; ++j) {
+    if (!(ttft[j] <= tau)) continue;
+    double pen = w_cost * cost_row[col[j]];
+    double u = acc_row[col[j]] - pen;
+    if (best < 0 || u > bu) { best = j; bu = u; }
+  }
+  if (best >= 0) return best;
+  double bt = 0.0;
+  for (int32_t j = 0; j < n_inst; ++j)
+    if (best < 0 || ttft[j] < bt) { best = j; bt = ttft[j]; }
+  return best;
+}
+
+/* TTFT target (appendix on TTFT latency assignment), evaluated in the written
+ * order: lin = 155 + 3.5e-3*p, raw = u + lin*v, then the clip to [150, 1120]. */
+double orc_ttft_target(int32_t p, double u_ms, double v) {
+  double lin = 155.0 + 3.5e-3 * (double)p;
+  double raw = u_ms + lin * v;
+  double lo = raw > 150.0 ? raw : 150.0;
+  return lo < 1120.0 ? lo : 1120.0;
+}
+
+void orc_ttft_targets(int32_t n, const int32_t *p, const double *u_ms, const double *v,
+                      double *tau) {
+  for (int32_t i = 0; i < n; ++i) tau[i] = orc_ttft_target(p[i], u_ms[i], v[i]);
+}
+
 /* ---------------------------------------------------------------- trace */
 
 /*
@@ -324,6 +370,7 @@ int32_t orc_route_row(int32_t n_inst, const double *ttft, const double *acc_row,
  *   advance every instance to t_0;
  *   for each query i: estimate every instance at t_i, route, append the query to
  *   the chosen instance, advance every instance to t_{i+1} (t_N := t_{N-1}).
+ * The route is the Lagrangian one, or Eq. 3 when tau (per query) is given.
  * Outputs per query: choice, TTFT at the choice, utility of Eq. 2 at the choice
  * (acc - w_cost*cost), and optionally the whole TTFT / iteration rows.
  * The final state is written to the out_* arrays when out_offsets != NULL (each
@@ -333,8 +380,9 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
               const int32_t *offsets, const int32_t *rp, const int32_t *rd, const int32_t *cx,
               const double *clock, int32_t n_q, const int32_t *q_p, const int32_t *q_d,
               const double *q_t, const double *acc, const double *cost, int32_t n_cols,
-              double w_cost, double w_lat, int32_t reading, int64_t max_iters,
-              int64_t queue_cap, int32_t *choice, double *ttft_chosen, double *util_chosen,
+              double w_cost, double w_lat, const double *tau, int32_t reading,
+              int64_t max_iters, int64_t queue_cap, int32_t *choice, double *ttft_chosen,
+              double *util_chosen,
               double *ttft_all, int32_t *iters_all, int32_t *out_offsets, int32_t *out_rp,
               int32_t *out_rd, int32_t *out_cx, double *out_clock, int64_t *out_iters,
               int64_t out_cap, int32_t *failed_query) {
@@ -364,7 +412,8 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
     if (st != ORC_OK) { *failed_query = i; break; }
     const double *arow = acc + (int64_t)i * n_cols;
     const double *crow = cost + (int64_t)i * n_cols;
-    int32_t m = orc_route_row(n_inst, row, arow, crow, col, w_cost, w_lat, NULL);
+    int32_t m = tau ? orc_route_row_constrained(n_inst, row, tau[i], arow, crow, col, w_cost)
+                    : orc_route_row(n_inst, row, arow, crow, col, w_cost, w_lat, NULL);
     choice[i] = m;
     if (ttft_chosen) ttft_chosen[i] = row[m];
     if (util_chosen) {
@@ -433,5 +482,23 @@ int orc_stats(int32_t n_q, const int32_t *choice, const double *ttft_chosen, con
   out5[3] = s[k50];
   out5[4] = s[k99];
   free(s);
+  return ORC_OK;
+}
+
+/* Eq. 4: left fold in query order of the utility (Eq. 2) at the chosen instance
+ * for queries whose TTFT at the choice is within the target, divided by N. */
+int orc_ontime_utility(int32_t n_q, const int32_t *choice, const double *ttft_chosen,
+                       const double *tau, const double *acc, const double *cost, int32_t n_cols,
+                       const int32_t *col, double w_cost, double *out) {
+  if (n_q < 1) return ORC_E_ARG;
+  double s = 0.0;
+  for (int32_t i = 0; i < n_q; ++i) {
+    if (!(ttft_chosen[i] <= tau[i])) continue;
+    double ac = acc[(int64_t)i * n_cols + col[choice[i]]];
+    double co = cost[(int64_t)i * n_cols + col[choice[i]]];
+    double pen = w_cost * co;
+    s = s + (ac - pen);
+  }
+  *out = s / (double)n_q;
   return ORC_OK;
 }

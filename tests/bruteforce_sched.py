@@ -137,8 +137,18 @@ def instances_of(wl):
     return out
 
 
-def trace(wl, scenario=0, n_q=None, reading=0):
-    """Sequential trace with the route computed by numpy (first maximum wins)."""
+def _pick_constrained(row, util, tau):
+    """Eq. 3 restated: the feasible instance with the best (utility, -index), or, if no
+    instance meets the target, the one with the smallest (TTFT, index)."""
+    feas = [j for j in range(len(row)) if row[j] <= tau]
+    if feas:
+        return max(feas, key=lambda j: (util[j], -j))
+    return min(range(len(row)), key=lambda j: (row[j], j))
+
+
+def trace(wl, scenario=0, n_q=None, reading=0, tau=None):
+    """Sequential trace with the route computed by numpy (first maximum wins), or by
+    the constrained rule of Eq. 3 when per-query targets ``tau`` are given."""
     insts = instances_of(wl)
     N = wl.n_q if n_q is None else n_q
     col = np.asarray(wl.col)
@@ -152,8 +162,11 @@ def trace(wl, scenario=0, n_q=None, reading=0):
         row = np.array([x.estimate(p, d, t, reading)[0] for x in insts])
         acc = wl.acc[i][col]
         cost = wl.cost[i][col]
-        u = (acc - wc * cost) - wlat * row
-        m = int(np.argmax(u))
+        if tau is None:
+            u = (acc - wc * cost) - wlat * row
+            m = int(np.argmax(u))
+        else:
+            m = _pick_constrained(row, acc - wc * cost, float(tau[i]))
         choices.append(m)
         rows.append(row)
         insts[m].append(p, d)

@@ -350,3 +350,117 @@ def test_error_paths():
     with pytest.raises(O.OracleError) as e:
         q.append(3, 1, queue_cap=1)
     assert e.value.code == O.E_CAPACITY
+
+
+# ------------------------------------------------------------------ constrained route (Eq. 3)
+def test_ttft_target_hand_values():
+    """TTFT targets (appendix on TTFT latency assignment), worked by hand:
+    p = 1000, u = 3, v = 1: 155 + 3.5 = 158.5, times 1, plus 3 -> 161.5;
+    p = 2000, u = 2.5, v = 1: 155 + 7 = 162, plus 2.5 -> 164.5;
+    p = 0, u = -100 (outside the drawn range), v = 1: 55 -> clipped up to 150;
+    p = 10^6, u = 1, v = 1: 3655 + 1 -> clipped down to 1120;
+    p = 0, u = 2, v = 0.5: 77.5 + 2 = 79.5 -> 150."""
+    assert O.ttft_target(1000, 3.0, 1.0) == 161.5
+    assert O.ttft_target(2000, 2.5, 1.0) == 164.5
+    assert O.ttft_target(0, -100.0, 1.0) == 150.0
+    assert O.ttft_target(10 ** 6, 1.0, 1.0) == 1120.0
+    assert O.ttft_target(0, 2.0, 0.5) == 150.0
+    p = np.array([1000, 2000, 0, 10 ** 6], np.int32)
+    got = O.ttft_targets(p, [3.0, 2.5, -100.0, 1.0], [1.0, 1.0, 1.0, 1.0])
+    assert list(got) == [161.5, 164.5, 150.0, 1120.0]
+
+
+@pytest.mark.parametrize("p", [0, 1000, 50000])
+def test_ttft_target_expectation(p):
+    """The paper gives E[tau] ~= 158 + 3.5e-3 * p ms for unclipped targets
+    (u ~ U(1, 5) ms, v ~ U(0.98, 1.02)); the sample mean of 200k targets is within
+    0.05 ms of it (standard error ~0.005 ms)."""
+    rng = np.random.default_rng(11)
+    n = 200_000
+    tau = O.ttft_targets(np.full(n, p, np.int32), rng.uniform(1, 5, n), rng.uniform(0.98, 1.02, n))
+    assert abs(tau.mean() - (158.0 + 3.5e-3 * p)) < 0.05
+    assert tau.min() >= 150.0 and tau.max() <= 1120.0
+
+
+def test_constrained_route_hand_cases():
+    """Eq. 3 on hand-made rows (utility = acc - 0.5 * cost, one column per instance):
+    utilities [0.9, 0.1, 0.5], TTFT [5, 3, 9]."""
+    col = np.array([0, 1, 2], np.int32)
+    acc, cost = np.array([1.0, 0.2, 0.75]), np.array([0.2, 0.2, 0.5])
+    ttft = np.array([5.0, 3.0, 9.0])
+    # only instance 1 meets tau = 4, although instance 0 has the higher utility
+    assert O.route_row_constrained(ttft, 4.0, acc, cost, col, 0.5) == 1
+    # the target is inclusive: tau = 5 admits instance 0, the best utility
+    assert O.route_row_constrained(ttft, 5.0, acc, cost, col, 0.5) == 0
+    # everything feasible: plain argmax of the utility
+    assert O.route_row_constrained(ttft, 100.0, acc, cost, col, 0.5) == 0
+    # nothing feasible: least estimated TTFT
+    assert O.route_row_constrained(ttft, 2.0, acc, cost, col, 0.5) == 1
+    # ties: equal utilities -> lower index; equal TTFT with nothing feasible -> lower index
+    assert O.route_row_constrained(np.array([1.0, 1.0]), 5.0, np.array([0.5, 0.5]),
+                                   np.zeros(2), np.array([0, 1], np.int32), 1.0) == 0
+    assert O.route_row_constrained(np.array([7.0, 7.0, 8.0]), 5.0, acc, cost, col, 0.5) == 0
+    # feasible set {2} only (instance 2 is the slowest but the only one within tau)
+    assert O.route_row_constrained(np.array([9.0, 9.5, 4.0]), 5.0, acc, cost, col, 0.5) == 2
+
+
+def test_constrained_route_special_cases_and_definition():
+    """tau = +inf reduces Eq. 3 to the Lagrangian route with delta = 0 (pinned above);
+    tau = -inf to numpy's argmin of the TTFT; random rows with coarse values (many
+    ties) match the set-based statement of Eq. 3."""
+    rng = np.random.default_rng(12)
+    for _ in range(500):
+        I = int(rng.integers(1, 30))
+        n_cols = int(rng.integers(1, 4))
+        col = rng.integers(0, n_cols, size=I).astype(np.int32)
+        ttft = rng.integers(0, 6, size=I) * 0.5
+        acc = rng.integers(0, 4, size=n_cols) / 4.0
+        cost = rng.integers(0, 4, size=n_cols) / 4.0
+        wc = float(rng.integers(0, 3)) / 2
+        m_inf = O.route_row_constrained(ttft, np.inf, acc, cost, col, wc)
+        assert m_inf == O.route_row(ttft, acc, cost, col, wc, 0.0)[0]
+        assert O.route_row_constrained(ttft, -np.inf, acc, cost, col, wc) == int(np.argmin(ttft))
+        tau = float(rng.integers(0, 6)) * 0.5
+        util = acc[col] - wc * cost[col]
+        assert O.route_row_constrained(ttft, tau, acc, cost, col, wc) == \
+            BF._pick_constrained(ttft, util, tau)
+
+
+def test_ontime_utility_cases():
+    """Eq. 4: with every TTFT within its target it is the mean utility of the stats
+    (same fold), with none it is 0, and a hand case: utilities [0.5, -0.25, 1.0],
+    on time [yes, yes, no] -> (0.5 - 0.25) / 3."""
+    rng = np.random.default_rng(13)
+    n, n_cols = 257, 3
+    col = np.array([0, 1, 2, 2], np.int32)
+    choice = rng.integers(0, 4, size=n).astype(np.int32)
+    ttft = rng.random(n) * 100
+    acc, cost = rng.random((n, n_cols)), rng.random((n, n_cols))
+    s = O.stats(choice, ttft, acc, cost, col, 0.3)
+    assert O.ontime_utility(choice, ttft, np.full(n, np.inf), acc, cost, col, 0.3) == s[2]
+    assert O.ontime_utility(choice, ttft, np.full(n, -np.inf), acc, cost, col, 0.3) == 0.0
+    acc3 = np.array([[0.5], [0.0], [1.0]])
+    cost3 = np.array([[0.0], [0.25], [0.0]])
+    got = O.ontime_utility(np.zeros(3, np.int32), np.array([1.0, 2.0, 3.0]),
+                           np.array([1.0, 5.0, 2.5]), acc3, cost3, np.array([0], np.int32), 1.0)
+    assert got == (0.5 - 0.25) / 3
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_bruteforce_constrained_traces(seed):
+    """Whole traces under Eq. 3 against the token-at-a-time scheduler with the
+    set-based route; targets drawn inside the range of the TTFTs so that both the
+    feasible branch and the empty-set fallback occur."""
+    wl = make_tiny_workload(200 + seed, n_inst=3, max_res=5, n_q=25, dyadic=(seed % 2 == 0),
+                            n_scen=1)
+    lam = O.trace(wl, full_rows=True, queue_cap=10 ** 6)
+    lo, hi = float(lam.ttft_all.min()), float(lam.ttft_all.max())
+    tau = np.random.default_rng(seed).uniform(lo, hi, size=wl.n_q)
+    r = O.trace(wl, full_rows=True, queue_cap=10 ** 6, tau=tau)
+    ch, rows, insts = BF.trace(wl, tau=tau)
+    np.testing.assert_array_equal(r.choice, ch)
+    assert np.array_equal(r.ttft_all.view(np.int64), rows.view(np.int64))
+    for j, x in enumerate(insts):
+        a, b = r.offsets[j], r.offsets[j + 1]
+        got = list(zip(r.rem_prefill[a:b], r.rem_decode[a:b], r.context[a:b]))
+        assert [tuple(int(v) for v in g) for g in got] == x.state()

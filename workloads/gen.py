@@ -8,6 +8,10 @@ Draw order for a config (one ``np.random.default_rng(seed)`` stream):
   3. accuracy predictions;
   4. cost predictions (only the uniform layout draws; the token-price layout is a
      deterministic function of the query lengths).
+Two more streams draw the per-query variables of the TTFT targets (appendix on
+TTFT latency assignment): ``default_rng([seed, 1])`` u ~ U(1, 5) ms and
+``default_rng([seed, 2])`` v ~ U(0.98, 1.02), [N] each.  The targets themselves are computed by the
+library and by the oracle, not here.
 
 Initial resident queue of an instance, in arrival (FCFS) order:
   * the first n_dec = min(R // 2, M - 1) requests are decoding:
@@ -57,6 +61,9 @@ class Workload:
     # routing weights per scenario
     w_cost: np.ndarray        # float64 [Z]   (lambda)
     w_lat_ms: np.ndarray      # float64 [Z]   (delta per ms = delta_per_s / 1000)
+    # draws of the TTFT targets, [N]
+    tau_u_ms: np.ndarray
+    tau_v: np.ndarray
     queue_cap: int
     max_prompt: int
     meta: dict = field(default_factory=dict)
@@ -72,6 +79,12 @@ class Workload:
     def instance_requests(self, j: int):
         lo, hi = int(self.offsets[j]), int(self.offsets[j + 1])
         return (self.rem_prefill[lo:hi], self.rem_decode[lo:hi], self.context[lo:hi])
+
+
+def _draw_target_vars(seed, n):
+    u = np.random.default_rng([int(seed), 1]).uniform(1.0, 5.0, size=n)
+    v = np.random.default_rng([int(seed), 2]).uniform(0.98, 1.02, size=n)
+    return np.ascontiguousarray(u), np.ascontiguousarray(v)
 
 
 def _draw_prompts(rng, spec, size):
@@ -173,6 +186,7 @@ def _build(cfg: dict) -> Workload:
         raise ValueError(cfg["cost"])
 
     w = np.asarray(cfg["weights"], np.float64).reshape(-1, 2)
+    tau_u, tau_v = _draw_target_vars(cfg["seed"], N)
     return Workload(
         name=cfg["name"], n_scen=int(w.shape[0]), n_inst=I,
         a=np.array([types[t]["a"] for t in tof]), b=np.array([types[t]["b"] for t in tof]),
@@ -188,6 +202,7 @@ def _build(cfg: dict) -> Workload:
         q_prefill=q_prefill, q_decode=q_decode, q_t_ms=t_ms,
         acc=np.ascontiguousarray(acc), cost=np.ascontiguousarray(cost),
         w_cost=np.ascontiguousarray(w[:, 0]), w_lat_ms=np.ascontiguousarray(w[:, 1] / 1000.0),
+        tau_u_ms=tau_u, tau_v=tau_v,
         queue_cap=int(cfg["queue_cap"]), max_prompt=int(cfg["max_prompt"]),
         meta=cfg,
     )
@@ -258,6 +273,7 @@ def make_tiny_workload(seed: int, *, n_inst: int = 3, max_res: int = 4, budget=(
         context=np.concatenate(cxs) if cxs else np.zeros(0, np.int32),
         clock_ms=np.zeros(I), q_prefill=q_prefill, q_decode=q_decode, q_t_ms=t_ms,
         acc=acc, cost=cost, w_cost=w_cost, w_lat_ms=w_lat,
+        tau_u_ms=_draw_target_vars(seed, n_q)[0], tau_v=_draw_target_vars(seed, n_q)[1],
         queue_cap=max_res + n_q + 1, max_prompt=int(prompt[1]),
         meta=dict(kind="tiny", seed=seed),
     )
