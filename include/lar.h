@@ -17,7 +17,10 @@
  * fused multiply-add; sums over batches are left folds in batch order.
  *
  * Routing follows the Lagrangian objective of Sec. 3 with the utility of Eq. 2:
- *     u_j = (acc_j - w_cost*cost_j) - w_lat*TTFT_j,   choice = lowest j with max u.
+ *     u_j = (acc_j - w_cost*cost_j) - w_lat*TTFT_j,   choice = lowest j with max u,
+ * or the constrained objective of Eq. 3 (the *_constrained calls): the lowest j of
+ * maximal utility acc_j - w_cost*cost_j among the instances with TTFT_j <= tau,
+ * and, when none is within the target tau, the lowest j of minimal TTFT_j.
  *
  * Conventions
  *  - Every call returns lar_status (LAR_OK == 0, errors < 0).
@@ -153,6 +156,33 @@ lar_status lar_route(lar_ctx *ctx, int32_t n_q, const double *ttft_ms, const dou
                      double *utility);
 
 /*
+ * Route under the constrained objective (Eq. 3, Sec. 3): per (z, q),
+ *   F = { j : ttft_ms[z][q][j] <= tau_ms[q] };
+ *   choice[z][q] = lowest j in F maximising acc[q][col_j] - w_cost[z]*cost[q][col_j]
+ *                  (Eq. 2) if F is not empty, else lowest j minimising ttft_ms[z][q][j].
+ *   ttft_ms  dev [Z][Q][I];  tau_ms dev [Q] TTFT targets (e.g. from lar_ttft_targets)
+ *   acc, cost dev [Q][n_cols];  w_cost dev [Z] (lambda of Eq. 2)
+ *   choice dev [Z][Q];  chosen_ttft, utility dev [Z][Q] as in lar_route (may be NULL)
+ * Errors: LAR_E_ARG for a null required pointer or n_cols not covering every
+ * instance's column.  NaN TTFTs are not supported.
+ */
+lar_status lar_route_constrained(lar_ctx *ctx, int32_t n_q, const double *ttft_ms,
+                                 const double *tau_ms, const double *acc, const double *cost,
+                                 int32_t n_cols, const double *w_cost, int32_t *choice,
+                                 double *chosen_ttft, double *utility);
+
+/*
+ * Per-query TTFT targets (appendix on TTFT latency assignment):
+ *   tau_ms[i] = min{1120, max{150, u_ms[i] + (155 + 3.5e-3*q_prefill[i])*v[i]}},
+ * evaluated in that order (155 + 3.5e-3*p first, then times v, then plus u), each
+ * operation binary64 round-to-nearest-even.  The caller draws u ~ U(1, 5) ms and
+ * v ~ U(0.98, 1.02) per query (seeded).  Needs no loaded state.
+ *   q_prefill dev [n] int32;  u_ms, v dev [n];  tau_ms dev [n] (output)
+ */
+lar_status lar_ttft_targets(lar_ctx *ctx, int32_t n, const int32_t *q_prefill,
+                            const double *u_ms, const double *v, double *tau_ms);
+
+/*
  * Commit one routed query and replay the instances to t_next_ms: in scenario z,
  * the query (q_prefill >= 1 prompt tokens, q_decode predicted decode tokens,
  * raised to 1) joins the FCFS tail of instance choice[z] as a waiting request
@@ -183,6 +213,22 @@ lar_status lar_route_trace(lar_ctx *ctx, int32_t n_q, const int32_t *q_prefill,
                            double *chosen_ttft, double *utility);
 
 /*
+ * lar_route_trace under the constrained objective (Eq. 3; see
+ * lar_route_constrained), with query i's TTFT target tau_ms[i]:
+ *   for i in 0..N-1:
+ *     lar_estimate_ttft(1 query q_prefill[i], t = q_t_ms[i])
+ *     lar_route_constrained(row i, tau_ms[i]) -> choice[z][i]
+ *     lar_commit(choice[.][i], q_prefill[i], q_decode[i], t_next)
+ *   tau_ms dev [N]; the other arguments as in lar_route_trace (no w_lat).
+ */
+lar_status lar_route_trace_constrained(lar_ctx *ctx, int32_t n_q, const int32_t *q_prefill,
+                                       const int32_t *q_decode, const double *q_t_ms,
+                                       double t_after_ms, const double *tau_ms,
+                                       const double *acc, const double *cost, int32_t n_cols,
+                                       const double *w_cost, int32_t *choice,
+                                       double *chosen_ttft, double *utility);
+
+/*
  * Per-scenario summary of a routed trace -- the two axes of the utility-latency
  * trade-off of Sec. 3, E[U] and E[L]:
  *   stats[z] = { mean acc, mean cost, mean (acc - w_cost[z]*cost) (Eq. 2),
@@ -195,6 +241,21 @@ lar_status lar_route_trace(lar_ctx *ctx, int32_t n_q, const int32_t *q_prefill,
 lar_status lar_stats(lar_ctx *ctx, int32_t n_q, const int32_t *choice, const double *chosen_ttft,
                      const double *acc, const double *cost, int32_t n_cols,
                      const double *w_cost, double *stats);
+
+/*
+ * OnTimeUtility (Eq. 4) of a routed trace, per scenario:
+ *   out[z] = (1/N) * sum over i, in query order, of
+ *            (acc[i][col_c] - w_cost[z]*cost[i][col_c]) if chosen_ttft[z][i] <= tau_ms[i],
+ *            c = choice[z][i]; queries past their target add nothing.
+ * The TTFT at the choice stands for the realised TTFT: the replay runs the same
+ * scheduler, and under FCFS a later query never takes budget ahead of an earlier one.
+ *   choice, chosen_ttft dev [Z][N];  tau_ms dev [N];  acc, cost dev [N][n_cols]
+ *   w_cost dev [Z];  out dev [Z] float64
+ */
+lar_status lar_ontime_utility(lar_ctx *ctx, int32_t n_q, const int32_t *choice,
+                              const double *chosen_ttft, const double *tau_ms, const double *acc,
+                              const double *cost, int32_t n_cols, const double *w_cost,
+                              double *out);
 
 /*
  * Copy scenario `scen`'s state out (synchronises): resident requests of every

@@ -370,22 +370,52 @@ lar_status lar_estimate_ttft(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill
   return LAR_OK;
 }
 
-lar_status lar_route(lar_ctx* ctx, int32_t n_q, const double* ttft_ms, const double* acc,
-                     const double* cost, int32_t n_cols, const double* w_cost,
-                     const double* w_lat, int32_t* choice, double* chosen_ttft,
-                     double* utility) {
+// Row argmax, Lagrangian (tau == nullptr, w_lat given) or constrained (tau given).
+static lar_status route_rows(lar_ctx* ctx, int32_t n_q, const double* ttft_ms,
+                             const double* tau_ms, const double* acc, const double* cost,
+                             int32_t n_cols, const double* w_cost, const double* w_lat,
+                             int32_t* choice, double* chosen_ttft, double* utility) {
   lar_status st = ready(ctx);
   if (st != LAR_OK) return st;
   if (n_q < 0) return fail(ctx, LAR_E_ARG, "n_q < 0");
   if (n_q == 0) return LAR_OK;
-  if (!ttft_ms || !acc || !cost || !w_cost || !w_lat || !choice)
+  if (!ttft_ms || !acc || !cost || !w_cost || !choice || (!tau_ms && !w_lat))
     return fail(ctx, LAR_E_ARG, "null argument");
   if (n_cols <= ctx->max_col)
     return fail(ctx, LAR_E_ARG, "n_cols %d does not cover instance column %d", n_cols, ctx->max_col);
   if ((int64_t)ctx->Z * n_q > INT32_MAX) return fail(ctx, LAR_E_ARG, "too many rows");
   const LaunchEnv env = env_of(ctx);
   HIP_TRY(ctx, lar::launch_route(env, n_q, ttft_ms, (int64_t)n_q * ctx->I, acc, cost, n_cols,
-                                 w_cost, w_lat, choice, chosen_ttft, utility, n_q, 0));
+                                 w_cost, tau_ms ? w_cost : w_lat, tau_ms, choice, chosen_ttft,
+                                 utility, n_q, 0));
+  return LAR_OK;
+}
+
+lar_status lar_route(lar_ctx* ctx, int32_t n_q, const double* ttft_ms, const double* acc,
+                     const double* cost, int32_t n_cols, const double* w_cost,
+                     const double* w_lat, int32_t* choice, double* chosen_ttft,
+                     double* utility) {
+  if (ctx && !w_lat) return fail(ctx, LAR_E_ARG, "null argument");
+  return route_rows(ctx, n_q, ttft_ms, nullptr, acc, cost, n_cols, w_cost, w_lat, choice,
+                    chosen_ttft, utility);
+}
+
+lar_status lar_route_constrained(lar_ctx* ctx, int32_t n_q, const double* ttft_ms,
+                                 const double* tau_ms, const double* acc, const double* cost,
+                                 int32_t n_cols, const double* w_cost, int32_t* choice,
+                                 double* chosen_ttft, double* utility) {
+  if (ctx && !tau_ms) return fail(ctx, LAR_E_ARG, "null argument");
+  return route_rows(ctx, n_q, ttft_ms, tau_ms, acc, cost, n_cols, w_cost, nullptr, choice,
+                    chosen_ttft, utility);
+}
+
+lar_status lar_ttft_targets(lar_ctx* ctx, int32_t n, const int32_t* q_prefill,
+                            const double* u_ms, const double* v, double* tau_ms) {
+  if (!ctx) return LAR_E_ARG;
+  if (n < 0) return fail(ctx, LAR_E_ARG, "n < 0");
+  if (n == 0) return LAR_OK;
+  if (!q_prefill || !u_ms || !v || !tau_ms) return fail(ctx, LAR_E_ARG, "null argument");
+  HIP_TRY(ctx, lar::launch_targets(ctx->stream, n, q_prefill, u_ms, v, tau_ms));
   return LAR_OK;
 }
 
@@ -401,16 +431,17 @@ lar_status lar_commit(lar_ctx* ctx, const int32_t* choice, int32_t q_prefill, in
   return LAR_OK;
 }
 
-lar_status lar_route_trace(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill,
-                           const int32_t* q_decode, const double* q_t_ms, double t_after_ms,
-                           const double* acc, const double* cost, int32_t n_cols,
-                           const double* w_cost, const double* w_lat, int32_t* choice,
-                           double* chosen_ttft, double* utility) {
+static lar_status trace_rows(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill,
+                             const int32_t* q_decode, const double* q_t_ms, double t_after_ms,
+                             const double* tau_ms, const double* acc, const double* cost,
+                             int32_t n_cols, const double* w_cost, const double* w_lat,
+                             int32_t* choice, double* chosen_ttft, double* utility) {
   lar_status st = ready(ctx);
   if (st != LAR_OK) return st;
   if (n_q < 0) return fail(ctx, LAR_E_ARG, "n_q < 0");
   if (n_q == 0) return LAR_OK;
-  if (!q_prefill || !q_decode || !q_t_ms || !acc || !cost || !w_cost || !w_lat || !choice)
+  if (!q_prefill || !q_decode || !q_t_ms || !acc || !cost || !w_cost || !choice ||
+      (!tau_ms && !w_lat))
     return fail(ctx, LAR_E_ARG, "null argument");
   if (n_cols <= ctx->max_col)
     return fail(ctx, LAR_E_ARG, "n_cols %d does not cover instance column %d", n_cols, ctx->max_col);
@@ -426,12 +457,33 @@ lar_status lar_route_trace(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill,
   ta.cost = cost;
   ta.n_cols = n_cols;
   ta.w_cost = w_cost;
-  ta.w_lat = w_lat;
+  ta.w_lat = tau_ms ? w_cost : w_lat;   // unused under the constrained objective
+  ta.tau = tau_ms;
   ta.choice = choice;
   ta.chosen_ttft = chosen_ttft;
   ta.utility = utility;
   HIP_TRY(ctx, lar::launch_trace(env, ta));
   return LAR_OK;
+}
+
+lar_status lar_route_trace(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill,
+                           const int32_t* q_decode, const double* q_t_ms, double t_after_ms,
+                           const double* acc, const double* cost, int32_t n_cols,
+                           const double* w_cost, const double* w_lat, int32_t* choice,
+                           double* chosen_ttft, double* utility) {
+  if (ctx && !w_lat) return fail(ctx, LAR_E_ARG, "null argument");
+  return trace_rows(ctx, n_q, q_prefill, q_decode, q_t_ms, t_after_ms, nullptr, acc, cost, n_cols,
+                    w_cost, w_lat, choice, chosen_ttft, utility);
+}
+
+lar_status lar_route_trace_constrained(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill,
+                                       const int32_t* q_decode, const double* q_t_ms,
+                                       double t_after_ms, const double* tau_ms, const double* acc,
+                                       const double* cost, int32_t n_cols, const double* w_cost,
+                                       int32_t* choice, double* chosen_ttft, double* utility) {
+  if (ctx && !tau_ms) return fail(ctx, LAR_E_ARG, "null argument");
+  return trace_rows(ctx, n_q, q_prefill, q_decode, q_t_ms, t_after_ms, tau_ms, acc, cost, n_cols,
+                    w_cost, nullptr, choice, chosen_ttft, utility);
 }
 
 lar_status lar_stats(lar_ctx* ctx, int32_t n_q, const int32_t* choice, const double* chosen_ttft,
@@ -446,6 +498,23 @@ lar_status lar_stats(lar_ctx* ctx, int32_t n_q, const int32_t* choice, const dou
     return fail(ctx, LAR_E_ARG, "n_cols %d does not cover instance column %d", n_cols, ctx->max_col);
   const LaunchEnv env = env_of(ctx);
   HIP_TRY(ctx, lar::launch_stats(env, n_q, choice, chosen_ttft, acc, cost, n_cols, w_cost, stats));
+  return LAR_OK;
+}
+
+lar_status lar_ontime_utility(lar_ctx* ctx, int32_t n_q, const int32_t* choice,
+                              const double* chosen_ttft, const double* tau_ms, const double* acc,
+                              const double* cost, int32_t n_cols, const double* w_cost,
+                              double* out) {
+  lar_status st = ready(ctx);
+  if (st != LAR_OK) return st;
+  if (n_q < 1) return fail(ctx, LAR_E_ARG, "n_q < 1");
+  if (!choice || !chosen_ttft || !tau_ms || !acc || !cost || !w_cost || !out)
+    return fail(ctx, LAR_E_ARG, "null argument");
+  if (n_cols <= ctx->max_col)
+    return fail(ctx, LAR_E_ARG, "n_cols %d does not cover instance column %d", n_cols, ctx->max_col);
+  const LaunchEnv env = env_of(ctx);
+  HIP_TRY(ctx, lar::launch_ontime(env, n_q, choice, chosen_ttft, tau_ms, acc, cost, n_cols, w_cost,
+                                  out));
   return LAR_OK;
 }
 

@@ -19,11 +19,36 @@
 
 namespace lar {
 
-// Total order for the argmax: larger utility first, then the lower instance index;
-// j < 0 marks "no candidate".  Written without branches so a lane-wise use stays a
-// few selects.
-__device__ __forceinline__ bool better(double u1, int j1, double u2, int j2) {
-  return (j1 >= 0) & ((j2 < 0) | (u1 > u2) | ((u1 == u2) & (j1 < j2)));
+// Candidates of the argmax are (value, key) pairs.  The key is the instance index
+// j, with bit 30 set when the candidate misses its TTFT target under the
+// constrained objective (Eq. 3); a negative key means "no candidate".  The order:
+// a candidate meeting its target beats one that misses it, then the larger value,
+// then the lower index.  Under the Lagrangian objective every key is the bare
+// index and the value is the Lagrangian utility; under Eq. 3 the value is the
+// utility of Eq. 2 for a candidate meeting its target and -TTFT otherwise (so the
+// empty feasible set falls back to the least estimated TTFT).  Written without
+// branches so a lane-wise use stays a few selects.
+constexpr int kLateBit = 1 << 30;
+__device__ __forceinline__ int key_index(int k) { return k & (kLateBit - 1); }
+
+__device__ __forceinline__ bool better(double u1, int k1, double u2, int k2) {
+  const int c1 = k1 >> 30, c2 = k2 >> 30;
+  return (k1 >= 0) &
+         ((k2 < 0) | (c1 < c2) | ((c1 == c2) & ((u1 > u2) | ((u1 == u2) & (k1 < k2)))));
+}
+
+// Value and key of instance j for one query: eq2 = acc - w_cost*cost (Eq. 2).
+// tau == nullptr: Lagrangian objective, value eq2 - w_lat*ttft; else Eq. 3 with the
+// query's target *tau.
+__device__ __forceinline__ double cand_value(double eq2, double ttft, double wl,
+                                             const double* tau, double tq, int j, int* key) {
+  if (!tau) {
+    *key = j;
+    return __dsub_rn(eq2, __dmul_rn(wl, ttft));
+  }
+  const bool ok = ttft <= tq;
+  *key = ok ? j : (j | kLateBit);
+  return ok ? eq2 : -ttft;
 }
 
 // One butterfly step of the lane argmax: take the partner lane's candidate (DPP
@@ -216,8 +241,9 @@ __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double
                                               int64_t ttft_zstride, const double* acc,
                                               const double* cost, int n_cols, const int32_t* col,
                                               const double* w_cost, const double* w_lat,
-                                              int32_t* choice, double* chosen_ttft,
-                                              double* utility, int64_t out_zstride, int out_q0) {
+                                              const double* tau, int32_t* choice,
+                                              double* chosen_ttft, double* utility,
+                                              int64_t out_zstride, int out_q0) {
   __shared__ double s_u[256 / kWave];
   __shared__ int s_j[256 / kWave];
   const int row = blockIdx.x;   // z * Q + q
@@ -228,14 +254,15 @@ __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double
   const double* trow = ttft + (int64_t)z * ttft_zstride + (int64_t)q * I;
   const double* arow = acc + (int64_t)q * n_cols;
   const double* crow = cost + (int64_t)q * n_cols;
+  const double tq = tau ? tau[q] : 0.0;
   double bu = 0.0;
   int bj = -1;
   for (int j = threadIdx.x; j < I; j += blockDim.x) {
     const int c = col[j];
-    const double pen = __dmul_rn(wc, crow[c]);
-    double u = __dsub_rn(arow[c], pen);
-    u = __dsub_rn(u, __dmul_rn(wl, trow[j]));
-    if (bj < 0 || u > bu) { bu = u; bj = j; }
+    const double eq2 = __dsub_rn(arow[c], __dmul_rn(wc, crow[c]));
+    int k;
+    const double u = cand_value(eq2, trow[j], wl, tau, tq, j, &k);
+    if (better(u, k, bu, bj)) { bu = u; bj = k; }
   }
 #pragma unroll
   for (int o = kWave / 2; o > 0; o >>= 1) {
@@ -250,6 +277,7 @@ __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double
     for (int w = 1; w < (int)(blockDim.x / kWave); ++w)
       if (better(s_u[w], s_j[w], bu, bj)) { bu = s_u[w]; bj = s_j[w]; }
     const int64_t o = (int64_t)z * out_zstride + out_q0 + q;
+    bj = bj >= 0 ? key_index(bj) : -1;
     choice[o] = bj;
     if (bj >= 0) {
       if (chosen_ttft) chosen_ttft[o] = trow[bj];
@@ -415,20 +443,23 @@ __device__ __forceinline__ double estimate(const Queue<KS>& q, const QEnv& e, in
 // l-th owned instance.
 struct QueryIn {
   int p, d;
-  double t, tn;
+  double t, tn, tau;
   double acc_l, cost_l;   // per lane
 };
 
 __device__ __forceinline__ QueryIn fetch_query(int i, int N, const int32_t* qp, const int32_t* qd,
                                                const double* qt, double t_after,
-                                               const double* acc, const double* cost,
-                                               int n_cols, int col_l, bool own_l) {
+                                               const double* tau, const double* acc,
+                                               const double* cost, int n_cols, int col_l,
+                                               bool own_l) {
   QueryIn q;
+  q.tau = 0.0;
   if (i < N) {
     q.p = qp[i];
     q.d = qd[i];
     q.t = qt[i];
     q.tn = (i + 1 < N) ? qt[i + 1] : t_after;
+    if (tau) q.tau = tau[i];
     const int64_t o = (int64_t)i * n_cols + col_l;
     q.acc_l = own_l ? acc[o] : 0.0;
     q.cost_l = own_l ? cost[o] : 0.0;
@@ -446,12 +477,13 @@ __device__ __forceinline__ double read_lane_f64(double v, int l) {
 }
 
 __device__ __forceinline__ double utility_lane(const QueryIn& q, int l, double wc, double wl,
-                                               double ttft, double* eq2) {
+                                               const double* tau, double ttft, int j, int* key,
+                                               double* eq2) {
   const double a = read_lane_f64(q.acc_l, l);
   const double c = read_lane_f64(q.cost_l, l);
   const double u = __dsub_rn(a, __dmul_rn(wc, c));
   *eq2 = u;
-  return __dsub_rn(u, __dmul_rn(wl, ttft));
+  return cand_value(u, ttft, wl, tau, q.tau, j, key);
 }
 
 // Workgroup argmax over the waves' candidates (double-buffered by query parity, so
@@ -472,6 +504,7 @@ __device__ __forceinline__ int trace_pick(double bu, int bj, double bt, double b
     if (better(s_u[buf][v], s_j[buf][v], mu, m)) {
       mu = s_u[buf][v]; m = s_j[buf][v]; mt = s_t[buf][v]; mq = s_q[buf][v];
     }
+  m = m >= 0 ? key_index(m) : -1;
   if (threadIdx.x == 0) {
     const int64_t o = (int64_t)z * N + i;
     choice[o] = m;
@@ -484,8 +517,9 @@ __device__ __forceinline__ int trace_pick(double bu, int bj, double bt, double b
 #define LAR_TRACE_PARAMS                                                                     \
   DevState S, DevParams pr, int Z, int I, int N, const int32_t *qp, const int32_t *qd,       \
       const double *qt, double t_after, const double *acc, const double *cost, int n_cols,   \
-      const double *w_cost, const double *w_lat, int reading, int max_prompt,                \
-      int64_t max_iters, int32_t *choice, double *chosen_ttft, double *utility, int32_t *err
+      const double *w_cost, const double *w_lat, const double *tau, int reading,             \
+      int max_prompt, int64_t max_iters, int32_t *choice, double *chosen_ttft,               \
+      double *utility, int32_t *err
 
 // The same trace for pools too large to keep in registers: each owned instance's
 // state is loaded from HBM (L2) when it is needed and written back after its commit.
@@ -504,10 +538,10 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
   const int j_l = wid + ln * nw;
   const bool own_l = j_l < I;
   const int col_l = own_l ? pr.col[j_l] : 0;
-  QueryIn nx = fetch_query(0, N, qp, qd, qt, t_after, acc, cost, n_cols, col_l, own_l);
+  QueryIn nx = fetch_query(0, N, qp, qd, qt, t_after, tau, acc, cost, n_cols, col_l, own_l);
   for (int i = 0; i < N; ++i) {
     const QueryIn q = nx;
-    nx = fetch_query(i + 1, N, qp, qd, qt, t_after, acc, cost, n_cols, col_l, own_l);
+    nx = fetch_query(i + 1, N, qp, qd, qt, t_after, tau, acc, cost, n_cols, col_l, own_l);
     const bool p_ok = q.p >= 1 && q.p <= max_prompt;
     if (!p_ok && threadIdx.x == 0) set_error(err, kErrArg);
     double bu = 0.0, bt = 0.0, bq = 0.0;
@@ -519,8 +553,9 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
       const double ttft = p_ok ? estimate(w, e, q.p, q.t, reading, max_iters, err)
                                : __builtin_nan("");
       double eq2;
-      const double u = utility_lane(q, v, wc, wl, ttft, &eq2);
-      if (bj < 0 || u > bu) { bu = u; bj = j; bt = ttft; bq = eq2; }
+      int k;
+      const double u = utility_lane(q, v, wc, wl, tau, ttft, j, &k, &eq2);
+      if (better(u, k, bu, bj)) { bu = u; bj = k; bt = ttft; bq = eq2; }
     }
     const int m = trace_pick<NW>(bu, bj, bt, bq, i, z, N, choice, chosen_ttft, utility, s_u,
                                  s_t, s_q, s_j);
@@ -539,21 +574,23 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
 template <int IPW>
 struct QueryBlock {
   int p, d;
-  double t;
+  double t, tau;
   double acc[IPW], cost[IPW];
 };
 
 template <int IPW>
 __device__ __forceinline__ QueryBlock<IPW> fetch_block(int base, int N, const int32_t* qp,
                                                        const int32_t* qd, const double* qt,
-                                                       const double* acc, const double* cost,
-                                                       int n_cols, const int* cols) {
+                                                       const double* tau, const double* acc,
+                                                       const double* cost, int n_cols,
+                                                       const int* cols) {
   QueryBlock<IPW> b;
   const int i = base + lane_id();
   const bool in = i < N;
   b.p = in ? qp[i] : 1;
   b.d = in ? qd[i] : 1;
   b.t = in ? qt[i] : 0.0;
+  b.tau = in && tau ? tau[i] : 0.0;
 #pragma unroll
   for (int r = 0; r < IPW; ++r) {
     const int64_t o = (int64_t)i * n_cols + cols[r];
@@ -569,8 +606,8 @@ struct Cand {
   int j;
 };
 
-__device__ __forceinline__ void cand_take(Cand& c, double u, int j, double ttft, double eq2) {
-  if (c.j < 0 || u > c.u) { c.u = u; c.j = j; c.ttft = ttft; c.eq2 = eq2; }
+__device__ __forceinline__ void cand_take(Cand& c, double u, int k, double ttft, double eq2) {
+  if (better(u, k, c.u, c.j)) { c.u = u; c.j = k; c.ttft = ttft; c.eq2 = eq2; }
 }
 
 // Candidate exchange between the workgroups of one scenario, run by one wave of
@@ -934,8 +971,8 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
       q.to_lds(sst[wid][r]);
     }
   }
-  QueryBlock<IPW> cur = fetch_block<IPW>(0, N, qp, qd, qt, acc, cost, n_cols, cols);
-  QueryBlock<IPW> nxt = fetch_block<IPW>(kWave, N, qp, qd, qt, acc, cost, n_cols, cols);
+  QueryBlock<IPW> cur = fetch_block<IPW>(0, N, qp, qd, qt, tau, acc, cost, n_cols, cols);
+  QueryBlock<IPW> nxt = fetch_block<IPW>(kWave, N, qp, qd, qt, tau, acc, cost, n_cols, cols);
   Cand c;
   c.j = -1; c.u = 0.0; c.ttft = 0.0; c.eq2 = 0.0;
   for (int i = -1; i < N; ++i) {
@@ -969,9 +1006,9 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
         bj = s_mj[buf];
         if (bj == -2) break;
       }
-      m = bj;
+      m = bj >= 0 ? key_index(bj) : -1;
       // the wave holding the winner (its own best) writes the outputs
-      const bool mine = m >= 0 ? c.j == m : (cid == 0 && wid == 0);
+      const bool mine = m >= 0 ? c.j == bj : (cid == 0 && wid == 0);
       if (mine && ln == 0) {
         const int64_t o = (int64_t)z * N + i;
         choice[o] = m;
@@ -1012,13 +1049,16 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
           const double a = read_lane_f64(in_nxt ? nxt.acc[r] : cur.acc[r], l1);
           const double co = read_lane_f64(in_nxt ? nxt.cost[r] : cur.cost[r], l1);
           const double eq2 = __dsub_rn(a, __dmul_rn(wc, co));
-          cand_take(c, __dsub_rn(eq2, __dmul_rn(wl, ttft)), j, ttft, eq2);
+          const double tq = tau ? read_lane_f64(in_nxt ? nxt.tau : cur.tau, l1) : 0.0;
+          int k;
+          const double u = cand_value(eq2, ttft, wl, tau, tq, j, &k);
+          cand_take(c, u, k, ttft, eq2);
         }
       }
     }
     if (last_in_block) {
       cur = nxt;
-      nxt = fetch_block<IPW>(i + 1 + kWave, N, qp, qd, qt, acc, cost, n_cols, cols);
+      nxt = fetch_block<IPW>(i + 1 + kWave, N, qp, qd, qt, tau, acc, cost, n_cols, cols);
     }
   }
 #pragma unroll
@@ -1128,6 +1168,62 @@ __global__ __launch_bounds__(256) void k_stats(int N, int I, const int32_t* choi
 }
 
 // A one-thread kernel instead of a memset node, so the clear can sit in a captured graph.
+// ------------------------------------------------------------------ targets, OnTimeUtility
+// TTFT target of each query (appendix on TTFT latency assignment), in the written
+// order: lin = 155 + 3.5e-3*p, raw = u + lin*v, clipped to [150, 1120] ms.
+__global__ __launch_bounds__(256) void k_targets(int n, const int32_t* p, const double* u_ms,
+                                                const double* v, double* tau) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const double lin = __dadd_rn(155.0, __dmul_rn(3.5e-3, (double)p[i]));
+  const double raw = __dadd_rn(u_ms[i], __dmul_rn(lin, v[i]));
+  const double lo = raw > 150.0 ? raw : 150.0;
+  tau[i] = lo < 1120.0 ? lo : 1120.0;
+}
+
+// OnTimeUtility (Eq. 4) per scenario: the utility of Eq. 2 at the chosen instance,
+// summed in query order over the queries whose TTFT at the choice is within the
+// target, divided by N.  The estimated TTFT stands for the realised one: the
+// replay runs the same scheduler, and a later arrival never takes a batch slot
+// ahead of an earlier one under FCFS.
+__global__ __launch_bounds__(256) void k_ontime(int N, int I, const int32_t* choice,
+                                               const double* chosen_ttft, const double* tau,
+                                               const double* acc, const double* cost, int n_cols,
+                                               const int32_t* col, const double* w_cost,
+                                               double* out) {
+  __shared__ double s_v[256];
+  __shared__ int s_on[256];
+  const int z = blockIdx.x;
+  const int32_t* ch = choice + (int64_t)z * N;
+  const double* tt = chosen_ttft + (int64_t)z * N;
+  const double wc = w_cost[z];
+  double s = 0.0;
+  for (int base = 0; base < N; base += 256) {
+    const int i = base + (int)threadIdx.x;
+    if (i < N) {
+      const int cj = ch[i];
+      const bool on = tt[i] <= tau[i];
+      s_on[threadIdx.x] = on;
+      if (cj >= 0 && cj < I) {
+        const int c = col[cj];
+        s_v[threadIdx.x] =
+            __dsub_rn(acc[(int64_t)i * n_cols + c], __dmul_rn(wc, cost[(int64_t)i * n_cols + c]));
+      } else {   // not a routed instance: poison the result
+        s_v[threadIdx.x] = __builtin_nan("");
+        s_on[threadIdx.x] = 1;
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {   // left fold in query order
+      const int m = N - base < 256 ? N - base : 256;
+      for (int r = 0; r < m; ++r)
+        if (s_on[r]) s = __dadd_rn(s, s_v[r]);
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[z] = __ddiv_rn(s, (double)N);
+}
+
 __global__ void k_clear_error(int32_t* err) { *err = 0; }
 
 // ------------------------------------------------------------------ launchers
@@ -1151,8 +1247,8 @@ static hipError_t launch_commit_ks(const LaunchEnv& env, const int32_t* choice,
 
 #define LAR_TRACE_ARGS                                                                   \
   env.S, env.P, env.Z, env.I, a.N, a.qp, a.qd, a.qt, a.t_after, a.acc, a.cost, a.n_cols,     \
-      a.w_cost, a.w_lat, env.reading, env.max_prompt, env.max_iters, a.choice, a.chosen_ttft, \
-      a.utility, env.err
+      a.w_cost, a.w_lat, a.tau, env.reading, env.max_prompt, env.max_iters, a.choice,        \
+      a.chosen_ttft, a.utility, env.err
 
 template <int KS, int NW>
 static hipError_t launch_trace_mem(const LaunchEnv& env, const TraceArgs& a) {
@@ -1255,11 +1351,25 @@ hipError_t launch_est(const LaunchEnv& env, int Q, const int32_t* q_prefill, con
 
 hipError_t launch_route(const LaunchEnv& env, int Q, const double* ttft, int64_t ttft_zstride,
                         const double* acc, const double* cost, int n_cols, const double* w_cost,
-                        const double* w_lat, int32_t* choice, double* chosen_ttft,
-                        double* utility, int64_t out_zstride, int out_q0) {
+                        const double* w_lat, const double* tau, int32_t* choice,
+                        double* chosen_ttft, double* utility, int64_t out_zstride, int out_q0) {
   hipLaunchKernelGGL(k_route, dim3(env.Z * Q), dim3(256), 0, env.stream, env.Z, Q, env.I, ttft,
-                     ttft_zstride, acc, cost, n_cols, env.P.col, w_cost, w_lat, choice,
+                     ttft_zstride, acc, cost, n_cols, env.P.col, w_cost, w_lat, tau, choice,
                      chosen_ttft, utility, out_zstride, out_q0);
+  return hipGetLastError();
+}
+
+hipError_t launch_targets(hipStream_t stream, int n, const int32_t* p, const double* u_ms,
+                          const double* v, double* tau) {
+  hipLaunchKernelGGL(k_targets, dim3((n + 255) / 256), dim3(256), 0, stream, n, p, u_ms, v, tau);
+  return hipGetLastError();
+}
+
+hipError_t launch_ontime(const LaunchEnv& env, int N, const int32_t* choice,
+                         const double* chosen_ttft, const double* tau, const double* acc,
+                         const double* cost, int n_cols, const double* w_cost, double* out) {
+  hipLaunchKernelGGL(k_ontime, dim3(env.Z), dim3(256), 0, env.stream, N, env.I, choice,
+                     chosen_ttft, tau, acc, cost, n_cols, env.P.col, w_cost, out);
   return hipGetLastError();
 }
 

@@ -33,6 +33,7 @@ struct TraceArgs {
   const double *acc, *cost;
   int n_cols;
   const double *w_cost, *w_lat;
+  const double* tau;   // per-query TTFT targets (constrained objective) or nullptr
   int32_t* choice;
   double *chosen_ttft, *utility;
 };
@@ -43,8 +44,13 @@ hipError_t launch_est(const LaunchEnv& env, int Q, const int32_t* q_prefill, con
                       double t_val, double* ttft, int32_t* iters);
 hipError_t launch_route(const LaunchEnv& env, int Q, const double* ttft, int64_t ttft_zstride,
                         const double* acc, const double* cost, int n_cols, const double* w_cost,
-                        const double* w_lat, int32_t* choice, double* chosen_ttft,
-                        double* utility, int64_t out_zstride, int out_q0);
+                        const double* w_lat, const double* tau, int32_t* choice,
+                        double* chosen_ttft, double* utility, int64_t out_zstride, int out_q0);
+hipError_t launch_targets(hipStream_t stream, int n, const int32_t* p, const double* u_ms,
+                          const double* v, double* tau);
+hipError_t launch_ontime(const LaunchEnv& env, int N, const int32_t* choice,
+                         const double* chosen_ttft, const double* tau, const double* acc,
+                         const double* cost, int n_cols, const double* w_cost, double* out);
 hipError_t launch_commit(const LaunchEnv& env, const int32_t* choice, int64_t choice_zstride,
                          const int32_t* qp_ptr, const int32_t* qd_ptr, int32_t qp, int32_t qd,
                          const double* t_ptr, double t_val);

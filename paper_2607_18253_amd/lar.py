@@ -19,8 +19,9 @@ LAR_OK, LAR_E_ARG, LAR_E_STATE, LAR_E_CAPACITY, LAR_E_ITER, LAR_E_HIP, LAR_E_SYN
 FIRST_TOKEN_DECODE_BATCH, FIRST_TOKEN_PREFILL_BATCH = 0, 1
 
 EXPORTED = ("lar_create", "lar_destroy", "lar_error_string", "lar_load_state", "lar_reload_state",
-            "lar_estimate_ttft", "lar_route", "lar_commit", "lar_route_trace", "lar_stats",
-            "lar_read_state", "lar_sync")
+            "lar_estimate_ttft", "lar_route", "lar_route_constrained", "lar_ttft_targets",
+            "lar_commit", "lar_route_trace", "lar_route_trace_constrained", "lar_stats",
+            "lar_ontime_utility", "lar_read_state", "lar_sync")
 
 
 class LarError(RuntimeError):
@@ -73,6 +74,15 @@ def load_library(path: str = LIB_PATH):
     L.lar_commit.argtypes = [vp, vp, i32, i32, dbl]
     L.lar_route_trace.restype = i32
     L.lar_route_trace.argtypes = [vp, i32, vp, vp, vp, dbl, vp, vp, i32, vp, vp, vp, vp, vp]
+    L.lar_route_constrained.restype = i32
+    L.lar_route_constrained.argtypes = [vp, i32, vp, vp, vp, vp, i32, vp, vp, vp, vp]
+    L.lar_ttft_targets.restype = i32
+    L.lar_ttft_targets.argtypes = [vp, i32, vp, vp, vp, vp]
+    L.lar_route_trace_constrained.restype = i32
+    L.lar_route_trace_constrained.argtypes = [vp, i32, vp, vp, vp, dbl, vp, vp, vp, i32, vp, vp,
+                                              vp, vp]
+    L.lar_ontime_utility.restype = i32
+    L.lar_ontime_utility.argtypes = [vp, i32, vp, vp, vp, vp, vp, i32, vp, vp]
     L.lar_stats.restype = i32
     L.lar_stats.argtypes = [vp, i32, vp, vp, vp, vp, i32, vp, vp]
     L.lar_read_state.restype = i32
@@ -207,6 +217,34 @@ class LarContext:
             _dev(utility, torch.float64, "utility", self.Z * Q)))
         return choice
 
+    def route_constrained(self, ttft, tau_ms, acc, cost, w_cost, choice=None, chosen_ttft=None,
+                          utility=None):
+        torch = self._torch
+        Q = int(acc.shape[0])
+        n_cols = int(acc.shape[1])
+        if choice is None:
+            choice = torch.empty((self.Z, Q), dtype=torch.int32, device=acc.device)
+        self._check(self._L.lar_route_constrained(
+            self._h, Q, _dev(ttft, torch.float64, "ttft", self.Z * Q * self.I),
+            _dev(tau_ms, torch.float64, "tau_ms", Q),
+            _dev(acc, torch.float64, "acc", Q * n_cols), _dev(cost, torch.float64, "cost", Q * n_cols),
+            n_cols, _dev(w_cost, torch.float64, "w_cost", self.Z),
+            _dev(choice, torch.int32, "choice", self.Z * Q),
+            _dev(chosen_ttft, torch.float64, "chosen_ttft", self.Z * Q),
+            _dev(utility, torch.float64, "utility", self.Z * Q)))
+        return choice
+
+    def ttft_targets(self, q_prefill, u_ms, v, out=None):
+        torch = self._torch
+        n = int(q_prefill.numel())
+        if out is None:
+            out = torch.empty(n, dtype=torch.float64, device=q_prefill.device)
+        self._check(self._L.lar_ttft_targets(
+            self._h, n, _dev(q_prefill, torch.int32, "q_prefill", n),
+            _dev(u_ms, torch.float64, "u_ms", n), _dev(v, torch.float64, "v", n),
+            _dev(out, torch.float64, "tau_ms", n)))
+        return out
+
     def commit(self, choice, q_prefill: int, q_decode: int, t_next_ms: float):
         torch = self._torch
         self._check(self._L.lar_commit(self._h, _dev(choice, torch.int32, "choice", self.Z),
@@ -233,6 +271,40 @@ class LarContext:
             _dev(chosen_ttft, torch.float64, "chosen_ttft", self.Z * N),
             _dev(utility, torch.float64, "utility", self.Z * N)))
         return choice
+
+    def route_trace_constrained(self, q_prefill, q_decode, q_t_ms, t_after_ms, tau_ms, acc, cost,
+                                w_cost, choice=None, chosen_ttft=None, utility=None):
+        torch = self._torch
+        N = int(q_prefill.numel())
+        n_cols = int(acc.shape[1])
+        if choice is None:
+            choice = torch.empty((self.Z, N), dtype=torch.int32, device=q_prefill.device)
+        self._check(self._L.lar_route_trace_constrained(
+            self._h, N, _dev(q_prefill, torch.int32, "q_prefill"),
+            _dev(q_decode, torch.int32, "q_decode", N), _dev(q_t_ms, torch.float64, "q_t_ms", N),
+            float(t_after_ms), _dev(tau_ms, torch.float64, "tau_ms", N),
+            _dev(acc, torch.float64, "acc", N * n_cols),
+            _dev(cost, torch.float64, "cost", N * n_cols), n_cols,
+            _dev(w_cost, torch.float64, "w_cost", self.Z),
+            _dev(choice, torch.int32, "choice", self.Z * N),
+            _dev(chosen_ttft, torch.float64, "chosen_ttft", self.Z * N),
+            _dev(utility, torch.float64, "utility", self.Z * N)))
+        return choice
+
+    def ontime_utility(self, choice, chosen_ttft, tau_ms, acc, cost, w_cost, out=None):
+        torch = self._torch
+        N = int(choice.shape[-1])
+        n_cols = int(acc.shape[1])
+        if out is None:
+            out = torch.empty(self.Z, dtype=torch.float64, device=choice.device)
+        self._check(self._L.lar_ontime_utility(
+            self._h, N, _dev(choice, torch.int32, "choice", self.Z * N),
+            _dev(chosen_ttft, torch.float64, "chosen_ttft", self.Z * N),
+            _dev(tau_ms, torch.float64, "tau_ms", N),
+            _dev(acc, torch.float64, "acc", N * n_cols), _dev(cost, torch.float64, "cost", N * n_cols),
+            n_cols, _dev(w_cost, torch.float64, "w_cost", self.Z),
+            _dev(out, torch.float64, "out", self.Z)))
+        return out
 
     def stats(self, choice, chosen_ttft, acc, cost, w_cost, out=None):
         torch = self._torch

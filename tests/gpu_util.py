@@ -46,3 +46,22 @@ def assert_state_equal(ctx, scen, ref):
     np.testing.assert_array_equal(st["context"], ref.context)
     np.testing.assert_array_equal(bits(st["clock_ms"]), bits(ref.clock_ms))
     np.testing.assert_array_equal(st["iterations"], ref.iterations)
+
+
+def gpu_trace_constrained(wl, tau, n_q=None, *, queue_cap=None):
+    """As gpu_trace, under the constrained objective (Eq. 3) with targets tau [N]."""
+    import torch
+    from paper_2607_18253_amd import context_for
+
+    N = wl.n_q if n_q is None else int(n_q)
+    ctx = context_for(wl, queue_cap=queue_cap)
+    ctx.advance(float(wl.q_t_ms[0]))
+    chosen = torch.full((wl.n_scen, N), -1.0, dtype=torch.float64, device=DEV)
+    util = torch.full((wl.n_scen, N), -1.0, dtype=torch.float64, device=DEV)
+    choice = ctx.route_trace_constrained(
+        T(wl.q_prefill[:N], torch.int32), T(wl.q_decode[:N], torch.int32),
+        T(wl.q_t_ms[:N], torch.float64), float(wl.q_t_ms[N - 1]), T(tau[:N], torch.float64),
+        T(wl.acc[:N], torch.float64), T(wl.cost[:N], torch.float64),
+        T(wl.w_cost, torch.float64), chosen_ttft=chosen, utility=util)
+    ctx.sync()
+    return choice.cpu().numpy(), chosen.cpu().numpy(), util.cpu().numpy(), ctx
