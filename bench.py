@@ -48,6 +48,9 @@ def _parse():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--n-q", type=int, default=None, help="shorten the trace (testing only)")
+    ap.add_argument("--objective", default="lagrangian", choices=["lagrangian", "constrained"],
+                    help="route by the Lagrangian objective or by Eq. 3 with the paper's "
+                         "per-query TTFT targets (sequential workloads)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="time budget of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -124,7 +127,7 @@ def dominant_kernel(workload):
     return "k_traj" if workload == "c3" else "k_trace_cl"
 
 
-def oracle_sample(wl, budget_s):
+def oracle_sample(wl, budget_s, tau=None):
     """The plain C oracle, single-threaded, on a prefix of the same trace (scenario 0).
 
     Returns the CPU baseline record and the oracle's count of simulated batches over
@@ -134,7 +137,7 @@ def oracle_sample(wl, budget_s):
     n = min(wl.n_q, 256)
     while True:
         t0 = time.perf_counter()
-        r = orc.trace(wl, scenario=0, n_q=n, full_rows=True, final_state=True)
+        r = orc.trace(wl, scenario=0, n_q=n, full_rows=True, final_state=True, tau=tau)
         dt = time.perf_counter() - t0
         if n >= wl.n_q or dt >= budget_s / 3:
             break
@@ -202,7 +205,12 @@ def main():
     ctx = context_for(wl)
     stream = ctx.stream
     whatif = args.workload == "c3"
+    constrained = args.objective == "constrained" and not whatif
     t_first, t_last = float(wl.q_t_ms[0]), float(wl.q_t_ms[-1])
+    tau = None
+    if constrained:   # the paper's per-query TTFT targets, computed once on the GPU
+        tau = ctx.ttft_targets(qp, T(wl.tau_u_ms, torch.float64), T(wl.tau_v, torch.float64))
+        ontime = torch.empty(Z, dtype=torch.float64, device=dev)
     if whatif:
         ttft = torch.empty((Z, N, I), dtype=torch.float64, device=dev)
     kev = []   # (start, end) events around the dominant kernel of each timed step
@@ -231,12 +239,18 @@ def main():
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-        ctx.route_trace(qp, qd, qt, t_last, acc, cost, wc, wlat, choice=choice,
-                        chosen_ttft=chosen, utility=util)
+        if constrained:
+            ctx.route_trace_constrained(qp, qd, qt, t_last, tau, acc, cost, wc, choice=choice,
+                                        chosen_ttft=chosen, utility=util)
+        else:
+            ctx.route_trace(qp, qd, qt, t_last, acc, cost, wc, wlat, choice=choice,
+                            chosen_ttft=chosen, utility=util)
         if record:
             e1.record(stream)
             kev.append((e0, e1))
         ctx.stats(choice, chosen, acc, cost, wc, out=stats)
+        if constrained:
+            ctx.ontime_utility(choice, chosen, tau, acc, cost, wc, out=ontime)
 
     for _ in range(args.warmup):
         step()
@@ -260,6 +274,8 @@ def main():
         "config": {"workload": f"{args.workload}: {wl.meta['title']}", "scenarios": Z,
                    "instances": I, "queries": N, "resident_per_instance": wl.meta["resident"],
                    "token_budget": int(wl.budget[0]), "max_seqs": int(wl.max_seqs[0]),
+                   "objective": "eq3-constrained" if constrained else
+                   ("what-if" if whatif else "lagrangian"),
                    "parallelism": "1 GPU"},
         "routed_queries_per_s": Z * N / (ms_per_step / 1000.0),
     }
@@ -268,6 +284,8 @@ def main():
     else:
         line["roofline_kernel"] = "k_trace_cl (lar_route_trace, one launch per step)"
         line["stats_scenario0"] = stats[0].tolist()
+        if constrained:
+            line["ontime_utility_scenario0"] = float(ontime[0])
     line["kernel_ms"] = kernel_ms
 
     roof = None
@@ -284,7 +302,8 @@ def main():
                             f"a literal per-pair SFS would simulate {batches_per_pair:.0f} "
                             "batches per pair"}
         else:
-            rec, n, batches = oracle_sample(wl, args.cpu_seconds)
+            rec, n, batches = oracle_sample(
+                wl, args.cpu_seconds, tau=None if tau is None else tau.cpu().numpy())
             line["cpu_baseline"] = rec
             if n == N:
                 flops = FLOPS_PER_BATCH * batches * Z
