@@ -230,6 +230,34 @@ def test_trace_c2_prefix():
     ctx.close()
 
 
+def test_trace_c2_full_bench_configuration():
+    """Config 2 at full size in the launch configuration bench.py times (100k queries,
+    32 instances, one trace launch): every choice, chosen TTFT and utility bit, and the
+    final state of every instance."""
+    wl = make_workload("c2")
+    choice, chosen, util, ctx = gpu_trace(wl)
+    ref = O.trace(wl)
+    np.testing.assert_array_equal(choice[0], ref.choice)
+    np.testing.assert_array_equal(bits(chosen[0]), bits(ref.ttft_chosen))
+    np.testing.assert_array_equal(bits(util[0]), bits(ref.util_chosen))
+    assert_state_equal(ctx, 0, ref)
+    ctx.close()
+
+
+def test_trace_c5_two_scenarios_1000():
+    """Config 5: all 64 scenarios routed together for 1000 queries; the two extreme
+    weight scenarios (0 and 63) checked in full, states included."""
+    wl = make_workload("c5", n_q=1000)
+    choice, chosen, util, ctx = gpu_trace(wl)
+    for z in (0, 63):
+        ref = O.trace(wl, scenario=z)
+        np.testing.assert_array_equal(choice[z], ref.choice, err_msg=f"scenario {z}")
+        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen))
+        np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
+        assert_state_equal(ctx, z, ref)
+    ctx.close()
+
+
 def test_trace_c4_prefix():
     wl = make_workload("c4", n_q=4)
     choice, chosen, util, ctx = gpu_trace(wl)
