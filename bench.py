@@ -46,7 +46,7 @@ def _parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5", "c6"])
     ap.add_argument("--n-q", type=int, default=None, help="shorten the trace (testing only)")
     ap.add_argument("--objective", default="lagrangian", choices=["lagrangian", "constrained"],
                     help="route by the Lagrangian objective or by Eq. 3 with the paper's "

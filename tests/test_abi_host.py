@@ -77,7 +77,7 @@ def _check_state(wl):
         assert np.sum(run) <= wl.max_seqs[j]
 
 
-@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5", "c6"])
 def test_generator_shapes_and_invariants(name):
     from workloads import make_workload
     kw = dict(n_q=500) if name != "c3" else {}

@@ -258,6 +258,19 @@ def test_trace_c5_two_scenarios_1000():
     ctx.close()
 
 
+def test_trace_c6_bursty_prefix():
+    """Config 6: the medium pool under MMPP-2 arrivals (bursts at 6x the low rate),
+    first 5000 queries."""
+    wl = make_workload("c6", n_q=5000)
+    choice, chosen, util, ctx = gpu_trace(wl)
+    ref = O.trace(wl)
+    np.testing.assert_array_equal(choice[0], ref.choice)
+    np.testing.assert_array_equal(bits(chosen[0]), bits(ref.ttft_chosen))
+    np.testing.assert_array_equal(bits(util[0]), bits(ref.util_chosen))
+    assert_state_equal(ctx, 0, ref)
+    ctx.close()
+
+
 def test_trace_c4_prefix():
     wl = make_workload("c4", n_q=4)
     choice, chosen, util, ctx = gpu_trace(wl)

@@ -86,6 +86,22 @@ CONFIGS = {
         weights=[(0.5, 0.01)],
         queue_cap=8192, max_prompt=131072, seed=0,
     ),
+    "c6": dict(
+        title="medium pool, bursty MMPP-2 arrivals",
+        n_inst=32, n_scen=1,
+        types=_scaled_types(),
+        type_of_inst=[j // 8 for j in range(32)],
+        budget=4096, max_seqs=256, resident=256,
+        prompt=("lognormal", 6.5, 1.0, 16, 32768), decode_mean=384,
+        n_q=100_000, rate_per_s=50.0,
+        # two-state Markov-modulated Poisson arrivals (appendix on correlated query
+        # arrivals): rate ratio r = 6, high-state fraction 0.2, transition rates
+        # L->H 0.1/s and H->L 0.4/s, long-run mean rate_per_s
+        arrivals=("mmpp2", 6.0, 0.2, 0.1, 0.4),
+        acc="per_type", cost="tokens_x_price",
+        weights=[(0.5, 1.0)],
+        queue_cap=8192, max_prompt=32768, seed=0,
+    ),
     "c5": dict(
         title="utility-weight sweep",
         n_inst=64, n_scen=64,

@@ -10,7 +10,10 @@ Draw order for a config (one ``np.random.default_rng(seed)`` stream):
      deterministic function of the query lengths).
 Two more streams draw the per-query variables of the TTFT targets (appendix on
 TTFT latency assignment): ``default_rng([seed, 1])`` u ~ U(1, 5) ms and
-``default_rng([seed, 2])`` v ~ U(0.98, 1.02), [N] each.  The targets themselves are computed by the
+``default_rng([seed, 2])`` v ~ U(0.98, 1.02), [N] each.  A config with MMPP-2
+arrivals (appendix on correlated query arrivals) still draws the Poisson gaps of
+step 2 and replaces the arrival times by an MMPP-2 path drawn from
+``default_rng([seed, 3])``, so its queries are those of the Poisson twin.  The targets themselves are computed by the
 library and by the oracle, not here.
 
 Initial resident queue of an instance, in arrival (FCFS) order:
@@ -87,6 +90,36 @@ def _draw_target_vars(seed, n):
     return np.ascontiguousarray(u), np.ascontiguousarray(v)
 
 
+def mmpp2_rates(mean_rate, r, p_high):
+    """Low- and high-state rates of a two-state Markov-modulated Poisson process with
+    long-run mean rate ``mean_rate``, rate ratio r = high/low and high-state time
+    fraction p_high (appendix on correlated query arrivals)."""
+    low = mean_rate / ((1.0 - p_high) + p_high * r)
+    return low, r * low
+
+
+def mmpp2_arrivals_ms(rng, n, mean_rate, r, p_high, z_lh, z_hl):
+    """n arrival times (ms, from t = 0) of an MMPP-2: a latent two-state Markov chain
+    (transition rates z_lh and z_hl per second, started from its stationary law)
+    modulating Poisson arrivals at the low or high rate.  Competing exponential
+    clocks: the next event is an arrival with probability rate / (rate + switch)."""
+    low, high = mmpp2_rates(mean_rate, r, p_high)
+    state = 1 if rng.random() < z_lh / (z_lh + z_hl) else 0
+    t = 0.0
+    out = np.empty(n)
+    k = 0
+    while k < n:
+        lam = high if state else low
+        sw = z_hl if state else z_lh
+        t += rng.exponential(1.0 / (lam + sw))
+        if rng.random() < lam / (lam + sw):
+            out[k] = t
+            k += 1
+        else:
+            state = 1 - state
+    return 1000.0 * out
+
+
 def _draw_prompts(rng, spec, size):
     kind = spec[0]
     if kind == "uniform":
@@ -160,6 +193,12 @@ def _build(cfg: dict) -> Workload:
     if cfg["rate_per_s"] is not None:
         inter = rng.exponential(1.0 / cfg["rate_per_s"], size=N)
         t_ms = 1000.0 * np.cumsum(inter)
+        arr = cfg.get("arrivals", ("poisson",))
+        if arr[0] == "mmpp2":   # drawn from a stream of its own: other draws unchanged
+            t_ms = mmpp2_arrivals_ms(np.random.default_rng([int(cfg["seed"]), 3]), N,
+                                     cfg["rate_per_s"], *arr[1:])
+        elif arr[0] != "poisson":
+            raise ValueError(arr)
     else:
         t_ms = np.zeros(N)
     q_prefill = _draw_prompts(rng, cfg["prompt"], N)
