@@ -269,6 +269,39 @@ lar_status lar_read_state(lar_ctx *ctx, int32_t scen, int32_t *offsets, int32_t 
                           int32_t *rem_decode, int32_t *context, double *clock_ms,
                           int64_t *iterations_run, int64_t out_cap, int64_t *n_total);
 
+/*
+ * Snapshot board (appendix on the system: query workload snapshots, robustness to
+ * incomplete snapshots).  Instances publish their resident requests while they
+ * keep generating; the router takes only complete, unmodified copies and keeps
+ * the last complete copy per instance.  Host memory only; no device work.
+ *
+ * lar_board_create: a board for n_inst >= 1 instances of at most max_requests
+ *   resident requests each.  *out is NULL on failure (LAR_E_ARG).
+ * lar_board_publish: instance `inst` replaces its snapshot (requests in FCFS
+ *   order, as in lar_load_state, and its clock).  One publisher per instance at a
+ *   time; publishers of different instances may run concurrently with each other
+ *   and with lar_board_collect.  LAR_E_ARG for a bad instance, a count above
+ *   max_requests or null arrays.
+ * lar_board_collect: for every instance, copy its snapshot if a newer complete one
+ *   is there (the slot's sequence number even before the copy and unchanged after
+ *   it, up to 4 tries), else keep the cached copy; then write all cached copies in
+ *   lar_load_state's layout (offsets host [I+1], request arrays host [out_cap],
+ *   clock_ms host [I]).  fresh [I] (may be NULL): 1 where a new copy was taken;
+ *   versions [I] (may be NULL): sequence number of each cached copy.
+ *   LAR_E_STATE while some instance has no complete snapshot yet (the copies
+ *   taken are cached all the same), LAR_E_CAPACITY if out_cap is too small.  One
+ *   collector at a time.
+ */
+typedef struct lar_board lar_board;
+lar_status lar_board_create(lar_board **out, int32_t n_inst, int32_t max_requests);
+lar_status lar_board_destroy(lar_board *board);
+lar_status lar_board_publish(lar_board *board, int32_t inst, int32_t n_req,
+                             const int32_t *rem_prefill, const int32_t *rem_decode,
+                             const int32_t *context, double clock_ms);
+lar_status lar_board_collect(lar_board *board, int32_t *offsets, int32_t *rem_prefill,
+                             int32_t *rem_decode, int32_t *context, double *clock_ms,
+                             int64_t out_cap, int32_t *fresh, uint64_t *versions);
+
 /* Synchronise the stream; return the sticky device error, if any. */
 lar_status lar_sync(lar_ctx *ctx);
 

@@ -21,7 +21,8 @@ FIRST_TOKEN_DECODE_BATCH, FIRST_TOKEN_PREFILL_BATCH = 0, 1
 EXPORTED = ("lar_create", "lar_destroy", "lar_error_string", "lar_load_state", "lar_reload_state",
             "lar_estimate_ttft", "lar_route", "lar_route_constrained", "lar_ttft_targets",
             "lar_commit", "lar_route_trace", "lar_route_trace_constrained", "lar_stats",
-            "lar_ontime_utility", "lar_read_state", "lar_sync")
+            "lar_ontime_utility", "lar_read_state", "lar_sync", "lar_board_create",
+            "lar_board_destroy", "lar_board_publish", "lar_board_collect")
 
 
 class LarError(RuntimeError):
@@ -83,6 +84,14 @@ def load_library(path: str = LIB_PATH):
                                               vp, vp]
     L.lar_ontime_utility.restype = i32
     L.lar_ontime_utility.argtypes = [vp, i32, vp, vp, vp, vp, vp, i32, vp, vp]
+    L.lar_board_create.restype = i32
+    L.lar_board_create.argtypes = [C.POINTER(vp), i32, i32]
+    L.lar_board_destroy.restype = i32
+    L.lar_board_destroy.argtypes = [vp]
+    L.lar_board_publish.restype = i32
+    L.lar_board_publish.argtypes = [vp, i32, i32, vp, vp, vp, dbl]
+    L.lar_board_collect.restype = i32
+    L.lar_board_collect.argtypes = [vp, vp, vp, vp, vp, vp, i64, vp, vp]
     L.lar_stats.restype = i32
     L.lar_stats.argtypes = [vp, i32, vp, vp, vp, vp, i32, vp, vp]
     L.lar_read_state.restype = i32
@@ -357,3 +366,54 @@ def context_for(wl, *, flags=FIRST_TOKEN_DECODE_BATCH, max_iters=10_000_000, str
                      stream=stream)
     ctx.load_workload(wl)
     return ctx
+
+
+class SnapshotBoard:
+    """Host-side snapshot board (seqlock per instance): publishers replace their
+    instance's snapshot, the router collects the latest complete copies in the
+    layout of LarContext.load_state."""
+
+    def __init__(self, n_inst: int, max_requests: int, lib_path: str = LIB_PATH):
+        self._L = load_library(lib_path)
+        self.I, self.max_req = int(n_inst), int(max_requests)
+        h = C.c_void_p()
+        st = self._L.lar_board_create(C.byref(h), self.I, self.max_req)
+        if st != LAR_OK:
+            raise LarError(st, "lar_board_create failed")
+        self._h = h
+
+    def publish(self, inst: int, rem_prefill, rem_decode, context, clock_ms: float):
+        rp = np.ascontiguousarray(rem_prefill, np.int32)
+        rd = np.ascontiguousarray(rem_decode, np.int32)
+        cx = np.ascontiguousarray(context, np.int32)
+        st = self._L.lar_board_publish(self._h, int(inst), len(rp), rp.ctypes.data,
+                                       rd.ctypes.data, cx.ctypes.data, float(clock_ms))
+        if st != LAR_OK:
+            raise LarError(st, "lar_board_publish failed")
+
+    def collect(self, cap: int | None = None):
+        cap = self.I * self.max_req if cap is None else int(cap)
+        off = np.zeros(self.I + 1, np.int32)
+        rp, rd, cx = (np.zeros(max(cap, 1), np.int32) for _ in range(3))
+        clk = np.zeros(self.I)
+        fresh = np.zeros(self.I, np.int32)
+        ver = np.zeros(self.I, np.uint64)
+        st = self._L.lar_board_collect(self._h, off.ctypes.data, rp.ctypes.data, rd.ctypes.data,
+                                       cx.ctypes.data, clk.ctypes.data, cap, fresh.ctypes.data,
+                                       ver.ctypes.data)
+        if st != LAR_OK:
+            raise LarError(st, "lar_board_collect failed")
+        n = int(off[-1])
+        return dict(offsets=off, rem_prefill=rp[:n], rem_decode=rd[:n], context=cx[:n],
+                    clock_ms=clk, fresh=fresh, versions=ver)
+
+    def close(self):
+        if self._h:
+            self._L.lar_board_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

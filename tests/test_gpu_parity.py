@@ -410,3 +410,30 @@ def test_host_argument_errors():
                   T(np.zeros((1, 1)), torch.float64), T([0.0], torch.float64),
                   T([0.0], torch.float64))
     ctx.close()
+
+
+def test_snapshot_board_feeds_the_estimator():
+    """Instances publish their snapshots on the board; the router's collected copy,
+    loaded with lar_load_state, gives bit for bit the estimates of the oracle on the
+    same snapshot (config 1, 16 resident requests per instance)."""
+    from paper_2607_18253_amd.lar import SnapshotBoard
+    wl = make_workload("c1")
+    board = SnapshotBoard(wl.n_inst, 64)
+    for j in range(wl.n_inst):
+        rp, rd, cx = wl.instance_requests(j)
+        board.publish(j, rp, rd, cx, float(wl.clock_ms[j]))
+    snap = board.collect()
+    board.close()
+    ctx = context_for(wl)
+    ctx.load_state(a=wl.a, b=wl.b, c=wl.c, d=wl.d, e=wl.e, budget=wl.budget,
+                   max_seqs=wl.max_seqs, col=wl.col, offsets=snap["offsets"],
+                   rem_prefill=snap["rem_prefill"], rem_decode=snap["rem_decode"],
+                   context=snap["context"], clock_ms=snap["clock_ms"])
+    qp = wl.q_prefill[:50]
+    tt, it = ctx.estimate(T(qp, torch.int32), 0.0)
+    ctx.sync()
+    tt, it = tt.cpu().numpy()[0], it.cpu().numpy()[0]
+    ref, ref_it = O.estimate_matrix(wl, range(50), range(wl.n_inst), 0.0)
+    np.testing.assert_array_equal(it, ref_it)
+    np.testing.assert_array_equal(bits(tt), bits(ref))
+    ctx.close()
