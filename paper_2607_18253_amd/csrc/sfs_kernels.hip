@@ -756,7 +756,8 @@ struct VisitOut {
 
 // One visit of a wave to one owned queue for one query.  wk enters as the instance
 // state (loaded from SL); the query is appended if it was routed here, the instance
-// is replayed to tn and written back to SL, and the frontier cache is kept in step.
+// is replayed to tn and written back to SL (unless nothing changed), and the
+// frontier cache (state F in LDS) is kept in step.
 // Every batch -- replayed, walked to a new admission point, or recorded as tail --
 // runs through the single Queue::step / quiet_run below, on wk.
 template <int KS>
@@ -1272,6 +1273,21 @@ static hipError_t launch_trace_mem(const LaunchEnv& env, const TraceArgs& a) {
   return hipGetLastError();
 }
 
+// Every active workgroup of a clustered trace must be resident at once (members wait
+// for each other), and a scenario's members share one XCD: per XCD, ceil(Z / 8) * G
+// workgroups must fit its compute units at the kernel's occupancy.
+template <class K>
+static bool co_resident(K kernel, int threads, int Z, int G) {
+  int dev = 0, n_cu = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return false;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess)
+    return false;
+  const int64_t per_xcd = (int64_t)((Z + 7) / 8) * G;
+  return per_cu > 0 && per_xcd <= (int64_t)(n_cu / 8) * per_cu;
+}
+
 template <int KS, int W, int IPW>
 static hipError_t launch_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
   const int per_wg = W * IPW;
@@ -1279,6 +1295,8 @@ static hipError_t launch_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
   if (G > kMaxCluster) return hipErrorInvalidValue;
   if ((uint64_t)a.N >= (1ull << 31)) return hipErrorInvalidValue;  // 32-bit post tags
   const int w_used = G == 1 ? (env.I + IPW - 1) / IPW : W;
+  if (!co_resident(k_trace_cl<KS, W, IPW>, w_used * kWave, env.Z, G))
+    return hipErrorInvalidConfiguration;
   if (G > 1) {
     const int64_t n = (int64_t)env.Z * 2 * kMaxCluster * 4;
     hipLaunchKernelGGL(k_clear_exchange, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
@@ -1305,12 +1323,19 @@ static hipError_t launch_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
     return G <= kMaxCluster && (uint64_t)a.N < (1ull << 31) && env.T.K >= 1 &&
            env.T.K <= kWave;
   };
+  // A shape whose workgroups cannot all be resident together reports
+  // hipErrorInvalidConfiguration without launching; the next one is tried.
+  hipError_t e = hipErrorInvalidConfiguration;
   if constexpr (KS <= 4) {
-    if (queues <= 1024 && fits(4)) return launch_trace_cl<KS, 4, 1>(env, a);
-    if (queues <= 4096 && fits(16)) return launch_trace_cl<KS, 16, 1>(env, a);
+    if (queues <= 1024 && fits(4)) e = launch_trace_cl<KS, 4, 1>(env, a);
+    if (e != hipErrorInvalidConfiguration) return e;
+    if (queues <= 4096 && fits(16)) e = launch_trace_cl<KS, 16, 1>(env, a);
+    if (e != hipErrorInvalidConfiguration) return e;
   } else if constexpr (KS == 8) {
-    if (queues <= 1024 && fits(4)) return launch_trace_cl<8, 4, 1>(env, a);
-    if (queues <= 2048 && fits(8)) return launch_trace_cl<8, 8, 1>(env, a);
+    if (queues <= 1024 && fits(4)) e = launch_trace_cl<8, 4, 1>(env, a);
+    if (e != hipErrorInvalidConfiguration) return e;
+    if (queues <= 2048 && fits(8)) e = launch_trace_cl<8, 8, 1>(env, a);
+    if (e != hipErrorInvalidConfiguration) return e;
   }
   // Otherwise the states stay in HBM (L2) and are loaded per use.
   return launch_trace_mem<KS, (KS <= 4 ? 8 : (KS == 8 ? 8 : 4))>(env, a);
