@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <algorithm>
 #include <cstring>
 #include <string>
@@ -30,6 +31,7 @@ struct lar_ctx {
   int32_t* pi = nullptr;  // [3][I]: B, M, col
   double* row_ttft = nullptr;  // [Z][I] scratch of the sequential trace
   uint64_t* xslot = nullptr;   // [Z][2][kMaxCluster][4] candidate posts of the clustered trace
+  lar::SyncCtl sync{1000000000ull, -1, -1};   // 10 s wait bound; no post left out
   lar::DevState snap{};        // one scenario's copy of the last loaded snapshot
   int32_t* err = nullptr;
   size_t tail_elems = 0;  // allocated K * Z * I
@@ -99,6 +101,7 @@ LaunchEnv env_of(const lar_ctx* ctx) {
   e.err = ctx->err;
   e.stream = ctx->stream;
   e.xslot = ctx->xslot;
+  e.sync = ctx->sync;
   return e;
 }
 
@@ -126,6 +129,20 @@ lar_status lar_create(lar_ctx** out, const lar_config* cfg) {
   if ((int64_t)cfg->n_scen * cfg->n_inst > (int64_t)1 << 24) return LAR_E_ARG;
   lar_ctx* ctx = new lar_ctx;
   ctx->cfg = *cfg;
+  // Test hooks of the cross-workgroup wait, from the environment: LAR_SYNC_TIMEOUT_MS
+  // bounds the wait (default 10 s); LAR_TEST_SKIP_POST="member:query" makes one
+  // workgroup leave out its post for one query, so the others reach the bound.
+  if (const char* v = std::getenv("LAR_SYNC_TIMEOUT_MS")) {
+    const long long ms = std::atoll(v);
+    if (ms > 0) ctx->sync.spin_ticks = (uint64_t)ms * 100000ull;
+  }
+  if (const char* v = std::getenv("LAR_TEST_SKIP_POST")) {
+    int m = -1, q = -1;
+    if (std::sscanf(v, "%d:%d", &m, &q) == 2 && m >= 0 && q >= 0) {
+      ctx->sync.skip_cid = m;
+      ctx->sync.skip_query = q;
+    }
+  }
   ctx->Z = cfg->n_scen;
   ctx->I = cfg->n_inst;
   ctx->mcap = cfg->max_seqs_cap;

@@ -618,18 +618,16 @@ __device__ __forceinline__ void cand_take(Cand& c, double u, int k, double ttft,
 // when it is whole, and the G posts arrive together with the poll: no counter, no
 // fence, one round trip after the last member posts.  All accesses are relaxed
 // agent-scope atomics on the same words, which the memory model keeps coherent.
-// The wait is bounded in wall-clock time (s_memrealtime runs at 100 MHz): a member
-// that never posts, or an error raised by another member, ends the trace with
-// kErrSync instead of a hang.  Two slot sets suffice: a member posts query i + 2
+// The wait is bounded in wall-clock time (s_memrealtime runs at 100 MHz; 10 s
+// unless the host sets another bound): a member that never posts, or an error
+// raised by another member, ends the trace with kErrSync instead of a hang.  Two slot sets suffice: a member posts query i + 2
 // only after every member has posted i + 1, i.e. has finished reading the posts of i.
-constexpr uint64_t kSpinTicks = 1000000000ull;   // 10 s
-
 __device__ __forceinline__ bool cluster_exchange(double& u, int& j, int i, int G, int cid,
-                                                 uint64_t* xs, int32_t* err) {
+                                                 uint64_t* xs, int32_t* err, SyncCtl sc) {
   const int ln = lane_id();
   uint64_t* base = xs + (int64_t)(i & 1) * kMaxCluster * 4;
   const uint32_t tag = (uint32_t)(i + 1);
-  if (ln == 0) {
+  if (ln == 0 && !(cid == sc.skip_cid && i == sc.skip_query)) {
     const uint64_t ub = (uint64_t)__double_as_longlong(u);
     const uint64_t hi = (uint64_t)tag << 32;
     uint64_t* sl = base + cid * 4;
@@ -668,7 +666,7 @@ __device__ __forceinline__ bool cluster_exchange(double& u, int& j, int i, int G
       int bad = 0;
       if (ln == 0)
         bad = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == kErrSync ||
-              __builtin_amdgcn_s_memrealtime() - t0 > kSpinTicks;
+              __builtin_amdgcn_s_memrealtime() - t0 > sc.spin_ticks;
       if (__builtin_amdgcn_readlane(bad, 0)) {
         if (ln == 0) set_error(err, kErrSync);
         return false;
@@ -948,7 +946,7 @@ __device__ __forceinline__ double estimate_visit(const FCache& fc, const Queue<K
 // Identical, operation for operation, to estimate + route + commit per query.
 template <int KS, int W, int IPW>
 __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G, uint64_t* xslot,
-                                                        int tail_k) {
+                                                        int tail_k, SyncCtl sc) {
   __shared__ double s_u[2][W];
   __shared__ int s_j[2][W];
   __shared__ double s_mu[2];
@@ -1012,7 +1010,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
       if (G > 1) {
         // wave 0 exchanges with the other workgroups, then broadcasts the winner
         if (wid == 0) {
-          const bool ok = cluster_exchange(bu, bj, i, G, cid, xs, err);
+          const bool ok = cluster_exchange(bu, bj, i, G, cid, xs, err, sc);
           if (ln == 0) { s_mu[buf] = bu; s_mj[buf] = ok ? bj : -2; }
         }
         __syncthreads();
@@ -1306,7 +1304,7 @@ static hipError_t launch_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
   }
   const int blocks = 8 * ((env.Z + 7) / 8) * G;
   hipLaunchKernelGGL((k_trace_cl<KS, W, IPW>), dim3(blocks), dim3(w_used * kWave), 0,
-                     env.stream, LAR_TRACE_ARGS, G, env.xslot, env.T.K);
+                     env.stream, LAR_TRACE_ARGS, G, env.xslot, env.T.K, env.sync);
   return hipGetLastError();
 }
 

@@ -8,6 +8,14 @@
 
 namespace lar {
 
+// Bound of the cross-workgroup wait of the clustered trace (s_memrealtime ticks,
+// 100 MHz) and a post that a member leaves out on purpose (skip_cid = -1: none).
+// The host sets skip_* only in tests of the timeout path.
+struct SyncCtl {
+  uint64_t spin_ticks;
+  int skip_cid, skip_query;
+};
+
 struct LaunchEnv {
   DevState S;
   DevParams P;
@@ -21,6 +29,7 @@ struct LaunchEnv {
   hipStream_t stream;
   // cross-workgroup candidate exchange of the clustered trace kernel
   uint64_t* xslot;    // [Z][2][kMaxCluster][4] tagged candidate posts
+  SyncCtl sync;
 };
 
 constexpr int kMaxCluster = 64;

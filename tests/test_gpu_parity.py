@@ -437,3 +437,29 @@ def test_snapshot_board_feeds_the_estimator():
     np.testing.assert_array_equal(it, ref_it)
     np.testing.assert_array_equal(bits(tt), bits(ref))
     ctx.close()
+
+
+def test_trace_sync_timeout_is_reported(monkeypatch):
+    """The bounded cross-workgroup wait, forced from the host: workgroup 3 of config
+    2's clustered trace (32 instances, 8 workgroups of 4) leaves out its post for
+    query 5; the other workgroups wait until the bound (2 ms here), and the trace ends
+    with the sticky LAR_E_SYNC instead of hanging.  A context created without the
+    hooks then routes the same trace like the oracle."""
+    wl = make_workload("c2", n_q=200)
+    monkeypatch.setenv("LAR_SYNC_TIMEOUT_MS", "2")
+    monkeypatch.setenv("LAR_TEST_SKIP_POST", "3:5")
+    ctx = context_for(wl)
+    monkeypatch.delenv("LAR_SYNC_TIMEOUT_MS")
+    monkeypatch.delenv("LAR_TEST_SKIP_POST")
+    ctx.advance(float(wl.q_t_ms[0]))
+    args = (T(wl.q_prefill, torch.int32), T(wl.q_decode, torch.int32),
+            T(wl.q_t_ms, torch.float64), float(wl.q_t_ms[-1]), T(wl.acc, torch.float64),
+            T(wl.cost, torch.float64), T(wl.w_cost, torch.float64),
+            T(wl.w_lat_ms, torch.float64))
+    ctx.route_trace(*args)
+    assert ctx.status() == L.LAR_E_SYNC
+    ctx.close()
+    choice, chosen, util, ctx = gpu_trace(wl)
+    ref = O.trace(wl)
+    np.testing.assert_array_equal(choice[0], ref.choice)
+    ctx.close()
