@@ -302,6 +302,17 @@ lar_status lar_board_collect(lar_board *board, int32_t *offsets, int32_t *rem_pr
                              int32_t *rem_decode, int32_t *context, double *clock_ms,
                              int64_t out_cap, int32_t *fresh, uint64_t *versions);
 
+/*
+ * Work of the last lar_route_trace / lar_route_trace_constrained call (synchronises):
+ * per scenario, the number of token batches its estimates stand for -- for every
+ * (query, instance) pair, the batches a literal SFS estimate would simulate from the
+ * instance state to the query's first-token batch (Sec. 4.1).  The batches of the
+ * replay between arrivals are in lar_read_state's iterations_run.  Zero before the
+ * first trace.
+ *   estimate_batches host [Z]
+ */
+lar_status lar_trace_work(lar_ctx *ctx, int64_t *estimate_batches);
+
 /* Synchronise the stream; return the sticky device error, if any. */
 lar_status lar_sync(lar_ctx *ctx);
 

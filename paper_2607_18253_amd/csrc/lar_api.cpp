@@ -32,6 +32,7 @@ struct lar_ctx {
   double* row_ttft = nullptr;  // [Z][I] scratch of the sequential trace
   uint64_t* xslot = nullptr;   // [Z][2][kMaxCluster][4] candidate posts of the clustered trace
   lar::SyncCtl sync{1000000000ull, -1, -1};   // 10 s wait bound; no post left out
+  unsigned long long* work = nullptr;          // [Z] estimate batches of the last trace
   lar::DevState snap{};        // one scenario's copy of the last loaded snapshot
   int32_t* err = nullptr;
   size_t tail_elems = 0;  // allocated K * Z * I
@@ -102,6 +103,7 @@ LaunchEnv env_of(const lar_ctx* ctx) {
   e.stream = ctx->stream;
   e.xslot = ctx->xslot;
   e.sync = ctx->sync;
+  e.work = ctx->work;
   return e;
 }
 
@@ -182,6 +184,9 @@ lar_status lar_create(lar_ctx** out, const lar_config* cfg) {
   chk(dev_alloc(ctx, &ctx->row_ttft, ZI));
   chk(dev_alloc(ctx, &ctx->err, 1));
   chk(dev_alloc(ctx, &ctx->xslot, (size_t)ctx->Z * 2 * lar::kMaxCluster * 4));
+  chk(dev_alloc(ctx, &ctx->work, (size_t)ctx->Z));
+  if (st == LAR_OK && hipMemset(ctx->work, 0, sizeof(unsigned long long) * ctx->Z) != hipSuccess)
+    st = fail(ctx, LAR_E_HIP, "hipMemset of the work counters failed");
   if (st != LAR_OK) {
     lar_destroy(ctx);
     return st;
@@ -532,6 +537,14 @@ lar_status lar_ontime_utility(lar_ctx* ctx, int32_t n_q, const int32_t* choice,
   const LaunchEnv env = env_of(ctx);
   HIP_TRY(ctx, lar::launch_ontime(env, n_q, choice, chosen_ttft, tau_ms, acc, cost, n_cols, w_cost,
                                   out));
+  return LAR_OK;
+}
+
+lar_status lar_trace_work(lar_ctx* ctx, int64_t* estimate_batches) {
+  if (!ctx || !estimate_batches) return LAR_E_ARG;
+  HIP_TRY(ctx, hipStreamSynchronize(ctx->stream));
+  HIP_TRY(ctx, hipMemcpy(estimate_batches, ctx->work, sizeof(int64_t) * ctx->Z,
+                         hipMemcpyDeviceToHost));
   return LAR_OK;
 }
 

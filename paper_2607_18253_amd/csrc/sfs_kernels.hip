@@ -360,7 +360,8 @@ __global__ __launch_bounds__(kWave) void k_commit(DevState S, DevParams pr, int 
 template <int KS>
 __device__ __forceinline__ double finish_estimate(Queue<KS>& w, const QEnv& e, double E,
                                                   int64_t it, int p, double t, int reading,
-                                                  int64_t max_iters, int32_t* err) {
+                                                  int64_t max_iters, int32_t* err,
+                                                  int64_t* it_out = nullptr) {
   const int ln = lane_id();
   const int aP = (int)w.pre_sum, aD = w.n_dec;
   const int64_t aC = e.need_C ? w.c0sum + (int64_t)aD * w.g : 0;
@@ -405,6 +406,7 @@ __device__ __forceinline__ double finish_estimate(Queue<KS>& w, const QEnv& e, d
     }
   }
   if (it > max_iters && ln == 0) set_error(err, kErrIter);
+  if (it_out) *it_out = it;
   return __dsub_rn(E, t);
 }
 
@@ -412,7 +414,8 @@ __device__ __forceinline__ double finish_estimate(Queue<KS>& w, const QEnv& e, d
 // not modified.  Returns NaN (and sets the error) when it cannot.
 template <int KS>
 __device__ __forceinline__ double estimate(const Queue<KS>& q, const QEnv& e, int p, double t,
-                                           int reading, int64_t max_iters, int32_t* err) {
+                                           int reading, int64_t max_iters, int32_t* err,
+                                           int64_t* it_out = nullptr) {
   const int ln = lane_id();
   if (q.clock < t) {
     if (ln == 0) set_error(err, kErrState);
@@ -435,7 +438,7 @@ __device__ __forceinline__ double estimate(const Queue<KS>& q, const QEnv& e, in
     ++it;
   }
   w.refill(e);
-  return finish_estimate(w, e, E, it, p, t, reading, max_iters, err);
+  return finish_estimate(w, e, E, it, p, t, reading, max_iters, err, it_out);
 }
 
 // Trace inputs of one query, loaded one query ahead so their memory latency hides
@@ -519,7 +522,7 @@ __device__ __forceinline__ int trace_pick(double bu, int bj, double bt, double b
       const double *qt, double t_after, const double *acc, const double *cost, int n_cols,   \
       const double *w_cost, const double *w_lat, const double *tau, int reading,             \
       int max_prompt, int64_t max_iters, int32_t *choice, double *chosen_ttft,               \
-      double *utility, int32_t *err
+      double *utility, int32_t *err, unsigned long long *work
 
 // The same trace for pools too large to keep in registers: each owned instance's
 // state is loaded from HBM (L2) when it is needed and written back after its commit.
@@ -539,6 +542,7 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
   const bool own_l = j_l < I;
   const int col_l = own_l ? pr.col[j_l] : 0;
   QueryIn nx = fetch_query(0, N, qp, qd, qt, t_after, tau, acc, cost, n_cols, col_l, own_l);
+  unsigned long long wbatch = 0;   // batches of this wave's estimates
   for (int i = 0; i < N; ++i) {
     const QueryIn q = nx;
     nx = fetch_query(i + 1, N, qp, qd, qt, t_after, tau, acc, cost, n_cols, col_l, own_l);
@@ -550,8 +554,10 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
       const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
       Queue<KS> w;
       w.load(S, e, z * I + j);
-      const double ttft = p_ok ? estimate(w, e, q.p, q.t, reading, max_iters, err)
+      int64_t it = 0;
+      const double ttft = p_ok ? estimate(w, e, q.p, q.t, reading, max_iters, err, &it)
                                : __builtin_nan("");
+      wbatch += it;
       double eq2;
       int k;
       const double u = utility_lane(q, v, wc, wl, tau, ttft, j, &k, &eq2);
@@ -567,6 +573,7 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
       w.store(S, e, z * I + j);
     }
   }
+  if (work && lane_id() == 0) atomicAdd(work + z, wbatch);
 }
 
 // Trace inputs of 64 consecutive queries, lane l holding query base + l; the acc /
@@ -683,6 +690,12 @@ __device__ __forceinline__ bool cluster_exchange(double& u, int& j, int i, int G
   u = bu;
   j = bj;
   return true;
+}
+
+// Zeroes the per-scenario estimate-batch counters before a trace.
+__global__ void k_clear_work(unsigned long long* w, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) w[i] = 0ull;
 }
 
 // Clears the exchange posts (tags included) of every scenario before a trace.
@@ -872,7 +885,8 @@ template <int KS>
 __device__ __forceinline__ double estimate_visit(const FCache& fc, const Queue<KS>& S,
                                                  const VisitOut& vo, const QEnv& e, int p,
                                                  double t, int reading, int kmax,
-                                                 int64_t max_iters, int32_t* err) {
+                                                 int64_t max_iters, int32_t* err,
+                                                 int64_t* it_out = nullptr) {
   const int ln = lane_id();
   if (vo.clock < t) {
     if (ln == 0) set_error(err, kErrState);
@@ -932,6 +946,7 @@ __device__ __forceinline__ double estimate_visit(const FCache& fc, const Queue<K
     if (!done && !cached) S.tail_next(e, tl);
   }
   if (it > max_iters && ln == 0) set_error(err, kErrIter);
+  if (it_out) *it_out = it;
   return __dsub_rn(E, t);
 }
 
@@ -985,6 +1000,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
   }
   QueryBlock<IPW> cur = fetch_block<IPW>(0, N, qp, qd, qt, tau, acc, cost, n_cols, cols);
   QueryBlock<IPW> nxt = fetch_block<IPW>(kWave, N, qp, qd, qt, tau, acc, cost, n_cols, cols);
+  unsigned long long wbatch = 0;   // batches of this wave's estimates
   Cand c;
   c.j = -1; c.u = 0.0; c.ttft = 0.0; c.eq2 = 0.0;
   for (int i = -1; i < N; ++i) {
@@ -1055,9 +1071,11 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
         const VisitOut vo = visit(wk, fc[r], e, i >= 0 && j == m, p, dq, tn, S.qcap, kmax,
                                   max_iters, err, sst[wid][r], fst[wid][r]);
         if (more) {
+          int64_t it = 0;
           const double ttft = p1_ok ? estimate_visit(fc[r], wk, vo, e, p1, t1, reading, kmax,
-                                                     max_iters, err)
+                                                     max_iters, err, &it)
                                     : __builtin_nan("");
+          wbatch += it;
           const double a = read_lane_f64(in_nxt ? nxt.acc[r] : cur.acc[r], l1);
           const double co = read_lane_f64(in_nxt ? nxt.cost[r] : cur.cost[r], l1);
           const double eq2 = __dsub_rn(a, __dmul_rn(wc, co));
@@ -1073,6 +1091,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
       nxt = fetch_block<IPW>(i + 1 + kWave, N, qp, qd, qt, tau, acc, cost, n_cols, cols);
     }
   }
+  if (work && ln == 0) atomicAdd(work + z, wbatch);
 #pragma unroll
   for (int r = 0; r < IPW; ++r) {
     const int j = jbase + r;
@@ -1260,7 +1279,7 @@ static hipError_t launch_commit_ks(const LaunchEnv& env, const int32_t* choice,
 #define LAR_TRACE_ARGS                                                                   \
   env.S, env.P, env.Z, env.I, a.N, a.qp, a.qd, a.qt, a.t_after, a.acc, a.cost, a.n_cols,     \
       a.w_cost, a.w_lat, a.tau, env.reading, env.max_prompt, env.max_iters, a.choice,        \
-      a.chosen_ttft, a.utility, env.err
+      a.chosen_ttft, a.utility, env.err, env.work
 
 template <int KS, int NW>
 static hipError_t launch_trace_mem(const LaunchEnv& env, const TraceArgs& a) {
@@ -1340,6 +1359,12 @@ static hipError_t launch_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
 }
 
 hipError_t launch_trace(const LaunchEnv& env, const TraceArgs& a) {
+  if (env.work) {
+    hipLaunchKernelGGL(k_clear_work, dim3((env.Z + 255) / 256), dim3(256), 0, env.stream,
+                       env.work, env.Z);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   switch (env.ks) {
     case 1: return launch_trace_ks<1>(env, a);
     case 2: return launch_trace_ks<2>(env, a);

@@ -30,6 +30,7 @@ struct LaunchEnv {
   // cross-workgroup candidate exchange of the clustered trace kernel
   uint64_t* xslot;    // [Z][2][kMaxCluster][4] tagged candidate posts
   SyncCtl sync;
+  unsigned long long* work;   // [Z] batches simulated by the estimates of the last trace
 };
 
 constexpr int kMaxCluster = 64;

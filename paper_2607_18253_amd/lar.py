@@ -21,7 +21,7 @@ FIRST_TOKEN_DECODE_BATCH, FIRST_TOKEN_PREFILL_BATCH = 0, 1
 EXPORTED = ("lar_create", "lar_destroy", "lar_error_string", "lar_load_state", "lar_reload_state",
             "lar_estimate_ttft", "lar_route", "lar_route_constrained", "lar_ttft_targets",
             "lar_commit", "lar_route_trace", "lar_route_trace_constrained", "lar_stats",
-            "lar_ontime_utility", "lar_read_state", "lar_sync", "lar_board_create",
+            "lar_ontime_utility", "lar_read_state", "lar_sync", "lar_trace_work", "lar_board_create",
             "lar_board_destroy", "lar_board_publish", "lar_board_collect")
 
 
@@ -84,6 +84,8 @@ def load_library(path: str = LIB_PATH):
                                               vp, vp]
     L.lar_ontime_utility.restype = i32
     L.lar_ontime_utility.argtypes = [vp, i32, vp, vp, vp, vp, vp, i32, vp, vp]
+    L.lar_trace_work.restype = i32
+    L.lar_trace_work.argtypes = [vp, vp]
     L.lar_board_create.restype = i32
     L.lar_board_create.argtypes = [C.POINTER(vp), i32, i32]
     L.lar_board_destroy.restype = i32
@@ -327,6 +329,12 @@ class LarContext:
             _dev(acc, torch.float64, "acc", N * n_cols), _dev(cost, torch.float64, "cost", N * n_cols),
             n_cols, _dev(w_cost, torch.float64, "w_cost", self.Z),
             _dev(out, torch.float64, "stats", self.Z * 5)))
+        return out
+
+    def trace_work(self):
+        """Per-scenario batches behind the last trace's estimates (synchronises)."""
+        out = np.zeros(self.Z, np.int64)
+        self._check(self._L.lar_trace_work(self._h, out.ctypes.data))
         return out
 
     def sync(self):
