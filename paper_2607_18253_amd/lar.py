@@ -366,9 +366,11 @@ class LarContext:
 
 
 def context_for(wl, *, flags=FIRST_TOKEN_DECODE_BATCH, max_iters=10_000_000, stream=None,
-                queue_cap=None) -> LarContext:
-    """A context sized for workload ``wl`` with its snapshot loaded."""
-    ctx = LarContext(wl.n_scen, wl.n_inst, max_seqs_cap=int(np.max(wl.max_seqs)),
+                queue_cap=None, max_seqs_cap=None) -> LarContext:
+    """A context sized for workload ``wl`` with its snapshot loaded (max_seqs_cap
+    defaults to the largest M of the pool)."""
+    mcap = int(np.max(wl.max_seqs)) if max_seqs_cap is None else int(max_seqs_cap)
+    ctx = LarContext(wl.n_scen, wl.n_inst, max_seqs_cap=mcap,
                      queue_cap=int(wl.queue_cap if queue_cap is None else queue_cap),
                      max_prompt=int(wl.max_prompt), flags=flags, max_iters=max_iters,
                      stream=stream)

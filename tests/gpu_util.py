@@ -16,7 +16,8 @@ def bits(x):
     return np.ascontiguousarray(x, dtype=np.float64).view(np.int64)
 
 
-def gpu_trace(wl, n_q=None, *, flags=0, max_iters=10_000_000, queue_cap=None):
+def gpu_trace(wl, n_q=None, *, flags=0, max_iters=10_000_000, queue_cap=None,
+              max_seqs_cap=None):
     """Sequential trace of every scenario of ``wl`` on the GPU (first n_q queries).
 
     Returns (choice [Z][N], chosen_ttft [Z][N], utility [Z][N], ctx) with ctx still
@@ -25,7 +26,8 @@ def gpu_trace(wl, n_q=None, *, flags=0, max_iters=10_000_000, queue_cap=None):
     from paper_2607_18253_amd import context_for
 
     N = wl.n_q if n_q is None else int(n_q)
-    ctx = context_for(wl, flags=flags, max_iters=max_iters, queue_cap=queue_cap)
+    ctx = context_for(wl, flags=flags, max_iters=max_iters, queue_cap=queue_cap,
+                      max_seqs_cap=max_seqs_cap)
     ctx.advance(float(wl.q_t_ms[0]))
     chosen = torch.full((wl.n_scen, N), -1.0, dtype=torch.float64, device=DEV)
     util = torch.full((wl.n_scen, N), -1.0, dtype=torch.float64, device=DEV)

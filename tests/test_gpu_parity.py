@@ -463,3 +463,22 @@ def test_trace_sync_timeout_is_reported(monkeypatch):
     ref = O.trace(wl)
     np.testing.assert_array_equal(choice[0], ref.choice)
     ctx.close()
+
+
+@pytest.mark.parametrize("mcap,kernel", [(100, "2 slots per lane"), (300, "8 slots per lane"),
+                                         (1024, "16 slots per lane: HBM-state kernel")])
+@pytest.mark.parametrize("seed", range(3))
+def test_trace_slot_widths(mcap, kernel, seed):
+    """The trace kernels instantiated for wider decode-slot arrays (the context's
+    max_seqs_cap sets the slots per lane): tiny pools routed in contexts of 100, 300
+    and 1024 sequence slots give the oracle's results."""
+    wl = make_tiny_workload(500 + seed, n_inst=5, max_res=6, n_q=40, n_scen=2,
+                            dyadic=(seed % 2 == 0))
+    choice, chosen, util, ctx = gpu_trace(wl, queue_cap=10 ** 4, max_seqs_cap=mcap)
+    for z in range(wl.n_scen):
+        ref = O.trace(wl, scenario=z, queue_cap=10 ** 4)
+        np.testing.assert_array_equal(choice[z], ref.choice)
+        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen))
+        np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
+        assert_state_equal(ctx, z, ref)
+    ctx.close()
