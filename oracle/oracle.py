@@ -99,7 +99,7 @@ def lib():
                             C.c_double, C.c_double, _opt(_f64p), C.c_int32, C.c_int64, C.c_int64,
                             _i32p, _opt(_f64p), _opt(_f64p), _opt(_f64p), _opt(_i32p),
                             _opt(_i32p), _opt(_i32p), _opt(_i32p), _opt(_i32p), _opt(_f64p),
-                            _opt(_i64p), C.c_int64, C.POINTER(C.c_int32)]
+                            _opt(_i64p), C.c_int64, _opt(_f64p), C.POINTER(C.c_int32)]
     L.orc_route_row_constrained.restype = C.c_int32
     L.orc_route_row_constrained.argtypes = [C.c_int32, _f64p, C.c_double, _f64p, _f64p, _i32p,
                                             C.c_double]
@@ -216,11 +216,11 @@ def ttft_targets(p, u_ms, v):
     return out
 
 
-def ontime_utility(choice, ttft_chosen, tau, acc, cost, col, w_cost):
-    """Eq. 4 over a routed trace (estimated TTFT at the choice taken as realised)."""
+def ontime_utility(choice, ttft_real, tau, acc, cost, col, w_cost):
+    """Eq. 4 over a routed trace, from the realised TTFT of each query."""
     n = len(choice)
     out = C.c_double(0)
-    st = lib().orc_ontime_utility(n, _i32(choice), np.ascontiguousarray(ttft_chosen, np.float64),
+    st = lib().orc_ontime_utility(n, _i32(choice), np.ascontiguousarray(ttft_real, np.float64),
                                   np.ascontiguousarray(tau[:n], np.float64),
                                   np.ascontiguousarray(acc[:n], np.float64),
                                   np.ascontiguousarray(cost[:n], np.float64), acc.shape[1],
@@ -243,6 +243,7 @@ class TraceResult:
     context: np.ndarray | None
     clock_ms: np.ndarray | None
     iterations: np.ndarray | None
+    realized: np.ndarray          # realised TTFT of each query in the replay
 
 
 def trace(wl, scenario: int = 0, *, n_q: int | None = None, reading=READING_DECODE_BATCH,
@@ -270,6 +271,7 @@ def trace(wl, scenario: int = 0, *, n_q: int | None = None, reading=READING_DECO
     else:
         out_cap = 0
         out_off = out_rp = out_rd = out_cx = out_clock = out_iters = None
+    realized = np.zeros(N)
     failed = C.c_int32(-1)
     st = L.orc_trace(I, params, _i32(wl.col), _i32(wl.offsets), _i32(wl.rem_prefill),
                      _i32(wl.rem_decode), _i32(wl.context),
@@ -283,14 +285,14 @@ def trace(wl, scenario: int = 0, *, n_q: int | None = None, reading=READING_DECO
                      int(reading),
                      int(max_iters), cap, choice, ttft_c, util_c, ttft_all, iters_all,
                      out_off, out_rp, out_rd, out_cx, out_clock, out_iters, out_cap,
-                     C.byref(failed))
+                     realized, C.byref(failed))
     if st != OK:
         raise OracleError(st, f"trace (query {failed.value})")
     if final_state:
         n = int(out_off[-1])
         out_rp, out_rd, out_cx = out_rp[:n], out_rd[:n], out_cx[:n]
     return TraceResult(choice, ttft_c, util_c, ttft_all, iters_all, out_off, out_rp, out_rd,
-                       out_cx, out_clock, out_iters)
+                       out_cx, out_clock, out_iters, realized)
 
 
 def stats(choice, ttft_chosen, acc, cost, col, w_cost):

@@ -58,9 +58,18 @@
  *       tau = min{1120, max{150, u + (155 + 3.5e-3*p)*v}}  (ms),
  *     u ~ U(1, 5) ms and v ~ U(0.98, 1.02) drawn by the caller.
  *
+ *   * Realised TTFT (the replay's own first-token times, against which Fig. 2 of
+ *     the paper sets the estimates): each routed query is tagged in the replay;
+ *     the first batch that produces its first token (the same reading as the
+ *     estimate) ends at its first-token time, and realised TTFT = that time minus
+ *     the arrival.  Queries still waiting for it when the trace ends are finished
+ *     on a copy of their instance with no further arrivals.
+ *
  *   * OnTimeUtility (Eq. 4): (1/N) * sum over queries, in query order, of the
- *     utility at the chosen instance when its TTFT is within the target, else 0.
+ *     utility at the chosen instance when its realised TTFT is within the target,
+ *     else 0.
  */
+#include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -82,9 +91,15 @@ typedef struct {
   int64_t n;        /* resident requests */
   int64_t alloc;    /* allocated entries */
   int32_t *rp, *rd, *cx;
+  int32_t *qid;     /* routed query still waiting for its first token, else -1 */
   int32_t *dec, *chunk; /* tokens of the batch being built, per request */
   double clock;
   int64_t iters;    /* batches run by advance() since creation */
+  /* first-token tracking of the replay (realised == NULL: off) */
+  double *realized;     /* [N] realised TTFT per query */
+  const double *q_t;    /* [N] arrival times */
+  int32_t reading;
+  int64_t tracked;      /* residents with qid >= 0 */
 } orc_queue;
 
 typedef struct {
@@ -97,8 +112,8 @@ static int q_reserve(orc_queue *q, int64_t need) {
   if (need <= q->alloc) return ORC_OK;
   int64_t cap = q->alloc ? q->alloc : 16;
   while (cap < need) cap *= 2;
-  int32_t **arrs[5] = {&q->rp, &q->rd, &q->cx, &q->dec, &q->chunk};
-  for (int k = 0; k < 5; ++k) {
+  int32_t **arrs[6] = {&q->rp, &q->rd, &q->cx, &q->qid, &q->dec, &q->chunk};
+  for (int k = 0; k < 6; ++k) {
     int32_t *p = (int32_t *)realloc(*arrs[k], (size_t)cap * sizeof(int32_t));
     if (!p) return ORC_E_ARG;
     *arrs[k] = p;
@@ -139,7 +154,9 @@ orc_queue *orc_queue_new(const orc_params *pr, int64_t n, const int32_t *rp,
   if (!q) { *status = ORC_E_ARG; return NULL; }
   q->pr = *pr;
   if (q_reserve(q, n + 1) != ORC_OK) { free(q); *status = ORC_E_ARG; return NULL; }
-  for (int64_t r = 0; r < n; ++r) { q->rp[r] = rp[r]; q->rd[r] = rd[r]; q->cx[r] = cx[r]; }
+  for (int64_t r = 0; r < n; ++r) {
+    q->rp[r] = rp[r]; q->rd[r] = rd[r]; q->cx[r] = cx[r]; q->qid[r] = -1;
+  }
   q->n = n;
   q->clock = clock;
   q->iters = 0;
@@ -148,14 +165,20 @@ orc_queue *orc_queue_new(const orc_params *pr, int64_t n, const int32_t *rp,
 
 void orc_queue_free(orc_queue *q) {
   if (!q) return;
-  free(q->rp); free(q->rd); free(q->cx); free(q->dec); free(q->chunk);
+  free(q->rp); free(q->rd); free(q->cx); free(q->qid); free(q->dec); free(q->chunk);
   free(q);
 }
 
 static orc_queue *q_clone(const orc_queue *src) {
   int st;
   orc_queue *q = orc_queue_new(&src->pr, src->n, src->rp, src->rd, src->cx, src->clock, &st);
-  if (q) q->iters = src->iters;
+  if (!q) return NULL;
+  q->iters = src->iters;
+  for (int64_t r = 0; r < src->n; ++r) q->qid[r] = src->qid[r];
+  q->realized = src->realized;
+  q->q_t = src->q_t;
+  q->reading = src->reading;
+  q->tracked = src->tracked;
   return q;
 }
 
@@ -235,11 +258,33 @@ static void apply(orc_queue *q) {
     if (q->dec[r]) { q->cx[r] += 1; q->rd[r] -= 1; }
     if (q->chunk[r]) { q->cx[r] += q->chunk[r]; q->rp[r] -= q->chunk[r]; }
     if (q->rd[r] > 0) {
-      q->rp[w] = q->rp[r]; q->rd[w] = q->rd[r]; q->cx[w] = q->cx[r];
+      q->rp[w] = q->rp[r]; q->rd[w] = q->rd[r]; q->cx[w] = q->cx[r]; q->qid[w] = q->qid[r];
       ++w;
     }
   }
   q->n = w;
+}
+
+/* First tokens of the batch built by compose(), which ends at q->clock: a tracked
+   query gets its first token in this batch when it decodes in it (reading 0; it
+   has not decoded before, or it would no longer be tracked) or when the batch
+   completes its prefill (reading 1).  Its realised TTFT is the batch's end minus
+   its arrival time, and it is tracked no longer. */
+static void record_first_tokens(orc_queue *q) {
+  for (int64_t r = 0; r < q->n; ++r) {
+    const int32_t i = q->qid[r];
+    if (i < 0) continue;
+    int first;
+    if (q->reading == 1)
+      first = q->chunk[r] > 0 && q->chunk[r] == q->rp[r];
+    else
+      first = q->dec[r] == 1;
+    if (first) {
+      q->realized[i] = q->clock - q->q_t[i];
+      q->qid[r] = -1;
+      q->tracked -= 1;
+    }
+  }
 }
 
 /* One batch of the replayed instance; returns its time and features. */
@@ -247,6 +292,7 @@ double orc_queue_step(orc_queue *q, int64_t *feat4) {
   orc_feat f = compose(q);
   double T = batch_time(&q->pr, f);
   q->clock = q->clock + T;
+  if (q->realized) record_first_tokens(q);
   apply(q);
   q->iters += 1;
   if (feat4) { feat4[0] = f.P; feat4[1] = f.D; feat4[2] = f.C; feat4[3] = f.A; }
@@ -265,16 +311,23 @@ int orc_queue_advance(orc_queue *q, double t, int64_t max_iters) {
   return ORC_OK;
 }
 
-/* Append a routed query as a waiting request. */
-int orc_queue_append(orc_queue *q, int32_t p, int32_t dhat, int64_t queue_cap) {
+/* Append a routed query as a waiting request; query index i >= 0 is tracked
+   until its first token (when tracking is on), i = -1 is not. */
+static int append_tagged(orc_queue *q, int32_t p, int32_t dhat, int64_t queue_cap, int32_t i) {
   if (p < 1) return ORC_E_ARG;
   if (orc_queue_waiting(q) + 1 > queue_cap) return ORC_E_CAPACITY;
   if (q_reserve(q, q->n + 2) != ORC_OK) return ORC_E_ARG;
   q->rp[q->n] = p;
   q->rd[q->n] = dhat < 1 ? 1 : dhat;
   q->cx[q->n] = 0;
+  q->qid[q->n] = q->realized ? i : -1;
+  if (q->realized && i >= 0) q->tracked += 1;
   q->n += 1;
   return ORC_OK;
+}
+
+int orc_queue_append(orc_queue *q, int32_t p, int32_t dhat, int64_t queue_cap) {
+  return append_tagged(q, p, dhat, queue_cap, -1);
 }
 
 /* SFS estimate for a query of p prompt tokens arriving at t (the instance must
@@ -374,7 +427,8 @@ void orc_ttft_targets(int32_t n, const int32_t *p, const double *u_ms, const dou
  * Outputs per query: choice, TTFT at the choice, utility of Eq. 2 at the choice
  * (acc - w_cost*cost), and optionally the whole TTFT / iteration rows.
  * The final state is written to the out_* arrays when out_offsets != NULL (each
- * out array must hold out_cap entries).
+ * out array must hold out_cap entries).  realized [N] (may be NULL) receives the
+ * realised TTFT of every query (NaN where an error stopped the trace first).
  */
 int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
               const int32_t *offsets, const int32_t *rp, const int32_t *rd, const int32_t *cx,
@@ -385,7 +439,7 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
               double *util_chosen,
               double *ttft_all, int32_t *iters_all, int32_t *out_offsets, int32_t *out_rp,
               int32_t *out_rd, int32_t *out_cx, double *out_clock, int64_t *out_iters,
-              int64_t out_cap, int32_t *failed_query) {
+              int64_t out_cap, double *realized, int32_t *failed_query) {
   int st = ORC_OK;
   *failed_query = -1;
   if (n_inst < 1 || n_q < 0 || n_cols < 1) return ORC_E_ARG;
@@ -398,7 +452,14 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
     int64_t lo = offsets[j], hi = offsets[j + 1];
     qs[j] = orc_queue_new(&params[j], hi - lo, rp + lo, rd + lo, cx + lo, clock[j], &st);
     if (st == ORC_OK && orc_queue_waiting(qs[j]) > queue_cap) st = ORC_E_CAPACITY;
+    if (st == ORC_OK && realized) {
+      qs[j]->realized = realized;
+      qs[j]->q_t = q_t;
+      qs[j]->reading = reading;
+    }
   }
+  if (realized)
+    for (int32_t i = 0; i < n_q; ++i) realized[i] = NAN;
   if (st == ORC_OK && n_q > 0)
     for (int32_t j = 0; j < n_inst && st == ORC_OK; ++j)
       st = orc_queue_advance(qs[j], q_t[0], max_iters);
@@ -420,11 +481,23 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
       double pen = w_cost * crow[col[m]];
       util_chosen[i] = arow[col[m]] - pen;
     }
-    st = orc_queue_append(qs[m], q_p[i], q_d[i], queue_cap);
+    st = append_tagged(qs[m], q_p[i], q_d[i], queue_cap, i);
     double t_next = (i + 1 < n_q) ? q_t[i + 1] : q_t[i];
     for (int32_t j = 0; j < n_inst && st == ORC_OK; ++j)
       st = orc_queue_advance(qs[j], t_next, max_iters);
     if (st != ORC_OK) *failed_query = i;
+  }
+  /* queries without their first token at the end: run a copy of each instance on,
+     with no further arrivals, until its last tracked query has it */
+  for (int32_t j = 0; j < n_inst && st == ORC_OK && realized; ++j) {
+    if (qs[j]->tracked == 0) continue;
+    orc_queue *w = q_clone(qs[j]);
+    if (!w) { st = ORC_E_ARG; break; }
+    for (int64_t k = 0; w->tracked > 0; ++k) {
+      if (k == max_iters) { st = ORC_E_ITER; break; }
+      orc_queue_step(w, NULL);
+    }
+    orc_queue_free(w);
   }
   if (st == ORC_OK && out_offsets) {
     int64_t pos = 0;
@@ -486,14 +559,14 @@ int orc_stats(int32_t n_q, const int32_t *choice, const double *ttft_chosen, con
 }
 
 /* Eq. 4: left fold in query order of the utility (Eq. 2) at the chosen instance
- * for queries whose TTFT at the choice is within the target, divided by N. */
-int orc_ontime_utility(int32_t n_q, const int32_t *choice, const double *ttft_chosen,
+ * for queries whose realised TTFT is within the target, divided by N. */
+int orc_ontime_utility(int32_t n_q, const int32_t *choice, const double *ttft_real,
                        const double *tau, const double *acc, const double *cost, int32_t n_cols,
                        const int32_t *col, double w_cost, double *out) {
   if (n_q < 1) return ORC_E_ARG;
   double s = 0.0;
   for (int32_t i = 0; i < n_q; ++i) {
-    if (!(ttft_chosen[i] <= tau[i])) continue;
+    if (!(ttft_real[i] <= tau[i])) continue;
     double ac = acc[(int64_t)i * n_cols + col[choice[i]]];
     double co = cost[(int64_t)i * n_cols + col[choice[i]]];
     double pen = w_cost * co;

@@ -17,10 +17,12 @@ import numpy as np
 
 
 class Req:
-    __slots__ = ("rp", "rd", "cx")
+    __slots__ = ("rp", "rd", "cx", "query", "prompt")
 
-    def __init__(self, rp, rd, cx):
+    def __init__(self, rp, rd, cx, query=-1):
         self.rp, self.rd, self.cx = int(rp), int(rd), int(cx)
+        self.query = int(query)     # index of the routed query, -1 for residents
+        self.prompt = int(rp) if cx == 0 else -1
 
     def tup(self):
         return (self.rp, self.rd, self.cx)
@@ -35,7 +37,11 @@ class BFInstance:
 
     def copy(self):
         o = BFInstance(*self.coef, self.B, self.M, clock=self.clock)
-        o.reqs = [Req(*r.tup()) for r in self.reqs]
+        o.reqs = []
+        for r in self.reqs:
+            x = Req(*r.tup(), query=r.query)
+            x.prompt = r.prompt
+            o.reqs.append(x)
         return o
 
     # -- one batch, token by token ---------------------------------------------------
@@ -88,20 +94,34 @@ class BFInstance:
                 keep.append(r)
         self.reqs = keep
 
-    def step(self):
+    def step(self, first_token=None, reading=0):
+        """One batch.  first_token(query, end_time) is called for every routed query
+        whose first token the batch produces: under reading 0 a query that decodes
+        while its context is still exactly its prompt (it has not decoded before);
+        under reading 1 a query whose remaining prefill reaches 0 in the batch."""
         T, f, gp, gd = self.batch()
         self.clock = self.clock + T
+        if first_token is not None:
+            for i, r in enumerate(self.reqs):
+                if r.query < 0:
+                    continue
+                if reading == 1:
+                    hit = r.rp > 0 and r.rp - gp[i] == 0
+                else:
+                    hit = gd[i] == 1 and r.cx == r.prompt
+                if hit:
+                    first_token(r.query, self.clock)
         self.apply(gp, gd)
         return T, f
 
-    def advance(self, t):
+    def advance(self, t, first_token=None, reading=0):
         while self.reqs and self.clock < t:
-            self.step()
+            self.step(first_token, reading)
         if not self.reqs and self.clock < t:
             self.clock = float(t)
 
-    def append(self, p, d):
-        self.reqs.append(Req(p, max(int(d), 1), 0))
+    def append(self, p, d, query=-1):
+        self.reqs.append(Req(p, max(int(d), 1), 0, query))
 
     def estimate(self, p, d, t, reading=0):
         w = self.copy()
@@ -146,17 +166,28 @@ def _pick_constrained(row, util, tau):
     return min(range(len(row)), key=lambda j: (row[j], j))
 
 
-def trace(wl, scenario=0, n_q=None, reading=0, tau=None):
+def trace(wl, scenario=0, n_q=None, reading=0, tau=None, realized=None):
     """Sequential trace with the route computed by numpy (first maximum wins), or by
-    the constrained rule of Eq. 3 when per-query targets ``tau`` are given."""
+    the constrained rule of Eq. 3 when per-query targets ``tau`` are given.
+
+    With an array ``realized`` [N], the replay records each query's first-token
+    time minus its arrival; queries without it at the end get it from a copy of
+    their instance run on with no further arrivals."""
     insts = instances_of(wl)
     N = wl.n_q if n_q is None else n_q
     col = np.asarray(wl.col)
     wc, wlat = float(wl.w_cost[scenario]), float(wl.w_lat_ms[scenario])
     choices, rows = [], []
+    ft = None
+    if realized is not None:
+        realized[:N] = np.nan
+
+        def ft(q, end):
+            assert np.isnan(realized[q]), "a query got two first tokens"
+            realized[q] = end - float(wl.q_t_ms[q])
     if N:
         for x in insts:
-            x.advance(wl.q_t_ms[0])
+            x.advance(wl.q_t_ms[0], ft, reading)
     for i in range(N):
         p, d, t = int(wl.q_prefill[i]), int(wl.q_decode[i]), float(wl.q_t_ms[i])
         row = np.array([x.estimate(p, d, t, reading)[0] for x in insts])
@@ -169,8 +200,14 @@ def trace(wl, scenario=0, n_q=None, reading=0, tau=None):
             m = _pick_constrained(row, acc - wc * cost, float(tau[i]))
         choices.append(m)
         rows.append(row)
-        insts[m].append(p, d)
+        insts[m].append(p, d, query=i if ft else -1)
         t_next = float(wl.q_t_ms[i + 1]) if i + 1 < N else t
         for x in insts:
-            x.advance(t_next)
+            x.advance(t_next, ft, reading)
+    if ft is not None:
+        for j, x in enumerate(insts):
+            mine = [i for i in range(N) if choices[i] == j]
+            w = x.copy()
+            while any(np.isnan(realized[i]) for i in mine):
+                w.step(ft, reading)
     return np.array(choices, np.int32), np.array(rows), insts

@@ -10,6 +10,7 @@
 * invariants: token budget, sequence cap, FCFS token conservation, monotonicity.
 """
 
+import dataclasses
 import itertools
 import json
 import math
@@ -248,9 +249,11 @@ def test_bruteforce_random_traces(seed):
                             n_scen=1)
     for reading in (0, 1):
         r = O.trace(wl, reading=reading, full_rows=True, queue_cap=10 ** 6)
-        ch, rows, insts = BF.trace(wl, reading=reading)
+        real = np.zeros(wl.n_q)
+        ch, rows, insts = BF.trace(wl, reading=reading, realized=real)
         np.testing.assert_array_equal(r.choice, ch)
         assert np.array_equal(r.ttft_all.view(np.int64), rows.view(np.int64))
+        assert np.array_equal(r.realized.view(np.int64), real.view(np.int64))
         for j, x in enumerate(insts):
             lo, hi = r.offsets[j], r.offsets[j + 1]
             got = list(zip(r.rem_prefill[lo:hi], r.rem_decode[lo:hi], r.context[lo:hi]))
@@ -457,10 +460,85 @@ def test_bruteforce_constrained_traces(seed):
     lo, hi = float(lam.ttft_all.min()), float(lam.ttft_all.max())
     tau = np.random.default_rng(seed).uniform(lo, hi, size=wl.n_q)
     r = O.trace(wl, full_rows=True, queue_cap=10 ** 6, tau=tau)
-    ch, rows, insts = BF.trace(wl, tau=tau)
+    real = np.zeros(wl.n_q)
+    ch, rows, insts = BF.trace(wl, tau=tau, realized=real)
     np.testing.assert_array_equal(r.choice, ch)
     assert np.array_equal(r.ttft_all.view(np.int64), rows.view(np.int64))
+    assert np.array_equal(r.realized.view(np.int64), real.view(np.int64))
     for j, x in enumerate(insts):
         a, b = r.offsets[j], r.offsets[j + 1]
         got = list(zip(r.rem_prefill[a:b], r.rem_decode[a:b], r.context[a:b]))
         assert [tuple(int(v) for v in g) for g in got] == x.state()
+
+
+# ------------------------------------------------------------------ realised TTFT
+def _hand_trace_workload():
+    """One empty instance, B = 8, M = 4, T = 1 + 0.5 P + 0.25 D; query 0 (p = 10,
+    d = 2) at 0 ms, query 1 (p = 5, d = 1) at 0.5 ms."""
+    base = make_tiny_workload(0, n_inst=1, n_q=2)
+    return dataclasses.replace(
+        base, n_inst=1, a=np.array([1.0]), b=np.array([0.5]), c=np.array([0.25]),
+        d=np.zeros(1), e=np.zeros(1), budget=np.array([8], np.int32),
+        max_seqs=np.array([4], np.int32), col=np.zeros(1, np.int32),
+        offsets=np.zeros(2, np.int32), rem_prefill=np.zeros(0, np.int32),
+        rem_decode=np.zeros(0, np.int32), context=np.zeros(0, np.int32),
+        clock_ms=np.zeros(1), q_prefill=np.array([10, 5], np.int32),
+        q_decode=np.array([2, 1], np.int32), q_t_ms=np.array([0.0, 0.5]),
+        acc=np.full((2, 1), 0.5), cost=np.zeros((2, 1)), w_cost=np.zeros(1),
+        w_lat_ms=np.zeros(1), queue_cap=8, max_prompt=16)
+
+
+@pytest.mark.parametrize("reading", [0, 1])
+def test_realized_hand_worked(reading):
+    """Worked by hand.  Query 0 alone: batches of 8 and 2 prefill tokens (5 and 2 ms)
+    and a decode batch (1.25 ms): estimate 8.25 ms (7 ms under reading 1).  The
+    replay runs the 8-token batch before query 1 arrives at 0.5 ms (clock 5); query
+    1 then shares the next batch: 2 + 5 prefill tokens (4.5 ms, both prefills done
+    at 9.5), then both decode (1.5 ms, 11.0).  Query 1's estimate is exact (10.5;
+    9.0 under reading 1); query 0's first token comes 2.75 ms (2.5 ms) later than
+    its estimate, because of query 1's tokens."""
+    wl = _hand_trace_workload()
+    r = O.trace(wl, reading=reading, queue_cap=8)
+    real = np.zeros(2)
+    BF.trace(wl, reading=reading, realized=real)
+    if reading == 0:
+        assert list(r.ttft_chosen) == [8.25, 10.5]
+        assert list(r.realized) == [11.0, 10.5]
+    else:
+        assert list(r.ttft_chosen) == [7.0, 9.0]
+        assert list(r.realized) == [9.5, 9.0]
+    assert list(real) == list(r.realized)
+    # the trace's own end state is the replay to the last arrival, not the drain
+    assert r.clock_ms[0] == 5.0
+
+
+def _realized_properties(wl, r):
+    """A later query only adds tokens to batches (under FCFS it never takes budget or
+    a slot ahead of an earlier one), and batch time does not decrease with tokens:
+    the realised TTFT is never below the estimate at the choice, and equals it when
+    no later query joins the same instance before the first token."""
+    N = len(r.choice)
+    assert not np.isnan(r.realized).any()
+    assert (r.realized >= r.ttft_chosen).all()
+    t = wl.q_t_ms[:N]
+    for i in range(N):
+        later = np.nonzero(r.choice[i + 1:] == r.choice[i])[0]
+        if later.size == 0 or t[i + 1 + later[0]] >= t[i] + r.realized[i]:
+            assert r.realized[i] == r.ttft_chosen[i], i
+
+
+@pytest.mark.parametrize("reading", [0, 1])
+def test_realized_properties_c1(reading):
+    from workloads import make_workload
+    wl = make_workload("c1")
+    r = O.trace(wl, reading=reading)
+    _realized_properties(wl, r)
+    assert (r.realized > r.ttft_chosen).sum() > 0   # the case the estimate misses occurs
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_realized_properties_tiny(seed):
+    wl = make_tiny_workload(400 + seed, n_inst=2, max_res=4, n_q=40, mean_gap_ms=1.0,
+                            n_scen=1)
+    for reading in (0, 1):
+        _realized_properties(wl, O.trace(wl, reading=reading, queue_cap=10 ** 6))
