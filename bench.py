@@ -51,6 +51,9 @@ def _parse():
     ap.add_argument("--objective", default="lagrangian", choices=["lagrangian", "constrained"],
                     help="route by the Lagrangian objective or by Eq. 3 with the paper's "
                          "per-query TTFT targets (sequential workloads)")
+    ap.add_argument("--realized", action="store_true",
+                    help="also track each query's realised TTFT in the replay (always on "
+                         "under --objective constrained, whose OnTimeUtility counts it)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="time budget of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -211,6 +214,8 @@ def main():
     if constrained:   # the paper's per-query TTFT targets, computed once on the GPU
         tau = ctx.ttft_targets(qp, T(wl.tau_u_ms, torch.float64), T(wl.tau_v, torch.float64))
         ontime = torch.empty(Z, dtype=torch.float64, device=dev)
+    track = (constrained or args.realized) and not whatif
+    real = torch.empty((Z, N), dtype=torch.float64, device=dev) if track else None
     if whatif:
         ttft = torch.empty((Z, N, I), dtype=torch.float64, device=dev)
     kev = []   # (start, end) events around the dominant kernel of each timed step
@@ -241,16 +246,16 @@ def main():
             e0.record(stream)
         if constrained:
             ctx.route_trace_constrained(qp, qd, qt, t_last, tau, acc, cost, wc, choice=choice,
-                                        chosen_ttft=chosen, utility=util)
+                                        chosen_ttft=chosen, utility=util, realized=real)
         else:
             ctx.route_trace(qp, qd, qt, t_last, acc, cost, wc, wlat, choice=choice,
-                            chosen_ttft=chosen, utility=util)
+                            chosen_ttft=chosen, utility=util, realized=real)
         if record:
             e1.record(stream)
             kev.append((e0, e1))
         ctx.stats(choice, chosen, acc, cost, wc, out=stats)
         if constrained:
-            ctx.ontime_utility(choice, chosen, tau, acc, cost, wc, out=ontime)
+            ctx.ontime_utility(choice, real, tau, acc, cost, wc, out=ontime)
 
     for _ in range(args.warmup):
         step()
@@ -286,6 +291,15 @@ def main():
         line["stats_scenario0"] = stats[0].tolist()
         if constrained:
             line["ontime_utility_scenario0"] = float(ontime[0])
+        if track:
+            # the replay's first-token times against the estimates at the choice
+            # (the comparison of Fig. 2), scenario 0
+            e0, r0 = chosen[0].cpu().numpy(), real[0].cpu().numpy()
+            line["realized_vs_estimated_scenario0"] = {
+                "mean_estimated_ms": float(e0.mean()), "mean_realized_ms": float(r0.mean()),
+                "frac_realized_later": float((r0 > e0).mean()),
+                "max_gap_ms": float((r0 - e0).max())}
+        line["config"]["realized_tracking"] = bool(track)
     line["kernel_ms"] = kernel_ms
 
     roof = None
@@ -300,10 +314,12 @@ def main():
         achieved = flops / (kernel_ms / 1000.0) / 1e12
         roof = {"bound": "alu", "achieved": achieved, "peak": FP64_VECTOR_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
-                "traffic": load_traffic(args.workload),
+                "traffic": None if track else load_traffic(args.workload),
                 "note": f"{batches} simulated token batches per step over {Z} scenario(s) "
                         f"({int(est_batches.sum())} behind the estimates, {int(sum(replay))} "
-                        "replayed) x 9 fp64 ops each; sequential trace, latency-bound"}
+                        "replayed) x 9 fp64 ops each; sequential trace, latency-bound"
+                        + ("; the batches run after the last arrival for realised TTFTs "
+                           "are not counted" if track else "")}
         line["batches_per_step"] = batches
     if not args.no_cpu_baseline:
         if whatif:

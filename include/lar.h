@@ -205,12 +205,23 @@ lar_status lar_commit(lar_ctx *ctx, const int32_t *choice, int32_t q_prefill, in
  *   q_prefill, q_decode dev [N] int32;  q_t_ms dev [N] non-decreasing
  *   acc, cost dev [N][n_cols];  w_cost, w_lat dev [Z]
  *   choice dev [Z][N];  chosen_ttft, utility dev [Z][N] (may be NULL)
+ *   realized_ttft dev [Z][N] (may be NULL): the TTFT each query sees in the replay
+ *     (the estimates set against measured TTFTs in Fig. 2; Eq. 4 counts it): the
+ *     end of the replayed batch that produces its first token (the same batch
+ *     reading as the estimate) minus q_t_ms[i].  It can exceed the estimate:
+ *     queries that arrive later take the budget a query leaves in its last prefill
+ *     batch and decode beside it, which lengthens those batches (Sec. 4.1 batch
+ *     time).  A query without its first token at t_after_ms gets it from a private
+ *     copy of its instance run on with no further arrivals; the state the call
+ *     leaves is not changed by this.  NaN marks a query the replay did not finish
+ *     (only after a device error).  Each call tracks its own queries: a query
+ *     routed by an earlier call, or committed by lar_commit, is not reported.
  */
 lar_status lar_route_trace(lar_ctx *ctx, int32_t n_q, const int32_t *q_prefill,
                            const int32_t *q_decode, const double *q_t_ms, double t_after_ms,
                            const double *acc, const double *cost, int32_t n_cols,
                            const double *w_cost, const double *w_lat, int32_t *choice,
-                           double *chosen_ttft, double *utility);
+                           double *chosen_ttft, double *utility, double *realized_ttft);
 
 /*
  * lar_route_trace under the constrained objective (Eq. 3; see
@@ -226,7 +237,8 @@ lar_status lar_route_trace_constrained(lar_ctx *ctx, int32_t n_q, const int32_t 
                                        double t_after_ms, const double *tau_ms,
                                        const double *acc, const double *cost, int32_t n_cols,
                                        const double *w_cost, int32_t *choice,
-                                       double *chosen_ttft, double *utility);
+                                       double *chosen_ttft, double *utility,
+                                       double *realized_ttft);
 
 /*
  * Per-scenario summary of a routed trace -- the two axes of the utility-latency
@@ -245,17 +257,15 @@ lar_status lar_stats(lar_ctx *ctx, int32_t n_q, const int32_t *choice, const dou
 /*
  * OnTimeUtility (Eq. 4) of a routed trace, per scenario:
  *   out[z] = (1/N) * sum over i, in query order, of
- *            (acc[i][col_c] - w_cost[z]*cost[i][col_c]) if chosen_ttft[z][i] <= tau_ms[i],
- *            c = choice[z][i]; queries past their target add nothing.
- * The TTFT at the choice stands for the realised TTFT: the replay runs the same
- * scheduler, and under FCFS a later query never takes budget ahead of an earlier one.
- *   choice, chosen_ttft dev [Z][N];  tau_ms dev [N];  acc, cost dev [N][n_cols]
- *   w_cost dev [Z];  out dev [Z] float64
+ *            (acc[i][col_c] - w_cost[z]*cost[i][col_c]) if realized_ttft[z][i] <= tau_ms[i],
+ *            c = choice[z][i]; queries past their target (or NaN) add nothing.
+ *   choice dev [Z][N];  realized_ttft dev [Z][N] (the trace's realised TTFT)
+ *   tau_ms dev [N];  acc, cost dev [N][n_cols];  w_cost dev [Z];  out dev [Z] float64
  */
 lar_status lar_ontime_utility(lar_ctx *ctx, int32_t n_q, const int32_t *choice,
-                              const double *chosen_ttft, const double *tau_ms, const double *acc,
-                              const double *cost, int32_t n_cols, const double *w_cost,
-                              double *out);
+                              const double *realized_ttft, const double *tau_ms,
+                              const double *acc, const double *cost, int32_t n_cols,
+                              const double *w_cost, double *out);
 
 /*
  * Copy scenario `scen`'s state out (synchronises): resident requests of every

@@ -33,6 +33,7 @@ struct lar_ctx {
   uint64_t* xslot = nullptr;   // [Z][2][kMaxCluster][4] candidate posts of the clustered trace
   lar::SyncCtl sync{1000000000ull, -1, -1};   // 10 s wait bound; no post left out
   unsigned long long* work = nullptr;          // [Z] estimate batches of the last trace
+  int32_t tag_next = 0;        // ring tag of the next query tracked for its realised TTFT
   lar::DevState snap{};        // one scenario's copy of the last loaded snapshot
   int32_t* err = nullptr;
   size_t tail_elems = 0;  // allocated K * Z * I
@@ -165,6 +166,7 @@ lar_status lar_create(lar_ctx** out, const lar_config* cfg) {
     chk(dev_alloc(ctx, &D.r_rd, nq * rcap));
     chk(dev_alloc(ctx, &D.r_cx, nq * rcap));
     chk(dev_alloc(ctx, &D.r_seq, nq * rcap));
+    chk(dev_alloc(ctx, &D.r_tag, nq * rcap));
     D.mcap = ctx->mcap;
     D.rcap = rcap;
     D.qcap = ctx->qcap;
@@ -249,7 +251,7 @@ lar_status lar_load_state(lar_ctx* ctx, const lar_instance_params* params, const
   const int rcap = qcap + mcap;
   std::vector<int32_t> d_last((size_t)I * mcap, 0), d_cx0((size_t)I * mcap, 0),
       d_seq((size_t)I * mcap, 0), r_rp((size_t)I * rcap, 0), r_rd((size_t)I * rcap, 0),
-      r_cx((size_t)I * rcap, 0), r_seq((size_t)I * rcap, 0);
+      r_cx((size_t)I * rcap, 0), r_seq((size_t)I * rcap, 0), r_tag((size_t)I * rcap, -1);
   std::vector<lar::QScal> sc(I);
   for (int j = 0; j < I; ++j) {
     int nr = 0, nw = 0, nd = 0, np = 0, npart = 0;
@@ -340,6 +342,7 @@ lar_status lar_load_state(lar_ctx* ctx, const lar_instance_params* params, const
   HIP_TRY(ctx, hipMemcpy(sn.r_rd, r_rd.data(), r_rd.size() * 4, hipMemcpyHostToDevice));
   HIP_TRY(ctx, hipMemcpy(sn.r_cx, r_cx.data(), r_cx.size() * 4, hipMemcpyHostToDevice));
   HIP_TRY(ctx, hipMemcpy(sn.r_seq, r_seq.data(), r_seq.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(ctx, hipMemcpy(sn.r_tag, r_tag.data(), r_tag.size() * 4, hipMemcpyHostToDevice));
   ctx->loaded = true;
   ctx->sticky = LAR_OK;
   {
@@ -370,7 +373,9 @@ lar_status lar_reload_state(lar_ctx* ctx) {
     HIP_TRY(ctx, hipMemcpyAsync(S.r_rd + o * rcap, sn.r_rd, I * rcap * 4, k, s));
     HIP_TRY(ctx, hipMemcpyAsync(S.r_cx + o * rcap, sn.r_cx, I * rcap * 4, k, s));
     HIP_TRY(ctx, hipMemcpyAsync(S.r_seq + o * rcap, sn.r_seq, I * rcap * 4, k, s));
+    HIP_TRY(ctx, hipMemcpyAsync(S.r_tag + o * rcap, sn.r_tag, I * rcap * 4, k, s));
   }
+  ctx->tag_next = 0;   // every ring entry is untracked again
   HIP_TRY(ctx, lar::launch_clear_error(env_of(ctx)));
   ctx->sticky = LAR_OK;
   return LAR_OK;
@@ -457,7 +462,8 @@ static lar_status trace_rows(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill
                              const int32_t* q_decode, const double* q_t_ms, double t_after_ms,
                              const double* tau_ms, const double* acc, const double* cost,
                              int32_t n_cols, const double* w_cost, const double* w_lat,
-                             int32_t* choice, double* chosen_ttft, double* utility) {
+                             int32_t* choice, double* chosen_ttft, double* utility,
+                             double* realized) {
   lar_status st = ready(ctx);
   if (st != LAR_OK) return st;
   if (n_q < 0) return fail(ctx, LAR_E_ARG, "n_q < 0");
@@ -484,6 +490,18 @@ static lar_status trace_rows(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill
   ta.choice = choice;
   ta.chosen_ttft = chosen_ttft;
   ta.utility = utility;
+  ta.realized = realized;
+  ta.tag0 = 0;
+  if (realized) {
+    // tags tag0 .. tag0 + N - 1 must stay positive int32; when the counter would run
+    // past that, every ring entry is marked untracked and the counter starts over
+    if (ctx->tag_next > INT32_MAX - n_q) {
+      HIP_TRY(ctx, lar::launch_untag(env));
+      ctx->tag_next = 0;
+    }
+    ta.tag0 = ctx->tag_next;
+    ctx->tag_next += n_q;
+  }
   HIP_TRY(ctx, lar::launch_trace(env, ta));
   return LAR_OK;
 }
@@ -492,20 +510,21 @@ lar_status lar_route_trace(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill,
                            const int32_t* q_decode, const double* q_t_ms, double t_after_ms,
                            const double* acc, const double* cost, int32_t n_cols,
                            const double* w_cost, const double* w_lat, int32_t* choice,
-                           double* chosen_ttft, double* utility) {
+                           double* chosen_ttft, double* utility, double* realized_ttft) {
   if (ctx && !w_lat) return fail(ctx, LAR_E_ARG, "null argument");
   return trace_rows(ctx, n_q, q_prefill, q_decode, q_t_ms, t_after_ms, nullptr, acc, cost, n_cols,
-                    w_cost, w_lat, choice, chosen_ttft, utility);
+                    w_cost, w_lat, choice, chosen_ttft, utility, realized_ttft);
 }
 
 lar_status lar_route_trace_constrained(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill,
                                        const int32_t* q_decode, const double* q_t_ms,
                                        double t_after_ms, const double* tau_ms, const double* acc,
                                        const double* cost, int32_t n_cols, const double* w_cost,
-                                       int32_t* choice, double* chosen_ttft, double* utility) {
+                                       int32_t* choice, double* chosen_ttft, double* utility,
+                                       double* realized_ttft) {
   if (ctx && !tau_ms) return fail(ctx, LAR_E_ARG, "null argument");
   return trace_rows(ctx, n_q, q_prefill, q_decode, q_t_ms, t_after_ms, tau_ms, acc, cost, n_cols,
-                    w_cost, nullptr, choice, chosen_ttft, utility);
+                    w_cost, nullptr, choice, chosen_ttft, utility, realized_ttft);
 }
 
 lar_status lar_stats(lar_ctx* ctx, int32_t n_q, const int32_t* choice, const double* chosen_ttft,
@@ -524,19 +543,19 @@ lar_status lar_stats(lar_ctx* ctx, int32_t n_q, const int32_t* choice, const dou
 }
 
 lar_status lar_ontime_utility(lar_ctx* ctx, int32_t n_q, const int32_t* choice,
-                              const double* chosen_ttft, const double* tau_ms, const double* acc,
+                              const double* realized_ttft, const double* tau_ms, const double* acc,
                               const double* cost, int32_t n_cols, const double* w_cost,
                               double* out) {
   lar_status st = ready(ctx);
   if (st != LAR_OK) return st;
   if (n_q < 1) return fail(ctx, LAR_E_ARG, "n_q < 1");
-  if (!choice || !chosen_ttft || !tau_ms || !acc || !cost || !w_cost || !out)
+  if (!choice || !realized_ttft || !tau_ms || !acc || !cost || !w_cost || !out)
     return fail(ctx, LAR_E_ARG, "null argument");
   if (n_cols <= ctx->max_col)
     return fail(ctx, LAR_E_ARG, "n_cols %d does not cover instance column %d", n_cols, ctx->max_col);
   const LaunchEnv env = env_of(ctx);
-  HIP_TRY(ctx, lar::launch_ontime(env, n_q, choice, chosen_ttft, tau_ms, acc, cost, n_cols, w_cost,
-                                  out));
+  HIP_TRY(ctx, lar::launch_ontime(env, n_q, choice, realized_ttft, tau_ms, acc, cost, n_cols,
+                                  w_cost, out));
   return LAR_OK;
 }
 

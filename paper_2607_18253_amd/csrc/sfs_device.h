@@ -14,7 +14,8 @@
 //     prefill gives every chunk of the batch.  Fully served entries are always a
 //     prefix of the window and move to the decode slots.
 // Every request carries its arrival sequence number, so the FCFS list can be
-// rebuilt on read-out.
+// rebuilt on read-out.  A routed query also carries a tag in the ring (its index
+// in a trace, -1 if untracked), read back when the query gets its first token.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -39,7 +40,10 @@ struct alignas(64) QScal {
   int64_t pre_sum;   // sum of remaining prefill over the prefill list
   double clock;      // instance clock, ms
   int64_t iters;     // batches replayed since the load
-  int32_t pad[2];
+  // first-token tracking, kept up to date only by a trace that reports realised
+  // TTFT (it zeroes both first)
+  int32_t pend;      // prefills completed by the last batch (they decode next batch)
+  int32_t ntrk;      // tracked queries of the running trace without a first token
 };
 static_assert(sizeof(QScal) == 64, "QScal is one 64-byte record");
 
@@ -49,6 +53,7 @@ struct DevState {
   QScal* sc;                          // [ZI]
   int32_t *d_last, *d_cx0, *d_seq;    // [ZI][mcap]
   int32_t *r_rp, *r_rd, *r_cx, *r_seq;  // [ZI][rcap]
+  int32_t* r_tag;                     // [ZI][rcap] query tag of each ring entry
   int32_t mcap, rcap, qcap;           // rcap = qcap + mcap
 };
 
@@ -191,7 +196,7 @@ template <int KS>
 struct LdsQueue {
   int dl[KS * kWave], dc[KS * kWave], ds[KS * kWave];
   int wrp[kWave], wrd[kWave], wcx[kWave], wseq[kWave];
-  int g, n_dec, n_part, n_pre, head, next_seq, woff, nwin;
+  int g, n_dec, n_part, n_pre, head, next_seq, woff, nwin, pend, ntrk;
   int64_t c0sum, pre_sum, iters;
   double clock;
 };
@@ -200,6 +205,9 @@ struct LdsQueue {
 struct StepOut {
   int P, D;
   int64_t C, A;
+  int h0;    // ring head before the batch
+  int pn;    // prefills completed by the batch before (first decode in this one)
+  int nd;    // prefills completed by this batch: ring entries h0 .. h0 + nd - 1
 };
 
 // What a wave needs besides the state to work on one queue: the batch-time
@@ -235,14 +243,18 @@ struct Queue {
   int woff, nwin;
   // scalars (wave-uniform)
   int g, n_dec, n_part, n_pre, head, next_seq;
+  int pend, ntrk;   // first-token tracking (TRK: copied in and out; else unused)
   int64_t c0sum, pre_sum;
   double clock;
   int64_t iters;
+  template <bool TRK = false>
   __device__ void load(const DevState& S, const QEnv& e, int qid) {
     const int ln = lane_id();
     const QScal* q = S.sc + qid;
     g = uni(q->g); n_dec = uni(q->n_dec); n_part = uni(q->n_part); n_pre = uni(q->n_pre);
     head = uni(q->head); next_seq = uni(q->next_seq);
+    if constexpr (TRK) { pend = uni(q->pend); ntrk = uni(q->ntrk); }
+    else { pend = 0; ntrk = 0; }
     c0sum = uni64(q->c0sum); pre_sum = uni64(q->pre_sum);
     clock = q->clock;
     iters = uni64(q->iters);
@@ -263,6 +275,7 @@ struct Queue {
   }
 
   // Copy to / from an LDS copy (same layout as the registers).
+  template <bool TRK = false>
   __device__ void to_lds(LdsQueue<KS>& L) const {
     const int ln = lane_id();
 #pragma unroll
@@ -273,11 +286,13 @@ struct Queue {
     if (ln == 0) {
       L.g = g; L.n_dec = n_dec; L.n_part = n_part; L.n_pre = n_pre; L.head = head;
       L.next_seq = next_seq; L.woff = woff; L.nwin = nwin; L.c0sum = c0sum;
+      if constexpr (TRK) { L.pend = pend; L.ntrk = ntrk; }
       L.pre_sum = pre_sum; L.iters = iters; L.clock = clock;
     }
     __builtin_amdgcn_wave_barrier();
   }
 
+  template <bool TRK = false>
   __device__ void from_lds(const LdsQueue<KS>& L) {
     const int ln = lane_id();
     __builtin_amdgcn_wave_barrier();
@@ -288,11 +303,13 @@ struct Queue {
     wrp = L.wrp[ln]; wrd = L.wrd[ln]; wcx = L.wcx[ln]; wseq = L.wseq[ln];
     g = uni(L.g); n_dec = uni(L.n_dec); n_part = uni(L.n_part); n_pre = uni(L.n_pre);
     head = uni(L.head); next_seq = uni(L.next_seq); woff = uni(L.woff); nwin = uni(L.nwin);
+    if constexpr (TRK) { pend = uni(L.pend); ntrk = uni(L.ntrk); }
     c0sum = uni64(L.c0sum); pre_sum = uni64(L.pre_sum); iters = uni64(L.iters);
     clock = L.clock;
   }
 
   // Write the queue back: decode slots compacted, window entries into the ring.
+  template <bool TRK = false>
   __device__ void store(const DevState& S, const QEnv& e, int qid) const {
     const int ln = lane_id();
     const int64_t db = (int64_t)qid * S.mcap;
@@ -318,6 +335,7 @@ struct Queue {
       q->g = g; q->n_dec = n_dec; q->n_part = n_part; q->n_pre = n_pre; q->head = head;
       q->next_seq = next_seq; q->c0sum = c0sum; q->pre_sum = pre_sum; q->clock = clock;
       q->iters = iters;
+      if constexpr (TRK) { q->pend = pend; q->ntrk = ntrk; }
     }
     // the same wave loads this queue again later in a persistent kernel
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
@@ -376,7 +394,11 @@ struct Queue {
   }
 
   // Append a waiting request at the FCFS tail (the caller checked the capacity).
-  __device__ void append(const QEnv& e, int p, int d) {
+  // A tracked query (tags: the queue's tag ring, non-null) leaves its tag in its
+  // ring slot, where it is looked up at its first token.  An untracked append
+  // leaves an older tag in the slot: tags only grow between the resets that clear
+  // every slot, so an older tag is below the running trace's first tag and ignored.
+  __device__ void append(const QEnv& e, int p, int d, int32_t* tags = nullptr, int tag = -1) {
     const int ln = lane_id();
     const int idx = n_pre;
     int pos = head + idx;
@@ -384,9 +406,18 @@ struct Queue {
     if (nwin == n_pre && idx < kWave) {     // the window holds the whole list: extend it
       if (woff + idx >= kWave) compact();
       if (ln == woff + idx) { wrp = p; wrd = d; wcx = 0; wseq = next_seq; }
+      if (tags) {
+        if (ln == 0) tags[pos] = tag;
+        // other lanes of this wave read the tag back at the first token
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+      }
       nwin = idx + 1;
     } else {                                // beyond the window: the ring, read on refill
-      if (ln == 0) { e.r_rp[pos] = p; e.r_rd[pos] = d; e.r_cx[pos] = 0; e.r_seq[pos] = next_seq; }
+      if (ln == 0) {
+        e.r_rp[pos] = p; e.r_rd[pos] = d; e.r_cx[pos] = 0; e.r_seq[pos] = next_seq;
+        if (tags) tags[pos] = tag;
+      }
       // other lanes of this wave read the entry back on refill
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
@@ -416,7 +447,9 @@ struct Queue {
     return wave_sum64(a);
   }
 
-  // Build the next token batch, apply it, return its features.
+  // Build the next token batch, apply it, return its features (TRK: and keep the
+  // count of completed prefills for first-token tracking).
+  template <bool TRK = false>
   __device__ StepOut step(const QEnv& e) {
     const int ln = lane_id();
     const Coef& k = e.k;
@@ -425,6 +458,8 @@ struct Queue {
     const int B = k.B;
     const int gn = g + 1;   // index of this batch
     StepOut o;
+    int nd = 0;
+    if constexpr (TRK) { o.h0 = head; o.pn = pend; }
     o.D = n_dec;
     o.C = need_C ? c0sum + (int64_t)n_dec * g : 0;
     int left = B - n_dec;
@@ -496,6 +531,7 @@ struct Queue {
         }
         __builtin_amdgcn_wave_barrier();
         n_dec += n_full;
+        if constexpr (TRK) nd += n_full;
         woff += n_full;
         nwin -= n_full;
         head += n_full;
@@ -510,8 +546,38 @@ struct Queue {
     if (nwin < n_pre && nwin < kWave / 2) refill(e);
     o.P = (int)P;
     o.A = need_A ? A : 0;
+    if constexpr (TRK) { o.nd = nd; pend = nd; }
     g = gn;
     return o;
+  }
+
+  // Realised TTFT of the tracked queries whose first token came in the batch just
+  // stepped (o, from step<true>), which ended at clk: the batch completing their prefill (reading 1)
+  // or the next one, their first decode (reading 0).  Those entries have left the
+  // prefill list (the ring slots just before the head), but their slots still hold
+  // their tags: appends fill the slots after the list, and the completed entries
+  // (running, so at most M minus the running partials) plus the list (at most qcap
+  // waiting entries plus the running partials) never exceed the ring's qcap + mcap
+  // slots.  Tags tag0 .. tag0 + N - 1 are the queries of the running trace;
+  // out[i] = clk, the first-token time (the arrival is subtracted after the trace).
+  __device__ void realize(const QEnv& e, const int32_t* tags, const StepOut& o, int reading,
+                          double clk, double* out, int tag0, int N) {
+    const int n = reading == 1 ? o.nd : o.pn;
+    if (n == 0) return;
+    int lo = reading == 1 ? o.h0 : o.h0 - o.pn;
+    if (lo < 0) lo += e.rcap;
+    int hit = 0;
+    for (int x = lane_id(); x < n; x += kWave) {
+      int pos = lo + x;
+      if (pos >= e.rcap) pos -= e.rcap;
+      const int tag = tags[pos];
+      const int q = tag - tag0;
+      if (tag >= 0 && q >= 0 && q < N) {
+        out[q] = clk;
+        ++hit;
+      }
+    }
+    ntrk -= wave_sum32(hit);
   }
 
   // The decode-only batches that follow the admission batch of a tail query, read
@@ -602,6 +668,7 @@ struct Queue {
         ++done;
       }
     }
+    // (a tracked replay folds quiet batches only with pend == 0, which they keep)
     return done;
   }
 };

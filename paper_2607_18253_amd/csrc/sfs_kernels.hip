@@ -290,12 +290,22 @@ __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double
 }
 
 // ------------------------------------------------------------------ k_commit
+// First-token tracking of a trace's replay: first-token time out[i] (this scenario's
+// row; nullptr: off) of the queries tagged tag0 .. tag0 + N - 1.
+struct Track {
+  double* out;
+  int tag0, N, reading;
+};
+
 // Append (p, d) when this queue is the chosen one, then replay every batch that
-// starts before t; an idle queue's clock jumps to t.
-template <int KS>
+// starts before t; an idle queue's clock jumps to t.  TRK: the query is tracked
+// (tag) and a batch that gives first tokens is stepped, not folded into a quiet
+// run, so that realize() sees it.
+template <int KS, bool TRK>
 __device__ __forceinline__ void commit_advance(Queue<KS>& w, const QEnv& e, bool chosen, int p,
                                                int d, double t, int qcap, int64_t max_iters,
-                                               int32_t* err) {
+                                               int32_t* err, int32_t* tags, int tag,
+                                               const Track& tk) {
   const int ln = lane_id();
   if (chosen) {
     d = d < 1 ? 1 : d;
@@ -304,7 +314,12 @@ __device__ __forceinline__ void commit_advance(Queue<KS>& w, const QEnv& e, bool
     } else if (w.n_pre - w.n_part + 1 > qcap) {
       if (ln == 0) set_error(err, kErrCapacity);
     } else {
-      w.append(e, p, d);
+      if constexpr (TRK) {
+        w.append(e, p, d, tags, tag);
+        w.ntrk += 1;
+      } else {
+        w.append(e, p, d);
+      }
     }
   }
   double clock = w.clock;
@@ -314,17 +329,42 @@ __device__ __forceinline__ void commit_advance(Queue<KS>& w, const QEnv& e, bool
       if (ln == 0) set_error(err, kErrIter);
       break;
     }
-    if (w.quiet(e)) {
+    if (w.quiet(e) && (!TRK || w.pend == 0)) {
       n += w.quiet_run(e, clock, t, n, max_iters);
       if (!(clock < t) || n == max_iters) continue;
     }
-    const StepOut o = w.step(e);
+    const StepOut o = w.template step<TRK>(e);
     clock = __dadd_rn(clock, batch_time(e.k, o.P, o.D, o.C, o.A));
     ++n;
+    if constexpr (TRK) w.realize(e, tags, o, tk.reading, clock, tk.out, tk.tag0, tk.N);
   }
   if (w.resident() == 0 && clock < t) clock = t;
   w.clock = clock;
   w.iters += n;
+}
+
+// Tracked queries still without a first token when the trace ends: a private copy
+// of the queue runs on, with no further arrivals, until each has had it.  The
+// queue's own state is left as the trace left it.
+template <int KS>
+__device__ __forceinline__ void drain(Queue<KS> w, const QEnv& e, const int32_t* tags,
+                                      const Track& tk, int64_t max_iters, int32_t* err) {
+  double clock = w.clock;
+  int64_t n = 0;
+  while (w.ntrk > 0) {
+    if (n == max_iters) {
+      if (lane_id() == 0) set_error(err, kErrIter);
+      break;
+    }
+    if (w.quiet(e) && w.pend == 0) {
+      n += w.quiet_run(e, clock, __builtin_inf(), n, max_iters);
+      if (n == max_iters) continue;
+    }
+    const StepOut o = w.template step<true>(e);
+    clock = __dadd_rn(clock, batch_time(e.k, o.P, o.D, o.C, o.A));
+    ++n;
+    w.realize(e, tags, o, tk.reading, clock, tk.out, tk.tag0, tk.N);
+  }
 }
 
 template <int KS>
@@ -346,7 +386,8 @@ __global__ __launch_bounds__(kWave) void k_commit(DevState S, DevParams pr, int 
   const bool chosen = choice && choice[(int64_t)z * choice_zstride] == j;
   const int p = qp_ptr ? *qp_ptr : qp_val;
   const int d = qd_ptr ? *qd_ptr : qd_val;
-  commit_advance(w, e, chosen, p, d, t, S.qcap, max_iters, err);
+  const Track off{nullptr, 0, 0, 0};
+  commit_advance<KS, false>(w, e, chosen, p, d, t, S.qcap, max_iters, err, nullptr, -1, off);
   w.store(S, e, qid);
 }
 
@@ -522,12 +563,13 @@ __device__ __forceinline__ int trace_pick(double bu, int bj, double bt, double b
       const double *qt, double t_after, const double *acc, const double *cost, int n_cols,   \
       const double *w_cost, const double *w_lat, const double *tau, int reading,             \
       int max_prompt, int64_t max_iters, int32_t *choice, double *chosen_ttft,               \
-      double *utility, int32_t *err, unsigned long long *work
+      double *utility, int32_t *err, unsigned long long *work, double *realized, int tag0
 
 // The same trace for pools too large to keep in registers: each owned instance's
 // state is loaded from HBM (L2) when it is needed and written back after its commit.
 // Wave w owns instances j = w + v*nw; lane v holds the inputs of the v-th one.
-template <int KS, int NW>
+// TRK: the replay also reports each query's realised TTFT.
+template <int KS, int NW, bool TRK>
 __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
   __shared__ double s_u[2][NW], s_t[2][NW], s_q[2][NW];
   __shared__ int s_j[2][NW];
@@ -542,6 +584,7 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
   const bool own_l = j_l < I;
   const int col_l = own_l ? pr.col[j_l] : 0;
   QueryIn nx = fetch_query(0, N, qp, qd, qt, t_after, tau, acc, cost, n_cols, col_l, own_l);
+  const Track tk{TRK ? realized + (int64_t)z * N : nullptr, tag0, N, reading};
   unsigned long long wbatch = 0;   // batches of this wave's estimates
   for (int i = 0; i < N; ++i) {
     const QueryIn q = nx;
@@ -568,12 +611,22 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
     for (int j = wid; j < I; j += nw) {
       const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
       Queue<KS> w;
-      w.load(S, e, z * I + j);
-      commit_advance(w, e, j == m, q.p, q.d, q.tn, S.qcap, max_iters, err);
-      w.store(S, e, z * I + j);
+      w.template load<TRK>(S, e, z * I + j);
+      commit_advance<KS, TRK>(w, e, j == m, q.p, q.d, q.tn, S.qcap, max_iters, err,
+                              TRK ? S.r_tag + (int64_t)(z * I + j) * S.rcap : nullptr,
+                              tag0 + i, tk);
+      w.template store<TRK>(S, e, z * I + j);
     }
   }
   if (work && lane_id() == 0) atomicAdd(work + z, wbatch);
+  if constexpr (TRK) {
+    for (int j = wid; j < I; j += nw) {
+      const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
+      Queue<KS> w;
+      w.template load<true>(S, e, z * I + j);
+      drain(w, e, S.r_tag + (int64_t)(z * I + j) * S.rcap, tk, max_iters, err);
+    }
+  }
 }
 
 // Trace inputs of 64 consecutive queries, lane l holding query base + l; the acc /
@@ -771,11 +824,12 @@ struct VisitOut {
 // frontier cache (state F in LDS) is kept in step.
 // Every batch -- replayed, walked to a new admission point, or recorded as tail --
 // runs through the single Queue::step / quiet_run below, on wk.
-template <int KS>
+template <int KS, bool TRK>
 __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv& e, bool chosen,
                                           int p, int d, double tn, int qcap, int kmax,
                                           int64_t max_iters, int32_t* err, LdsQueue<KS>& SL,
-                                          LdsQueue<KS>& F) {
+                                          LdsQueue<KS>& F, int32_t* tags, int tag,
+                                          const Track& tk) {
   const int ln = lane_id();
   VisitOut vo;
   vo.direct = false;
@@ -787,7 +841,12 @@ __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv&
     } else if (wk.n_pre - wk.n_part + 1 > qcap) {
       if (ln == 0) set_error(err, kErrCapacity);
     } else {
-      wk.append(e, p, d);
+      if constexpr (TRK) {
+        wk.append(e, p, d, tags, tag);
+        wk.ntrk += 1;
+      } else {
+        wk.append(e, p, d);
+      }
       joined = true;
     }
   }
@@ -816,14 +875,14 @@ __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv&
         if (wk.resident() == 0 && clk < stop_t) clk = stop_t;
         wk.clock = clk;
         wk.iters += n;
-        if (joined || n > 0 || clk != clk0) wk.to_lds(SL);   // the instance moved on
+        if (joined || n > 0 || clk != clk0) wk.template to_lds<TRK>(SL);   // it moved on
         vo.g = wk.g;
         vo.clock = clk;
         // the instance ran the admission batch, or sat idle at F and its clock jumped
         if (fc.valid && (wk.g > fc.g || (wk.g == fc.g && clk != fc.E))) fc.valid = false;
         if (joined && fc.valid) {
           wk.from_lds(F);
-          wk.append(e, p, d);
+          wk.append(e, p, d);   // F shares the instance's ring: same slot, entry and tag
           clk = fc.E;
         } else if (!fc.valid) {
           wk.refill(e);
@@ -859,16 +918,20 @@ __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv&
       }
       break;
     }
-    if (phase != kTail && wk.quiet(e)) {
+    if (phase != kTail && wk.quiet(e) && (!TRK || phase != kReplay || wk.pend == 0)) {
       // a quiet run ends before the batch in which a decode finishes (or at the stop
-      // time or the cap); that batch is then stepped below
+      // time or the cap); that batch is then stepped below.  A replayed batch that
+      // gives first tokens is always stepped.
       n += wk.quiet_run(e, clk, stop_t, n, max_iters);
       if (!(clk < stop_t) || n == max_iters) continue;
     }
-    const StepOut o = wk.step(e);
+    const StepOut o = wk.template step<TRK>(e);
     if (phase != kTail) {
       clk = __dadd_rn(clk, batch_time(e.k, o.P, o.D, o.C, o.A));
       ++n;
+      if constexpr (TRK)
+        if (phase == kReplay)
+          wk.realize(e, tags, o, tk.reading, clk, tk.out, tk.tag0, tk.N);
     } else {
       if (kk >= 0 && ln == kk) { fc.tD = o.D; fc.tC = o.C; }
       ++kk;
@@ -959,7 +1022,7 @@ __device__ __forceinline__ double estimate_visit(const FCache& fc, const Queue<K
 // G > 1) of query i, then per owned instance one visit (commit of query i, replay,
 // frontier cache) and the estimate of query i + 1.
 // Identical, operation for operation, to estimate + route + commit per query.
-template <int KS, int W, int IPW>
+template <int KS, int W, int IPW, bool TRK>
 __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G, uint64_t* xslot,
                                                         int tail_k, SyncCtl sc) {
   __shared__ double s_u[2][W];
@@ -981,6 +1044,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
   uint64_t* xs = xslot + (int64_t)z * 2 * kMaxCluster * 4;
   const int jbase = (cid * W + wid) * IPW;
   const int kmax = tail_k;   // <= 64, checked at launch
+  const Track tk{TRK ? realized + (int64_t)z * N : nullptr, tag0, N, reading};
   int cols[IPW];
   FCache fc[IPW];
   QEnv env[IPW];   // per owned instance: coefficients, ring, staging (loop invariant)
@@ -994,8 +1058,8 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
     if (j < I) {
       env[r] = make_env(S, pr, z * I + j, j, stage[wid]);
       Queue<KS> q;
-      q.load(S, env[r], z * I + j);
-      q.to_lds(sst[wid][r]);
+      q.template load<TRK>(S, env[r], z * I + j);
+      q.template to_lds<TRK>(sst[wid][r]);
     }
   }
   QueryBlock<IPW> cur = fetch_block<IPW>(0, N, qp, qd, qt, tau, acc, cost, n_cols, cols);
@@ -1067,9 +1131,12 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
       if (j < I) {
         const QEnv& e = env[r];
         Queue<KS> wk;
-        wk.from_lds(sst[wid][r]);
-        const VisitOut vo = visit(wk, fc[r], e, i >= 0 && j == m, p, dq, tn, S.qcap, kmax,
-                                  max_iters, err, sst[wid][r], fst[wid][r]);
+        wk.template from_lds<TRK>(sst[wid][r]);
+        const VisitOut vo = visit<KS, TRK>(wk, fc[r], e, i >= 0 && j == m, p, dq, tn, S.qcap,
+                                           kmax, max_iters, err, sst[wid][r], fst[wid][r],
+                                           TRK ? S.r_tag + (int64_t)(z * I + j) * S.rcap
+                                               : nullptr,
+                                           tag0 + i, tk);
         if (more) {
           int64_t it = 0;
           const double ttft = p1_ok ? estimate_visit(fc[r], wk, vo, e, p1, t1, reading, kmax,
@@ -1097,10 +1164,33 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
     const int j = jbase + r;
     if (j < I) {
       Queue<KS> q;
-      q.from_lds(sst[wid][r]);
-      q.store(S, make_env(S, pr, z * I + j, j, stage[wid]), z * I + j);
+      q.template from_lds<TRK>(sst[wid][r]);
+      q.template store<TRK>(S, env[r], z * I + j);
+      if constexpr (TRK)
+        drain(q, env[r], S.r_tag + (int64_t)(z * I + j) * S.rcap, tk, max_iters, err);
     }
   }
+}
+
+// Before a trace that reports realised TTFT: no query of it is tracked yet, no
+// completed prefill is pending a first decode (earlier requests are not tracked),
+// and every output entry is NaN until its first token is seen.
+__global__ void k_track_begin(QScal* sc, int64_t n_queues, double* realized, int64_t n_out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n_queues) { sc[i].ntrk = 0; sc[i].pend = 0; }
+  if (i < n_out) realized[i] = __builtin_nan("");
+}
+
+// After such a trace: realised TTFT = first-token time - arrival (NaN stays NaN).
+__global__ void k_track_end(double* realized, const double* qt, int N, int64_t n_out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n_out) realized[i] = __dsub_rn(realized[i], qt[i % N]);
+}
+
+// Marks every ring entry untracked (when the tag counter starts over).
+__global__ void k_untag(int32_t* tags, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) tags[i] = -1;
 }
 
 // ------------------------------------------------------------------ k_stats
@@ -1213,12 +1303,10 @@ __global__ __launch_bounds__(256) void k_targets(int n, const int32_t* p, const 
 }
 
 // OnTimeUtility (Eq. 4) per scenario: the utility of Eq. 2 at the chosen instance,
-// summed in query order over the queries whose TTFT at the choice is within the
-// target, divided by N.  The estimated TTFT stands for the realised one: the
-// replay runs the same scheduler, and a later arrival never takes a batch slot
-// ahead of an earlier one under FCFS.
+// summed in query order over the queries whose realised TTFT (the replay's, as a
+// trace reports it) is within the target, divided by N.
 __global__ __launch_bounds__(256) void k_ontime(int N, int I, const int32_t* choice,
-                                               const double* chosen_ttft, const double* tau,
+                                               const double* ttft_real, const double* tau,
                                                const double* acc, const double* cost, int n_cols,
                                                const int32_t* col, const double* w_cost,
                                                double* out) {
@@ -1226,7 +1314,7 @@ __global__ __launch_bounds__(256) void k_ontime(int N, int I, const int32_t* cho
   __shared__ int s_on[256];
   const int z = blockIdx.x;
   const int32_t* ch = choice + (int64_t)z * N;
-  const double* tt = chosen_ttft + (int64_t)z * N;
+  const double* tt = ttft_real + (int64_t)z * N;
   const double wc = w_cost[z];
   double s = 0.0;
   for (int base = 0; base < N; base += 256) {
@@ -1279,14 +1367,18 @@ static hipError_t launch_commit_ks(const LaunchEnv& env, const int32_t* choice,
 #define LAR_TRACE_ARGS                                                                   \
   env.S, env.P, env.Z, env.I, a.N, a.qp, a.qd, a.qt, a.t_after, a.acc, a.cost, a.n_cols,     \
       a.w_cost, a.w_lat, a.tau, env.reading, env.max_prompt, env.max_iters, a.choice,        \
-      a.chosen_ttft, a.utility, env.err, env.work
+      a.chosen_ttft, a.utility, env.err, env.work, a.realized, a.tag0
 
 template <int KS, int NW>
 static hipError_t launch_trace_mem(const LaunchEnv& env, const TraceArgs& a) {
   const int nw = env.I < NW ? env.I : NW;
   if ((env.I + nw - 1) / nw > kWave) return hipErrorInvalidValue;   // 64 instances per wave
-  hipLaunchKernelGGL((k_trace_mem<KS, NW>), dim3(env.Z), dim3(nw * kWave), 0, env.stream,
-                     LAR_TRACE_ARGS);
+  if (a.realized)
+    hipLaunchKernelGGL((k_trace_mem<KS, NW, true>), dim3(env.Z), dim3(nw * kWave), 0,
+                       env.stream, LAR_TRACE_ARGS);
+  else
+    hipLaunchKernelGGL((k_trace_mem<KS, NW, false>), dim3(env.Z), dim3(nw * kWave), 0,
+                       env.stream, LAR_TRACE_ARGS);
   return hipGetLastError();
 }
 
@@ -1305,14 +1397,14 @@ static bool co_resident(K kernel, int threads, int Z, int G) {
   return per_cu > 0 && per_xcd <= (int64_t)(n_cu / 8) * per_cu;
 }
 
-template <int KS, int W, int IPW>
+template <int KS, int W, int IPW, bool TRK>
 static hipError_t launch_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
   const int per_wg = W * IPW;
   const int G = (env.I + per_wg - 1) / per_wg;
   if (G > kMaxCluster) return hipErrorInvalidValue;
   if ((uint64_t)a.N >= (1ull << 31)) return hipErrorInvalidValue;  // 32-bit post tags
   const int w_used = G == 1 ? (env.I + IPW - 1) / IPW : W;
-  if (!co_resident(k_trace_cl<KS, W, IPW>, w_used * kWave, env.Z, G))
+  if (!co_resident(k_trace_cl<KS, W, IPW, TRK>, w_used * kWave, env.Z, G))
     return hipErrorInvalidConfiguration;
   if (G > 1) {
     const int64_t n = (int64_t)env.Z * 2 * kMaxCluster * 4;
@@ -1322,9 +1414,16 @@ static hipError_t launch_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
     if (e != hipSuccess) return e;
   }
   const int blocks = 8 * ((env.Z + 7) / 8) * G;
-  hipLaunchKernelGGL((k_trace_cl<KS, W, IPW>), dim3(blocks), dim3(w_used * kWave), 0,
+  hipLaunchKernelGGL((k_trace_cl<KS, W, IPW, TRK>), dim3(blocks), dim3(w_used * kWave), 0,
                      env.stream, LAR_TRACE_ARGS, G, env.xslot, env.T.K, env.sync);
   return hipGetLastError();
+}
+
+// The clustered trace with (realised TTFT requested) or without first-token tracking.
+template <int KS, int W, int IPW>
+static hipError_t launch_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
+  return a.realized ? launch_trace_cl<KS, W, IPW, true>(env, a)
+                    : launch_trace_cl<KS, W, IPW, false>(env, a);
 }
 
 template <int KS>
@@ -1365,14 +1464,28 @@ hipError_t launch_trace(const LaunchEnv& env, const TraceArgs& a) {
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  if (a.realized) {
+    const int64_t nq = (int64_t)env.Z * env.I, no = (int64_t)env.Z * a.N;
+    const int64_t n = nq > no ? nq : no;
+    hipLaunchKernelGGL(k_track_begin, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                       env.stream, env.S.sc, nq, a.realized, no);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e;
   switch (env.ks) {
-    case 1: return launch_trace_ks<1>(env, a);
-    case 2: return launch_trace_ks<2>(env, a);
-    case 4: return launch_trace_ks<4>(env, a);
-    case 8: return launch_trace_ks<8>(env, a);
-    case 16: return launch_trace_ks<16>(env, a);
+    case 1: e = launch_trace_ks<1>(env, a); break;
+    case 2: e = launch_trace_ks<2>(env, a); break;
+    case 4: e = launch_trace_ks<4>(env, a); break;
+    case 8: e = launch_trace_ks<8>(env, a); break;
+    case 16: e = launch_trace_ks<16>(env, a); break;
     default: return hipErrorInvalidValue;
   }
+  if (e != hipSuccess || !a.realized) return e;
+  const int64_t no = (int64_t)env.Z * a.N;
+  hipLaunchKernelGGL(k_track_end, dim3((unsigned)((no + 255) / 256)), dim3(256), 0, env.stream,
+                     a.realized, a.qt, a.N, no);
+  return hipGetLastError();
 }
 
 hipError_t launch_traj(const LaunchEnv& env, const double* t_ptr, double t_val) {
@@ -1427,10 +1540,17 @@ hipError_t launch_targets(hipStream_t stream, int n, const int32_t* p, const dou
 }
 
 hipError_t launch_ontime(const LaunchEnv& env, int N, const int32_t* choice,
-                         const double* chosen_ttft, const double* tau, const double* acc,
+                         const double* ttft_real, const double* tau, const double* acc,
                          const double* cost, int n_cols, const double* w_cost, double* out) {
   hipLaunchKernelGGL(k_ontime, dim3(env.Z), dim3(256), 0, env.stream, N, env.I, choice,
-                     chosen_ttft, tau, acc, cost, n_cols, env.P.col, w_cost, out);
+                     ttft_real, tau, acc, cost, n_cols, env.P.col, w_cost, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_untag(const LaunchEnv& env) {
+  const int64_t n = (int64_t)env.Z * env.I * env.S.rcap;
+  hipLaunchKernelGGL(k_untag, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, env.stream,
+                     env.S.r_tag, n);
   return hipGetLastError();
 }
 

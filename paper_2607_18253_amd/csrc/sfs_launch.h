@@ -46,6 +46,8 @@ struct TraceArgs {
   const double* tau;   // per-query TTFT targets (constrained objective) or nullptr
   int32_t* choice;
   double *chosen_ttft, *utility;
+  double* realized;    // [Z][N] realised TTFT of each query, or nullptr (no tracking)
+  int tag0;            // tag of query 0 in the ring (queries tag0 .. tag0 + N - 1)
 };
 
 hipError_t launch_trace(const LaunchEnv& env, const TraceArgs& a);
@@ -59,12 +61,13 @@ hipError_t launch_route(const LaunchEnv& env, int Q, const double* ttft, int64_t
 hipError_t launch_targets(hipStream_t stream, int n, const int32_t* p, const double* u_ms,
                           const double* v, double* tau);
 hipError_t launch_ontime(const LaunchEnv& env, int N, const int32_t* choice,
-                         const double* chosen_ttft, const double* tau, const double* acc,
+                         const double* ttft_real, const double* tau, const double* acc,
                          const double* cost, int n_cols, const double* w_cost, double* out);
 hipError_t launch_commit(const LaunchEnv& env, const int32_t* choice, int64_t choice_zstride,
                          const int32_t* qp_ptr, const int32_t* qd_ptr, int32_t qp, int32_t qd,
                          const double* t_ptr, double t_val);
 hipError_t launch_clear_error(const LaunchEnv& env);
+hipError_t launch_untag(const LaunchEnv& env);
 hipError_t launch_stats(const LaunchEnv& env, int N, const int32_t* choice,
                         const double* chosen_ttft, const double* acc, const double* cost,
                         int n_cols, const double* w_cost, double* out);

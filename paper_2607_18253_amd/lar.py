@@ -74,14 +74,14 @@ def load_library(path: str = LIB_PATH):
     L.lar_commit.restype = i32
     L.lar_commit.argtypes = [vp, vp, i32, i32, dbl]
     L.lar_route_trace.restype = i32
-    L.lar_route_trace.argtypes = [vp, i32, vp, vp, vp, dbl, vp, vp, i32, vp, vp, vp, vp, vp]
+    L.lar_route_trace.argtypes = [vp, i32, vp, vp, vp, dbl, vp, vp, i32, vp, vp, vp, vp, vp, vp]
     L.lar_route_constrained.restype = i32
     L.lar_route_constrained.argtypes = [vp, i32, vp, vp, vp, vp, i32, vp, vp, vp, vp]
     L.lar_ttft_targets.restype = i32
     L.lar_ttft_targets.argtypes = [vp, i32, vp, vp, vp, vp]
     L.lar_route_trace_constrained.restype = i32
     L.lar_route_trace_constrained.argtypes = [vp, i32, vp, vp, vp, dbl, vp, vp, vp, i32, vp, vp,
-                                              vp, vp]
+                                              vp, vp, vp]
     L.lar_ontime_utility.restype = i32
     L.lar_ontime_utility.argtypes = [vp, i32, vp, vp, vp, vp, vp, i32, vp, vp]
     L.lar_trace_work.restype = i32
@@ -265,7 +265,7 @@ class LarContext:
         self.commit(None, 1, 1, t_ms)
 
     def route_trace(self, q_prefill, q_decode, q_t_ms, t_after_ms, acc, cost, w_cost, w_lat,
-                    choice=None, chosen_ttft=None, utility=None):
+                    choice=None, chosen_ttft=None, utility=None, realized=None):
         torch = self._torch
         N = int(q_prefill.numel())
         n_cols = int(acc.shape[1])
@@ -280,11 +280,13 @@ class LarContext:
             _dev(w_cost, torch.float64, "w_cost", self.Z), _dev(w_lat, torch.float64, "w_lat", self.Z),
             _dev(choice, torch.int32, "choice", self.Z * N),
             _dev(chosen_ttft, torch.float64, "chosen_ttft", self.Z * N),
-            _dev(utility, torch.float64, "utility", self.Z * N)))
+            _dev(utility, torch.float64, "utility", self.Z * N),
+            _dev(realized, torch.float64, "realized", self.Z * N)))
         return choice
 
     def route_trace_constrained(self, q_prefill, q_decode, q_t_ms, t_after_ms, tau_ms, acc, cost,
-                                w_cost, choice=None, chosen_ttft=None, utility=None):
+                                w_cost, choice=None, chosen_ttft=None, utility=None,
+                                realized=None):
         torch = self._torch
         N = int(q_prefill.numel())
         n_cols = int(acc.shape[1])
@@ -299,10 +301,11 @@ class LarContext:
             _dev(w_cost, torch.float64, "w_cost", self.Z),
             _dev(choice, torch.int32, "choice", self.Z * N),
             _dev(chosen_ttft, torch.float64, "chosen_ttft", self.Z * N),
-            _dev(utility, torch.float64, "utility", self.Z * N)))
+            _dev(utility, torch.float64, "utility", self.Z * N),
+            _dev(realized, torch.float64, "realized", self.Z * N)))
         return choice
 
-    def ontime_utility(self, choice, chosen_ttft, tau_ms, acc, cost, w_cost, out=None):
+    def ontime_utility(self, choice, realized, tau_ms, acc, cost, w_cost, out=None):
         torch = self._torch
         N = int(choice.shape[-1])
         n_cols = int(acc.shape[1])
@@ -310,7 +313,7 @@ class LarContext:
             out = torch.empty(self.Z, dtype=torch.float64, device=choice.device)
         self._check(self._L.lar_ontime_utility(
             self._h, N, _dev(choice, torch.int32, "choice", self.Z * N),
-            _dev(chosen_ttft, torch.float64, "chosen_ttft", self.Z * N),
+            _dev(realized, torch.float64, "realized", self.Z * N),
             _dev(tau_ms, torch.float64, "tau_ms", N),
             _dev(acc, torch.float64, "acc", N * n_cols), _dev(cost, torch.float64, "cost", N * n_cols),
             n_cols, _dev(w_cost, torch.float64, "w_cost", self.Z),
