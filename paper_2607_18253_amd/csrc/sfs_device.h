@@ -196,10 +196,21 @@ template <int KS>
 struct LdsQueue {
   int dl[KS * kWave], dc[KS * kWave], ds[KS * kWave];
   int wrp[kWave], wrd[kWave], wcx[kWave], wseq[kWave];
-  int g, n_dec, n_part, n_pre, head, next_seq, woff, nwin, pend, ntrk;
+  int g, n_dec, n_part, n_pre, head, next_seq, woff, nwin, pend, ntrk, ptag_ok;
   int64_t c0sum, pre_sum, iters;
   double clock;
 };
+
+// The per-lane tracking registers of a queue (see Queue), kept beside its LDS copy
+// by kernels that track first tokens.
+struct LdsTags {
+  int wtag[kWave], ptag[kWave];
+};
+
+// LDS words per wave of the staging area that step() uses to move completed
+// prefills into decode slots (one more row when it also moves their tags).
+template <bool TRK>
+constexpr int stage_words() { return (TRK ? 4 : 3) * kWave; }
 
 // ------------------------------------------------------------------ the batch engine
 struct StepOut {
@@ -208,6 +219,8 @@ struct StepOut {
   int h0;    // ring head before the batch
   int pn;    // prefills completed by the batch before (first decode in this one)
   int nd;    // prefills completed by this batch: ring entries h0 .. h0 + nd - 1
+  int pt;    // lane x < 64: tag of the x-th prefill completed by the batch before
+  bool pt_ok;   // pt holds them (else they are read from the ring)
 };
 
 // What a wave needs besides the state to work on one queue: the batch-time
@@ -240,6 +253,11 @@ struct Queue {
   int dl[KS], dc[KS], ds[KS];
   // prefill-list window: lane woff + i holds entry i of the list, i < nwin
   int wrp, wrd, wcx, wseq;
+  // first-token tracking (TRK paths only): tag of the window entry, and in lane
+  // x < 64 the tag of the x-th prefill completed by the last batch (valid while
+  // ptag_ok; a queue loaded from HBM reads them from the ring instead)
+  int wtag, ptag;
+  bool ptag_ok;
   int woff, nwin;
   // scalars (wave-uniform)
   int g, n_dec, n_part, n_pre, head, next_seq;
@@ -248,7 +266,7 @@ struct Queue {
   double clock;
   int64_t iters;
   template <bool TRK = false>
-  __device__ void load(const DevState& S, const QEnv& e, int qid) {
+  __device__ void load(const DevState& S, const QEnv& e, int qid, const int32_t* tags = nullptr) {
     const int ln = lane_id();
     const QScal* q = S.sc + qid;
     g = uni(q->g); n_dec = uni(q->n_dec); n_part = uni(q->n_part); n_pre = uni(q->n_pre);
@@ -271,29 +289,32 @@ struct Queue {
     woff = 0;
     nwin = 0;
     wrp = 0; wrd = 0; wcx = 0; wseq = 0;
-    refill(e);
+    if constexpr (TRK) { wtag = -1; ptag = -1; ptag_ok = false; }
+    refill<TRK>(e, tags);
   }
 
-  // Copy to / from an LDS copy (same layout as the registers).
+  // Copy to / from an LDS copy (same layout as the registers); TRK: the tracking
+  // state too, the per-lane part in Tg.
   template <bool TRK = false>
-  __device__ void to_lds(LdsQueue<KS>& L) const {
+  __device__ void to_lds(LdsQueue<KS>& L, LdsTags* Tg = nullptr) const {
     const int ln = lane_id();
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       L.dl[s * kWave + ln] = dl[s]; L.dc[s * kWave + ln] = dc[s]; L.ds[s * kWave + ln] = ds[s];
     }
     L.wrp[ln] = wrp; L.wrd[ln] = wrd; L.wcx[ln] = wcx; L.wseq[ln] = wseq;
+    if constexpr (TRK) { Tg->wtag[ln] = wtag; Tg->ptag[ln] = ptag; }
     if (ln == 0) {
       L.g = g; L.n_dec = n_dec; L.n_part = n_part; L.n_pre = n_pre; L.head = head;
       L.next_seq = next_seq; L.woff = woff; L.nwin = nwin; L.c0sum = c0sum;
-      if constexpr (TRK) { L.pend = pend; L.ntrk = ntrk; }
+      if constexpr (TRK) { L.pend = pend; L.ntrk = ntrk; L.ptag_ok = ptag_ok; }
       L.pre_sum = pre_sum; L.iters = iters; L.clock = clock;
     }
     __builtin_amdgcn_wave_barrier();
   }
 
   template <bool TRK = false>
-  __device__ void from_lds(const LdsQueue<KS>& L) {
+  __device__ void from_lds(const LdsQueue<KS>& L, const LdsTags* Tg = nullptr) {
     const int ln = lane_id();
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
@@ -301,9 +322,10 @@ struct Queue {
       dl[s] = L.dl[s * kWave + ln]; dc[s] = L.dc[s * kWave + ln]; ds[s] = L.ds[s * kWave + ln];
     }
     wrp = L.wrp[ln]; wrd = L.wrd[ln]; wcx = L.wcx[ln]; wseq = L.wseq[ln];
+    if constexpr (TRK) { wtag = Tg->wtag[ln]; ptag = Tg->ptag[ln]; }
     g = uni(L.g); n_dec = uni(L.n_dec); n_part = uni(L.n_part); n_pre = uni(L.n_pre);
     head = uni(L.head); next_seq = uni(L.next_seq); woff = uni(L.woff); nwin = uni(L.nwin);
-    if constexpr (TRK) { pend = uni(L.pend); ntrk = uni(L.ntrk); }
+    if constexpr (TRK) { pend = uni(L.pend); ntrk = uni(L.ntrk); ptag_ok = uni(L.ptag_ok) != 0; }
     c0sum = uni64(L.c0sum); pre_sum = uni64(L.pre_sum); iters = uni64(L.iters);
     clock = L.clock;
   }
@@ -343,6 +365,7 @@ struct Queue {
   }
 
   // Move the window down to lane 0.
+  template <bool TRK = false>
   __device__ void compact() {
     if (woff == 0) return;
     const int src = min(lane_id() + woff, kWave - 1);
@@ -350,19 +373,23 @@ struct Queue {
     wrd = __shfl(wrd, src, kWave);
     wcx = __shfl(wcx, src, kWave);
     wseq = __shfl(wseq, src, kWave);
+    if constexpr (TRK) wtag = __shfl(wtag, src, kWave);
     woff = 0;
   }
 
-  // Make min(n_pre, 64) list entries visible in the window.
-  __device__ void refill(const QEnv& e) {
+  // Make min(n_pre, 64) list entries visible in the window (TRK: with their tags
+  // from the queue's tag ring).
+  template <bool TRK = false>
+  __device__ void refill(const QEnv& e, const int32_t* tags = nullptr) {
     const int want = min(n_pre, kWave);
     if (nwin >= want) return;
-    if (woff + want > kWave) compact();
+    if (woff + want > kWave) compact<TRK>();
     const int idx = lane_id() - woff;
     if (idx >= nwin && idx < want) {
       int pos = head + idx;
       if (pos >= e.rcap) pos -= e.rcap;
       wrp = e.r_rp[pos]; wrd = e.r_rd[pos]; wcx = e.r_cx[pos]; wseq = e.r_seq[pos];
+      if constexpr (TRK) wtag = tags[pos];
     }
     nwin = want;
   }
@@ -404,9 +431,12 @@ struct Queue {
     int pos = head + idx;
     if (pos >= e.rcap) pos -= e.rcap;
     if (nwin == n_pre && idx < kWave) {     // the window holds the whole list: extend it
-      if (woff + idx >= kWave) compact();
+      if (woff + idx >= kWave) {
+        if (tags) compact<true>(); else compact<false>();
+      }
       if (ln == woff + idx) { wrp = p; wrd = d; wcx = 0; wseq = next_seq; }
       if (tags) {
+        if (ln == woff + idx) wtag = tag;
         if (ln == 0) tags[pos] = tag;
         // other lanes of this wave read the tag back at the first token
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
@@ -448,9 +478,10 @@ struct Queue {
   }
 
   // Build the next token batch, apply it, return its features (TRK: and keep the
-  // count of completed prefills for first-token tracking).
+  // completed prefills' count and tags for first-token tracking; tags is the queue's
+  // tag ring).
   template <bool TRK = false>
-  __device__ StepOut step(const QEnv& e) {
+  __device__ StepOut step(const QEnv& e, const int32_t* tags = nullptr) {
     const int ln = lane_id();
     const Coef& k = e.k;
     const bool need_C = e.need_C, need_A = e.need_A;
@@ -458,8 +489,8 @@ struct Queue {
     const int B = k.B;
     const int gn = g + 1;   // index of this batch
     StepOut o;
-    int nd = 0;
-    if constexpr (TRK) { o.h0 = head; o.pn = pend; }
+    int nd = 0, pt_new = -1;
+    if constexpr (TRK) { o.h0 = head; o.pn = pend; o.pt = ptag; o.pt_ok = ptag_ok; }
     o.D = n_dec;
     o.C = need_C ? c0sum + (int64_t)n_dec * g : 0;
     int left = B - n_dec;
@@ -478,7 +509,7 @@ struct Queue {
     int64_t P = 0, A = 0;
     int free_slots = k.M - (int)o.D - n_part;   // slots for waiting admissions
     while (n_pre > 0 && left > 0 && (n_part > 0 || free_slots > 0)) {
-      if (nwin == 0) refill(e);
+      if (nwin == 0) refill<TRK>(e, tags);
       const int nw0 = nwin;
       const int idx = ln - woff;
       const bool valid = idx >= 0 && idx < nw0;
@@ -514,10 +545,17 @@ struct Queue {
         const int nc = wcx - gn;
         if (need_C) c0sum += sum_lanes64(nc, fullm);
         const bool full = ((fullm >> ln) & 1ull) != 0;
-        if (full) { stg[idx] = nl; stg[kWave + idx] = nc; stg[2 * kWave + idx] = wseq; }
+        if (full) {
+          stg[idx] = nl; stg[kWave + idx] = nc; stg[2 * kWave + idx] = wseq;
+          if constexpr (TRK) stg[3 * kWave + idx] = wtag;
+        }
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if constexpr (TRK) {   // lanes nd .. nd + n_full - 1 (below 64) take their tags
+          const int x = ln - nd;
+          if (x >= 0 && x < n_full) pt_new = stg[3 * kWave + x];
+        }
         int placed = 0;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
@@ -541,12 +579,12 @@ struct Queue {
       n_part = n_part - min(n_full, n_part) + (part_waiting ? 1 : 0);
       // continue only if the whole window was served (more entries may wait in the ring)
       if (n_full < nw0) break;
-      refill(e);
+      refill<TRK>(e, tags);
     }
-    if (nwin < n_pre && nwin < kWave / 2) refill(e);
+    if (nwin < n_pre && nwin < kWave / 2) refill<TRK>(e, tags);
     o.P = (int)P;
     o.A = need_A ? A : 0;
-    if constexpr (TRK) { o.nd = nd; pend = nd; }
+    if constexpr (TRK) { o.nd = nd; pend = nd; ptag = pt_new; ptag_ok = true; }
     g = gn;
     return o;
   }
@@ -564,10 +602,21 @@ struct Queue {
                           double clk, double* out, int tag0, int N) {
     const int n = reading == 1 ? o.nd : o.pn;
     if (n == 0) return;
+    const int ln = lane_id();
+    int hit = 0;
+    // the first 64 tags from registers (captured by step), the rest from the ring
+    const bool regs = reading == 1 || o.pt_ok;
+    if (regs && ln < n) {
+      const int tag = reading == 1 ? ptag : o.pt;
+      const int q = tag - tag0;
+      if (tag >= 0 && q >= 0 && q < N) {
+        out[q] = clk;
+        ++hit;
+      }
+    }
     int lo = reading == 1 ? o.h0 : o.h0 - o.pn;
     if (lo < 0) lo += e.rcap;
-    int hit = 0;
-    for (int x = lane_id(); x < n; x += kWave) {
+    for (int x = regs ? kWave + ln : ln; x < n; x += kWave) {
       int pos = lo + x;
       if (pos >= e.rcap) pos -= e.rcap;
       const int tag = tags[pos];

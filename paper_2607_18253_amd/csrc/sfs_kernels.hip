@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kWave) void k_traj(DevState S, DevParams pr, DevTra
   const int j = qid % I;
   const double t = t_ptr ? *t_ptr : t_val;
   const int ln = lane_id();
-  __shared__ int stage[3 * kWave];
+  __shared__ int stage[stage_words<false>()];
   const QEnv e = make_env(S, pr, qid, j, stage);
   Queue<KS> w;
   w.load(S, e, qid);
@@ -297,10 +297,34 @@ struct Track {
   int tag0, N, reading;
 };
 
+// A quiet stretch of a replay (call when w.quiet(e) holds; clk < t_stop): folds the
+// quiet batches before the next decode finish, stopping at t_stop or the cap, and
+// returns true when it folded any (the caller re-checks its loop condition), false
+// when the next batch must be stepped.  TRK, first token = first decode: when the
+// last batch completed prefills, the next batch is their first decode batch; it is
+// folded alone and their first tokens recorded at its end.
+template <int KS, bool TRK>
+__device__ __forceinline__ bool replay_quiet(Queue<KS>& w, const QEnv& e, double& clk,
+                                             double t_stop, int64_t& n, int64_t max_iters,
+                                             const int32_t* tags, const Track& tk) {
+  if constexpr (TRK) {
+    if (tk.reading == 0 && w.pend > 0) {
+      StepOut pq;
+      pq.h0 = w.head; pq.pn = w.pend; pq.nd = 0; pq.pt = w.ptag; pq.pt_ok = w.ptag_ok;
+      if (w.quiet_run(e, clk, t_stop, n, n + 1) == 0) return false;
+      ++n;
+      w.pend = 0;
+      w.realize(e, tags, pq, 0, clk, tk.out, tk.tag0, tk.N);
+      return true;
+    }
+  }
+  n += w.quiet_run(e, clk, t_stop, n, max_iters);
+  return !(clk < t_stop) || n == max_iters;
+}
+
 // Append (p, d) when this queue is the chosen one, then replay every batch that
 // starts before t; an idle queue's clock jumps to t.  TRK: the query is tracked
-// (tag) and a batch that gives first tokens is stepped, not folded into a quiet
-// run, so that realize() sees it.
+// (tag) and the first tokens of the replayed batches are recorded.
 template <int KS, bool TRK>
 __device__ __forceinline__ void commit_advance(Queue<KS>& w, const QEnv& e, bool chosen, int p,
                                                int d, double t, int qcap, int64_t max_iters,
@@ -329,11 +353,8 @@ __device__ __forceinline__ void commit_advance(Queue<KS>& w, const QEnv& e, bool
       if (ln == 0) set_error(err, kErrIter);
       break;
     }
-    if (w.quiet(e) && (!TRK || w.pend == 0)) {
-      n += w.quiet_run(e, clock, t, n, max_iters);
-      if (!(clock < t) || n == max_iters) continue;
-    }
-    const StepOut o = w.template step<TRK>(e);
+    if (w.quiet(e) && replay_quiet<KS, TRK>(w, e, clock, t, n, max_iters, tags, tk)) continue;
+    const StepOut o = w.template step<TRK>(e, tags);
     clock = __dadd_rn(clock, batch_time(e.k, o.P, o.D, o.C, o.A));
     ++n;
     if constexpr (TRK) w.realize(e, tags, o, tk.reading, clock, tk.out, tk.tag0, tk.N);
@@ -356,11 +377,10 @@ __device__ __forceinline__ void drain(Queue<KS> w, const QEnv& e, const int32_t*
       if (lane_id() == 0) set_error(err, kErrIter);
       break;
     }
-    if (w.quiet(e) && w.pend == 0) {
-      n += w.quiet_run(e, clock, __builtin_inf(), n, max_iters);
-      if (n == max_iters) continue;
-    }
-    const StepOut o = w.template step<true>(e);
+    if (w.quiet(e) &&
+        replay_quiet<KS, true>(w, e, clock, __builtin_inf(), n, max_iters, tags, tk))
+      continue;
+    const StepOut o = w.template step<true>(e, tags);
     clock = __dadd_rn(clock, batch_time(e.k, o.P, o.D, o.C, o.A));
     ++n;
     w.realize(e, tags, o, tk.reading, clock, tk.out, tk.tag0, tk.N);
@@ -379,7 +399,7 @@ __global__ __launch_bounds__(kWave) void k_commit(DevState S, DevParams pr, int 
   const int z = qid / I;
   const int j = qid % I;
   const double t = t_ptr ? *t_ptr : t_val;
-  __shared__ int stage[3 * kWave];
+  __shared__ int stage[stage_words<false>()];
   const QEnv e = make_env(S, pr, qid, j, stage);
   Queue<KS> w;
   w.load(S, e, qid);
@@ -573,7 +593,7 @@ template <int KS, int NW, bool TRK>
 __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
   __shared__ double s_u[2][NW], s_t[2][NW], s_q[2][NW];
   __shared__ int s_j[2][NW];
-  __shared__ int stage[NW][3 * kWave];
+  __shared__ int stage[NW][stage_words<TRK>()];
   const int z = blockIdx.x;
   const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
   const int nw = blockDim.x / kWave;
@@ -611,22 +631,14 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
     for (int j = wid; j < I; j += nw) {
       const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
       Queue<KS> w;
-      w.template load<TRK>(S, e, z * I + j);
-      commit_advance<KS, TRK>(w, e, j == m, q.p, q.d, q.tn, S.qcap, max_iters, err,
-                              TRK ? S.r_tag + (int64_t)(z * I + j) * S.rcap : nullptr,
+      int32_t* tags = TRK ? S.r_tag + (int64_t)(z * I + j) * S.rcap : nullptr;
+      w.template load<TRK>(S, e, z * I + j, tags);
+      commit_advance<KS, TRK>(w, e, j == m, q.p, q.d, q.tn, S.qcap, max_iters, err, tags,
                               tag0 + i, tk);
       w.template store<TRK>(S, e, z * I + j);
     }
   }
   if (work && lane_id() == 0) atomicAdd(work + z, wbatch);
-  if constexpr (TRK) {
-    for (int j = wid; j < I; j += nw) {
-      const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
-      Queue<KS> w;
-      w.template load<true>(S, e, z * I + j);
-      drain(w, e, S.r_tag + (int64_t)(z * I + j) * S.rcap, tk, max_iters, err);
-    }
-  }
 }
 
 // Trace inputs of 64 consecutive queries, lane l holding query base + l; the acc /
@@ -828,7 +840,7 @@ template <int KS, bool TRK>
 __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv& e, bool chosen,
                                           int p, int d, double tn, int qcap, int kmax,
                                           int64_t max_iters, int32_t* err, LdsQueue<KS>& SL,
-                                          LdsQueue<KS>& F, int32_t* tags, int tag,
+                                          LdsTags* SLt, LdsQueue<KS>& F, int32_t* tags, int tag,
                                           const Track& tk) {
   const int ln = lane_id();
   VisitOut vo;
@@ -875,7 +887,7 @@ __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv&
         if (wk.resident() == 0 && clk < stop_t) clk = stop_t;
         wk.clock = clk;
         wk.iters += n;
-        if (joined || n > 0 || clk != clk0) wk.template to_lds<TRK>(SL);   // it moved on
+        if (joined || n > 0 || clk != clk0) wk.template to_lds<TRK>(SL, SLt);   // it moved on
         vo.g = wk.g;
         vo.clock = clk;
         // the instance ran the admission batch, or sat idle at F and its clock jumped
@@ -918,14 +930,18 @@ __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv&
       }
       break;
     }
-    if (phase != kTail && wk.quiet(e) && (!TRK || phase != kReplay || wk.pend == 0)) {
+    if (phase != kTail && wk.quiet(e)) {
       // a quiet run ends before the batch in which a decode finishes (or at the stop
-      // time or the cap); that batch is then stepped below.  A replayed batch that
-      // gives first tokens is always stepped.
-      n += wk.quiet_run(e, clk, stop_t, n, max_iters);
-      if (!(clk < stop_t) || n == max_iters) continue;
+      // time or the cap); that batch is then stepped below
+      if (phase == kReplay) {
+        if (replay_quiet<KS, TRK>(wk, e, clk, stop_t, n, max_iters, tags, tk)) continue;
+      } else {
+        n += wk.quiet_run(e, clk, stop_t, n, max_iters);
+        if (!(clk < stop_t) || n == max_iters) continue;
+      }
     }
-    const StepOut o = wk.template step<TRK>(e);
+    // (one step for every phase: TRK bookkeeping on the walk's copies is harmless)
+    const StepOut o = wk.template step<TRK>(e, tags);
     if (phase != kTail) {
       clk = __dadd_rn(clk, batch_time(e.k, o.P, o.D, o.C, o.A));
       ++n;
@@ -1029,9 +1045,10 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
   __shared__ int s_j[2][W];
   __shared__ double s_mu[2];
   __shared__ int s_mj[2];
-  __shared__ int stage[W][3 * kWave];
+  __shared__ int stage[W][stage_words<TRK>()];
   __shared__ LdsQueue<KS> sst[W][IPW];   // instance states
   __shared__ LdsQueue<KS> fst[W][IPW];   // frontier states
+  __shared__ LdsTags stags[TRK ? W : 1][IPW];   // instance states' tracking registers
   const int b = blockIdx.x;
   const int z = (b / 8 / G) * 8 + b % 8;
   const int cid = (b / 8) % G;
@@ -1058,8 +1075,9 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
     if (j < I) {
       env[r] = make_env(S, pr, z * I + j, j, stage[wid]);
       Queue<KS> q;
-      q.template load<TRK>(S, env[r], z * I + j);
-      q.template to_lds<TRK>(sst[wid][r]);
+      q.template load<TRK>(S, env[r], z * I + j,
+                           TRK ? S.r_tag + (int64_t)(z * I + j) * S.rcap : nullptr);
+      q.template to_lds<TRK>(sst[wid][r], &stags[TRK ? wid : 0][r]);
     }
   }
   QueryBlock<IPW> cur = fetch_block<IPW>(0, N, qp, qd, qt, tau, acc, cost, n_cols, cols);
@@ -1131,9 +1149,10 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
       if (j < I) {
         const QEnv& e = env[r];
         Queue<KS> wk;
-        wk.template from_lds<TRK>(sst[wid][r]);
+        wk.template from_lds<TRK>(sst[wid][r], &stags[TRK ? wid : 0][r]);
         const VisitOut vo = visit<KS, TRK>(wk, fc[r], e, i >= 0 && j == m, p, dq, tn, S.qcap,
-                                           kmax, max_iters, err, sst[wid][r], fst[wid][r],
+                                           kmax, max_iters, err, sst[wid][r],
+                                           &stags[TRK ? wid : 0][r], fst[wid][r],
                                            TRK ? S.r_tag + (int64_t)(z * I + j) * S.rcap
                                                : nullptr,
                                            tag0 + i, tk);
@@ -1164,12 +1183,31 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
     const int j = jbase + r;
     if (j < I) {
       Queue<KS> q;
-      q.template from_lds<TRK>(sst[wid][r]);
+      q.template from_lds<TRK>(sst[wid][r], &stags[TRK ? wid : 0][r]);
       q.template store<TRK>(S, env[r], z * I + j);
-      if constexpr (TRK)
-        drain(q, env[r], S.r_tag + (int64_t)(z * I + j) * S.rcap, tk, max_iters, err);
     }
   }
+}
+
+// After a trace that reports realised TTFT, one wave per queue: the tracked queries
+// still without a first token (drain() on a private copy of the stored state).  A
+// kernel of its own, so the trace kernels carry none of its code.
+template <int KS>
+__global__ __launch_bounds__(kWave) void k_drain(DevState S, DevParams pr, int Z, int I,
+                                                 double* realized, int tag0, int N, int reading,
+                                                 int64_t max_iters, int32_t* err) {
+  const int qid = blockIdx.x;
+  if (qid >= Z * I) return;
+  const int z = qid / I;
+  const int j = qid % I;
+  __shared__ int stage[stage_words<true>()];
+  const QEnv e = make_env(S, pr, qid, j, stage);
+  const int32_t* tags = S.r_tag + (int64_t)qid * S.rcap;
+  if (S.sc[qid].ntrk <= 0) return;
+  Queue<KS> w;
+  w.template load<true>(S, e, qid, tags);
+  const Track tk{realized + (int64_t)z * N, tag0, N, reading};
+  drain(w, e, tags, tk, max_iters, err);
 }
 
 // Before a trace that reports realised TTFT: no query of it is tracked yet, no
@@ -1457,6 +1495,9 @@ static hipError_t launch_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
   return launch_trace_mem<KS, (KS <= 4 ? 8 : (KS == 8 ? 8 : 4))>(env, a);
 }
 
+#define DRAIN_ARGS \
+  env.S, env.P, env.Z, env.I, a.realized, a.tag0, a.N, env.reading, env.max_iters, env.err
+
 hipError_t launch_trace(const LaunchEnv& env, const TraceArgs& a) {
   if (env.work) {
     hipLaunchKernelGGL(k_clear_work, dim3((env.Z + 255) / 256), dim3(256), 0, env.stream,
@@ -1482,6 +1523,15 @@ hipError_t launch_trace(const LaunchEnv& env, const TraceArgs& a) {
     default: return hipErrorInvalidValue;
   }
   if (e != hipSuccess || !a.realized) return e;
+  switch (env.ks) {
+    case 1: hipLaunchKernelGGL(k_drain<1>, dim3(env.Z * env.I), dim3(kWave), 0, env.stream, DRAIN_ARGS); break;
+    case 2: hipLaunchKernelGGL(k_drain<2>, dim3(env.Z * env.I), dim3(kWave), 0, env.stream, DRAIN_ARGS); break;
+    case 4: hipLaunchKernelGGL(k_drain<4>, dim3(env.Z * env.I), dim3(kWave), 0, env.stream, DRAIN_ARGS); break;
+    case 8: hipLaunchKernelGGL(k_drain<8>, dim3(env.Z * env.I), dim3(kWave), 0, env.stream, DRAIN_ARGS); break;
+    default: hipLaunchKernelGGL(k_drain<16>, dim3(env.Z * env.I), dim3(kWave), 0, env.stream, DRAIN_ARGS); break;
+  }
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const int64_t no = (int64_t)env.Z * a.N;
   hipLaunchKernelGGL(k_track_end, dim3((unsigned)((no + 255) / 256)), dim3(256), 0, env.stream,
                      a.realized, a.qt, a.N, no);
