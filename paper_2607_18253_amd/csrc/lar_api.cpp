@@ -34,6 +34,7 @@ struct lar_ctx {
   lar::SyncCtl sync{1000000000ull, -1, -1};   // 10 s wait bound; no post left out
   unsigned long long* work = nullptr;          // [Z] estimate batches of the last trace
   int32_t tag_next = 0;        // ring tag of the next query tracked for its realised TTFT
+  int32_t tag_start = 0;       // tag_next after a (re)load
   lar::DevState snap{};        // one scenario's copy of the last loaded snapshot
   int32_t* err = nullptr;
   size_t tail_elems = 0;  // allocated K * Z * I
@@ -145,6 +146,12 @@ lar_status lar_create(lar_ctx** out, const lar_config* cfg) {
       ctx->sync.skip_cid = m;
       ctx->sync.skip_query = q;
     }
+  }
+  // Test hook of the realised-TTFT tags: LAR_TEST_TAG_START starts the tag counter
+  // near its end, so that a test reaches the wrap (every slot untagged, restart at 0).
+  if (const char* v = std::getenv("LAR_TEST_TAG_START")) {
+    const long long t0 = std::atoll(v);
+    if (t0 > 0 && t0 <= INT32_MAX) ctx->tag_start = (int32_t)t0;
   }
   ctx->Z = cfg->n_scen;
   ctx->I = cfg->n_inst;
@@ -375,7 +382,7 @@ lar_status lar_reload_state(lar_ctx* ctx) {
     HIP_TRY(ctx, hipMemcpyAsync(S.r_seq + o * rcap, sn.r_seq, I * rcap * 4, k, s));
     HIP_TRY(ctx, hipMemcpyAsync(S.r_tag + o * rcap, sn.r_tag, I * rcap * 4, k, s));
   }
-  ctx->tag_next = 0;   // every ring entry is untracked again
+  ctx->tag_next = ctx->tag_start;   // every ring entry is untracked again
   HIP_TRY(ctx, lar::launch_clear_error(env_of(ctx)));
   ctx->sticky = LAR_OK;
   return LAR_OK;

@@ -158,3 +158,30 @@ def test_realized_split_calls():
     np.testing.assert_array_equal(bits(reals[0].cpu().numpy()[0]), bits(pre.realized))
     np.testing.assert_array_equal(bits(reals[1].cpu().numpy()[0]), bits(full.realized[N1:]))
     ctx.close()
+
+
+def test_realized_tag_counter_wrap(monkeypatch):
+    """The tag counter starts just below its end: the first call's tags run up to it,
+    the second call wraps (every ring slot untagged, tags from 0 again); both calls
+    still report exactly the oracle's realised TTFTs."""
+    monkeypatch.setenv("LAR_TEST_TAG_START", str(2 ** 31 - 1 - 1000))
+    wl = make_workload("c2", n_q=1200, n_inst=8)
+    N, N1 = wl.n_q, 500
+    ctx = context_for(wl)
+    monkeypatch.delenv("LAR_TEST_TAG_START")
+    ctx.advance(float(wl.q_t_ms[0]))
+    reals = []
+    for lo, hi, t_after in ((0, N1, float(wl.q_t_ms[N1])), (N1, N, float(wl.q_t_ms[-1]))):
+        r = torch.full((1, hi - lo), -1.0, dtype=torch.float64, device="cuda:0")
+        ctx.route_trace(T(wl.q_prefill[lo:hi], torch.int32), T(wl.q_decode[lo:hi], torch.int32),
+                        T(wl.q_t_ms[lo:hi], torch.float64), t_after,
+                        T(wl.acc[lo:hi], torch.float64), T(wl.cost[lo:hi], torch.float64),
+                        T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64),
+                        realized=r)
+        reals.append(r)
+    ctx.sync()
+    pre = O.trace(wl, n_q=N1, final_state=False)
+    full = O.trace(wl, final_state=False)
+    np.testing.assert_array_equal(bits(reals[0].cpu().numpy()[0]), bits(pre.realized))
+    np.testing.assert_array_equal(bits(reals[1].cpu().numpy()[0]), bits(full.realized[N1:]))
+    ctx.close()
