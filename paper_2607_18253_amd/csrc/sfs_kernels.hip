@@ -1030,10 +1030,10 @@ __device__ __forceinline__ double estimate_visit(const FCache& fc, const Queue<K
 }
 
 // The whole sequential trace with each wave owning IPW instances whose states stay
-// in LDS for the whole trace (one working copy in VGPRs per visit).  A scenario spans G workgroups of W waves; block b
-// serves scenario z = (b / 8 / G) * 8 + b % 8 as cluster member (b / 8) % G, so the
-// members of a scenario share one XCD (blocks are dispatched to the 8 XCDs
-// round-robin) and exchange through that XCD's L2.  Iteration i (from -1): the
+// in LDS for the whole trace (one working copy in VGPRs per visit).  A scenario spans
+// G workgroups of W waves; block b serves scenario z = b / G as cluster member b % G
+// (consecutive blocks go to different XCDs; the members meet in device-coherent
+// memory, which measured faster than keeping each scenario on one XCD).  Iteration i (from -1): the
 // workgroup argmax (LDS, one barrier) and the cluster argmax (global exchange, when
 // G > 1) of query i, then per owned instance one visit (commit of query i, replay,
 // frontier cache) and the estimate of query i + 1.
@@ -1050,8 +1050,8 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
   __shared__ LdsQueue<KS> fst[W][IPW];   // frontier states
   __shared__ LdsTags stags[TRK ? W : 1][IPW];   // instance states' tracking registers
   const int b = blockIdx.x;
-  const int z = (b / 8 / G) * 8 + b % 8;
-  const int cid = (b / 8) % G;
+  const int z = b / G;
+  const int cid = b % G;
   if (z >= Z) return;
   const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
   const int nw = blockDim.x / kWave;   // waves launched (<= W)
@@ -1420,9 +1420,9 @@ static hipError_t launch_trace_mem(const LaunchEnv& env, const TraceArgs& a) {
   return hipGetLastError();
 }
 
-// Every active workgroup of a clustered trace must be resident at once (members wait
-// for each other), and a scenario's members share one XCD: per XCD, ceil(Z / 8) * G
-// workgroups must fit its compute units at the kernel's occupancy.
+// Every workgroup of a clustered trace must be resident at once (members wait for
+// each other): with the blocks dealt to the 8 XCDs in turn, ceil(Z * G / 8) per XCD
+// must fit its compute units at the kernel's occupancy.
 template <class K>
 static bool co_resident(K kernel, int threads, int Z, int G) {
   int dev = 0, n_cu = 0, per_cu = 0;
@@ -1431,7 +1431,7 @@ static bool co_resident(K kernel, int threads, int Z, int G) {
     return false;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess)
     return false;
-  const int64_t per_xcd = (int64_t)((Z + 7) / 8) * G;
+  const int64_t per_xcd = ((int64_t)Z * G + 7) / 8;
   return per_cu > 0 && per_xcd <= (int64_t)(n_cu / 8) * per_cu;
 }
 
@@ -1451,7 +1451,7 @@ static hipError_t launch_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  const int blocks = 8 * ((env.Z + 7) / 8) * G;
+  const int blocks = env.Z * G;
   hipLaunchKernelGGL((k_trace_cl<KS, W, IPW, TRK>), dim3(blocks), dim3(w_used * kWave), 0,
                      env.stream, LAR_TRACE_ARGS, G, env.xslot, env.T.K, env.sync);
   return hipGetLastError();
