@@ -225,7 +225,7 @@ struct StepOut {
 
 // What a wave needs besides the state to work on one queue: the batch-time
 // coefficients, the queue's prefill ring in HBM, and the wave's LDS staging area
-// (3 x 64 ints).  Rebuilt from the parameters whenever a wave picks the queue up.
+// (3 or 4 x 64 ints, 16-byte aligned).  Rebuilt from the parameters whenever a wave picks the queue up.
 struct QEnv {
   Coef k;
   bool need_C, need_A;   // d != 0, e != 0: only then are C / A accumulated

@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kWave) void k_traj(DevState S, DevParams pr, DevTra
   const int j = qid % I;
   const double t = t_ptr ? *t_ptr : t_val;
   const int ln = lane_id();
-  __shared__ int stage[stage_words<false>()];
+  __shared__ alignas(16) int stage[stage_words<false>()];
   const QEnv e = make_env(S, pr, qid, j, stage);
   Queue<KS> w;
   w.load(S, e, qid);
@@ -399,7 +399,7 @@ __global__ __launch_bounds__(kWave) void k_commit(DevState S, DevParams pr, int 
   const int z = qid / I;
   const int j = qid % I;
   const double t = t_ptr ? *t_ptr : t_val;
-  __shared__ int stage[stage_words<false>()];
+  __shared__ alignas(16) int stage[stage_words<false>()];
   const QEnv e = make_env(S, pr, qid, j, stage);
   Queue<KS> w;
   w.load(S, e, qid);
@@ -593,7 +593,7 @@ template <int KS, int NW, bool TRK>
 __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
   __shared__ double s_u[2][NW], s_t[2][NW], s_q[2][NW];
   __shared__ int s_j[2][NW];
-  __shared__ int stage[NW][stage_words<TRK>()];
+  __shared__ alignas(16) int stage[NW][stage_words<TRK>()];
   const int z = blockIdx.x;
   const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
   const int nw = blockDim.x / kWave;
@@ -807,17 +807,88 @@ __device__ __forceinline__ void admission_summary(FCache& fc, const Queue<KS>& w
   fc.left = e.k.B - fc.aD - fc.aP;
 }
 
-// Record the decode-only tail read-only from w (whole prefill list in the window).
+// Suffix sums over the lanes (lane l gets the sum over lanes l .. 63).
+__device__ __forceinline__ int suffix_sum32(int x) {
+  const int ln = lane_id();
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_down(x, o, kWave);
+    if (ln + o < kWave) x += y;
+  }
+  return x;
+}
+
+__device__ __forceinline__ int64_t suffix_sum64(int64_t x) {
+  const int ln = lane_id();
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int lo = __shfl_down((int)(uint32_t)(uint64_t)x, o, kWave);
+    const int hi = __shfl_down((int)(uint32_t)((uint64_t)x >> 32), o, kWave);
+    if (ln + o < kWave) x += (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
+  }
+  return x;
+}
+
+// Record the decode-only tail read-only from w (whole prefill list in the window):
+// lane k - 1 gets D and C of tail batch k (batch g + 1 + k), k = 1 .. kmax.  After the
+// admission batch g + 1 every request decodes until its last batch: a decoding
+// request until its slot's dl, a list entry until g + 1 + rd.  So a request is in
+// tail batches 1 .. k_last, and D_k, and the cx0 sum behind C_k, are suffix sums
+// over k_last: requests with k_last < kmax are binned in LDS (the staging area), the
+// rest (most of them) counted with one wave reduction and put in the last bin.
 template <int KS>
 __device__ __forceinline__ void tail_readonly(FCache& fc, const Queue<KS>& w, const QEnv& e,
                                               int kmax) {
   const int ln = lane_id();
-  typename Queue<KS>::Tail tl = w.tail_begin(e);
-  for (int k = 0; k < kmax; ++k) {
-    const int64_t C = e.need_C ? tl.c0 + tl.D * (int64_t)(w.g + tl.k) : 0;
-    if (ln == k) { fc.tD = (int)tl.D; fc.tC = C; }
-    w.tail_next(e, tl);
+  const bool need_C = e.need_C;
+  const int g1 = w.g + 1;   // the admission batch
+  int* cnt = e.stg;                                                            // [64]
+  unsigned long long* csum = reinterpret_cast<unsigned long long*>(e.stg + kWave);  // [64]
+  cnt[ln] = 0;
+  csum[ln] = 0ull;
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  int far_n = 0;
+  int64_t far_c = 0;
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    const int kl = w.dl[s] - g1;   // >= 1: survives the admission batch
+    if (kl >= kmax) {
+      ++far_n;
+      far_c += w.dc[s];
+    } else if (kl >= 1) {
+      atomicAdd(&cnt[kl - 1], 1);
+      if (need_C) atomicAdd(&csum[kl - 1], (unsigned long long)(int64_t)w.dc[s]);
+    }
   }
+  const int idx = ln - w.woff;
+  if (idx >= 0 && idx < w.nwin) {   // rd >= 1
+    const int64_t c0 = (int64_t)(w.wcx + w.wrp) - g1;
+    if (w.wrd >= kmax) {
+      ++far_n;
+      far_c += c0;
+    } else {
+      atomicAdd(&cnt[w.wrd - 1], 1);
+      if (need_C) atomicAdd(&csum[w.wrd - 1], (unsigned long long)c0);
+    }
+  }
+  far_n = wave_sum32(far_n);
+  if (need_C) far_c = wave_sum64(far_c);
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  int D = ln < kmax ? cnt[ln] : 0;
+  int64_t c0 = need_C && ln < kmax ? (int64_t)csum[ln] : 0;
+  if (ln == kmax - 1) {
+    D += far_n;
+    c0 += far_c;
+  }
+  __builtin_amdgcn_wave_barrier();   // the staging area is free again
+  D = suffix_sum32(D);
+  if (need_C) c0 = suffix_sum64(c0);
+  fc.tD = ln < kmax ? D : 0;
+  fc.tC = need_C && ln < kmax ? c0 + (int64_t)D * (w.g + ln + 1) : 0;
 }
 
 // What the estimate needs of the instance after a visit: its batch counter and
@@ -1045,7 +1116,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
   __shared__ int s_j[2][W];
   __shared__ double s_mu[2];
   __shared__ int s_mj[2];
-  __shared__ int stage[W][stage_words<TRK>()];
+  __shared__ alignas(16) int stage[W][stage_words<TRK>()];
   __shared__ LdsQueue<KS> sst[W][IPW];   // instance states
   __shared__ LdsQueue<KS> fst[W][IPW];   // frontier states
   __shared__ LdsTags stags[TRK ? W : 1][IPW];   // instance states' tracking registers
@@ -1200,7 +1271,7 @@ __global__ __launch_bounds__(kWave) void k_drain(DevState S, DevParams pr, int Z
   if (qid >= Z * I) return;
   const int z = qid / I;
   const int j = qid % I;
-  __shared__ int stage[stage_words<true>()];
+  __shared__ alignas(16) int stage[stage_words<true>()];
   const QEnv e = make_env(S, pr, qid, j, stage);
   const int32_t* tags = S.r_tag + (int64_t)qid * S.rcap;
   if (S.sc[qid].ntrk <= 0) return;
