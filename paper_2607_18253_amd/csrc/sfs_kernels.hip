@@ -901,6 +901,119 @@ struct VisitOut {
   bool direct;
 };
 
+// F + query (p prompt tokens, rdq >= 1 decodes) walked towards its next admission
+// point without stepping the background batch by batch.  F's admission batch is
+// stepped: it serves every list entry of F in full and gives the query its first
+// chunk.  After it the background is decode-only, and its batches are the cached
+// tail of F (lane k - 1: decode tokens and context sum of tail batch k), which the
+// query does not change (it is last in FCFS order and takes only what is left).  The
+// query's chunks, then its decodes, are folded on top of those batches, one batch
+// time each in batch order, until the state would admit a new tail query; then the
+// queue is brought to that batch in one go (decoding requests are lazy: the batch
+// counter moves and the live slots are recounted; the query, once its prefill is
+// complete, takes a free slot).  Features, batch times and the resulting state are
+// those of stepping every batch.  Stops early, at the last folded batch, when the
+// cached batches run out or the cap is reached; the stepped walk then continues.
+template <int KS>
+__device__ __forceinline__ void walk_fast(Queue<KS>& wk, const FCache& fc, const QEnv& e, int p,
+                                          int rdq, double& clk, int64_t& n, int kmax,
+                                          int64_t max_iters) {
+  const Coef& kc = e.k;
+  const int ln = lane_id();
+  if (wk.tail_admitted_next(e) || n >= max_iters) return;
+  {
+    const StepOut o = wk.step(e);   // F's admission batch, with the query's first chunk
+    clk = __dadd_rn(clk, batch_time(kc, o.P, o.D, o.C, o.A));
+    ++n;
+  }
+  if (wk.tail_admitted_next(e)) return;
+  const int gA = wk.g;
+  // the query: the list's only entry, or decoding since the admission batch
+  int rem = 0, cxq = 0, k_done = -1, cx_done = 0, ctxq = 0;
+  if (wk.n_pre > 0) {
+    rem = (int)wk.pre_sum;
+    cxq = __builtin_amdgcn_readlane(wk.wcx, wk.woff);
+  } else {
+    k_done = 0;
+    cx_done = p;
+    ctxq = p;
+  }
+  int folded = 0;
+  for (int k = 1; k < kmax && n < max_iters; ++k) {   // lanes k - 1 and k are read
+    const int Dk = __builtin_amdgcn_readlane(fc.tD, k - 1);
+    int P = 0, D = Dk;
+    int64_t C = read_lane_i64(fc.tC, k - 1), A = 0;
+    if (rem > 0) {
+      const int c = min(rem, kc.B - Dk);
+      P = c;
+      A = (int64_t)c * cxq + (int64_t)c * (c + 1) / 2;
+      rem -= c;
+      cxq += c;
+      if (rem == 0) {
+        k_done = k;
+        cx_done = cxq;
+        ctxq = cxq;
+      }
+    } else if (k_done >= 0 && k <= k_done + rdq) {   // the query decodes
+      D += 1;
+      C += ctxq;
+      ctxq += 1;
+    }
+    clk = __dadd_rn(clk, batch_time(kc, P, D, e.need_C ? C : 0, e.need_A ? A : 0));
+    ++n;
+    folded = k;
+    // the state for the next batch: the background's decoders of tail batch k + 1,
+    // the query as a decoder then or as the list's only entry
+    const int nd = __builtin_amdgcn_readlane(fc.tD, k) +
+                   ((k_done >= 0 && k + 1 <= k_done + rdq) ? 1 : 0);
+    if (nd + (rem > 0 ? 1 : 0) < kc.M && (int64_t)nd + rem < (int64_t)kc.B) break;
+  }
+  if (folded == 0) return;
+  const int gN = gA + folded;
+  if (k_done >= 1) {   // prefill completed during the fold: off the list, into a slot
+    const int seqq = __builtin_amdgcn_readlane(wk.wseq, wk.woff);
+    wk.woff += 1;
+    wk.nwin -= 1;
+    wk.head = wk.head + 1 == e.rcap ? 0 : wk.head + 1;
+    wk.n_pre = 0;
+    wk.n_part = 0;
+    wk.pre_sum = 0;
+    const int gc = gA + k_done;
+    if (gc + rdq > gN) {   // still decoding; at most M - 1 others run, so a slot is free
+      bool placed = false;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const uint64_t fm = ballot(wk.dl[s] <= gN);
+        if (!placed && fm) {
+          if (ln == __builtin_ctzll(fm)) {
+            wk.dl[s] = gc + rdq;
+            wk.dc[s] = cx_done - gc;
+            wk.ds[s] = seqq;
+          }
+          placed = true;
+        }
+      }
+    }
+  } else if (rem > 0) {
+    if (ln == wk.woff) {
+      wk.wrp = rem;
+      wk.wcx = cxq;
+    }
+    wk.pre_sum = rem;
+  }
+  wk.g = gN;
+  int nd = 0;
+  int64_t c0 = 0;
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    const bool live = wk.dl[s] > gN;
+    nd += popc(ballot(live));
+    if (e.need_C && live) c0 += wk.dc[s];
+  }
+  wk.n_dec = nd;
+  if (e.need_C) wk.c0sum = wave_sum64(c0);
+}
+
 // One visit of a wave to one owned queue for one query.  wk enters as the instance
 // state (loaded from SL); the query is appended if it was routed here, the instance
 // is replayed to tn and written back to SL (unless nothing changed), and the
@@ -963,7 +1076,8 @@ __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv&
         vo.clock = clk;
         // the instance ran the admission batch, or sat idle at F and its clock jumped
         if (fc.valid && (wk.g > fc.g || (wk.g == fc.g && clk != fc.E))) fc.valid = false;
-        if (joined && fc.valid) {
+        const bool from_f = joined && fc.valid;
+        if (from_f) {
           wk.from_lds(F);
           wk.append(e, p, d);   // F shares the instance's ring: same slot, entry and tag
           clk = fc.E;
@@ -979,6 +1093,10 @@ __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv&
         phase = kWalk;
         stop_t = __builtin_inf();
         n = 0;
+        // (pools of <= 256 slots per queue step cheaply enough; the larger code would
+        // cost them more than the fold saves)
+        if constexpr (KS >= 8)
+          if (from_f) walk_fast(wk, fc, e, p, d, clk, n, kmax, max_iters);
         continue;
       }
       if (phase == kWalk) {

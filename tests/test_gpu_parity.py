@@ -281,6 +281,22 @@ def test_trace_c4_prefix():
     ctx.close()
 
 
+@pytest.mark.parametrize("n_inst,n_q", [(8, 80), (4, 120)])
+def test_trace_c4_instances_shared(n_inst, n_q):
+    """Config 4's instances (512 slots, 1024-deep queues, prompts up to 131k tokens,
+    context-dependent batch time), few of them so that many queries join the same
+    instance: each joins at the instance's cached admission point and is walked to
+    the next one over the cached decode-only batches."""
+    wl = make_workload("c4", n_q=n_q, n_inst=n_inst)
+    choice, chosen, util, ctx = gpu_trace(wl)
+    ref = O.trace(wl)
+    np.testing.assert_array_equal(choice[0], ref.choice)
+    np.testing.assert_array_equal(bits(chosen[0]), bits(ref.ttft_chosen))
+    np.testing.assert_array_equal(bits(util[0]), bits(ref.util_chosen))
+    assert_state_equal(ctx, 0, ref)
+    ctx.close()
+
+
 def test_trace_c5_all_scenarios_prefix_and_stats():
     wl = make_workload("c5", n_q=24)
     choice, chosen, util, ctx = gpu_trace(wl)
