@@ -163,31 +163,53 @@ __device__ __forceinline__ int64_t sum_lanes64(int64_t v, uint64_t m) {
   return s;
 }
 
-__device__ __forceinline__ int64_t shfl_xor64(int64_t x, int m) {
-  int lo = (int)(uint32_t)(uint64_t)x;
-  int hi = (int)(uint32_t)((uint64_t)x >> 32);
-  lo = __shfl_xor(lo, m, kWave);
-  hi = __shfl_xor(hi, m, kWave);
-  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
-}
-
 __device__ __forceinline__ int64_t uni64(int64_t x) {
   int lo = uni((int)(uint32_t)(uint64_t)x);
   int hi = uni((int)(uint32_t)((uint64_t)x >> 32));
   return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
 }
 
-__device__ __forceinline__ int64_t wave_sum64(int64_t x) {
-#pragma unroll
-  for (int o = kWave / 2; o > 0; o >>= 1) x += shfl_xor64(x, o);
-  return uni64(x);
+// Inclusive prefix sums over the wave with DPP lane moves (row_shr within 16-lane
+// rows, then row_bcast:15 / row_bcast:31 across rows; lanes without a source add 0).
+__device__ __forceinline__ int scan_add32(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false); // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false); // row_bcast:31
+  return x;
 }
 
-__device__ __forceinline__ int wave_sum32(int x) {
-#pragma unroll
-  for (int o = kWave / 2; o > 0; o >>= 1) x += __shfl_xor(x, o, kWave);
-  return uni(x);
+// The same in 64 bits: both halves move together, the carry of the low half goes
+// into the high one.
+__device__ __forceinline__ int64_t scan_add64(int64_t v) {
+  uint32_t lo = (uint32_t)(uint64_t)v, hi = (uint32_t)((uint64_t)v >> 32);
+#define LAR_SCAN64_STEP(ctrl, rows, bc)                                                    \
+  {                                                                                        \
+    const uint32_t l2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)lo, ctrl, rows, 0xf, bc); \
+    const uint32_t h2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)hi, ctrl, rows, 0xf, bc); \
+    const uint32_t nl = lo + l2;                                                           \
+    hi = hi + h2 + (nl < lo ? 1u : 0u);                                                    \
+    lo = nl;                                                                               \
+  }
+  LAR_SCAN64_STEP(0x111, 0xf, true)
+  LAR_SCAN64_STEP(0x112, 0xf, true)
+  LAR_SCAN64_STEP(0x114, 0xf, true)
+  LAR_SCAN64_STEP(0x118, 0xf, true)
+  LAR_SCAN64_STEP(0x142, 0xa, false)
+  LAR_SCAN64_STEP(0x143, 0xc, false)
+#undef LAR_SCAN64_STEP
+  return (int64_t)(((uint64_t)hi << 32) | lo);
 }
+
+__device__ __forceinline__ int64_t wave_sum64(int64_t x) {
+  const int64_t s = scan_add64(x);
+  return uni64((int64_t)(((uint64_t)(uint32_t)lane_last((int)(uint32_t)((uint64_t)s >> 32)) << 32) |
+                         (uint64_t)(uint32_t)lane_last((int)(uint32_t)(uint64_t)s)));
+}
+
+__device__ __forceinline__ int wave_sum32(int x) { return uni(lane_last(scan_add32(x))); }
 
 // ------------------------------------------------------------------ LDS copies of queues
 // A queue's state kept in LDS by a persistent kernel: decode slots in the register

@@ -807,26 +807,18 @@ __device__ __forceinline__ void admission_summary(FCache& fc, const Queue<KS>& w
   fc.left = e.k.B - fc.aD - fc.aP;
 }
 
-// Suffix sums over the lanes (lane l gets the sum over lanes l .. 63).
+// Suffix sums over the lanes (lane l gets the sum over lanes l .. 63): the total
+// minus the inclusive prefix, plus the lane's own value.
 __device__ __forceinline__ int suffix_sum32(int x) {
-  const int ln = lane_id();
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int y = __shfl_down(x, o, kWave);
-    if (ln + o < kWave) x += y;
-  }
-  return x;
+  const int incl = scan_add32(x);
+  return lane_last(incl) - incl + x;
 }
 
 __device__ __forceinline__ int64_t suffix_sum64(int64_t x) {
-  const int ln = lane_id();
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int lo = __shfl_down((int)(uint32_t)(uint64_t)x, o, kWave);
-    const int hi = __shfl_down((int)(uint32_t)((uint64_t)x >> 32), o, kWave);
-    if (ln + o < kWave) x += (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
-  }
-  return x;
+  const int64_t incl = scan_add64(x);
+  const int64_t tot = (int64_t)(((uint64_t)(uint32_t)lane_last((int)(uint32_t)((uint64_t)incl >> 32)) << 32) |
+                                (uint64_t)(uint32_t)lane_last((int)(uint32_t)(uint64_t)incl));
+  return tot - incl + x;
 }
 
 // Record the decode-only tail read-only from w (whole prefill list in the window):
