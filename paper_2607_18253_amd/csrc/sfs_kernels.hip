@@ -65,29 +65,43 @@ __device__ __forceinline__ void best_step_dpp(double& u, int& j) {
   j = t ? xj : j;
 }
 
-__device__ __forceinline__ void best_step_xor(double& u, int& j, int m) {
-  const double xu = __shfl_xor(u, m, kWave);
-  const int xj = __shfl_xor(j, m, kWave);
+// One step across 16-lane rows: the rows in ROWS take the candidate that DPP
+// pattern CTRL broadcasts to them (row_bcast) when it is better; other rows keep
+// their own.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ void best_step_bcast(double& u, int& j) {
+  const long long b = __double_as_longlong(u);
+  const int lo = __builtin_amdgcn_update_dpp((int)b, (int)b, CTRL, ROWS, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp((int)(b >> 32), (int)(b >> 32), CTRL, ROWS, 0xf, false);
+  const double xu = __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+  const int xj = __builtin_amdgcn_update_dpp(j, j, CTRL, ROWS, 0xf, false);
   const bool t = better(xu, xj, u, j);
   u = t ? xu : u;
   j = t ? xj : j;
 }
 
-// Argmax of the candidates in lanes [0, n) (lanes from n up to the next power of two
-// must hold j = -1); the result is returned wave-uniform.  Quad permutations and the
-// row mirrors combine 2, 4, 8 and 16 lanes; larger n continue with lane shuffles.
+// Argmax of the candidates in lanes [0, n) (every lane from n on must hold j = -1);
+// the result is returned wave-uniform.  Quad permutations and the
+// row mirrors combine 2, 4, 8 and 16 lanes (every lane of a row then holds the row's
+// best); beyond 16, row 0's best moves into row 1 and row 2's into row 3
+// (row_bcast:15), then rows 0-1's into rows 2-3 (row_bcast:31), so lane 63 holds the
+// best of all.
 __device__ __forceinline__ void lane_best(double& u, int& j, int n) {
   if (n > 1) best_step_dpp<0xB1>(u, j);    // quad_perm [1,0,3,2]
   if (n > 2) best_step_dpp<0x4E>(u, j);    // quad_perm [2,3,0,1]
   if (n > 4) best_step_dpp<0x141>(u, j);   // row_half_mirror
   if (n > 8) best_step_dpp<0x140>(u, j);   // row_mirror
-  if (n > 16) best_step_xor(u, j, 16);
-  if (n > 32) best_step_xor(u, j, 32);
+  int src = 0;
+  if (n > 16) {
+    best_step_bcast<0x142, 0xa>(u, j);     // row_bcast:15 into rows 1 and 3
+    best_step_bcast<0x143, 0xc>(u, j);     // row_bcast:31 into rows 2 and 3
+    src = kWave - 1;
+  }
   const long long b = __double_as_longlong(u);
-  const unsigned lo = (unsigned)__builtin_amdgcn_readfirstlane((int)b);
-  const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((int)(b >> 32));
+  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)b, src);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(b >> 32), src);
   u = __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
-  j = __builtin_amdgcn_readfirstlane(j);
+  j = __builtin_amdgcn_readlane(j, src);
 }
 
 // ------------------------------------------------------------------ k_traj
