@@ -5,7 +5,7 @@ include/lar.h; ``paper_2607_18253_amd.lar`` is its Python binding.
 """
 
 from .lar import (EXPORTED, FIRST_TOKEN_DECODE_BATCH, FIRST_TOKEN_PREFILL_BATCH, LarContext,
-                  LarError, context_for, load_library)
+                  LarError, SnapshotBoard, context_for, load_library)
 
 __all__ = ["EXPORTED", "FIRST_TOKEN_DECODE_BATCH", "FIRST_TOKEN_PREFILL_BATCH", "LarContext",
-           "LarError", "context_for", "load_library"]
+           "LarError", "SnapshotBoard", "context_for", "load_library"]
