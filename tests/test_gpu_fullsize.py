@@ -1,5 +1,4 @@
-"""GPU parity at the full sizes of the weight-sweep and long-context workloads, in
-the launch configurations bench.py times.
+"""GPU parity at full size, in the launch configurations bench.py times.
 
 * c5: all 64 scenarios x 100k queries x 64 instances routed together; four scenarios
   checked in full against the oracle (every choice and chosen-TTFT bit, the
@@ -10,6 +9,7 @@ the launch configurations bench.py times.
   (validated on load: every resident list invariant) and routes the last 8 queries
   from it, and the GPU's last 8 choices, chosen TTFTs and final state must be the
   oracle's.
+* c6 in full, and c2 in full under Eq. 3 with realised-TTFT tracking.
 """
 
 from __future__ import annotations
@@ -88,4 +88,38 @@ def test_c4_full_size_last_queries():
     np.testing.assert_array_equal(fin["context"], ref.context)
     np.testing.assert_array_equal(bits(fin["clock_ms"]), bits(ref.clock_ms))
     np.testing.assert_array_equal(fin["iterations"] - s["iterations"], ref.iterations)
+    ctx.close()
+
+
+def test_c6_full_size():
+    """c6 (c2's pool under two-state MMPP arrivals), 100k queries."""
+    wl = make_workload("c6")
+    choice, chosen, util, ctx = gpu_trace(wl)
+    ref = O.trace(wl)
+    np.testing.assert_array_equal(choice[0], ref.choice)
+    np.testing.assert_array_equal(bits(chosen[0]), bits(ref.ttft_chosen))
+    np.testing.assert_array_equal(bits(util[0]), bits(ref.util_chosen))
+    assert_state_equal(ctx, 0, ref)
+    ctx.close()
+
+
+def test_c2_full_size_constrained_realized():
+    """c2, 100k queries under Eq. 3 with the paper's targets and realised-TTFT
+    tracking, as bench.py --objective constrained runs it: choices, estimated and
+    realised TTFT bits, OnTimeUtility and the final state."""
+    from gpu_util import gpu_trace_realized
+    wl = make_workload("c2")
+    tau = O.ttft_targets(wl.q_prefill, wl.tau_u_ms, wl.tau_v)
+    choice, chosen, real, ctx = gpu_trace_realized(wl, tau=tau)
+    ref = O.trace(wl, tau=tau)
+    np.testing.assert_array_equal(choice[0], ref.choice)
+    np.testing.assert_array_equal(bits(chosen[0]), bits(ref.ttft_chosen))
+    np.testing.assert_array_equal(bits(real[0]), bits(ref.realized))
+    assert_state_equal(ctx, 0, ref)
+    out = ctx.ontime_utility(T(choice, torch.int32), T(real, torch.float64), T(tau, torch.float64),
+                             T(wl.acc, torch.float64), T(wl.cost, torch.float64),
+                             T(wl.w_cost, torch.float64))
+    ctx.sync()
+    want = O.ontime_utility(ref.choice, ref.realized, tau, wl.acc, wl.cost, wl.col, wl.w_cost[0])
+    assert bits(out.cpu().numpy()[0]) == bits(want)
     ctx.close()
