@@ -205,8 +205,9 @@ __device__ __forceinline__ int64_t scan_add64(int64_t v) {
 
 __device__ __forceinline__ int64_t wave_sum64(int64_t x) {
   const int64_t s = scan_add64(x);
-  return uni64((int64_t)(((uint64_t)(uint32_t)lane_last((int)(uint32_t)((uint64_t)s >> 32)) << 32) |
-                         (uint64_t)(uint32_t)lane_last((int)(uint32_t)(uint64_t)s)));
+  const uint32_t hi = (uint32_t)lane_last((int)(uint32_t)((uint64_t)s >> 32));
+  const uint32_t lo = (uint32_t)lane_last((int)(uint32_t)(uint64_t)s);
+  return uni64((int64_t)(((uint64_t)hi << 32) | lo));
 }
 
 __device__ __forceinline__ int wave_sum32(int x) { return uni(lane_last(scan_add32(x))); }

@@ -13,7 +13,15 @@
 //            with ties to the lowest instance (Sec. 3, Eq. 2).
 //   k_commit one wave per (scenario, instance): append the routed query, then
 //            replay batches until the clock reaches the next arrival.
+//   k_trace_cl  a whole sequential trace in one launch: G workgroups per scenario,
+//            one wave per instance (states in LDS), per query a workgroup and a
+//            cross-workgroup argmax, then commit + replay + the next estimate from a
+//            cached admission point (frontier) of each instance.
+//   k_trace_mem the same trace with the states in HBM, for pools too large for LDS.
+//   k_drain, k_track_begin, k_track_end  first-token tracking around a trace
+//            (realised TTFT of each query in the replay).
 //   k_stats  one block per scenario: means in query order, nearest-rank p50/p99.
+//   k_targets, k_ontime  TTFT targets per query; OnTimeUtility (Eq. 4).
 #include "sfs_device.h"
 #include "sfs_launch.h"
 
@@ -71,8 +79,9 @@ __device__ __forceinline__ void best_step_dpp(double& u, int& j) {
 template <int CTRL, int ROWS>
 __device__ __forceinline__ void best_step_bcast(double& u, int& j) {
   const long long b = __double_as_longlong(u);
-  const int lo = __builtin_amdgcn_update_dpp((int)b, (int)b, CTRL, ROWS, 0xf, false);
-  const int hi = __builtin_amdgcn_update_dpp((int)(b >> 32), (int)(b >> 32), CTRL, ROWS, 0xf, false);
+  const int b_lo = (int)b, b_hi = (int)(b >> 32);
+  const int lo = __builtin_amdgcn_update_dpp(b_lo, b_lo, CTRL, ROWS, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(b_hi, b_hi, CTRL, ROWS, 0xf, false);
   const double xu = __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
   const int xj = __builtin_amdgcn_update_dpp(j, j, CTRL, ROWS, 0xf, false);
   const bool t = better(xu, xj, u, j);
@@ -706,8 +715,9 @@ __device__ __forceinline__ void cand_take(Cand& c, double u, int k, double ttft,
 // agent-scope atomics on the same words, which the memory model keeps coherent.
 // The wait is bounded in wall-clock time (s_memrealtime runs at 100 MHz; 10 s
 // unless the host sets another bound): a member that never posts, or an error
-// raised by another member, ends the trace with kErrSync instead of a hang.  Two slot sets suffice: a member posts query i + 2
-// only after every member has posted i + 1, i.e. has finished reading the posts of i.
+// raised by another member, ends the trace with kErrSync instead of a hang.  Two slot
+// sets suffice: a member posts query i + 2 only after every member has posted i + 1,
+// i.e. has finished reading the posts of i.
 __device__ __forceinline__ bool cluster_exchange(double& u, int& j, int i, int G, int cid,
                                                  uint64_t* xs, int32_t* err, SyncCtl sc) {
   const int ln = lane_id();
@@ -830,8 +840,9 @@ __device__ __forceinline__ int suffix_sum32(int x) {
 
 __device__ __forceinline__ int64_t suffix_sum64(int64_t x) {
   const int64_t incl = scan_add64(x);
-  const int64_t tot = (int64_t)(((uint64_t)(uint32_t)lane_last((int)(uint32_t)((uint64_t)incl >> 32)) << 32) |
-                                (uint64_t)(uint32_t)lane_last((int)(uint32_t)(uint64_t)incl));
+  const uint32_t t_hi = (uint32_t)lane_last((int)(uint32_t)((uint64_t)incl >> 32));
+  const uint32_t t_lo = (uint32_t)lane_last((int)(uint32_t)(uint64_t)incl);
+  const int64_t tot = (int64_t)(((uint64_t)t_hi << 32) | t_lo);
   return tot - incl + x;
 }
 
@@ -1228,10 +1239,10 @@ __device__ __forceinline__ double estimate_visit(const FCache& fc, const Queue<K
 // in LDS for the whole trace (one working copy in VGPRs per visit).  A scenario spans
 // G workgroups of W waves; block b serves scenario z = b / G as cluster member b % G
 // (consecutive blocks go to different XCDs; the members meet in device-coherent
-// memory, which measured faster than keeping each scenario on one XCD).  Iteration i (from -1): the
-// workgroup argmax (LDS, one barrier) and the cluster argmax (global exchange, when
-// G > 1) of query i, then per owned instance one visit (commit of query i, replay,
-// frontier cache) and the estimate of query i + 1.
+// memory, which measured faster than keeping each scenario on one XCD).
+// Iteration i (from -1): the workgroup argmax (LDS, one barrier) and the cluster
+// argmax (global exchange, when G > 1) of query i, then per owned instance one visit
+// (commit of query i, replay, frontier cache) and the estimate of query i + 1.
 // Identical, operation for operation, to estimate + route + commit per query.
 template <int KS, int W, int IPW, bool TRK>
 __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G, uint64_t* xslot,
@@ -1718,12 +1729,13 @@ hipError_t launch_trace(const LaunchEnv& env, const TraceArgs& a) {
     default: return hipErrorInvalidValue;
   }
   if (e != hipSuccess || !a.realized) return e;
+  const dim3 dg(env.Z * env.I), db(kWave);
   switch (env.ks) {
-    case 1: hipLaunchKernelGGL(k_drain<1>, dim3(env.Z * env.I), dim3(kWave), 0, env.stream, DRAIN_ARGS); break;
-    case 2: hipLaunchKernelGGL(k_drain<2>, dim3(env.Z * env.I), dim3(kWave), 0, env.stream, DRAIN_ARGS); break;
-    case 4: hipLaunchKernelGGL(k_drain<4>, dim3(env.Z * env.I), dim3(kWave), 0, env.stream, DRAIN_ARGS); break;
-    case 8: hipLaunchKernelGGL(k_drain<8>, dim3(env.Z * env.I), dim3(kWave), 0, env.stream, DRAIN_ARGS); break;
-    default: hipLaunchKernelGGL(k_drain<16>, dim3(env.Z * env.I), dim3(kWave), 0, env.stream, DRAIN_ARGS); break;
+    case 1: hipLaunchKernelGGL(k_drain<1>, dg, db, 0, env.stream, DRAIN_ARGS); break;
+    case 2: hipLaunchKernelGGL(k_drain<2>, dg, db, 0, env.stream, DRAIN_ARGS); break;
+    case 4: hipLaunchKernelGGL(k_drain<4>, dg, db, 0, env.stream, DRAIN_ARGS); break;
+    case 8: hipLaunchKernelGGL(k_drain<8>, dg, db, 0, env.stream, DRAIN_ARGS); break;
+    default: hipLaunchKernelGGL(k_drain<16>, dg, db, 0, env.stream, DRAIN_ARGS); break;
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
