@@ -498,3 +498,24 @@ def test_trace_slot_widths(mcap, kernel, seed):
         np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
         assert_state_equal(ctx, z, ref)
     ctx.close()
+
+
+@pytest.mark.parametrize("seed", range(10))
+@pytest.mark.parametrize("flags", [0, 1])
+def test_trace_fast_walk_tiny_pools(seed, flags):
+    """Queues of 8 decode slots per lane take the fast walk (a query joining an
+    instance at its cached admission point is folded over the cached decode-only
+    batches).  Tiny random pools with backlogs -- budgets of 1..8 tokens, 1..4
+    sequences, prompts up to 40 tokens and 1..3 decode tokens, so that a query
+    often completes its prefill, or even its decodes, inside the fold -- against the
+    oracle, both first-token readings, all coefficient terms."""
+    wl = make_tiny_workload(700 + seed, n_inst=3, max_res=8, n_q=60, prompt=(1, 40),
+                            decode=(1, 3), mean_gap_ms=0.5, n_scen=2, dyadic=(seed % 2 == 0))
+    choice, chosen, util, ctx = gpu_trace(wl, flags=flags, queue_cap=10 ** 4, max_seqs_cap=300)
+    for z in range(wl.n_scen):
+        ref = O.trace(wl, scenario=z, reading=flags, queue_cap=10 ** 4)
+        np.testing.assert_array_equal(choice[z], ref.choice)
+        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen))
+        np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
+        assert_state_equal(ctx, z, ref)
+    ctx.close()
