@@ -88,7 +88,15 @@ typedef struct {
   void *stream;           /* hipStream_t to enqueue on; NULL = null stream          */
 } lar_config;
 
-/* Create a context and allocate its device state.  *out is NULL on failure. */
+/*
+ * Create a context and allocate its device state.  *out is NULL on failure.
+ * Read from the environment at creation (tests of the failure paths, not needed in
+ * use): LAR_SYNC_TIMEOUT_MS bounds the wait of a multi-workgroup trace for its
+ * other workgroups (default 10000 ms, then LAR_E_SYNC); LAR_TEST_SKIP_POST=m:q makes
+ * workgroup m of every scenario skip its post for query q (so the others reach the
+ * bound); LAR_TEST_TAG_START starts the realised-TTFT tag counter at that value (so
+ * a test reaches its wrap).
+ */
 lar_status lar_create(lar_ctx **out, const lar_config *cfg);
 
 /* Free the context (synchronises its stream first).  NULL is accepted. */
