@@ -203,6 +203,29 @@ lar_status lar_commit(lar_ctx *ctx, const int32_t *choice, int32_t q_prefill, in
                       double t_next_ms);
 
 /*
+ * One routing step with every query value in device memory, so that a caller can
+ * capture it once in a HIP graph and replay it per arriving query after writing the
+ * query into the same buffers.  Exactly the call sequence
+ *   lar_estimate_ttft(1 query *q_prefill, t = *t_ms)
+ *   lar_route (tau_ms == NULL) or lar_route_constrained (row of acc / cost)
+ *   lar_commit(choice, *q_prefill, *q_decode, *t_next_ms)
+ * with the values read when the step runs.  The instances must be advanced to *t_ms
+ * (the previous step's *t_next_ms, or lar_commit(NULL, ...) before the first step).
+ * Enqueues four kernels; allocates nothing, does not synchronise.
+ *   q_prefill, q_decode dev [1] int32;  t_ms, t_next_ms dev [1]
+ *   acc, cost dev [n_cols] (this query's row);  w_cost dev [Z]
+ *   w_lat dev [Z] (Lagrangian objective) or tau_ms dev [1] (Eq. 3; w_lat unused)
+ *   choice dev [Z] int32;  chosen_ttft, utility dev [Z] (may be NULL)
+ * Device-found errors (prompt outside 1..max_prompt, queue full, iteration cap) are
+ * sticky as for the separate calls.
+ */
+lar_status lar_route_step(lar_ctx *ctx, const int32_t *q_prefill, const int32_t *q_decode,
+                          const double *t_ms, const double *t_next_ms, const double *acc,
+                          const double *cost, int32_t n_cols, const double *w_cost,
+                          const double *w_lat, const double *tau_ms, int32_t *choice,
+                          double *chosen_ttft, double *utility);
+
+/*
  * Sequential routing of N queries, exactly the call sequence
  *   for i in 0..N-1:
  *     lar_estimate_ttft(1 query q_prefill[i], t = q_t_ms[i])

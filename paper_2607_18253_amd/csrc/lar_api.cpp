@@ -29,7 +29,7 @@ struct lar_ctx {
   // parameters on device
   double* pa = nullptr;   // [5][I]: a, b, c, d, e
   int32_t* pi = nullptr;  // [3][I]: B, M, col
-  double* row_ttft = nullptr;  // [Z][I] scratch of the sequential trace
+  double* row_ttft = nullptr;  // [Z][I] TTFT row of lar_route_step
   uint64_t* xslot = nullptr;   // [Z][2][kMaxCluster][4] candidate posts of the clustered trace
   lar::SyncCtl sync{1000000000ull, -1, -1};   // 10 s wait bound; no post left out
   unsigned long long* work = nullptr;          // [Z] estimate batches of the last trace
@@ -462,6 +462,29 @@ lar_status lar_commit(lar_ctx* ctx, const int32_t* choice, int32_t q_prefill, in
   const LaunchEnv env = env_of(ctx);
   HIP_TRY(ctx, lar::launch_commit(env, choice, 1, nullptr, nullptr, q_prefill, q_decode, nullptr,
                                   t_next_ms));
+  return LAR_OK;
+}
+
+lar_status lar_route_step(lar_ctx* ctx, const int32_t* q_prefill, const int32_t* q_decode,
+                          const double* t_ms, const double* t_next_ms, const double* acc,
+                          const double* cost, int32_t n_cols, const double* w_cost,
+                          const double* w_lat, const double* tau_ms, int32_t* choice,
+                          double* chosen_ttft, double* utility) {
+  lar_status st = ready(ctx);
+  if (st != LAR_OK) return st;
+  if (!q_prefill || !q_decode || !t_ms || !t_next_ms || !acc || !cost || !w_cost || !choice ||
+      (!tau_ms && !w_lat))
+    return fail(ctx, LAR_E_ARG, "null argument");
+  if (n_cols <= ctx->max_col)
+    return fail(ctx, LAR_E_ARG, "n_cols %d does not cover instance column %d", n_cols, ctx->max_col);
+  // the four calls of one routing step, every query value read from device memory
+  const LaunchEnv env = env_of(ctx);
+  HIP_TRY(ctx, lar::launch_traj(env, t_ms, 0.0));
+  HIP_TRY(ctx, lar::launch_est(env, 1, q_prefill, t_ms, 0.0, ctx->row_ttft, nullptr));
+  HIP_TRY(ctx, lar::launch_route(env, 1, ctx->row_ttft, (int64_t)ctx->I, acc, cost, n_cols,
+                                 w_cost, tau_ms ? w_cost : w_lat, tau_ms, choice, chosen_ttft,
+                                 utility, 1, 0));
+  HIP_TRY(ctx, lar::launch_commit(env, choice, 1, q_prefill, q_decode, 0, 0, t_next_ms, 0.0));
   return LAR_OK;
 }
 

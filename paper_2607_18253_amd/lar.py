@@ -20,7 +20,8 @@ FIRST_TOKEN_DECODE_BATCH, FIRST_TOKEN_PREFILL_BATCH = 0, 1
 
 EXPORTED = ("lar_create", "lar_destroy", "lar_error_string", "lar_load_state", "lar_reload_state",
             "lar_estimate_ttft", "lar_route", "lar_route_constrained", "lar_ttft_targets",
-            "lar_commit", "lar_route_trace", "lar_route_trace_constrained", "lar_stats",
+            "lar_commit", "lar_route_step", "lar_route_trace", "lar_route_trace_constrained",
+            "lar_stats",
             "lar_ontime_utility", "lar_read_state", "lar_sync", "lar_trace_work", "lar_board_create",
             "lar_board_destroy", "lar_board_publish", "lar_board_collect")
 
@@ -73,6 +74,8 @@ def load_library(path: str = LIB_PATH):
     L.lar_route.argtypes = [vp, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp]
     L.lar_commit.restype = i32
     L.lar_commit.argtypes = [vp, vp, i32, i32, dbl]
+    L.lar_route_step.restype = i32
+    L.lar_route_step.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, vp]
     L.lar_route_trace.restype = i32
     L.lar_route_trace.argtypes = [vp, i32, vp, vp, vp, dbl, vp, vp, i32, vp, vp, vp, vp, vp, vp]
     L.lar_route_constrained.restype = i32
@@ -263,6 +266,27 @@ class LarContext:
 
     def advance(self, t_ms: float):
         self.commit(None, 1, 1, t_ms)
+
+    def route_step(self, q_prefill, q_decode, t_ms, t_next_ms, acc_row, cost_row, w_cost,
+                   w_lat=None, tau_ms=None, choice=None, chosen_ttft=None, utility=None):
+        """One routing step (estimate, route, commit) with the query's values in device
+        tensors ([1] each; acc_row / cost_row [n_cols]), read when the step runs:
+        capturable in a CUDA/HIP graph and replayed per query."""
+        torch = self._torch
+        n_cols = int(acc_row.numel())
+        if choice is None:
+            choice = torch.empty(self.Z, dtype=torch.int32, device=acc_row.device)
+        self._check(self._L.lar_route_step(
+            self._h, _dev(q_prefill, torch.int32, "q_prefill", 1),
+            _dev(q_decode, torch.int32, "q_decode", 1), _dev(t_ms, torch.float64, "t_ms", 1),
+            _dev(t_next_ms, torch.float64, "t_next_ms", 1),
+            _dev(acc_row, torch.float64, "acc_row", n_cols),
+            _dev(cost_row, torch.float64, "cost_row", n_cols), n_cols,
+            _dev(w_cost, torch.float64, "w_cost", self.Z), _dev(w_lat, torch.float64, "w_lat", self.Z),
+            _dev(tau_ms, torch.float64, "tau_ms", 1), _dev(choice, torch.int32, "choice", self.Z),
+            _dev(chosen_ttft, torch.float64, "chosen_ttft", self.Z),
+            _dev(utility, torch.float64, "utility", self.Z)))
+        return choice
 
     def route_trace(self, q_prefill, q_decode, q_t_ms, t_after_ms, acc, cost, w_cost, w_lat,
                     choice=None, chosen_ttft=None, utility=None, realized=None):

@@ -53,7 +53,7 @@ def test_null_arguments_rejected_without_gpu():
     for name, n_args in (("lar_route", 11), ("lar_route_constrained", 11),
                          ("lar_ttft_targets", 6), ("lar_route_trace_constrained", 15),
                          ("lar_route_trace", 15), ("lar_ontime_utility", 10), ("lar_stats", 9),
-                         ("lar_reload_state", 1)):
+                         ("lar_reload_state", 1), ("lar_route_step", 14)):
         f = getattr(lib, name)
         f.restype = ctypes.c_int32
         args = [None] * n_args
@@ -63,6 +63,9 @@ def test_null_arguments_rejected_without_gpu():
                          [ctypes.c_int32] + [ctypes.c_void_p] * 5
             args = [None, 1, None, None, None, 0.0, None, None, None, 1, None, None, None, None,
                     None]
+        if name == "lar_route_step":
+            f.argtypes = [ctypes.c_void_p] * 7 + [ctypes.c_int32] + [ctypes.c_void_p] * 6
+            args = [None] * 7 + [1] + [None] * 6
         if name == "lar_route_trace":
             f.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                           ctypes.c_void_p, ctypes.c_double] + [ctypes.c_void_p] * 2 + \
