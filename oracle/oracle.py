@@ -99,7 +99,12 @@ def lib():
                             C.c_double, C.c_double, _opt(_f64p), C.c_int32, C.c_int64, C.c_int64,
                             _i32p, _opt(_f64p), _opt(_f64p), _opt(_f64p), _opt(_i32p),
                             _opt(_i32p), _opt(_i32p), _opt(_i32p), _opt(_i32p), _opt(_f64p),
-                            _opt(_i64p), C.c_int64, _opt(_f64p), C.POINTER(C.c_int32)]
+                            _opt(_i64p), C.c_int64, _opt(_f64p), _opt(_i32p),
+                            C.POINTER(C.c_int32)]
+    L.orc_queue_preemptions.restype = C.c_int64
+    L.orc_queue_preemptions.argtypes = [C.c_void_p]
+    L.orc_queue_set_sched.restype = C.c_int
+    L.orc_queue_set_sched.argtypes = [C.c_void_p, _i32p]
     L.orc_route_row_constrained.restype = C.c_int32
     L.orc_route_row_constrained.argtypes = [C.c_int32, _f64p, C.c_double, _f64p, _f64p, _i32p,
                                             C.c_double]
@@ -132,7 +137,7 @@ def _i32(x):
 class Queue:
     """One instance's resident list with its clock (the oracle's state)."""
 
-    def __init__(self, params: Params, rp, rd, cx, clock=0.0):
+    def __init__(self, params: Params, rp, rd, cx, clock=0.0, sched=None):
         self._L = lib()
         st = C.c_int(0)
         rp, rd, cx = _i32(rp), _i32(rd), _i32(cx)
@@ -141,6 +146,14 @@ class Queue:
                                         C.byref(st))
         if st.value != OK:
             raise OracleError(st.value, "queue_new")
+        if sched is not None:
+            self.set_sched(sched)
+
+    def set_sched(self, sched):
+        """Scheduler limits (chunk_cap, kv_blocks, block_size, max_ctx); 0 = none."""
+        st = self._L.orc_queue_set_sched(self._q, _i32(sched))
+        if st != OK:
+            raise OracleError(st, "set_sched")
 
     def __del__(self):
         q = getattr(self, "_q", None)
@@ -150,6 +163,10 @@ class Queue:
 
     def size(self) -> int:
         return int(self._L.orc_queue_size(self._q))
+
+    def preemptions(self) -> int:
+        """Requests preempted since the queue was created (its clones start at 0)."""
+        return int(self._L.orc_queue_preemptions(self._q))
 
     def waiting(self) -> int:
         return int(self._L.orc_queue_waiting(self._q))
@@ -251,7 +268,8 @@ def trace(wl, scenario: int = 0, *, n_q: int | None = None, reading=READING_DECO
           tau=None) -> TraceResult:
     """Sequential routing trace of one scenario of workload ``wl`` (first n_q queries);
     Lagrangian route, or the constrained route of Eq. 3 when per-query targets
-    ``tau`` (ms) are given."""
+    ``tau`` (ms) are given.  The workload's scheduler limits (``wl.sched``, [I][4])
+    apply when set."""
     L = lib()
     I = wl.n_inst
     N = wl.n_q if n_q is None else int(n_q)
@@ -285,7 +303,7 @@ def trace(wl, scenario: int = 0, *, n_q: int | None = None, reading=READING_DECO
                      int(reading),
                      int(max_iters), cap, choice, ttft_c, util_c, ttft_all, iters_all,
                      out_off, out_rp, out_rd, out_cx, out_clock, out_iters, out_cap,
-                     realized, C.byref(failed))
+                     realized, sched_of(wl), C.byref(failed))
     if st != OK:
         raise OracleError(st, f"trace (query {failed.value})")
     if final_state:
@@ -308,9 +326,17 @@ def stats(choice, ttft_chosen, acc, cost, col, w_cost):
     return out
 
 
+def sched_of(wl):
+    """The workload's scheduler limits as a flat int32 [I*4] array, or None."""
+    sc = getattr(wl, "sched", None)
+    return None if sc is None else _i32(np.asarray(sc).reshape(-1))
+
+
 def instance_queue(wl, j) -> Queue:
     rp, rd, cx = wl.instance_requests(j)
-    return Queue(params_of(wl, j), rp, rd, cx, wl.clock_ms[j])
+    sc = getattr(wl, "sched", None)
+    return Queue(params_of(wl, j), rp, rd, cx, wl.clock_ms[j],
+                 sched=None if sc is None else np.asarray(sc)[j])
 
 
 def estimate_matrix(wl, queries, instances, t_ms=0.0, reading=READING_DECODE_BATCH,

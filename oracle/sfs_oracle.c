@@ -68,6 +68,29 @@
  *   * OnTimeUtility (Eq. 4): (1/N) * sum over queries, in query order, of the
  *     utility at the chosen instance when its realised TTFT is within the target,
  *     else 0.
+ *
+ *   * Scheduler limits (appendix on the system: the simulation follows the
+ *     engine's context limits, KV-cache allocation and preemption; Sec. 2 on paged
+ *     KV caches and chunked prefill).  The paper names them without defining them;
+ *     the reading taken here, per instance and each optional:
+ *       - chunk cap H: a request receives at most H prefill tokens per batch;
+ *       - context limit X: a request's context (prompt plus generated tokens) never
+ *         exceeds X, so its remaining decode is at most X - (cx + rp); a request
+ *         needs cx + rp < X;
+ *       - KV cache of K blocks of S tokens: a running request holds
+ *         ceil(cx / S) blocks, and a batch that gives it n more tokens needs
+ *         ceil((cx + n) / S) of them.  Requires X > 0 and K*S >= X.
+ *     With limits set, a batch serves the running requests in list order, first
+ *     one decode token to each decoding one, then a chunk min(rp, H, budget left)
+ *     to each partially prefilled one.  When a request's blocks do not fit, the
+ *     last running request is preempted, repeatedly, until they fit: it frees its
+ *     blocks (with any taken in this batch), loses the tokens given to it in this
+ *     batch, and becomes the first waiting request with its whole context to
+ *     prefill again (recompute).  A request that preempts itself gets nothing.
+ *     Only in a batch without preemption are waiting requests admitted, in FCFS
+ *     order, each while budget is left, fewer than M run and the blocks of its
+ *     first chunk fit; the first that cannot be admitted stops the admissions.
+ *     With no limit set this is the batch described above.
  */
 #include <math.h>
 #include <stdint.h>
@@ -93,6 +116,7 @@ typedef struct {
   int32_t *rp, *rd, *cx;
   int32_t *qid;     /* routed query still waiting for its first token, else -1 */
   int32_t *dec, *chunk; /* tokens of the batch being built, per request */
+  int32_t *blk;         /* KV blocks taken in the batch being built, per request */
   double clock;
   int64_t iters;    /* batches run by advance() since creation */
   /* first-token tracking of the replay (realised == NULL: off) */
@@ -100,6 +124,13 @@ typedef struct {
   const double *q_t;    /* [N] arrival times */
   int32_t reading;
   int64_t tracked;      /* residents with qid >= 0 */
+  /* scheduler limits (has_sched == 0: none, the default batch) */
+  int has_sched;
+  int32_t chunk_cap;    /* H, 0 = none */
+  int32_t kv_blocks;    /* K, 0 = unlimited */
+  int32_t block_size;   /* S */
+  int32_t max_ctx;      /* X, 0 = none */
+  int64_t preemptions;  /* requests preempted since creation */
 } orc_queue;
 
 typedef struct {
@@ -112,8 +143,8 @@ static int q_reserve(orc_queue *q, int64_t need) {
   if (need <= q->alloc) return ORC_OK;
   int64_t cap = q->alloc ? q->alloc : 16;
   while (cap < need) cap *= 2;
-  int32_t **arrs[6] = {&q->rp, &q->rd, &q->cx, &q->qid, &q->dec, &q->chunk};
-  for (int k = 0; k < 6; ++k) {
+  int32_t **arrs[7] = {&q->rp, &q->rd, &q->cx, &q->qid, &q->dec, &q->chunk, &q->blk};
+  for (int k = 0; k < 7; ++k) {
     int32_t *p = (int32_t *)realloc(*arrs[k], (size_t)cap * sizeof(int32_t));
     if (!p) return ORC_E_ARG;
     *arrs[k] = p;
@@ -166,6 +197,7 @@ orc_queue *orc_queue_new(const orc_params *pr, int64_t n, const int32_t *rp,
 void orc_queue_free(orc_queue *q) {
   if (!q) return;
   free(q->rp); free(q->rd); free(q->cx); free(q->qid); free(q->dec); free(q->chunk);
+  free(q->blk);
   free(q);
 }
 
@@ -179,10 +211,48 @@ static orc_queue *q_clone(const orc_queue *src) {
   q->q_t = src->q_t;
   q->reading = src->reading;
   q->tracked = src->tracked;
+  q->has_sched = src->has_sched;
+  q->chunk_cap = src->chunk_cap;
+  q->kv_blocks = src->kv_blocks;
+  q->block_size = src->block_size;
+  q->max_ctx = src->max_ctx;
   return q;
 }
 
+/* KV blocks that hold `tokens` cached tokens. */
+static int64_t blocks_for(const orc_queue *q, int64_t tokens) {
+  return (tokens + q->block_size - 1) / q->block_size;
+}
+
+/* Put the scheduler limits (chunk_cap, kv_blocks, block_size, max_ctx; see the
+   header) on a queue.  The residents must fit them: cx + rp < max_ctx for each, and
+   the running ones' blocks within kv_blocks.  Each resident's remaining decode is
+   cut to what the context limit leaves. */
+int orc_queue_set_sched(orc_queue *q, const int32_t *lim4) {
+  const int32_t H = lim4[0], K = lim4[1], S = lim4[2], X = lim4[3];
+  if (H < 0 || K < 0 || X < 0) return ORC_E_ARG;
+  if (K > 0 && (S < 1 || X < 1 || (int64_t)K * S < X)) return ORC_E_ARG;
+  q->has_sched = 1;
+  q->chunk_cap = H;
+  q->kv_blocks = K;
+  q->block_size = K > 0 ? S : 1;
+  q->max_ctx = X;
+  int64_t held = 0;
+  for (int64_t r = 0; r < q->n; ++r) {
+    const int64_t total = (int64_t)q->cx[r] + q->rp[r];
+    if (X > 0) {
+      if (total >= X) return ORC_E_STATE;
+      if (q->rd[r] > X - total) q->rd[r] = (int32_t)(X - total);
+    }
+    if (q->cx[r] > 0) held += blocks_for(q, q->cx[r]);
+  }
+  if (K > 0 && held > K) return ORC_E_STATE;
+  return ORC_OK;
+}
+
 int64_t orc_queue_size(const orc_queue *q) { return q->n; }
+
+int64_t orc_queue_preemptions(const orc_queue *q) { return q->preemptions; }
 
 int64_t orc_queue_waiting(const orc_queue *q) {
   int64_t w = 0;
@@ -200,8 +270,104 @@ void orc_queue_get(const orc_queue *q, int32_t *rp, int32_t *rd, int32_t *cx, do
 
 /* ---------------------------------------------------------------- one batch */
 
+static orc_feat features(const orc_queue *q) {
+  orc_feat f = {0, 0, 0, 0};
+  for (int64_t r = 0; r < q->n; ++r) {
+    int64_t ch = q->chunk[r];
+    f.P += ch;
+    f.D += q->dec[r];
+    f.C += (int64_t)q->dec[r] * q->cx[r];
+    f.A += ch * (int64_t)q->cx[r] + ch * (ch + 1) / 2;
+  }
+  return f;
+}
+
+/* Preempt the last running request (index *running - 1): its blocks, with those
+   taken in this batch, return to the pool, the tokens given to it in this batch
+   return to the budget, and it becomes the first waiting request, to prefill its
+   whole context again. */
+static void preempt_last(orc_queue *q, int64_t *running, int64_t *left, int64_t *free_blk) {
+  const int64_t v = *running - 1;
+  *free_blk += blocks_for(q, q->cx[v]) + q->blk[v];
+  *left += q->dec[v] + q->chunk[v];
+  q->dec[v] = 0;
+  q->chunk[v] = 0;
+  q->blk[v] = 0;
+  q->rp[v] += q->cx[v];
+  q->cx[v] = 0;
+  *running = v;
+  q->preemptions += 1;
+}
+
+/* The batch under scheduler limits (see the header). */
+static orc_feat compose_sched(orc_queue *q) {
+  const int64_t n = q->n;
+  const int kv = q->kv_blocks > 0;
+  const int64_t cap = q->chunk_cap > 0 ? q->chunk_cap : INT64_MAX;
+  int64_t left = q->pr.budget, running = 0, free_blk = q->kv_blocks;
+  int preempted = 0;
+  for (int64_t r = 0; r < n; ++r) {
+    q->dec[r] = 0;
+    q->chunk[r] = 0;
+    q->blk[r] = 0;
+    if (q->cx[r] > 0) {
+      ++running;
+      if (kv) free_blk -= blocks_for(q, q->cx[r]);
+    }
+  }
+  /* running requests in list order: decode tokens first */
+  for (int64_t r = 0; r < running; ++r) {
+    if (q->rp[r] != 0) continue;
+    const int64_t need = kv ? blocks_for(q, q->cx[r] + 1) - blocks_for(q, q->cx[r]) : 0;
+    while (free_blk < need && r < running) {   /* until it fits, or r itself is out */
+      preempt_last(q, &running, &left, &free_blk);
+      preempted = 1;
+    }
+    if (r >= running) break;
+    q->dec[r] = 1;
+    q->blk[r] = (int32_t)need;
+    free_blk -= need;
+    left -= 1;
+  }
+  /* then prefill chunks of the partially prefilled ones */
+  for (int64_t r = 0; r < running; ++r) {
+    if (q->rp[r] == 0) continue;
+    int64_t g = q->rp[r] < cap ? q->rp[r] : cap;
+    if (left < g) g = left;
+    if (g == 0) continue;
+    const int64_t need = kv ? blocks_for(q, q->cx[r] + g) - blocks_for(q, q->cx[r]) : 0;
+    while (free_blk < need && r < running) {   /* until it fits, or r itself is out */
+      preempt_last(q, &running, &left, &free_blk);
+      preempted = 1;
+    }
+    if (r >= running) break;
+    q->chunk[r] = (int32_t)g;
+    q->blk[r] = (int32_t)need;
+    free_blk -= need;
+    left -= g;
+  }
+  /* admissions, FCFS, in a batch without preemption */
+  if (!preempted) {
+    const int64_t first_waiting = running;
+    for (int64_t r = first_waiting; r < n; ++r) {
+      if (left == 0 || running == q->pr.max_seqs) break;
+      int64_t g = q->rp[r] < cap ? q->rp[r] : cap;
+      if (left < g) g = left;
+      const int64_t need = kv ? blocks_for(q, g) : 0;
+      if (need > free_blk) break;
+      q->chunk[r] = (int32_t)g;
+      q->blk[r] = (int32_t)need;
+      free_blk -= need;
+      left -= g;
+      running += 1;
+    }
+  }
+  return features(q);
+}
+
 /* Build the next token batch: dec[r] in {0,1}, chunk[r] >= 0; return its features. */
 static orc_feat compose(orc_queue *q) {
+  if (q->has_sched) return compose_sched(q);
   const int64_t n = q->n;
   int64_t left = q->pr.budget;
   int64_t running = 0;
@@ -229,15 +395,7 @@ static orc_feat compose(orc_queue *q) {
     q->chunk[r] = (int32_t)ch;
     left -= ch;
   }
-  orc_feat f = {0, 0, 0, 0};
-  for (int64_t r = 0; r < n; ++r) {
-    int64_t ch = q->chunk[r];
-    f.P += ch;
-    f.D += q->dec[r];
-    f.C += (int64_t)q->dec[r] * q->cx[r];
-    f.A += ch * (int64_t)q->cx[r] + ch * (ch + 1) / 2;
-  }
-  return f;
+  return features(q);
 }
 
 static double batch_time(const orc_params *pr, orc_feat f) {
@@ -313,12 +471,23 @@ int orc_queue_advance(orc_queue *q, double t, int64_t max_iters) {
 
 /* Append a routed query as a waiting request; query index i >= 0 is tracked
    until its first token (when tracking is on), i = -1 is not. */
+/* Predicted decode of a new request of p prompt tokens: at least 1, and no more
+   than the context limit leaves (0 when p does not fit the limit). */
+static int32_t decode_of(const orc_queue *q, int32_t p, int32_t dhat) {
+  int32_t d = dhat < 1 ? 1 : dhat;
+  if (q->has_sched && q->max_ctx > 0) {
+    if (p >= q->max_ctx) return 0;
+    if (d > q->max_ctx - p) d = q->max_ctx - p;
+  }
+  return d;
+}
+
 static int append_tagged(orc_queue *q, int32_t p, int32_t dhat, int64_t queue_cap, int32_t i) {
-  if (p < 1) return ORC_E_ARG;
+  if (p < 1 || decode_of(q, p, dhat) < 1) return ORC_E_ARG;
   if (orc_queue_waiting(q) + 1 > queue_cap) return ORC_E_CAPACITY;
   if (q_reserve(q, q->n + 2) != ORC_OK) return ORC_E_ARG;
   q->rp[q->n] = p;
-  q->rd[q->n] = dhat < 1 ? 1 : dhat;
+  q->rd[q->n] = decode_of(q, p, dhat);
   q->cx[q->n] = 0;
   q->qid[q->n] = q->realized ? i : -1;
   if (q->realized && i >= 0) q->tracked += 1;
@@ -334,12 +503,12 @@ int orc_queue_append(orc_queue *q, int32_t p, int32_t dhat, int64_t queue_cap) {
    already be advanced to t).  Pure: the queue is not modified. */
 int orc_queue_estimate(const orc_queue *q, int32_t p, int32_t dhat, double t, int32_t reading,
                        int64_t max_iters, double *ttft, int32_t *iters) {
-  if (p < 1) return ORC_E_ARG;
+  if (p < 1 || decode_of(q, p, dhat) < 1) return ORC_E_ARG;
   if (q->clock < t) return ORC_E_STATE;
   orc_queue *w = q_clone(q);
   if (!w) return ORC_E_ARG;
   w->rp[w->n] = p;
-  w->rd[w->n] = dhat < 1 ? 1 : dhat;
+  w->rd[w->n] = decode_of(q, p, dhat);
   w->cx[w->n] = 0;
   w->n += 1;
   double E = w->clock;
@@ -429,6 +598,7 @@ void orc_ttft_targets(int32_t n, const int32_t *p, const double *u_ms, const dou
  * The final state is written to the out_* arrays when out_offsets != NULL (each
  * out array must hold out_cap entries).  realized [N] (may be NULL) receives the
  * realised TTFT of every query (NaN where an error stopped the trace first).
+ * sched [n_inst][4] (may be NULL) puts scheduler limits on every instance.
  */
 int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
               const int32_t *offsets, const int32_t *rp, const int32_t *rd, const int32_t *cx,
@@ -439,7 +609,8 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
               double *util_chosen,
               double *ttft_all, int32_t *iters_all, int32_t *out_offsets, int32_t *out_rp,
               int32_t *out_rd, int32_t *out_cx, double *out_clock, int64_t *out_iters,
-              int64_t out_cap, double *realized, int32_t *failed_query) {
+              int64_t out_cap, double *realized, const int32_t *sched,
+              int32_t *failed_query) {
   int st = ORC_OK;
   *failed_query = -1;
   if (n_inst < 1 || n_q < 0 || n_cols < 1) return ORC_E_ARG;
@@ -451,6 +622,7 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
   for (int32_t j = 0; j < n_inst && st == ORC_OK; ++j) {
     int64_t lo = offsets[j], hi = offsets[j + 1];
     qs[j] = orc_queue_new(&params[j], hi - lo, rp + lo, rd + lo, cx + lo, clock[j], &st);
+    if (st == ORC_OK && sched) st = orc_queue_set_sched(qs[j], sched + 4 * (int64_t)j);
     if (st == ORC_OK && orc_queue_waiting(qs[j]) > queue_cap) st = ORC_E_CAPACITY;
     if (st == ORC_OK && realized) {
       qs[j]->realized = realized;

@@ -1,0 +1,229 @@
+"""Pins of the oracle's scheduler limits (chunk cap, context limit, KV-cache blocks
+with recompute preemption), taken from the system appendix's list of what the SFS
+simulation follows and Sec. 2 on paged KV caches and chunked prefill.
+
+* hand-worked cases (tests/golden/sched_hand_worked.json);
+* reduction: limits that are off, or that never bind, give the pinned default batch
+  bit for bit;
+* an independent token-at-a-time scheduler with numbered KV blocks and separate
+  running / waiting lists (tests/bruteforce_sched.py) on random tiny traces, both
+  readings and both objectives, with realised TTFT;
+* invariants after every batch; error paths.
+"""
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from workloads import make_tiny_workload
+from workloads.gen import make_tiny_sched_workload, make_workload
+import bruteforce_sched as BF
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden", "sched_hand_worked.json")
+
+
+def _lim(d):
+    return [d["chunk_cap"], d["kv_blocks"], d["block_size"], d["max_ctx"]]
+
+
+def _queue(coef, B, M, reqs, lim):
+    return O.Queue(O.make_params(coef["a"], coef["b"], coef["c"], coef["d"], coef["e"], B, M),
+                   [r[0] for r in reqs], [r[1] for r in reqs], [r[2] for r in reqs], 0.0,
+                   sched=lim)
+
+
+def bits(x):
+    return np.ascontiguousarray(x, dtype=np.float64).view(np.int64)
+
+
+# ------------------------------------------------------------------ hand-worked
+def test_sched_hand_worked():
+    g = json.load(open(GOLD))
+    for case in g["cases"]:
+        lim = _lim(case["limits"])
+        q = _queue(g["coef"], case["budget"], case["max_seqs"], case["requests"], lim)
+        tb, ib = q.estimate(case["p"], case["dhat"], case["t"], O.READING_DECODE_BATCH)
+        ta, ia = q.estimate(case["p"], case["dhat"], case["t"], O.READING_PREFILL_BATCH)
+        assert (tb, ib) == (case["ttft_B"], case["iters_B"]), case["name"]
+        assert (ta, ia) == (case["ttft_A"], case["iters_A"]), case["name"]
+        # the same through a replay: append the query, step to its first decode
+        q.append(case["p"], case["dhat"])
+        clk = 0.0
+        for _ in range(case["iters_B"]):
+            T, _f = q.step()
+            clk = clk + T
+        assert clk == case["ttft_B"], case["name"]
+        assert q.preemptions() == case["preemptions_B"], case["name"]
+        # and the brute force agrees
+        c = g["coef"]
+        bf = BF.BFSchedInstance(c["a"], c["b"], c["c"], c["d"], c["e"], case["budget"],
+                                case["max_seqs"], lim, *zip(*case["requests"])
+                                if case["requests"] else ((), (), ()))
+        assert bf.estimate(case["p"], case["dhat"], case["t"], 0) == (tb, ib), case["name"]
+        assert bf.estimate(case["p"], case["dhat"], case["t"], 1) == (ta, ia), case["name"]
+
+
+def test_sched_hand_worked_batches():
+    g = json.load(open(GOLD))
+    c = g["coef"]
+    for case in g["batch_cases"]:
+        lim = _lim(case["limits"])
+        q = _queue(c, case["budget"], case["max_seqs"], case["requests"], lim)
+        _, f = q.step()
+        rp, rd, cx, _, _ = q.state()
+        assert list(f) == case["features"], case["name"]
+        assert [list(x) for x in zip(rp, rd, cx)] == case["after"], case["name"]
+        assert q.preemptions() == case["preemptions"], case["name"]
+        bf = BF.BFSchedInstance(c["a"], c["b"], c["c"], c["d"], c["e"], case["budget"],
+                                case["max_seqs"], lim, *zip(*case["requests"]))
+        _, fb, _ = bf.batch()
+        assert list(fb) == case["features"], case["name"]
+        assert [list(x) for x in bf.state()] == case["after"], case["name"]
+
+
+def test_context_limit_cuts_resident_decode():
+    g = json.load(open(GOLD))
+    case = g["cases"][1]
+    q = _queue(g["coef"], case["budget"], case["max_seqs"], case["requests"],
+               _lim(case["limits"]))
+    rp, rd, cx, _, _ = q.state()
+    assert list(rd) == [3]           # 100 predicted decodes cut to 13 - 10
+
+
+# ------------------------------------------------------------------ reduction
+def _trace_pair(wl, **kw):
+    r0 = O.trace(wl, full_rows=True, **kw)
+    return r0
+
+
+def _same(r1, r2):
+    np.testing.assert_array_equal(r1.choice, r2.choice)
+    np.testing.assert_array_equal(bits(r1.ttft_all), bits(r2.ttft_all))
+    np.testing.assert_array_equal(r1.iters_all, r2.iters_all)
+    np.testing.assert_array_equal(bits(r1.realized), bits(r2.realized))
+    for f in ("offsets", "rem_prefill", "rem_decode", "context", "iterations"):
+        np.testing.assert_array_equal(getattr(r1, f), getattr(r2, f))
+    np.testing.assert_array_equal(bits(r1.clock_ms), bits(r2.clock_ms))
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_limits_off_or_slack_reduce_to_default(seed):
+    """No limit set, or limits that cannot bind (chunk cap >= budget, a KV cache and a
+    context limit larger than anything the trace reaches), give the default batch."""
+    wl = make_tiny_workload(seed, n_q=30)
+    reading = seed % 2
+    base = O.trace(wl, full_rows=True, reading=reading)
+    wl.sched = np.zeros((wl.n_inst, 4), np.int32)
+    _same(base, O.trace(wl, full_rows=True, reading=reading))
+    big = 1 << 20
+    wl.sched = np.array([[int(wl.budget[j]), big, 4, big] for j in range(wl.n_inst)], np.int32)
+    _same(base, O.trace(wl, full_rows=True, reading=reading))
+
+
+# ------------------------------------------------------------------ brute force
+@pytest.mark.parametrize("seed", range(40))
+def test_sched_bruteforce_traces(seed):
+    wl = make_tiny_sched_workload(seed, n_q=25, max_res=5)
+    reading = seed % 2
+    tau = None
+    if seed % 4 >= 2:      # Eq. 3 with targets inside the estimates' range
+        rng = np.random.default_rng(seed)
+        tau = rng.uniform(0.0, 40.0, size=wl.n_q)
+    real_bf = np.zeros(wl.n_q)
+    ch, rows, insts = BF.trace(wl, reading=reading, tau=tau, realized=real_bf)
+    r = O.trace(wl, full_rows=True, reading=reading, tau=tau)
+    np.testing.assert_array_equal(r.choice, ch)
+    np.testing.assert_array_equal(bits(r.ttft_all), bits(rows))
+    np.testing.assert_array_equal(bits(r.realized), bits(real_bf))
+    for j, x in enumerate(insts):
+        lo, hi = r.offsets[j], r.offsets[j + 1]
+        got = list(zip(r.rem_prefill[lo:hi], r.rem_decode[lo:hi], r.context[lo:hi]))
+        assert got == x.state(), (seed, j)
+        assert r.clock_ms[j] == x.clock
+
+
+def test_sched_bruteforce_exercises_every_limit():
+    """The random tiny traces above preempt, cut chunks and end decodes at the
+    context limit (counted on the brute force's side)."""
+    pre = cut = 0
+    for seed in range(40):
+        wl = make_tiny_sched_workload(seed, n_q=25, max_res=5)
+        _, _, insts = BF.trace(wl, reading=seed % 2)
+        pre += sum(x.preemptions for x in insts)
+        for j in range(wl.n_inst):
+            H, K, S, X = wl.sched[j]
+            rp, rd, cx = wl.instance_requests(j)
+            cut += int(np.sum(rd > X - (cx + rp)))
+    assert pre >= 50 and cut >= 5, (pre, cut)
+
+
+# ------------------------------------------------------------------ invariants
+@pytest.mark.parametrize("seed", range(10))
+def test_sched_invariants(seed):
+    wl = make_tiny_sched_workload(seed, n_q=1, max_res=6)
+    for j in range(wl.n_inst):
+        H, K, S, X = (int(v) for v in wl.sched[j])
+        q = O.instance_queue(wl, j)
+        for p in range(1, 9):
+            q.append(p, 3)
+        for _ in range(60):
+            if q.size() == 0:
+                break
+            rp0, _, cx0, _, _ = q.state()
+            T, (P, D, C, A) = q.step()
+            rp, rd, cx, _, _ = q.state()
+            running = cx > 0
+            assert running.sum() <= wl.max_seqs[j]
+            assert P + D <= wl.budget[j]
+            if K > 0:
+                assert sum(-(-int(c) // S) for c in cx[running]) <= K
+            if X > 0:
+                assert np.all(cx + rp <= X) and np.all(rd <= X - (cx + rp))
+            if H > 0:
+                # no request's prefill shrinks by more than the cap in one batch
+                n = min(len(rp0), len(rp))
+                assert np.all(np.maximum(rp0[:n] - rp[:n], 0) <= H) or len(rp0) != len(rp)
+
+
+# ------------------------------------------------------------------ errors
+def test_sched_errors():
+    pr = O.make_params(1, 1, 1, 0, 0, 8, 4)
+    with pytest.raises(O.OracleError) as e:
+        O.Queue(pr, [0], [3], [5], sched=[0, 4, 2, 0])      # KV cache without a context limit
+    assert e.value.code == O.E_ARG
+    with pytest.raises(O.OracleError) as e:
+        O.Queue(pr, [0], [3], [5], sched=[0, 2, 2, 6])      # 2 blocks of 2 < limit 6
+    assert e.value.code == O.E_ARG
+    with pytest.raises(O.OracleError) as e:
+        O.Queue(pr, [0], [3], [6], sched=[0, 0, 1, 6])      # context at the limit
+    assert e.value.code == O.E_STATE
+    with pytest.raises(O.OracleError) as e:
+        O.Queue(pr, [0, 0], [3, 3], [5, 5], sched=[0, 5, 2, 8])   # 6 blocks held > 5
+    assert e.value.code == O.E_STATE
+    q = O.Queue(pr, [], [], [], sched=[0, 0, 1, 6])
+    with pytest.raises(O.OracleError) as e:
+        q.append(6, 1)                                      # no room for a decode
+    assert e.value.code == O.E_ARG
+    with pytest.raises(O.OracleError):
+        q.estimate(6, 1, 0.0)
+
+
+def test_c7_limits_bind():
+    """The c7 pool: its residents fit the limits, and routing its first queries makes
+    the KV cache preempt (counted by the oracle)."""
+    wl = make_workload("c7", n_q=300)
+    qs = [O.instance_queue(wl, j) for j in range(wl.n_inst)]
+    for q in qs:
+        q.advance(float(wl.q_t_ms[0]))
+    for i in range(wl.n_q):
+        p, d, t = int(wl.q_prefill[i]), int(wl.q_decode[i]), float(wl.q_t_ms[i])
+        row = np.array([q.estimate(p, d, t)[0] for q in qs])
+        u = (wl.acc[i][wl.col] - wl.w_cost[0] * wl.cost[i][wl.col]) - wl.w_lat_ms[0] * row
+        qs[int(np.argmax(u))].append(p, d)
+        t_next = float(wl.q_t_ms[i + 1]) if i + 1 < wl.n_q else t
+        for q in qs:
+            q.advance(t_next)
+    assert sum(q.preemptions() for q in qs) > 0

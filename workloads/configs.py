@@ -1,4 +1,4 @@
-"""The five synthetic workloads, with every constant pinned.
+"""The synthetic workloads, with every constant pinned.
 
 Each entry fixes the instance pool (model types and their batch-time
 coefficients, token budget B, sequence cap M), the initial resident queue depth R,
@@ -101,6 +101,26 @@ CONFIGS = {
         acc="per_type", cost="tokens_x_price",
         weights=[(0.5, 1.0)],
         queue_cap=8192, max_prompt=32768, seed=0,
+    ),
+    "c7": dict(
+        title="medium pool under KV-cache, chunk and context limits",
+        n_inst=32, n_scen=1,
+        types=_scaled_types(),
+        type_of_inst=[j // 8 for j in range(32)],
+        budget=4096, max_seqs=256, resident=256,
+        # prompts clipped so that every resident (prompt + up to 255 decoded tokens)
+        # is below the context limit
+        prompt=("lognormal", 6.5, 1.0, 16, 7936), decode_mean=384,
+        n_q=100_000, rate_per_s=50.0,
+        # scheduler limits of a paged-KV engine (Sec. 2; appendix on the system):
+        # 512-token prefill chunks per request, 16-token KV blocks, 8192-token context
+        # limit, 18432 blocks (294,912 tokens) per instance: the residents hold
+        # 9.7k-11.8k blocks at the start, so admissions and preemptions are bound by
+        # the KV cache until the initial backlog drains
+        sched=dict(chunk_cap=512, kv_blocks=18432, block_size=16, max_ctx=8192),
+        acc="per_type", cost="tokens_x_price",
+        weights=[(0.5, 1.0)],
+        queue_cap=8192, max_prompt=7936, seed=0,
     ),
     "c5": dict(
         title="utility-weight sweep",

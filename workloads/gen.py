@@ -70,6 +70,9 @@ class Workload:
     queue_cap: int
     max_prompt: int
     meta: dict = field(default_factory=dict)
+    # scheduler limits per instance, int32 [I][4]: chunk cap, KV blocks, block size,
+    # context limit (0 = none); None: the default batch with no limits
+    sched: np.ndarray | None = None
 
     @property
     def n_q(self) -> int:
@@ -226,6 +229,11 @@ def _build(cfg: dict) -> Workload:
 
     w = np.asarray(cfg["weights"], np.float64).reshape(-1, 2)
     tau_u, tau_v = _draw_target_vars(cfg["seed"], N)
+    sched = None
+    if cfg.get("sched") is not None:
+        lim = cfg["sched"]
+        sched = np.tile(np.array([lim["chunk_cap"], lim["kv_blocks"], lim["block_size"],
+                                  lim["max_ctx"]], np.int32), (I, 1))
     return Workload(
         name=cfg["name"], n_scen=int(w.shape[0]), n_inst=I,
         a=np.array([types[t]["a"] for t in tof]), b=np.array([types[t]["b"] for t in tof]),
@@ -243,7 +251,7 @@ def _build(cfg: dict) -> Workload:
         w_cost=np.ascontiguousarray(w[:, 0]), w_lat_ms=np.ascontiguousarray(w[:, 1] / 1000.0),
         tau_u_ms=tau_u, tau_v=tau_v,
         queue_cap=int(cfg["queue_cap"]), max_prompt=int(cfg["max_prompt"]),
-        meta=cfg,
+        meta=cfg, sched=sched,
     )
 
 
@@ -316,3 +324,28 @@ def make_tiny_workload(seed: int, *, n_inst: int = 3, max_res: int = 4, budget=(
         queue_cap=max_res + n_q + 1, max_prompt=int(prompt[1]),
         meta=dict(kind="tiny", seed=seed),
     )
+
+
+def make_tiny_sched_workload(seed: int, **kw) -> Workload:
+    """A tiny random pool (as ``make_tiny_workload``) with random scheduler limits that
+    its residents fit: a chunk cap (or none), a context limit a little above the
+    longest resident or query, and (mostly) a KV cache of power-of-two blocks only a
+    little larger than one request can need, so that preemption is frequent."""
+    wl = make_tiny_workload(seed, **kw)
+    rng = np.random.default_rng([int(seed), 7])
+    I = wl.n_inst
+    sched = np.zeros((I, 4), np.int32)
+    for j in range(I):
+        rp, rd, cx = wl.instance_requests(j)
+        longest = int((rp + cx).max()) if len(rp) else 0
+        X = max(longest + 1, wl.max_prompt + 1) + int(rng.integers(0, 6))
+        S = int(rng.choice([1, 2, 4]))
+        held = int(sum(-(-int(c) // S) for c in cx if c > 0))
+        K = 0
+        if rng.random() < 0.8:
+            K = max(-(-X // S), held) + int(rng.integers(0, 4))
+        H = 0 if rng.random() < 0.3 else int(rng.integers(1, 6))
+        sched[j] = (H, K, S, X)
+    wl.sched = sched
+    wl.name = f"tinysched{seed}"
+    return wl
