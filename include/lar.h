@@ -126,6 +126,47 @@ lar_status lar_load_state(lar_ctx *ctx, const lar_instance_params *params,
                           const double *clock_ms);
 
 /*
+ * Scheduler limits of an instance (the system appendix lists context limits,
+ * KV-cache allocation and preemption among what the SFS simulation follows; Sec. 2
+ * describes paged KV caches and chunked prefill).  Each is optional (0 = none):
+ *   chunk_cap   a request receives at most this many prefill tokens per batch;
+ *   max_ctx     context limit: a request's context (prompt + generated tokens) never
+ *               exceeds it.  A request entering with cx + rp tokens has its predicted
+ *               decode cut to max_ctx - (cx + rp); cx + rp < max_ctx is required (a
+ *               query with prompt >= max_ctx is an error);
+ *   kv_blocks   KV cache of kv_blocks blocks of block_size tokens (block_size a power
+ *               of two, 1 .. 65536): a running request holds ceil(cx / block_size)
+ *               blocks.  Requires max_ctx > 0 and kv_blocks * block_size >= max_ctx.
+ * With limits, a batch gives each running request in list order one decode token
+ * (decoding ones), then min(rp, chunk_cap, budget left) (partially prefilled ones).
+ * When a request's new blocks do not fit, the last running request is preempted
+ * (recompute), repeatedly, until they fit or the request itself is out: its blocks,
+ * including those taken in this batch, and its tokens of this batch are returned,
+ * and it becomes the first waiting request with its whole context to prefill again.
+ * Waiting requests are admitted only in a batch without preemption, in FCFS order,
+ * while budget is left, fewer than max_seqs run and the first chunk's blocks fit.
+ * With every limit 0 the batches are the default ones bit for bit.
+ */
+typedef struct {
+  int32_t chunk_cap;
+  int32_t kv_blocks;
+  int32_t block_size;
+  int32_t max_ctx;
+} lar_sched_limits;
+
+/*
+ * Put scheduler limits on every instance (host [I]), or remove them (NULL).  The
+ * state is laid out for the scheduler in use, so a lar_load_state must follow
+ * before any other call (until then they return LAR_E_STATE).  With limits set,
+ * estimates and traces simulate each (query, instance) pair from the instance state
+ * (the shared-trajectory shortcuts of the default scheduler are not used); the
+ * snapshot validation also requires cx + rp < max_ctx for every request and at most
+ * kv_blocks blocks held by the running ones (LAR_E_STATE).  Bad limits: LAR_E_ARG,
+ * nothing changed.  Synchronises the stream.
+ */
+lar_status lar_set_scheduler(lar_ctx *ctx, const lar_sched_limits *limits);
+
+/*
  * Re-install the snapshot of the last lar_load_state (kept in device memory) into
  * every scenario, with device-to-device copies enqueued on the stream: no host
  * traffic, no synchronisation.  Clears the sticky device error.  Use it to replay

@@ -18,6 +18,7 @@ LIB = os.path.join(HERE, "liblar.so")
 SOURCES = [os.path.join(CSRC, "sfs_kernels.hip"), os.path.join(CSRC, "lar_api.cpp"),
            os.path.join(CSRC, "lar_board.cpp")]
 HEADERS = [os.path.join(CSRC, "sfs_device.h"), os.path.join(CSRC, "sfs_launch.h"),
+           os.path.join(CSRC, "sfs_limits.h"),
            os.path.join(ROOT, "include", "lar.h")]
 ARCH = "gfx950"
 

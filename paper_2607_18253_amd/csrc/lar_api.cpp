@@ -36,6 +36,11 @@ struct lar_ctx {
   int32_t tag_next = 0;        // ring tag of the next query tracked for its realised TTFT
   int32_t tag_start = 0;       // tag_next after a (re)load
   lar::DevState snap{};        // one scenario's copy of the last loaded snapshot
+  // scheduler limits (lar_set_scheduler): host copy and device [4][I] (chunk cap, KV
+  // blocks, log2 block size, context limit)
+  bool limited = false;
+  std::vector<lar_sched_limits> lim;
+  int32_t* plim = nullptr;
   int32_t* err = nullptr;
   size_t tail_elems = 0;  // allocated K * Z * I
   bool loaded = false;
@@ -106,6 +111,11 @@ LaunchEnv env_of(const lar_ctx* ctx) {
   e.xslot = ctx->xslot;
   e.sync = ctx->sync;
   e.work = ctx->work;
+  e.limited = ctx->limited;
+  e.L.H = ctx->plim;
+  e.L.K = ctx->plim + ctx->I;
+  e.L.sh = ctx->plim + 2 * ctx->I;
+  e.L.X = ctx->plim + 3 * ctx->I;
   return e;
 }
 
@@ -194,6 +204,7 @@ lar_status lar_create(lar_ctx** out, const lar_config* cfg) {
   chk(dev_alloc(ctx, &ctx->err, 1));
   chk(dev_alloc(ctx, &ctx->xslot, (size_t)ctx->Z * 2 * lar::kMaxCluster * 4));
   chk(dev_alloc(ctx, &ctx->work, (size_t)ctx->Z));
+  chk(dev_alloc(ctx, &ctx->plim, 4 * (size_t)ctx->I));
   if (st == LAR_OK && hipMemset(ctx->work, 0, sizeof(unsigned long long) * ctx->Z) != hipSuccess)
     st = fail(ctx, LAR_E_HIP, "hipMemset of the work counters failed");
   if (st != LAR_OK) {
@@ -260,7 +271,58 @@ lar_status lar_load_state(lar_ctx* ctx, const lar_instance_params* params, const
       d_seq((size_t)I * mcap, 0), r_rp((size_t)I * rcap, 0), r_rd((size_t)I * rcap, 0),
       r_cx((size_t)I * rcap, 0), r_seq((size_t)I * rcap, 0), r_tag((size_t)I * rcap, -1);
   std::vector<lar::QScal> sc(I);
-  for (int j = 0; j < I; ++j) {
+  if (ctx->limited) {
+    // under scheduler limits every request stays in the ring, in FCFS order, with
+    // its predicted decode cut to the context limit
+    for (int j = 0; j < I; ++j) {
+      const lar_sched_limits& L = ctx->lim[j];
+      int nr = 0, nw = 0, n = 0;
+      int64_t held = 0, ps = 0;
+      for (int r = offsets[j]; r < offsets[j + 1]; ++r) {
+        const int32_t rp = rem_prefill[r], cx = context[r];
+        int32_t rd = rem_decode[r];
+        if (rp < 0 || rd < 1 || cx < 0 || (rp == 0 && cx == 0))
+          return fail(ctx, LAR_E_STATE, "instance %d request %d: invalid (rp %d, rd %d, cx %d)", j,
+                      n, rp, rd, cx);
+        const int64_t total = (int64_t)cx + rp;
+        if (L.max_ctx > 0) {
+          if (total >= L.max_ctx)
+            return fail(ctx, LAR_E_STATE, "instance %d request %d: context %lld >= max_ctx %d",
+                        j, n, (long long)total, L.max_ctx);
+          if (rd > L.max_ctx - total) rd = (int32_t)(L.max_ctx - total);
+        }
+        if (cx > 0) {
+          if (nw > 0)
+            return fail(ctx, LAR_E_STATE, "instance %d: running request after a waiting one", j);
+          if (nr >= params[j].max_seqs)
+            return fail(ctx, LAR_E_STATE, "instance %d: more than max_seqs running", j);
+          ++nr;
+          if (L.kv_blocks > 0) held += (cx + (int64_t)L.block_size - 1) / L.block_size;
+        } else {
+          if (nw >= qcap)
+            return fail(ctx, LAR_E_CAPACITY, "instance %d: more than queue_cap waiting", j);
+          ++nw;
+        }
+        const size_t x = (size_t)j * rcap + n;
+        r_rp[x] = rp; r_rd[x] = rd; r_cx[x] = cx; r_seq[x] = n;
+        ps += rp;
+        ++n;
+      }
+      if (L.kv_blocks > 0 && held > L.kv_blocks)
+        return fail(ctx, LAR_E_STATE, "instance %d: running requests hold %lld > %d KV blocks", j,
+                    (long long)held, L.kv_blocks);
+      lar::QScal q{};
+      q.n_dec = 0;
+      q.n_part = nr;
+      q.n_pre = n;
+      q.head = 0;
+      q.next_seq = n;
+      q.pre_sum = ps;
+      q.clock = clock_ms[j];
+      sc[j] = q;
+    }
+  }
+  for (int j = 0; j < I && !ctx->limited; ++j) {
     int nr = 0, nw = 0, nd = 0, np = 0, npart = 0;
     int64_t c0 = 0, ps = 0;
     for (int r = offsets[j]; r < offsets[j + 1]; ++r) {
@@ -358,6 +420,41 @@ lar_status lar_load_state(lar_ctx* ctx, const lar_instance_params* params, const
   }
   HIP_TRY(ctx, hipStreamSynchronize(s));
   ctx->max_col = max_col;
+  ctx->msg.clear();
+  return LAR_OK;
+}
+
+lar_status lar_set_scheduler(lar_ctx* ctx, const lar_sched_limits* limits) {
+  if (!ctx) return LAR_E_ARG;
+  const int I = ctx->I;
+  std::vector<int32_t> dev(4 * (size_t)I, 0);
+  if (limits) {
+    for (int j = 0; j < I; ++j) {
+      const lar_sched_limits& L = limits[j];
+      if (L.chunk_cap < 0 || L.kv_blocks < 0 || L.max_ctx < 0)
+        return fail(ctx, LAR_E_ARG, "instance %d: negative limit", j);
+      int sh = 0;
+      if (L.kv_blocks > 0) {
+        if (L.block_size < 1 || L.block_size > 65536 || (L.block_size & (L.block_size - 1)))
+          return fail(ctx, LAR_E_ARG, "instance %d: block_size %d not a power of two in "
+                      "[1, 65536]", j, L.block_size);
+        if (L.max_ctx < 1 || (int64_t)L.kv_blocks * L.block_size < L.max_ctx)
+          return fail(ctx, LAR_E_ARG, "instance %d: a KV cache needs max_ctx > 0 and "
+                      "kv_blocks * block_size >= max_ctx", j);
+        while ((1 << sh) < L.block_size) ++sh;
+      }
+      dev[j] = L.chunk_cap;
+      dev[I + j] = L.kv_blocks;
+      dev[2 * I + j] = sh;
+      dev[3 * I + j] = L.max_ctx;
+    }
+  }
+  HIP_TRY(ctx, hipStreamSynchronize(ctx->stream));
+  HIP_TRY(ctx, hipMemcpy(ctx->plim, dev.data(), dev.size() * sizeof(int32_t),
+                         hipMemcpyHostToDevice));
+  ctx->limited = limits != nullptr;
+  ctx->lim.assign(limits ? limits : nullptr, limits ? limits + I : nullptr);
+  ctx->loaded = false;   // the state layout depends on the scheduler: load again
   ctx->msg.clear();
   return LAR_OK;
 }

@@ -22,8 +22,13 @@
 //            (realised TTFT of each query in the replay).
 //   k_stats  one block per scenario: means in query order, nearest-rank p50/p99.
 //   k_targets, k_ontime  TTFT targets per query; OnTimeUtility (Eq. 4).
+//   k_lest, k_lcommit, k_ltrace, k_ldrain  the same calls under scheduler limits
+//            (chunk cap, context limit, KV-cache blocks with preemption): literal
+//            per-(query, instance) simulation on the explicit-list engine of
+//            sfs_limits.h.
 #include "sfs_device.h"
 #include "sfs_launch.h"
+#include "sfs_limits.h"
 
 namespace lar {
 
@@ -1587,6 +1592,225 @@ __global__ __launch_bounds__(256) void k_ontime(int N, int I, const int32_t* cho
   if (threadIdx.x == 0) out[z] = __ddiv_rn(s, (double)N);
 }
 
+// ------------------------------------------------------------------ scheduler limits
+// SFS estimate under limits: a private copy of the queue with the query appended at
+// the tail, stepped until the query's first decode (reading 1: its prefill
+// completes).  NaN with an error when the state is behind t, the prompt does not fit
+// the context limit or the batch cap is reached.
+template <int KS>
+__device__ __forceinline__ double lim_estimate(const LQueue<KS>& q, const LEnv& e, int p, int d,
+                                               double t, int reading, int64_t max_iters,
+                                               int32_t* err, int64_t* it_out) {
+  const int ln = lane_id();
+  *it_out = 0;
+  if (q.clock < t) {
+    if (ln == 0) set_error(err, kErrState);
+    return __builtin_nan("");
+  }
+  const int dq = entry_decode(e, p, d);
+  if (p < 1 || dq < 1) {
+    if (ln == 0) set_error(err, kErrArg);
+    return __builtin_nan("");
+  }
+  LQueue<KS> w = q;
+  w.template append<false>(e, p, dq, false, nullptr, -1);
+  double E = w.clock;
+  int64_t it = 0;
+  for (;;) {
+    if (it == max_iters) {
+      if (ln == 0) set_error(err, kErrIter);
+      *it_out = it;
+      return __builtin_nan("");
+    }
+    const LStep o = w.template step<false>(e, nullptr, 0.0, nullptr);
+    E = __dadd_rn(E, o.T);
+    ++it;
+    if (reading == 1 ? o.last_fill : o.last_dec) break;
+  }
+  *it_out = it;
+  return __dsub_rn(E, t);
+}
+
+// Append the query when this queue is the chosen one, then replay every batch that
+// starts before t; an idle queue's clock jumps to t.  TRK: the query is tracked
+// (tag) and first tokens of the replayed batches are recorded.
+template <int KS, bool TRK>
+__device__ __forceinline__ void lim_commit_advance(LQueue<KS>& w, const LEnv& e, bool chosen,
+                                                   int p, int d, double t, int qcap,
+                                                   int64_t max_iters, int32_t* err,
+                                                   int32_t* tags, int tag, const LTrack& tk) {
+  const int ln = lane_id();
+  if (chosen) {
+    const int dq = entry_decode(e, p, d);
+    if (p < 1 || dq < 1) {
+      if (ln == 0) set_error(err, kErrArg);
+    } else if (w.waiting() + 1 > qcap) {
+      if (ln == 0) set_error(err, kErrCapacity);
+    } else {
+      w.template append<TRK>(e, p, dq, true, tags, tag);
+      if constexpr (TRK) w.ntrk += 1;
+    }
+  }
+  double clock = w.clock;
+  int64_t n = 0;
+  while (w.n_list > 0 && clock < t) {
+    if (n == max_iters) {
+      if (ln == 0) set_error(err, kErrIter);
+      break;
+    }
+    const LStep o = w.template step<TRK>(e, tags, clock, &tk);
+    clock = __dadd_rn(clock, o.T);
+    ++n;
+  }
+  if (w.n_list == 0 && clock < t) clock = t;
+  w.clock = clock;
+  w.iters += n;
+}
+
+// What-if estimates under limits: one wave per (scenario, query, instance), instance
+// fastest; reads the state, changes nothing.
+template <int KS>
+__global__ __launch_bounds__(kWave) void k_lest(DevState S, DevParams pr, DevLimits lm, int Z,
+                                               int Q, int I, const int32_t* q_prefill,
+                                               const double* t_ptr, double t_val,
+                                               int max_prompt, int reading, int64_t max_iters,
+                                               double* ttft, int32_t* iters, int32_t* err) {
+  const int64_t pair = blockIdx.x;
+  if (pair >= (int64_t)Z * Q * I) return;
+  const int j = (int)(pair % I);
+  const int z = (int)(pair / ((int64_t)Q * I));
+  const int q = (int)((pair / I) % Q);
+  const int qid = z * I + j;
+  const double t = t_ptr ? *t_ptr : t_val;
+  __shared__ alignas(16) int lds[lim_lds_words<KS>()];
+  const LEnv e = make_lenv(S, pr, lm, qid, j, lds);
+  const int p = q_prefill[q];
+  double v = __builtin_nan("");
+  int64_t it = -1;
+  if (p < 1 || p > max_prompt) {
+    if (lane_id() == 0) set_error(err, kErrArg);
+  } else {
+    LQueue<KS> w;
+    w.template load<false>(S, e, qid, nullptr);
+    v = lim_estimate(w, e, p, 1, t, reading, max_iters, err, &it);
+    if (v != v) it = -1;
+  }
+  if (lane_id() == 0) {
+    ttft[pair] = v;
+    if (iters) iters[pair] = (int32_t)(it < 0x7fffffff ? it : 0x7fffffff);
+  }
+}
+
+template <int KS>
+__global__ __launch_bounds__(kWave) void k_lcommit(DevState S, DevParams pr, DevLimits lm, int Z,
+                                                  int I, const int32_t* choice,
+                                                  int64_t choice_zstride, const int32_t* qp_ptr,
+                                                  const int32_t* qd_ptr, int32_t qp_val,
+                                                  int32_t qd_val, const double* t_ptr,
+                                                  double t_val, int64_t max_iters, int32_t* err) {
+  const int qid = blockIdx.x;
+  if (qid >= Z * I) return;
+  const int z = qid / I;
+  const int j = qid % I;
+  const double t = t_ptr ? *t_ptr : t_val;
+  __shared__ alignas(16) int lds[lim_lds_words<KS>()];
+  const LEnv e = make_lenv(S, pr, lm, qid, j, lds);
+  LQueue<KS> w;
+  w.template load<false>(S, e, qid, nullptr);
+  const bool chosen = choice && choice[(int64_t)z * choice_zstride] == j;
+  const int p = qp_ptr ? *qp_ptr : qp_val;
+  const int d = qd_ptr ? *qd_ptr : qd_val;
+  const LTrack off{nullptr, 0, 0, 0};
+  lim_commit_advance<KS, false>(w, e, chosen, p, d, t, S.qcap, max_iters, err, nullptr, -1, off);
+  w.template store<false>(S, e, qid, nullptr);
+}
+
+// A whole sequential trace under limits, one workgroup per scenario: wave w of nw
+// owns instances j = w + v*nw (states in HBM, loaded per use); per query every owned
+// instance is estimated, the workgroup picks the best, and every instance commits
+// and replays to the next arrival.  TRK: the replay reports realised TTFT.
+template <int KS, int NW, bool TRK>
+__global__ __launch_bounds__(NW * kWave) void k_ltrace(LAR_TRACE_PARAMS, DevLimits lm) {
+  __shared__ double s_u[2][NW], s_t[2][NW], s_q[2][NW];
+  __shared__ int s_j[2][NW];
+  __shared__ alignas(16) int lds[NW][lim_lds_words<KS>()];
+  const int z = blockIdx.x;
+  const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
+  const int nw = blockDim.x / kWave;                 // waves launched (<= NW)
+  const int ln = lane_id();
+  const double wc = w_cost[z];
+  const double wl = w_lat[z];
+  const int j_l = wid + ln * nw;
+  const bool own_l = j_l < I;
+  const int col_l = own_l ? pr.col[j_l] : 0;
+  QueryIn nx = fetch_query(0, N, qp, qd, qt, t_after, tau, acc, cost, n_cols, col_l, own_l);
+  const LTrack tk{TRK ? realized + (int64_t)z * N : nullptr, tag0, N, reading};
+  unsigned long long wbatch = 0;   // batches of this wave's estimates
+  for (int i = 0; i < N; ++i) {
+    const QueryIn q = nx;
+    nx = fetch_query(i + 1, N, qp, qd, qt, t_after, tau, acc, cost, n_cols, col_l, own_l);
+    const bool p_ok = q.p >= 1 && q.p <= max_prompt;
+    if (!p_ok && threadIdx.x == 0) set_error(err, kErrArg);
+    double bu = 0.0, bt = 0.0, bq = 0.0;
+    int bj = -1;
+    for (int v = 0, j = wid; j < I; ++v, j += nw) {
+      const LEnv e = make_lenv(S, pr, lm, z * I + j, j, lds[wid]);
+      LQueue<KS> w;
+      w.template load<false>(S, e, z * I + j, nullptr);
+      int64_t it = 0;
+      const double ttft = p_ok ? lim_estimate(w, e, q.p, q.d, q.t, reading, max_iters, err, &it)
+                               : __builtin_nan("");
+      wbatch += it;
+      double eq2;
+      int k;
+      const double u = utility_lane(q, v, wc, wl, tau, ttft, j, &k, &eq2);
+      if (better(u, k, bu, bj)) { bu = u; bj = k; bt = ttft; bq = eq2; }
+    }
+    const int m = trace_pick<NW>(bu, bj, bt, bq, i, z, N, choice, chosen_ttft, utility, s_u,
+                                 s_t, s_q, s_j);
+    for (int j = wid; j < I; j += nw) {
+      const LEnv e = make_lenv(S, pr, lm, z * I + j, j, lds[wid]);
+      int32_t* tags = TRK ? S.r_tag + (int64_t)(z * I + j) * S.rcap : nullptr;
+      LQueue<KS> w;
+      w.template load<TRK>(S, e, z * I + j, tags);
+      lim_commit_advance<KS, TRK>(w, e, j == m, q.p, q.d, q.tn, S.qcap, max_iters, err, tags,
+                                  tag0 + i, tk);
+      w.template store<TRK>(S, e, z * I + j, tags);
+    }
+  }
+  if (work && lane_id() == 0) atomicAdd(work + z, wbatch);
+}
+
+// Tracked queries still without a first token when a trace under limits ends: a
+// private copy of the queue runs on with no further arrivals until each has it.
+template <int KS>
+__global__ __launch_bounds__(kWave) void k_ldrain(DevState S, DevParams pr, DevLimits lm, int Z,
+                                                 int I, double* realized, int tag0, int N,
+                                                 int reading, int64_t max_iters, int32_t* err) {
+  const int qid = blockIdx.x;
+  if (qid >= Z * I) return;
+  if (S.sc[qid].ntrk <= 0) return;
+  const int z = qid / I;
+  const int j = qid % I;
+  __shared__ alignas(16) int lds[lim_lds_words<KS>()];
+  const LEnv e = make_lenv(S, pr, lm, qid, j, lds);
+  const int32_t* tags = S.r_tag + (int64_t)qid * S.rcap;
+  LQueue<KS> w;
+  w.template load<true>(S, e, qid, tags);
+  const LTrack tk{realized + (int64_t)z * N, tag0, N, reading};
+  double clock = w.clock;
+  int64_t n = 0;
+  while (w.ntrk > 0 && w.n_list > 0) {
+    if (n == max_iters) {
+      if (lane_id() == 0) set_error(err, kErrIter);
+      break;
+    }
+    const LStep o = w.template step<true>(e, tags, clock, &tk);
+    clock = __dadd_rn(clock, o.T);
+    ++n;
+  }
+}
+
 __global__ void k_clear_error(int32_t* err) { *err = 0; }
 
 // ------------------------------------------------------------------ launchers
@@ -1704,6 +1928,68 @@ static hipError_t launch_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
 #define DRAIN_ARGS \
   env.S, env.P, env.Z, env.I, a.realized, a.tag0, a.N, env.reading, env.max_iters, env.err
 
+// Scheduler-limit paths: one switch over the slot width each.
+#define LIM_SWITCH(KSV, CALL)                   \
+  switch (env.ks) {                             \
+    case 1: { constexpr int KSV = 1; CALL; } break;   \
+    case 2: { constexpr int KSV = 2; CALL; } break;   \
+    case 4: { constexpr int KSV = 4; CALL; } break;   \
+    case 8: { constexpr int KSV = 8; CALL; } break;   \
+    case 16: { constexpr int KSV = 16; CALL; } break; \
+    default: return hipErrorInvalidValue;       \
+  }
+
+static hipError_t launch_lim_est(const LaunchEnv& env, int Q, const int32_t* q_prefill,
+                                 const double* t_ptr, double t_val, double* ttft,
+                                 int32_t* iters) {
+  const int64_t total = (int64_t)env.Z * Q * env.I;
+  if (total > 0x7fffffff) return hipErrorInvalidValue;
+  LIM_SWITCH(KSV, hipLaunchKernelGGL(k_lest<KSV>, dim3((unsigned)total), dim3(kWave), 0,
+                                     env.stream, env.S, env.P, env.L, env.Z, Q, env.I,
+                                     q_prefill, t_ptr, t_val, env.max_prompt, env.reading,
+                                     env.max_iters, ttft, iters, env.err))
+  return hipGetLastError();
+}
+
+static hipError_t launch_lim_commit(const LaunchEnv& env, const int32_t* choice,
+                                    int64_t choice_zstride, const int32_t* qp_ptr,
+                                    const int32_t* qd_ptr, int32_t qp, int32_t qd,
+                                    const double* t_ptr, double t_val) {
+  LIM_SWITCH(KSV, hipLaunchKernelGGL(k_lcommit<KSV>, dim3(env.Z * env.I), dim3(kWave), 0,
+                                     env.stream, env.S, env.P, env.L, env.Z, env.I, choice,
+                                     choice_zstride, qp_ptr, qd_ptr, qp, qd, t_ptr, t_val,
+                                     env.max_iters, env.err))
+  return hipGetLastError();
+}
+
+// Waves per workgroup of the trace under limits: their LDS areas fill about 80 KiB.
+template <int KS>
+constexpr int lim_trace_waves() { return KS <= 4 ? 16 : (KS == 8 ? 8 : 4); }
+
+template <int KS>
+static hipError_t launch_lim_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
+  constexpr int NW = lim_trace_waves<KS>();
+  const int nw = env.I < NW ? env.I : NW;
+  if ((env.I + nw - 1) / nw > kWave) return hipErrorInvalidValue;   // 64 instances per wave
+  if (a.realized)
+    hipLaunchKernelGGL((k_ltrace<KS, NW, true>), dim3(env.Z), dim3(nw * kWave), 0, env.stream,
+                       LAR_TRACE_ARGS, env.L);
+  else
+    hipLaunchKernelGGL((k_ltrace<KS, NW, false>), dim3(env.Z), dim3(nw * kWave), 0,
+                       env.stream, LAR_TRACE_ARGS, env.L);
+  return hipGetLastError();
+}
+
+static hipError_t launch_lim_trace(const LaunchEnv& env, const TraceArgs& a) {
+  hipError_t e = hipSuccess;
+  LIM_SWITCH(KSV, e = launch_lim_trace_ks<KSV>(env, a))
+  if (e != hipSuccess || !a.realized) return e;
+  LIM_SWITCH(KSV, hipLaunchKernelGGL(k_ldrain<KSV>, dim3(env.Z * env.I), dim3(kWave), 0,
+                                     env.stream, env.S, env.P, env.L, env.Z, env.I, a.realized,
+                                     a.tag0, a.N, env.reading, env.max_iters, env.err))
+  return hipGetLastError();
+}
+
 hipError_t launch_trace(const LaunchEnv& env, const TraceArgs& a) {
   if (env.work) {
     hipLaunchKernelGGL(k_clear_work, dim3((env.Z + 255) / 256), dim3(256), 0, env.stream,
@@ -1720,6 +2006,14 @@ hipError_t launch_trace(const LaunchEnv& env, const TraceArgs& a) {
     if (e != hipSuccess) return e;
   }
   hipError_t e;
+  if (env.limited) {
+    e = launch_lim_trace(env, a);
+    if (e != hipSuccess || !a.realized) return e;
+    const int64_t no = (int64_t)env.Z * a.N;
+    hipLaunchKernelGGL(k_track_end, dim3((unsigned)((no + 255) / 256)), dim3(256), 0,
+                       env.stream, a.realized, a.qt, a.N, no);
+    return hipGetLastError();
+  }
   switch (env.ks) {
     case 1: e = launch_trace_ks<1>(env, a); break;
     case 2: e = launch_trace_ks<2>(env, a); break;
@@ -1746,6 +2040,7 @@ hipError_t launch_trace(const LaunchEnv& env, const TraceArgs& a) {
 }
 
 hipError_t launch_traj(const LaunchEnv& env, const double* t_ptr, double t_val) {
+  if (env.limited) return hipSuccess;   // estimates under limits simulate from the state
   switch (env.ks) {
     case 1: return launch_traj_ks<1>(env, t_ptr, t_val);
     case 2: return launch_traj_ks<2>(env, t_ptr, t_val);
@@ -1759,6 +2054,8 @@ hipError_t launch_traj(const LaunchEnv& env, const double* t_ptr, double t_val) 
 hipError_t launch_commit(const LaunchEnv& env, const int32_t* choice, int64_t choice_zstride,
                          const int32_t* qp_ptr, const int32_t* qd_ptr, int32_t qp, int32_t qd,
                          const double* t_ptr, double t_val) {
+  if (env.limited)
+    return launch_lim_commit(env, choice, choice_zstride, qp_ptr, qd_ptr, qp, qd, t_ptr, t_val);
   switch (env.ks) {
     case 1: return launch_commit_ks<1>(env, choice, choice_zstride, qp_ptr, qd_ptr, qp, qd, t_ptr, t_val);
     case 2: return launch_commit_ks<2>(env, choice, choice_zstride, qp_ptr, qd_ptr, qp, qd, t_ptr, t_val);
@@ -1771,6 +2068,7 @@ hipError_t launch_commit(const LaunchEnv& env, const int32_t* choice, int64_t ch
 
 hipError_t launch_est(const LaunchEnv& env, int Q, const int32_t* q_prefill, const double* t_ptr,
                       double t_val, double* ttft, int32_t* iters) {
+  if (env.limited) return launch_lim_est(env, Q, q_prefill, t_ptr, t_val, ttft, iters);
   const int64_t total = (int64_t)env.Z * Q * env.I;
   const int64_t blocks = (total + 255) / 256;
   hipLaunchKernelGGL(k_est, dim3((unsigned)blocks), dim3(256), 0, env.stream, env.P, env.T,

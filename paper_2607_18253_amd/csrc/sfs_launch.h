@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "sfs_device.h"
+#include "sfs_limits.h"
 
 namespace lar {
 
@@ -31,6 +32,10 @@ struct LaunchEnv {
   uint64_t* xslot;    // [Z][2][kMaxCluster][4] tagged candidate posts
   SyncCtl sync;
   unsigned long long* work;   // [Z] batches simulated by the estimates of the last trace
+  // scheduler limits: when set, estimates, commits and traces run the explicit-list
+  // engine of sfs_limits.h on the state laid out for it
+  bool limited;
+  DevLimits L;
 };
 
 constexpr int kMaxCluster = 64;

@@ -21,7 +21,7 @@ FIRST_TOKEN_DECODE_BATCH, FIRST_TOKEN_PREFILL_BATCH = 0, 1
 EXPORTED = ("lar_create", "lar_destroy", "lar_error_string", "lar_load_state", "lar_reload_state",
             "lar_estimate_ttft", "lar_route", "lar_route_constrained", "lar_ttft_targets",
             "lar_commit", "lar_route_step", "lar_route_trace", "lar_route_trace_constrained",
-            "lar_stats",
+            "lar_stats", "lar_set_scheduler",
             "lar_ontime_utility", "lar_read_state", "lar_sync", "lar_trace_work", "lar_board_create",
             "lar_board_destroy", "lar_board_publish", "lar_board_collect")
 
@@ -36,6 +36,11 @@ class Config(C.Structure):
     _fields_ = [("n_scen", C.c_int32), ("n_inst", C.c_int32), ("max_seqs_cap", C.c_int32),
                 ("queue_cap", C.c_int32), ("max_prompt", C.c_int32), ("flags", C.c_int32),
                 ("max_iters", C.c_int64), ("stream", C.c_void_p)]
+
+
+class SchedLimits(C.Structure):
+    _fields_ = [("chunk_cap", C.c_int32), ("kv_blocks", C.c_int32), ("block_size", C.c_int32),
+                ("max_ctx", C.c_int32)]
 
 
 class InstanceParams(C.Structure):
@@ -68,6 +73,8 @@ def load_library(path: str = LIB_PATH):
     L.lar_load_state.argtypes = [vp, C.POINTER(InstanceParams), vp, vp, vp, vp, vp]
     L.lar_reload_state.restype = i32
     L.lar_reload_state.argtypes = [vp]
+    L.lar_set_scheduler.restype = i32
+    L.lar_set_scheduler.argtypes = [vp, vp]
     L.lar_estimate_ttft.restype = i32
     L.lar_estimate_ttft.argtypes = [vp, i32, vp, dbl, vp, vp]
     L.lar_route.restype = i32
@@ -193,6 +200,18 @@ class LarContext:
 
     def reload_state(self):
         self._check(self._L.lar_reload_state(self._h))
+
+    def set_scheduler(self, limits):
+        """Scheduler limits per instance, [I][4] (chunk cap, KV blocks, block size,
+        context limit; 0 = none), or None for the default scheduler.  A load_state
+        must follow."""
+        if limits is None:
+            self._check(self._L.lar_set_scheduler(self._h, None))
+            return
+        lim = np.asarray(limits, np.int32).reshape(self.I, 4)
+        arr = (SchedLimits * self.I)(*[SchedLimits(*(int(v) for v in lim[j]))
+                                       for j in range(self.I)])
+        self._check(self._L.lar_set_scheduler(self._h, C.cast(arr, C.c_void_p)))
 
     def load_workload(self, wl):
         self.load_state(a=wl.a, b=wl.b, c=wl.c, d=wl.d, e=wl.e, budget=wl.budget,
@@ -395,12 +414,15 @@ class LarContext:
 def context_for(wl, *, flags=FIRST_TOKEN_DECODE_BATCH, max_iters=10_000_000, stream=None,
                 queue_cap=None, max_seqs_cap=None) -> LarContext:
     """A context sized for workload ``wl`` with its snapshot loaded (max_seqs_cap
-    defaults to the largest M of the pool)."""
+    defaults to the largest M of the pool), under the workload's scheduler limits
+    when it has them."""
     mcap = int(np.max(wl.max_seqs)) if max_seqs_cap is None else int(max_seqs_cap)
     ctx = LarContext(wl.n_scen, wl.n_inst, max_seqs_cap=mcap,
                      queue_cap=int(wl.queue_cap if queue_cap is None else queue_cap),
                      max_prompt=int(wl.max_prompt), flags=flags, max_iters=max_iters,
                      stream=stream)
+    if getattr(wl, "sched", None) is not None:
+        ctx.set_scheduler(wl.sched)
     ctx.load_workload(wl)
     return ctx
 

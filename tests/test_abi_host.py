@@ -53,7 +53,8 @@ def test_null_arguments_rejected_without_gpu():
     for name, n_args in (("lar_route", 11), ("lar_route_constrained", 11),
                          ("lar_ttft_targets", 6), ("lar_route_trace_constrained", 15),
                          ("lar_route_trace", 15), ("lar_ontime_utility", 10), ("lar_stats", 9),
-                         ("lar_reload_state", 1), ("lar_route_step", 14)):
+                         ("lar_reload_state", 1), ("lar_route_step", 14),
+                         ("lar_set_scheduler", 2)):
         f = getattr(lib, name)
         f.restype = ctypes.c_int32
         args = [None] * n_args
@@ -88,7 +89,7 @@ def _check_state(wl):
         assert np.sum(run) <= wl.max_seqs[j]
 
 
-@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5", "c6"])
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5", "c6", "c7"])
 def test_generator_shapes_and_invariants(name):
     from workloads import make_workload
     kw = dict(n_q=500) if name != "c3" else {}
@@ -109,6 +110,18 @@ def test_generator_shapes_and_invariants(name):
     assert np.sum((rp == 0) & (cx > 0)) == n_dec
     assert np.sum((rp > 0) & (cx > 0)) == 1
     assert np.sum(cx == 0) == R - n_dec - 1
+
+
+def test_generator_c7_fits_its_limits():
+    from workloads import make_workload
+    wl = make_workload("c7", n_q=500)
+    for j in range(wl.n_inst):
+        H, K, S, X = (int(v) for v in wl.sched[j])
+        rp, rd, cx = wl.instance_requests(j)
+        assert np.all(rp + cx < X)
+        assert sum(-(-int(c) // S) for c in cx if c > 0) <= K
+        assert K * S >= X and S & (S - 1) == 0
+    assert wl.q_prefill.max() < int(wl.sched[0][3])
 
 
 def test_generator_is_deterministic():

@@ -1,0 +1,169 @@
+"""GPU parity of the scheduler limits (chunk cap, context limit, KV-cache blocks with
+recompute preemption; the system appendix lists them among what the SFS simulation
+follows) against the oracle, bit for bit: traces under both objectives and both
+readings with realised TTFT, what-if estimates, single routing steps, final states;
+and the limits engine with every limit off against the default engine."""
+
+from __future__ import annotations
+
+import os
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+from gpu_util import DEV, T, assert_state_equal, bits  # noqa: E402
+from oracle import oracle as O  # noqa: E402
+from paper_2607_18253_amd import context_for  # noqa: E402
+from workloads import make_tiny_workload, make_workload  # noqa: E402
+from workloads.gen import make_tiny_sched_workload  # noqa: E402
+
+MAX_ITERS = 200_000   # bounds every estimate and replay call of these tests
+
+
+def _trace(wl, n_q=None, *, flags=0, tau=None, realized=True, max_seqs_cap=None):
+    N = wl.n_q if n_q is None else int(n_q)
+    ctx = context_for(wl, flags=flags, max_iters=MAX_ITERS, max_seqs_cap=max_seqs_cap)
+    ctx.advance(float(wl.q_t_ms[0]))
+    Z = wl.n_scen
+    chosen = torch.full((Z, N), -1.0, dtype=torch.float64, device=DEV)
+    util = torch.full((Z, N), -1.0, dtype=torch.float64, device=DEV)
+    real = torch.full((Z, N), -1.0, dtype=torch.float64, device=DEV) if realized else None
+    args = (T(wl.q_prefill[:N], torch.int32), T(wl.q_decode[:N], torch.int32),
+            T(wl.q_t_ms[:N], torch.float64), float(wl.q_t_ms[N - 1]))
+    if tau is None:
+        choice = ctx.route_trace(*args, T(wl.acc[:N], torch.float64),
+                                 T(wl.cost[:N], torch.float64), T(wl.w_cost, torch.float64),
+                                 T(wl.w_lat_ms, torch.float64), chosen_ttft=chosen,
+                                 utility=util, realized=real)
+    else:
+        choice = ctx.route_trace_constrained(*args, T(tau[:N], torch.float64),
+                                             T(wl.acc[:N], torch.float64),
+                                             T(wl.cost[:N], torch.float64),
+                                             T(wl.w_cost, torch.float64), chosen_ttft=chosen,
+                                             utility=util, realized=real)
+    ctx.sync()
+    return (choice.cpu().numpy(), chosen.cpu().numpy(), util.cpu().numpy(),
+            None if real is None else real.cpu().numpy(), ctx)
+
+
+def _check(wl, got, *, reading=0, tau=None, scenarios=(0,), state=(0,)):
+    choice, chosen, util, real, ctx = got
+    N = choice.shape[1]
+    for z in scenarios:
+        ref = O.trace(wl, scenario=z, n_q=N, reading=reading, tau=tau, max_iters=MAX_ITERS,
+                      final_state=z in state)
+        np.testing.assert_array_equal(choice[z], ref.choice, err_msg=f"{wl.name} scenario {z}")
+        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen),
+                                      err_msg=f"{wl.name} scenario {z}")
+        np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
+        if real is not None:
+            np.testing.assert_array_equal(bits(real[z]), bits(ref.realized),
+                                          err_msg=f"{wl.name} realised, scenario {z}")
+        if z in state:
+            assert_state_equal(ctx, z, ref)
+    ctx.close()
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_limits_tiny_pools(seed):
+    wl = make_tiny_sched_workload(seed, n_q=25, max_res=5)
+    reading = seed % 2
+    print(f"tiny limits seed {seed} reading {reading}", flush=True)
+    _check(wl, _trace(wl, flags=reading), reading=reading)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_limits_tiny_pools_constrained(seed):
+    wl = make_tiny_sched_workload(100 + seed, n_q=25, max_res=5)
+    tau = np.random.default_rng(seed).uniform(0.0, 40.0, size=wl.n_q)
+    print(f"tiny limits constrained seed {seed}", flush=True)
+    _check(wl, _trace(wl, tau=tau), tau=tau)
+
+
+@pytest.mark.parametrize("seed,cap", [(0, None), (1, 100), (2, 200), (3, 300), (4, 1000)])
+def test_limits_tiny_pools_scenarios_and_wide_slots(seed, cap):
+    """Several scenarios at once; every slot width (64, 128, 256, 512, 1024 entries in
+    registers) through a larger max_seqs_cap."""
+    wl = make_tiny_sched_workload(200 + seed, n_q=20, max_res=6, n_scen=3)
+    print(f"tiny limits scenarios seed {seed} cap {cap}", flush=True)
+    _check(wl, _trace(wl, max_seqs_cap=cap), scenarios=(0, 1, 2), state=(0, 2))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_limits_off_equals_default_engine(seed):
+    """The limits engine with every limit 0 against the default engine and the oracle."""
+    wl = make_tiny_workload(seed, n_q=30)
+    base = _trace(wl, realized=True)
+    ref_c, ref_t = base[0].copy(), base[1].copy()
+    base[4].close()
+    wl.sched = np.zeros((wl.n_inst, 4), np.int32)
+    got = _trace(wl, realized=True)
+    np.testing.assert_array_equal(got[0], ref_c)
+    np.testing.assert_array_equal(bits(got[1]), bits(ref_t))
+    _check(wl, got)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_limits_what_if_matrix(seed):
+    """lar_estimate_ttft under limits: every (query, instance) pair against the
+    oracle's literal estimate, after a replay to a common time."""
+    wl = make_tiny_sched_workload(300 + seed, n_q=12, max_res=6)
+    reading = seed % 2
+    ctx = context_for(wl, flags=reading, max_iters=MAX_ITERS)
+    t = float(wl.q_t_ms[3])
+    ctx.advance(t)
+    qp = T(wl.q_prefill, torch.int32)
+    ttft, _ = ctx.estimate(qp, t)
+    ctx.sync()
+    got = ttft.cpu().numpy().reshape(wl.n_q, wl.n_inst)
+    for j in range(wl.n_inst):
+        q = O.instance_queue(wl, j)
+        q.advance(t, max_iters=MAX_ITERS)
+        for i in range(wl.n_q):
+            want, _ = q.estimate(int(wl.q_prefill[i]), 1, t, reading)
+            assert bits(got[i, j]) == bits(want), (seed, i, j)
+    ctx.close()
+
+
+def test_limits_commit_and_route_step():
+    """Single routing steps (lar_route_step) and plain commits under limits follow the
+    oracle's trace."""
+    wl = make_tiny_sched_workload(400, n_q=30, max_res=5)
+    ref = O.trace(wl, max_iters=MAX_ITERS)
+    ctx = context_for(wl, max_iters=MAX_ITERS)
+    ctx.advance(float(wl.q_t_ms[0]))
+    got = []
+    for i in range(wl.n_q):
+        tn = float(wl.q_t_ms[i + 1]) if i + 1 < wl.n_q else float(wl.q_t_ms[i])
+        c = ctx.route_step(T(wl.q_prefill[i:i + 1], torch.int32),
+                           T(wl.q_decode[i:i + 1], torch.int32),
+                           T(wl.q_t_ms[i:i + 1], torch.float64),
+                           T(np.array([tn]), torch.float64), T(wl.acc[i:i + 1], torch.float64),
+                           T(wl.cost[i:i + 1], torch.float64), T(wl.w_cost, torch.float64),
+                           T(wl.w_lat_ms, torch.float64))
+        got.append(int(c.cpu().numpy().reshape(-1)[0]))
+    ctx.sync()
+    np.testing.assert_array_equal(np.array(got), ref.choice)
+    assert_state_equal(ctx, 0, ref)
+    ctx.close()
+
+
+def test_limits_c7_prefix():
+    """The c7 pool (32 instances, 512-token chunks, 16-token KV blocks, 8192-token
+    context limit), its first 3000 queries: the initial backlog, where the KV cache
+    preempts."""
+    wl = make_workload("c7", n_q=3000)
+    print("c7 prefix 3000", flush=True)
+    _check(wl, _trace(wl))
+
+
+def test_limits_c7_prefix_reading_prefill_constrained():
+    wl = make_workload("c7", n_q=1500)
+    tau = O.ttft_targets(wl.q_prefill, wl.tau_u_ms, wl.tau_v)
+    print("c7 prefix 1500 constrained reading 1", flush=True)
+    _check(wl, _trace(wl, flags=1, tau=tau), reading=1, tau=tau)
