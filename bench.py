@@ -10,7 +10,8 @@ resident in HBM before the timed region.  For the sequential-routing workloads
   one persistent kernel, then the per-scenario summary (mean accuracy / cost /
   utility, p50 and p99 TTFT).
 For the batched what-if workload (c3): one estimate call for 4096 queries x 1024
-instances followed by the row argmax.
+instances followed by the row argmax.  The c7 pool runs the sequential trace under
+scheduler limits (chunk cap, context limit, KV-cache blocks with preemption).
 
 Prints ONE JSON line.  ``value`` = TTFT estimates per second (scenarios x queries x
 instances per step / step time); routed queries per second are reported next to it.
@@ -46,7 +47,8 @@ def _parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5", "c6"])
+    ap.add_argument("--workload", default="c2",
+                    choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7"])
     ap.add_argument("--n-q", type=int, default=None, help="shorten the trace (testing only)")
     ap.add_argument("--objective", default="lagrangian", choices=["lagrangian", "constrained"],
                     help="route by the Lagrangian objective or by Eq. 3 with the paper's "
@@ -66,13 +68,17 @@ def _parse():
 
 
 COPY_PROBE_BYTES = 256 << 20
-KERNEL_SOURCES = ("paper_2607_18253_amd/csrc/sfs_kernels.hip",
-                  "paper_2607_18253_amd/csrc/sfs_device.h")
+_CSRC = "paper_2607_18253_amd/csrc/"
+KERNEL_SOURCES = tuple(_CSRC + f for f in ("sfs_kernels.hip", "sfs_device.h", "sfs_route.h"))
+LIMIT_KERNEL_SOURCES = tuple(_CSRC + f for f in ("sfs_limits.hip", "sfs_limits.h", "sfs_device.h",
+                                                 "sfs_route.h"))
 
 
-def kernel_source_hash():
+def kernel_source_hash(workload=None):
+    """Hash of the sources of the workload's trace kernel (a measured traffic figure
+    is reported only while they are unchanged)."""
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in (LIMIT_KERNEL_SOURCES if workload == "c7" else KERNEL_SOURCES):
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -105,7 +111,7 @@ def summarize_pmc(fetch_csv, write_csv, workload):
         factor = max(copy) * 1024.0 / COPY_PROBE_BYTES   # KiB counted per true byte
         out[counter] = {"kib_per_launch": sum(dom) / len(dom), "copy_probe_kib": max(copy),
                         "scale": factor, "bytes_per_launch": sum(dom) / len(dom) * 1024.0 / factor}
-    rec = {"workload": workload, "kernel": dominant_kernel(workload), "source_hash": kernel_source_hash(),
+    rec = {"workload": workload, "kernel": dominant_kernel(workload), "source_hash": kernel_source_hash(workload),
            "fetch": out["FETCH_SIZE"], "write": out["WRITE_SIZE"],
            "bytes_per_launch": out["FETCH_SIZE"]["bytes_per_launch"]
            + out["WRITE_SIZE"]["bytes_per_launch"]}
@@ -121,13 +127,15 @@ def load_traffic(workload):
             rec = json.load(fh)
     except (OSError, ValueError):
         return None
-    if rec.get("source_hash") != kernel_source_hash():
+    if rec.get("source_hash") != kernel_source_hash(workload):
         return None
     return rec["bytes_per_launch"]
 
 
 def dominant_kernel(workload):
-    return "k_traj" if workload == "c3" else "k_trace_cl"
+    if workload == "c3":
+        return "k_traj"
+    return "k_ltrace" if workload == "c7" else "k_trace_cl"
 
 
 def oracle_sample(wl, budget_s, tau=None):
@@ -287,7 +295,9 @@ def main():
     if whatif:
         line["roofline_kernel"] = "k_traj + k_est (lar_estimate_ttft)"
     else:
-        line["roofline_kernel"] = "k_trace_cl (lar_route_trace, one launch per step)"
+        line["roofline_kernel"] = (
+            "k_ltrace (lar_route_trace under scheduler limits, one launch per step)"
+            if wl.sched is not None else "k_trace_cl (lar_route_trace, one launch per step)")
         line["stats_scenario0"] = stats[0].tolist()
         if constrained:
             line["ontime_utility_scenario0"] = float(ontime[0])
@@ -300,6 +310,10 @@ def main():
                 "frac_realized_later": float((r0 > e0).mean()),
                 "max_gap_ms": float((r0 - e0).max())}
         line["config"]["realized_tracking"] = bool(track)
+        if wl.sched is not None:
+            H, K, S, X = (int(v) for v in wl.sched[0])
+            line["config"]["scheduler_limits"] = {"chunk_cap": H, "kv_blocks": K,
+                                                  "block_size": S, "max_ctx": X}
     line["kernel_ms"] = kernel_ms
 
     roof = None

@@ -15,10 +15,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "liblar.so")
-SOURCES = [os.path.join(CSRC, "sfs_kernels.hip"), os.path.join(CSRC, "lar_api.cpp"),
+SOURCES = [os.path.join(CSRC, "sfs_kernels.hip"), os.path.join(CSRC, "sfs_limits.hip"),
+           os.path.join(CSRC, "lar_api.cpp"),
            os.path.join(CSRC, "lar_board.cpp")]
 HEADERS = [os.path.join(CSRC, "sfs_device.h"), os.path.join(CSRC, "sfs_launch.h"),
-           os.path.join(CSRC, "sfs_limits.h"),
+           os.path.join(CSRC, "sfs_limits.h"), os.path.join(CSRC, "sfs_route.h"),
            os.path.join(ROOT, "include", "lar.h")]
 ARCH = "gfx950"
 

@@ -22,101 +22,12 @@
 //            (realised TTFT of each query in the replay).
 //   k_stats  one block per scenario: means in query order, nearest-rank p50/p99.
 //   k_targets, k_ontime  TTFT targets per query; OnTimeUtility (Eq. 4).
-//   k_lest, k_lcommit, k_ltrace, k_ldrain  the same calls under scheduler limits
-//            (chunk cap, context limit, KV-cache blocks with preemption): literal
-//            per-(query, instance) simulation on the explicit-list engine of
-//            sfs_limits.h.
+// Under scheduler limits the same calls dispatch to sfs_limits.hip.
 #include "sfs_device.h"
 #include "sfs_launch.h"
-#include "sfs_limits.h"
+#include "sfs_route.h"
 
 namespace lar {
-
-// Candidates of the argmax are (value, key) pairs.  The key is the instance index
-// j, with bit 30 set when the candidate misses its TTFT target under the
-// constrained objective (Eq. 3); a negative key means "no candidate".  The order:
-// a candidate meeting its target beats one that misses it, then the larger value,
-// then the lower index.  Under the Lagrangian objective every key is the bare
-// index and the value is the Lagrangian utility; under Eq. 3 the value is the
-// utility of Eq. 2 for a candidate meeting its target and -TTFT otherwise (so the
-// empty feasible set falls back to the least estimated TTFT).  Written without
-// branches so a lane-wise use stays a few selects.
-constexpr int kLateBit = 1 << 30;
-__device__ __forceinline__ int key_index(int k) { return k & (kLateBit - 1); }
-
-__device__ __forceinline__ bool better(double u1, int k1, double u2, int k2) {
-  const int c1 = k1 >> 30, c2 = k2 >> 30;
-  return (k1 >= 0) &
-         ((k2 < 0) | (c1 < c2) | ((c1 == c2) & ((u1 > u2) | ((u1 == u2) & (k1 < k2)))));
-}
-
-// Value and key of instance j for one query: eq2 = acc - w_cost*cost (Eq. 2).
-// tau == nullptr: Lagrangian objective, value eq2 - w_lat*ttft; else Eq. 3 with the
-// query's target *tau.
-__device__ __forceinline__ double cand_value(double eq2, double ttft, double wl,
-                                             const double* tau, double tq, int j, int* key) {
-  if (!tau) {
-    *key = j;
-    return __dsub_rn(eq2, __dmul_rn(wl, ttft));
-  }
-  const bool ok = ttft <= tq;
-  *key = ok ? j : (j | kLateBit);
-  return ok ? eq2 : -ttft;
-}
-
-// One butterfly step of the lane argmax: take the partner lane's candidate (DPP
-// pattern CTRL) when it is better.
-template <int CTRL>
-__device__ __forceinline__ void best_step_dpp(double& u, int& j) {
-  const long long b = __double_as_longlong(u);
-  const int lo = __builtin_amdgcn_mov_dpp((int)b, CTRL, 0xf, 0xf, false);
-  const int hi = __builtin_amdgcn_mov_dpp((int)(b >> 32), CTRL, 0xf, 0xf, false);
-  const double xu = __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
-  const int xj = __builtin_amdgcn_mov_dpp(j, CTRL, 0xf, 0xf, false);
-  const bool t = better(xu, xj, u, j);
-  u = t ? xu : u;
-  j = t ? xj : j;
-}
-
-// One step across 16-lane rows: the rows in ROWS take the candidate that DPP
-// pattern CTRL broadcasts to them (row_bcast) when it is better; other rows keep
-// their own.
-template <int CTRL, int ROWS>
-__device__ __forceinline__ void best_step_bcast(double& u, int& j) {
-  const long long b = __double_as_longlong(u);
-  const int b_lo = (int)b, b_hi = (int)(b >> 32);
-  const int lo = __builtin_amdgcn_update_dpp(b_lo, b_lo, CTRL, ROWS, 0xf, false);
-  const int hi = __builtin_amdgcn_update_dpp(b_hi, b_hi, CTRL, ROWS, 0xf, false);
-  const double xu = __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
-  const int xj = __builtin_amdgcn_update_dpp(j, j, CTRL, ROWS, 0xf, false);
-  const bool t = better(xu, xj, u, j);
-  u = t ? xu : u;
-  j = t ? xj : j;
-}
-
-// Argmax of the candidates in lanes [0, n) (every lane from n on must hold j = -1);
-// the result is returned wave-uniform.  Quad permutations and the
-// row mirrors combine 2, 4, 8 and 16 lanes (every lane of a row then holds the row's
-// best); beyond 16, row 0's best moves into row 1 and row 2's into row 3
-// (row_bcast:15), then rows 0-1's into rows 2-3 (row_bcast:31), so lane 63 holds the
-// best of all.
-__device__ __forceinline__ void lane_best(double& u, int& j, int n) {
-  if (n > 1) best_step_dpp<0xB1>(u, j);    // quad_perm [1,0,3,2]
-  if (n > 2) best_step_dpp<0x4E>(u, j);    // quad_perm [2,3,0,1]
-  if (n > 4) best_step_dpp<0x141>(u, j);   // row_half_mirror
-  if (n > 8) best_step_dpp<0x140>(u, j);   // row_mirror
-  int src = 0;
-  if (n > 16) {
-    best_step_bcast<0x142, 0xa>(u, j);     // row_bcast:15 into rows 1 and 3
-    best_step_bcast<0x143, 0xc>(u, j);     // row_bcast:31 into rows 2 and 3
-    src = kWave - 1;
-  }
-  const long long b = __double_as_longlong(u);
-  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)b, src);
-  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(b >> 32), src);
-  u = __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
-  j = __builtin_amdgcn_readlane(j, src);
-}
 
 // ------------------------------------------------------------------ k_traj
 template <int KS>
@@ -530,89 +441,6 @@ __device__ __forceinline__ double estimate(const Queue<KS>& q, const QEnv& e, in
   return finish_estimate(w, e, E, it, p, t, reading, max_iters, err, it_out);
 }
 
-// Trace inputs of one query, loaded one query ahead so their memory latency hides
-// behind the previous query's work.  Lane l of a wave holds acc / cost of the wave's
-// l-th owned instance.
-struct QueryIn {
-  int p, d;
-  double t, tn, tau;
-  double acc_l, cost_l;   // per lane
-};
-
-__device__ __forceinline__ QueryIn fetch_query(int i, int N, const int32_t* qp, const int32_t* qd,
-                                               const double* qt, double t_after,
-                                               const double* tau, const double* acc,
-                                               const double* cost, int n_cols, int col_l,
-                                               bool own_l) {
-  QueryIn q;
-  q.tau = 0.0;
-  if (i < N) {
-    q.p = qp[i];
-    q.d = qd[i];
-    q.t = qt[i];
-    q.tn = (i + 1 < N) ? qt[i + 1] : t_after;
-    if (tau) q.tau = tau[i];
-    const int64_t o = (int64_t)i * n_cols + col_l;
-    q.acc_l = own_l ? acc[o] : 0.0;
-    q.cost_l = own_l ? cost[o] : 0.0;
-  } else {
-    q.p = 1; q.d = 1; q.t = 0.0; q.tn = 0.0; q.acc_l = 0.0; q.cost_l = 0.0;
-  }
-  return q;
-}
-
-__device__ __forceinline__ double read_lane_f64(double v, int l) {
-  const uint64_t b = (uint64_t)__double_as_longlong(v);
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, l);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), l);
-  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
-}
-
-__device__ __forceinline__ double utility_lane(const QueryIn& q, int l, double wc, double wl,
-                                               const double* tau, double ttft, int j, int* key,
-                                               double* eq2) {
-  const double a = read_lane_f64(q.acc_l, l);
-  const double c = read_lane_f64(q.cost_l, l);
-  const double u = __dsub_rn(a, __dmul_rn(wc, c));
-  *eq2 = u;
-  return cand_value(u, ttft, wl, tau, q.tau, j, key);
-}
-
-// Workgroup argmax over the waves' candidates (double-buffered by query parity, so
-// one barrier per query suffices); thread 0 writes the outputs.
-template <int NW>
-__device__ __forceinline__ int trace_pick(double bu, int bj, double bt, double bq, int i, int z,
-                                          int N, int32_t* choice, double* chosen_ttft,
-                                          double* utility, double (*s_u)[NW], double (*s_t)[NW],
-                                          double (*s_q)[NW], int (*s_j)[NW]) {
-  const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
-  const int nw = blockDim.x / kWave;
-  const int buf = i & 1;
-  if (lane_id() == 0) { s_u[buf][wid] = bu; s_j[buf][wid] = bj; s_t[buf][wid] = bt; s_q[buf][wid] = bq; }
-  __syncthreads();
-  double mu = s_u[buf][0], mt = s_t[buf][0], mq = s_q[buf][0];
-  int m = s_j[buf][0];
-  for (int v = 1; v < nw; ++v)
-    if (better(s_u[buf][v], s_j[buf][v], mu, m)) {
-      mu = s_u[buf][v]; m = s_j[buf][v]; mt = s_t[buf][v]; mq = s_q[buf][v];
-    }
-  m = m >= 0 ? key_index(m) : -1;
-  if (threadIdx.x == 0) {
-    const int64_t o = (int64_t)z * N + i;
-    choice[o] = m;
-    if (chosen_ttft) chosen_ttft[o] = mt;
-    if (utility && m >= 0) utility[o] = mq;
-  }
-  return m;
-}
-
-#define LAR_TRACE_PARAMS                                                                     \
-  DevState S, DevParams pr, int Z, int I, int N, const int32_t *qp, const int32_t *qd,       \
-      const double *qt, double t_after, const double *acc, const double *cost, int n_cols,   \
-      const double *w_cost, const double *w_lat, const double *tau, int reading,             \
-      int max_prompt, int64_t max_iters, int32_t *choice, double *chosen_ttft,               \
-      double *utility, int32_t *err, unsigned long long *work, double *realized, int tag0
-
 // The same trace for pools too large to keep in registers: each owned instance's
 // state is loaded from HBM (L2) when it is needed and written back after its commit.
 // Wave w owns instances j = w + v*nw; lane v holds the inputs of the v-th one.
@@ -667,123 +495,6 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
     }
   }
   if (work && lane_id() == 0) atomicAdd(work + z, wbatch);
-}
-
-// Trace inputs of 64 consecutive queries, lane l holding query base + l; the acc /
-// cost values are those of the wave's IPW owned instances.
-template <int IPW>
-struct QueryBlock {
-  int p, d;
-  double t, tau;
-  double acc[IPW], cost[IPW];
-};
-
-template <int IPW>
-__device__ __forceinline__ QueryBlock<IPW> fetch_block(int base, int N, const int32_t* qp,
-                                                       const int32_t* qd, const double* qt,
-                                                       const double* tau, const double* acc,
-                                                       const double* cost, int n_cols,
-                                                       const int* cols) {
-  QueryBlock<IPW> b;
-  const int i = base + lane_id();
-  const bool in = i < N;
-  b.p = in ? qp[i] : 1;
-  b.d = in ? qd[i] : 1;
-  b.t = in ? qt[i] : 0.0;
-  b.tau = in && tau ? tau[i] : 0.0;
-#pragma unroll
-  for (int r = 0; r < IPW; ++r) {
-    const int64_t o = (int64_t)i * n_cols + cols[r];
-    b.acc[r] = in && cols[r] >= 0 ? acc[o] : 0.0;
-    b.cost[r] = in && cols[r] >= 0 ? cost[o] : 0.0;
-  }
-  return b;
-}
-
-// Candidate of one wave for one query.
-struct Cand {
-  double u, ttft, eq2;
-  int j;
-};
-
-__device__ __forceinline__ void cand_take(Cand& c, double u, int k, double ttft, double eq2) {
-  if (better(u, k, c.u, c.j)) { c.u = u; c.j = k; c.ttft = ttft; c.eq2 = eq2; }
-}
-
-// Candidate exchange between the workgroups of one scenario, run by one wave of
-// each.  Lane 0 posts the workgroup's best (utility, instance) for query i as three
-// 64-bit words -- low and high half of the utility's bits, and the instance index --
-// each carrying the tag i + 1 in its upper 32 bits, into slot set (i & 1).  Lane v
-// polls post v until all three of its words carry the tag, so a post is taken only
-// when it is whole, and the G posts arrive together with the poll: no counter, no
-// fence, one round trip after the last member posts.  All accesses are relaxed
-// agent-scope atomics on the same words, which the memory model keeps coherent.
-// The wait is bounded in wall-clock time (s_memrealtime runs at 100 MHz; 10 s
-// unless the host sets another bound): a member that never posts, or an error
-// raised by another member, ends the trace with kErrSync instead of a hang.  Two slot
-// sets suffice: a member posts query i + 2 only after every member has posted i + 1,
-// i.e. has finished reading the posts of i.
-__device__ __forceinline__ bool cluster_exchange(double& u, int& j, int i, int G, int cid,
-                                                 uint64_t* xs, int32_t* err, SyncCtl sc) {
-  const int ln = lane_id();
-  uint64_t* base = xs + (int64_t)(i & 1) * kMaxCluster * 4;
-  const uint32_t tag = (uint32_t)(i + 1);
-  if (ln == 0 && !(cid == sc.skip_cid && i == sc.skip_query)) {
-    const uint64_t ub = (uint64_t)__double_as_longlong(u);
-    const uint64_t hi = (uint64_t)tag << 32;
-    uint64_t* sl = base + cid * 4;
-    __hip_atomic_store(sl + 0, hi | (ub & 0xffffffffull), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(sl + 1, hi | (ub >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(sl + 2, hi | (uint32_t)j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  // Two polls in flight: while one round trip is under way the other is issued, so
-  // a post is seen about half a round trip sooner than with one poll at a time.
-  uint64_t w0 = 0, w1 = 0, w2 = 0;
-  bool ready = ln >= G;
-  const uint64_t* o = base + (ln < G ? ln : 0) * 4;
-  uint64_t x0 = 0, x1 = 0, x2 = 0;
-  if (!ready) {
-    x0 = __hip_atomic_load(o + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    x1 = __hip_atomic_load(o + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    x2 = __hip_atomic_load(o + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-  for (uint32_t polls = 1;; ++polls) {
-    uint64_t y0 = 0, y1 = 0, y2 = 0;
-    if (!ready) {   // next poll, issued before the previous one is looked at
-      y0 = __hip_atomic_load(o + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      y1 = __hip_atomic_load(o + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      y2 = __hip_atomic_load(o + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if ((uint32_t)(x0 >> 32) == tag && (uint32_t)(x1 >> 32) == tag &&
-          (uint32_t)(x2 >> 32) == tag) {
-        w0 = x0; w1 = x1; w2 = x2;
-        ready = true;
-      }
-    }
-    x0 = y0; x1 = y1; x2 = y2;
-    if (ballot(!ready) == 0) break;
-    // the escape checks cost a round trip of their own: every 256th poll only
-    if ((polls & 255u) == 0) {
-      int bad = 0;
-      if (ln == 0)
-        bad = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == kErrSync ||
-              __builtin_amdgcn_s_memrealtime() - t0 > sc.spin_ticks;
-      if (__builtin_amdgcn_readlane(bad, 0)) {
-        if (ln == 0) set_error(err, kErrSync);
-        return false;
-      }
-    }
-  }
-  double bu = 0.0;
-  int bj = -1;
-  if (ln < G) {
-    bu = __longlong_as_double((long long)((w0 & 0xffffffffull) | (w1 << 32)));
-    bj = (int)(uint32_t)w2;
-  }
-  lane_best(bu, bj, G);
-  u = bu;
-  j = bj;
-  return true;
 }
 
 // Zeroes the per-scenario estimate-batch counters before a trace.
@@ -1592,225 +1303,6 @@ __global__ __launch_bounds__(256) void k_ontime(int N, int I, const int32_t* cho
   if (threadIdx.x == 0) out[z] = __ddiv_rn(s, (double)N);
 }
 
-// ------------------------------------------------------------------ scheduler limits
-// SFS estimate under limits: a private copy of the queue with the query appended at
-// the tail, stepped until the query's first decode (reading 1: its prefill
-// completes).  NaN with an error when the state is behind t, the prompt does not fit
-// the context limit or the batch cap is reached.
-template <int KS>
-__device__ __forceinline__ double lim_estimate(const LQueue<KS>& q, const LEnv& e, int p, int d,
-                                               double t, int reading, int64_t max_iters,
-                                               int32_t* err, int64_t* it_out) {
-  const int ln = lane_id();
-  *it_out = 0;
-  if (q.clock < t) {
-    if (ln == 0) set_error(err, kErrState);
-    return __builtin_nan("");
-  }
-  const int dq = entry_decode(e, p, d);
-  if (p < 1 || dq < 1) {
-    if (ln == 0) set_error(err, kErrArg);
-    return __builtin_nan("");
-  }
-  LQueue<KS> w = q;
-  w.template append<false>(e, p, dq, false, nullptr, -1);
-  double E = w.clock;
-  int64_t it = 0;
-  for (;;) {
-    if (it == max_iters) {
-      if (ln == 0) set_error(err, kErrIter);
-      *it_out = it;
-      return __builtin_nan("");
-    }
-    const LStep o = w.template step<false>(e, nullptr, 0.0, nullptr);
-    E = __dadd_rn(E, o.T);
-    ++it;
-    if (reading == 1 ? o.last_fill : o.last_dec) break;
-  }
-  *it_out = it;
-  return __dsub_rn(E, t);
-}
-
-// Append the query when this queue is the chosen one, then replay every batch that
-// starts before t; an idle queue's clock jumps to t.  TRK: the query is tracked
-// (tag) and first tokens of the replayed batches are recorded.
-template <int KS, bool TRK>
-__device__ __forceinline__ void lim_commit_advance(LQueue<KS>& w, const LEnv& e, bool chosen,
-                                                   int p, int d, double t, int qcap,
-                                                   int64_t max_iters, int32_t* err,
-                                                   int32_t* tags, int tag, const LTrack& tk) {
-  const int ln = lane_id();
-  if (chosen) {
-    const int dq = entry_decode(e, p, d);
-    if (p < 1 || dq < 1) {
-      if (ln == 0) set_error(err, kErrArg);
-    } else if (w.waiting() + 1 > qcap) {
-      if (ln == 0) set_error(err, kErrCapacity);
-    } else {
-      w.template append<TRK>(e, p, dq, true, tags, tag);
-      if constexpr (TRK) w.ntrk += 1;
-    }
-  }
-  double clock = w.clock;
-  int64_t n = 0;
-  while (w.n_list > 0 && clock < t) {
-    if (n == max_iters) {
-      if (ln == 0) set_error(err, kErrIter);
-      break;
-    }
-    const LStep o = w.template step<TRK>(e, tags, clock, &tk);
-    clock = __dadd_rn(clock, o.T);
-    ++n;
-  }
-  if (w.n_list == 0 && clock < t) clock = t;
-  w.clock = clock;
-  w.iters += n;
-}
-
-// What-if estimates under limits: one wave per (scenario, query, instance), instance
-// fastest; reads the state, changes nothing.
-template <int KS>
-__global__ __launch_bounds__(kWave) void k_lest(DevState S, DevParams pr, DevLimits lm, int Z,
-                                               int Q, int I, const int32_t* q_prefill,
-                                               const double* t_ptr, double t_val,
-                                               int max_prompt, int reading, int64_t max_iters,
-                                               double* ttft, int32_t* iters, int32_t* err) {
-  const int64_t pair = blockIdx.x;
-  if (pair >= (int64_t)Z * Q * I) return;
-  const int j = (int)(pair % I);
-  const int z = (int)(pair / ((int64_t)Q * I));
-  const int q = (int)((pair / I) % Q);
-  const int qid = z * I + j;
-  const double t = t_ptr ? *t_ptr : t_val;
-  __shared__ alignas(16) int lds[lim_lds_words<KS>()];
-  const LEnv e = make_lenv(S, pr, lm, qid, j, lds);
-  const int p = q_prefill[q];
-  double v = __builtin_nan("");
-  int64_t it = -1;
-  if (p < 1 || p > max_prompt) {
-    if (lane_id() == 0) set_error(err, kErrArg);
-  } else {
-    LQueue<KS> w;
-    w.template load<false>(S, e, qid, nullptr);
-    v = lim_estimate(w, e, p, 1, t, reading, max_iters, err, &it);
-    if (v != v) it = -1;
-  }
-  if (lane_id() == 0) {
-    ttft[pair] = v;
-    if (iters) iters[pair] = (int32_t)(it < 0x7fffffff ? it : 0x7fffffff);
-  }
-}
-
-template <int KS>
-__global__ __launch_bounds__(kWave) void k_lcommit(DevState S, DevParams pr, DevLimits lm, int Z,
-                                                  int I, const int32_t* choice,
-                                                  int64_t choice_zstride, const int32_t* qp_ptr,
-                                                  const int32_t* qd_ptr, int32_t qp_val,
-                                                  int32_t qd_val, const double* t_ptr,
-                                                  double t_val, int64_t max_iters, int32_t* err) {
-  const int qid = blockIdx.x;
-  if (qid >= Z * I) return;
-  const int z = qid / I;
-  const int j = qid % I;
-  const double t = t_ptr ? *t_ptr : t_val;
-  __shared__ alignas(16) int lds[lim_lds_words<KS>()];
-  const LEnv e = make_lenv(S, pr, lm, qid, j, lds);
-  LQueue<KS> w;
-  w.template load<false>(S, e, qid, nullptr);
-  const bool chosen = choice && choice[(int64_t)z * choice_zstride] == j;
-  const int p = qp_ptr ? *qp_ptr : qp_val;
-  const int d = qd_ptr ? *qd_ptr : qd_val;
-  const LTrack off{nullptr, 0, 0, 0};
-  lim_commit_advance<KS, false>(w, e, chosen, p, d, t, S.qcap, max_iters, err, nullptr, -1, off);
-  w.template store<false>(S, e, qid, nullptr);
-}
-
-// A whole sequential trace under limits, one workgroup per scenario: wave w of nw
-// owns instances j = w + v*nw (states in HBM, loaded per use); per query every owned
-// instance is estimated, the workgroup picks the best, and every instance commits
-// and replays to the next arrival.  TRK: the replay reports realised TTFT.
-template <int KS, int NW, bool TRK>
-__global__ __launch_bounds__(NW * kWave) void k_ltrace(LAR_TRACE_PARAMS, DevLimits lm) {
-  __shared__ double s_u[2][NW], s_t[2][NW], s_q[2][NW];
-  __shared__ int s_j[2][NW];
-  __shared__ alignas(16) int lds[NW][lim_lds_words<KS>()];
-  const int z = blockIdx.x;
-  const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
-  const int nw = blockDim.x / kWave;                 // waves launched (<= NW)
-  const int ln = lane_id();
-  const double wc = w_cost[z];
-  const double wl = w_lat[z];
-  const int j_l = wid + ln * nw;
-  const bool own_l = j_l < I;
-  const int col_l = own_l ? pr.col[j_l] : 0;
-  QueryIn nx = fetch_query(0, N, qp, qd, qt, t_after, tau, acc, cost, n_cols, col_l, own_l);
-  const LTrack tk{TRK ? realized + (int64_t)z * N : nullptr, tag0, N, reading};
-  unsigned long long wbatch = 0;   // batches of this wave's estimates
-  for (int i = 0; i < N; ++i) {
-    const QueryIn q = nx;
-    nx = fetch_query(i + 1, N, qp, qd, qt, t_after, tau, acc, cost, n_cols, col_l, own_l);
-    const bool p_ok = q.p >= 1 && q.p <= max_prompt;
-    if (!p_ok && threadIdx.x == 0) set_error(err, kErrArg);
-    double bu = 0.0, bt = 0.0, bq = 0.0;
-    int bj = -1;
-    for (int v = 0, j = wid; j < I; ++v, j += nw) {
-      const LEnv e = make_lenv(S, pr, lm, z * I + j, j, lds[wid]);
-      LQueue<KS> w;
-      w.template load<false>(S, e, z * I + j, nullptr);
-      int64_t it = 0;
-      const double ttft = p_ok ? lim_estimate(w, e, q.p, q.d, q.t, reading, max_iters, err, &it)
-                               : __builtin_nan("");
-      wbatch += it;
-      double eq2;
-      int k;
-      const double u = utility_lane(q, v, wc, wl, tau, ttft, j, &k, &eq2);
-      if (better(u, k, bu, bj)) { bu = u; bj = k; bt = ttft; bq = eq2; }
-    }
-    const int m = trace_pick<NW>(bu, bj, bt, bq, i, z, N, choice, chosen_ttft, utility, s_u,
-                                 s_t, s_q, s_j);
-    for (int j = wid; j < I; j += nw) {
-      const LEnv e = make_lenv(S, pr, lm, z * I + j, j, lds[wid]);
-      int32_t* tags = TRK ? S.r_tag + (int64_t)(z * I + j) * S.rcap : nullptr;
-      LQueue<KS> w;
-      w.template load<TRK>(S, e, z * I + j, tags);
-      lim_commit_advance<KS, TRK>(w, e, j == m, q.p, q.d, q.tn, S.qcap, max_iters, err, tags,
-                                  tag0 + i, tk);
-      w.template store<TRK>(S, e, z * I + j, tags);
-    }
-  }
-  if (work && lane_id() == 0) atomicAdd(work + z, wbatch);
-}
-
-// Tracked queries still without a first token when a trace under limits ends: a
-// private copy of the queue runs on with no further arrivals until each has it.
-template <int KS>
-__global__ __launch_bounds__(kWave) void k_ldrain(DevState S, DevParams pr, DevLimits lm, int Z,
-                                                 int I, double* realized, int tag0, int N,
-                                                 int reading, int64_t max_iters, int32_t* err) {
-  const int qid = blockIdx.x;
-  if (qid >= Z * I) return;
-  if (S.sc[qid].ntrk <= 0) return;
-  const int z = qid / I;
-  const int j = qid % I;
-  __shared__ alignas(16) int lds[lim_lds_words<KS>()];
-  const LEnv e = make_lenv(S, pr, lm, qid, j, lds);
-  const int32_t* tags = S.r_tag + (int64_t)qid * S.rcap;
-  LQueue<KS> w;
-  w.template load<true>(S, e, qid, tags);
-  const LTrack tk{realized + (int64_t)z * N, tag0, N, reading};
-  double clock = w.clock;
-  int64_t n = 0;
-  while (w.ntrk > 0 && w.n_list > 0) {
-    if (n == max_iters) {
-      if (lane_id() == 0) set_error(err, kErrIter);
-      break;
-    }
-    const LStep o = w.template step<true>(e, tags, clock, &tk);
-    clock = __dadd_rn(clock, o.T);
-    ++n;
-  }
-}
-
 __global__ void k_clear_error(int32_t* err) { *err = 0; }
 
 // ------------------------------------------------------------------ launchers
@@ -1832,11 +1324,6 @@ static hipError_t launch_commit_ks(const LaunchEnv& env, const int32_t* choice,
   return hipGetLastError();
 }
 
-#define LAR_TRACE_ARGS                                                                   \
-  env.S, env.P, env.Z, env.I, a.N, a.qp, a.qd, a.qt, a.t_after, a.acc, a.cost, a.n_cols,     \
-      a.w_cost, a.w_lat, a.tau, env.reading, env.max_prompt, env.max_iters, a.choice,        \
-      a.chosen_ttft, a.utility, env.err, env.work, a.realized, a.tag0
-
 template <int KS, int NW>
 static hipError_t launch_trace_mem(const LaunchEnv& env, const TraceArgs& a) {
   const int nw = env.I < NW ? env.I : NW;
@@ -1848,21 +1335,6 @@ static hipError_t launch_trace_mem(const LaunchEnv& env, const TraceArgs& a) {
     hipLaunchKernelGGL((k_trace_mem<KS, NW, false>), dim3(env.Z), dim3(nw * kWave), 0,
                        env.stream, LAR_TRACE_ARGS);
   return hipGetLastError();
-}
-
-// Every workgroup of a clustered trace must be resident at once (members wait for
-// each other): with the blocks dealt to the 8 XCDs in turn, ceil(Z * G / 8) per XCD
-// must fit its compute units at the kernel's occupancy.
-template <class K>
-static bool co_resident(K kernel, int threads, int Z, int G) {
-  int dev = 0, n_cu = 0, per_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return false;
-  if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-    return false;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess)
-    return false;
-  const int64_t per_xcd = ((int64_t)Z * G + 7) / 8;
-  return per_cu > 0 && per_xcd <= (int64_t)(n_cu / 8) * per_cu;
 }
 
 template <int KS, int W, int IPW, bool TRK>
@@ -1927,68 +1399,6 @@ static hipError_t launch_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
 
 #define DRAIN_ARGS \
   env.S, env.P, env.Z, env.I, a.realized, a.tag0, a.N, env.reading, env.max_iters, env.err
-
-// Scheduler-limit paths: one switch over the slot width each.
-#define LIM_SWITCH(KSV, CALL)                   \
-  switch (env.ks) {                             \
-    case 1: { constexpr int KSV = 1; CALL; } break;   \
-    case 2: { constexpr int KSV = 2; CALL; } break;   \
-    case 4: { constexpr int KSV = 4; CALL; } break;   \
-    case 8: { constexpr int KSV = 8; CALL; } break;   \
-    case 16: { constexpr int KSV = 16; CALL; } break; \
-    default: return hipErrorInvalidValue;       \
-  }
-
-static hipError_t launch_lim_est(const LaunchEnv& env, int Q, const int32_t* q_prefill,
-                                 const double* t_ptr, double t_val, double* ttft,
-                                 int32_t* iters) {
-  const int64_t total = (int64_t)env.Z * Q * env.I;
-  if (total > 0x7fffffff) return hipErrorInvalidValue;
-  LIM_SWITCH(KSV, hipLaunchKernelGGL(k_lest<KSV>, dim3((unsigned)total), dim3(kWave), 0,
-                                     env.stream, env.S, env.P, env.L, env.Z, Q, env.I,
-                                     q_prefill, t_ptr, t_val, env.max_prompt, env.reading,
-                                     env.max_iters, ttft, iters, env.err))
-  return hipGetLastError();
-}
-
-static hipError_t launch_lim_commit(const LaunchEnv& env, const int32_t* choice,
-                                    int64_t choice_zstride, const int32_t* qp_ptr,
-                                    const int32_t* qd_ptr, int32_t qp, int32_t qd,
-                                    const double* t_ptr, double t_val) {
-  LIM_SWITCH(KSV, hipLaunchKernelGGL(k_lcommit<KSV>, dim3(env.Z * env.I), dim3(kWave), 0,
-                                     env.stream, env.S, env.P, env.L, env.Z, env.I, choice,
-                                     choice_zstride, qp_ptr, qd_ptr, qp, qd, t_ptr, t_val,
-                                     env.max_iters, env.err))
-  return hipGetLastError();
-}
-
-// Waves per workgroup of the trace under limits: their LDS areas fill about 80 KiB.
-template <int KS>
-constexpr int lim_trace_waves() { return KS <= 4 ? 16 : (KS == 8 ? 8 : 4); }
-
-template <int KS>
-static hipError_t launch_lim_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
-  constexpr int NW = lim_trace_waves<KS>();
-  const int nw = env.I < NW ? env.I : NW;
-  if ((env.I + nw - 1) / nw > kWave) return hipErrorInvalidValue;   // 64 instances per wave
-  if (a.realized)
-    hipLaunchKernelGGL((k_ltrace<KS, NW, true>), dim3(env.Z), dim3(nw * kWave), 0, env.stream,
-                       LAR_TRACE_ARGS, env.L);
-  else
-    hipLaunchKernelGGL((k_ltrace<KS, NW, false>), dim3(env.Z), dim3(nw * kWave), 0,
-                       env.stream, LAR_TRACE_ARGS, env.L);
-  return hipGetLastError();
-}
-
-static hipError_t launch_lim_trace(const LaunchEnv& env, const TraceArgs& a) {
-  hipError_t e = hipSuccess;
-  LIM_SWITCH(KSV, e = launch_lim_trace_ks<KSV>(env, a))
-  if (e != hipSuccess || !a.realized) return e;
-  LIM_SWITCH(KSV, hipLaunchKernelGGL(k_ldrain<KSV>, dim3(env.Z * env.I), dim3(kWave), 0,
-                                     env.stream, env.S, env.P, env.L, env.Z, env.I, a.realized,
-                                     a.tag0, a.N, env.reading, env.max_iters, env.err))
-  return hipGetLastError();
-}
 
 hipError_t launch_trace(const LaunchEnv& env, const TraceArgs& a) {
   if (env.work) {
@@ -2106,6 +1516,13 @@ hipError_t launch_untag(const LaunchEnv& env) {
   const int64_t n = (int64_t)env.Z * env.I * env.S.rcap;
   hipLaunchKernelGGL(k_untag, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, env.stream,
                      env.S.r_tag, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_clear_exchange(const LaunchEnv& env) {
+  const int64_t n = (int64_t)env.Z * 2 * kMaxCluster * 4;
+  hipLaunchKernelGGL(k_clear_exchange, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                     env.stream, env.xslot, n);
   return hipGetLastError();
 }
 

@@ -72,9 +72,32 @@ hipError_t launch_commit(const LaunchEnv& env, const int32_t* choice, int64_t ch
                          const int32_t* qp_ptr, const int32_t* qd_ptr, int32_t qp, int32_t qd,
                          const double* t_ptr, double t_val);
 hipError_t launch_clear_error(const LaunchEnv& env);
+hipError_t launch_clear_exchange(const LaunchEnv& env);   // clears every scenario's posts
+// the same calls under scheduler limits (sfs_limits.hip)
+hipError_t launch_lim_est(const LaunchEnv& env, int Q, const int32_t* q_prefill,
+                          const double* t_ptr, double t_val, double* ttft, int32_t* iters);
+hipError_t launch_lim_commit(const LaunchEnv& env, const int32_t* choice, int64_t choice_zstride,
+                             const int32_t* qp_ptr, const int32_t* qd_ptr, int32_t qp, int32_t qd,
+                             const double* t_ptr, double t_val);
+hipError_t launch_lim_trace(const LaunchEnv& env, const TraceArgs& a);
 hipError_t launch_untag(const LaunchEnv& env);
 hipError_t launch_stats(const LaunchEnv& env, int N, const int32_t* choice,
                         const double* chosen_ttft, const double* acc, const double* cost,
                         int n_cols, const double* w_cost, double* out);
+
+// Every workgroup of a clustered trace must be resident at once (members wait for
+// each other): with the blocks dealt to the 8 XCDs in turn, ceil(Z * G / 8) per XCD
+// must fit its compute units at the kernel's occupancy.
+template <class K>
+inline bool co_resident(K kernel, int threads, int Z, int G) {
+  int dev = 0, n_cu = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return false;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess)
+    return false;
+  const int64_t per_xcd = ((int64_t)Z * G + 7) / 8;
+  return per_cu > 0 && per_xcd <= (int64_t)(n_cu / 8) * per_cu;
+}
 
 }  // namespace lar

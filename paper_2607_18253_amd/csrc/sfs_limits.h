@@ -217,66 +217,106 @@ struct LQueue {
     next_seq += 1;
   }
 
-  // The batch when it must preempt: lane 0 takes the running requests in list order
-  // over an LDS copy, as the rule states it.  On return dec / chk hold each running
-  // request's tokens, the victims are waiting again (rp, cx updated) and n_run is the
-  // new running count.  Admissions do not happen in such a batch.
+  // The batch when it must preempt, following the rule step by step on an LDS copy
+  // of the running requests.  Only three kinds of request can change the outcome: the
+  // decoding ones that need a new block (in list order), the partial prefills (in
+  // list order) and the victims (from the end); the wave lists the first two and one
+  // lane walks them.  Every other decoding request is served exactly when it is still
+  // running after the walk.  On return dec / chk hold the tokens of each running
+  // request, the victims are waiting again (rp, cx updated) and n_run is the new
+  // running count.  Admissions do not happen in such a batch.
   __device__ void compose_serial(const LEnv& e, int free0, int (&dec)[KS], int (&chk)[KS]) {
     const int ln = lane_id();
+    const int sh = e.sh;
     int* Lrp = e.lds;
     int* Lcx = Lrp + KS * kWave;
-    int* Ldec = Lcx + KS * kWave;
-    int* Lch = Ldec + KS * kWave;
-    int* Lblk = Lch + KS * kWave;
-    int* Lsc = Lblk + KS * kWave;
+    int* Lch = Lcx + KS * kWave;
+    int* Lnd = Lch + KS * kWave;   // positions of the decoding requests that need a block
+    int* Lpt = Lnd + KS * kWave;   // positions of the partial prefills
+    int* Lsc = Lpt + KS * kWave;
+    int nn = 0, np = 0, ndec = 0;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const int i = s * kWave + ln;
-      Lrp[i] = rp[s]; Lcx[i] = cx[s]; Ldec[i] = 0; Lch[i] = 0; Lblk[i] = 0;
+      const bool run = i < n_run;
+      if (run) { Lrp[i] = rp[s]; Lcx[i] = cx[s]; Lch[i] = 0; }
+      const bool isdec = run && rp[s] == 0;
+      const bool needy = isdec && kv_blocks(cx[s] + 1, sh) > kv_blocks(cx[s], sh);
+      const bool part = run && rp[s] > 0;
+      const uint64_t mn = ballot(needy), mp = ballot(part);
+      if (needy) Lnd[nn + mbcnt(mn)] = i;
+      if (part) Lpt[np + mbcnt(mp)] = i;
+      nn += popc(mn);
+      np += popc(mp);
+      ndec += popc(ballot(isdec));
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     if (ln == 0) {
-      const int sh = e.sh;
-      int run = n_run, left = e.k.B, freeb = free0;
-      auto preempt_last = [&]() {
-        const int v = run - 1;
-        freeb += kv_blocks(Lcx[v], sh) + Lblk[v];
-        left += Ldec[v] + Lch[v];
-        Ldec[v] = 0; Lch[v] = 0; Lblk[v] = 0;
-        Lrp[v] += Lcx[v];
-        Lcx[v] = 0;
-        run = v;
-      };
-      for (int r = 0; r < run; ++r) {          // decode tokens
-        if (Lrp[r] != 0) continue;
-        const int need = kv_blocks(Lcx[r] + 1, sh) - kv_blocks(Lcx[r], sh);
-        while (freeb < need && r < run) preempt_last();
+      int run = n_run, freeb = free0, dvict = 0;
+      // decode tokens: each decoding request that needs a block takes one, preempting
+      // from the end while none is free
+      for (int k = 0; k < nn; ++k) {
+        const int r = Lnd[k];
+        while (freeb < 1 && r < run) {
+          const int v = run - 1;
+          const int rv = Lrp[v], cv = Lcx[v];
+          freeb += kv_blocks(cv, sh);
+          dvict += rv == 0 ? 1 : 0;
+          Lrp[v] = rv + cv;
+          Lcx[v] = 0;
+          run = v;
+        }
         if (r >= run) break;
-        Ldec[r] = 1; Lblk[r] = need; freeb -= need; left -= 1;
+        freeb -= 1;
       }
-      for (int r = 0; r < run; ++r) {          // chunks of the partial prefills
-        const int rpr = Lrp[r];
-        if (rpr == 0) continue;
-        int g = min(min(rpr, e.H), left);
-        if (g == 0) continue;
-        const int need = kv_blocks(Lcx[r] + g, sh) - kv_blocks(Lcx[r], sh);
-        while (freeb < need && r < run) preempt_last();
+      const int run1 = run;   // decoding requests below run1 hold a decode token
+      int left = e.k.B - (ndec - dvict);
+      // chunks of the partial prefills; a victim that decodes in this batch returns
+      // its token and the block it took for it
+      for (int k = 0; k < np; ++k) {
+        const int r = Lpt[k];
+        if (r >= run || left == 0) break;
+        const int g = min(min(Lrp[r], e.H), left);
+        const int cr = Lcx[r];
+        const int need = kv_blocks(cr + g, sh) - kv_blocks(cr, sh);
+        while (freeb < need && r < run) {
+          const int v = run - 1;
+          const int rv = Lrp[v], cv = Lcx[v];
+          if (rv == 0 && v < run1) {
+            freeb += kv_blocks(cv + 1, sh);
+            left += 1;
+          } else {
+            freeb += kv_blocks(cv, sh);
+          }
+          Lrp[v] = rv + cv;
+          Lcx[v] = 0;
+          run = v;
+        }
         if (r >= run) break;
-        Lch[r] = g; Lblk[r] = need; freeb -= need; left -= g;
+        Lch[r] = g;
+        freeb -= need;
+        left -= g;
       }
       Lsc[0] = run;
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const int run_end = uni(Lsc[0]);
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const int i = s * kWave + ln;
-      if (i < n_run) { rp[s] = Lrp[i]; cx[s] = Lcx[i]; dec[s] = Ldec[i]; chk[s] = Lch[i]; }
+      if (i < n_run) {
+        const bool isdec = rp[s] == 0;
+        dec[s] = (isdec && i < run_end) ? 1 : 0;
+        chk[s] = (!isdec && i < run_end) ? Lch[i] : 0;
+        rp[s] = Lrp[i];
+        cx[s] = Lcx[i];
+      }
     }
-    n_run = uni(Lsc[0]);
+    n_run = run_end;
     // the LDS area is reused by the next batch
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -329,44 +369,58 @@ struct LQueue {
   }
 
   // One batch: compose, time, (TRK) first tokens at the batch end clk0 + T, apply.
+  // Only the window rows that hold entries are visited (wave-uniform row count), the
+  // chunk pass is skipped when no request has prefill left, and the admission pass
+  // when no request waits.
   template <bool TRK>
   __device__ LStep step(const LEnv& e, const int32_t* tags, double clk0, const LTrack* tk) {
     const int ln = lane_id();
     const int sh = e.sh;
     const bool kv = e.K > 0;
     const int B = e.k.B, M = e.k.M;
+    const int nrows = (nwin + kWave - 1) >> 6;
     int dec[KS], chk[KS];
     bool wait[KS];
     // decoding requests, their new blocks, the blocks held
     int nd = 0, held = 0, need = 0;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      const int i = s * kWave + ln;
-      const bool run = i < n_run;
-      dec[s] = (run && rp[s] == 0) ? 1 : 0;
-      nd += dec[s];
-      if (kv && run) {
-        const int h = kv_blocks(cx[s], sh);
-        held += h;
-        if (dec[s]) need += kv_blocks(cx[s] + 1, sh) - h;
+      dec[s] = 0; chk[s] = 0; wait[s] = false;
+      if (s < nrows) {
+        const int i = s * kWave + ln;
+        const bool run = i < n_run;
+        dec[s] = (run && rp[s] == 0) ? 1 : 0;
+        nd += dec[s];
+        if (kv && run) {
+          const int h = kv_blocks(cx[s], sh);
+          held += h;
+          if (dec[s]) need += kv_blocks(cx[s] + 1, sh) - h;
+        }
       }
     }
     int D = wave_sum32(nd);
     const int L1 = B - D;
+    const bool waiting_any = n_list > n_run;
+    const bool prefill_any = waiting_any || n_run > D;
     // chunks: each partial prefill, then each waiting request within the sequence
     // cap, wants min(rp, H); the budget left after the decodes goes to them in list
     // order (exclusive saturating prefix sums, row by row)
-    unsigned carry = 0;
+    if (prefill_any) {
+      unsigned carry = 0;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const int i = s * kWave + ln;
-      const bool part = i < n_run && rp[s] > 0;
-      wait[s] = i >= n_run && i < nwin && i < M;
-      const int want = (part || wait[s]) ? min(min(rp[s], e.H), L1) : 0;
-      const unsigned excl = min((unsigned)scan_sat(prev_lane(want), L1) + carry, (unsigned)L1);
-      chk[s] = min(want, L1 - (int)excl);
-      carry = (unsigned)uni(lane_last((int)min(excl + (unsigned)want, (unsigned)L1)));
-      if (kv && part) need += kv_blocks(cx[s] + chk[s], sh) - kv_blocks(cx[s], sh);
+      for (int s = 0; s < KS; ++s) {
+        if (s < nrows) {
+          const int i = s * kWave + ln;
+          const bool part = i < n_run && rp[s] > 0;
+          wait[s] = i >= n_run && i < nwin && i < M;
+          const int want = (part || wait[s]) ? min(min(rp[s], e.H), L1) : 0;
+          const unsigned excl =
+              min((unsigned)scan_sat(prev_lane(want), L1) + carry, (unsigned)L1);
+          chk[s] = min(want, L1 - (int)excl);
+          carry = (unsigned)uni(lane_last((int)min(excl + (unsigned)want, (unsigned)L1)));
+          if (kv && part) need += kv_blocks(cx[s] + chk[s], sh) - kv_blocks(cx[s], sh);
+        }
+      }
     }
     bool preempted = false;
     int room = 0;
@@ -385,18 +439,23 @@ struct LQueue {
 #pragma unroll
       for (int s = 0; s < KS; ++s) x += dec[s];
       D = wave_sum32(x);
-    } else {
+    } else if (waiting_any) {
       // admissions: a prefix of the waiting requests, cut where the budget, the
       // sequence cap or the blocks of a first chunk run out
       int bcarry = 0, nadm = 0;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
-        const int need3 = (kv && wait[s] && chk[s] > 0) ? kv_blocks(chk[s], sh) : 0;
-        const int cum = scan_add32(need3) + bcarry;
-        bcarry = uni(lane_last(cum));
-        const bool ok = wait[s] && chk[s] > 0 && (!kv || cum <= room);
-        if (wait[s] && !ok) chk[s] = 0;
-        nadm += ok ? 1 : 0;
+        if (s < nrows && (s + 1) * kWave > n_run) {
+          const int need3 = (kv && wait[s] && chk[s] > 0) ? kv_blocks(chk[s], sh) : 0;
+          int cum = bcarry;
+          if (kv) {
+            cum += scan_add32(need3);
+            bcarry = uni(lane_last(cum));
+          }
+          const bool ok = wait[s] && chk[s] > 0 && (!kv || cum <= room);
+          if (wait[s] && !ok) chk[s] = 0;
+          nadm += ok ? 1 : 0;
+        }
       }
       admitted = wave_sum32(nadm);
     }
@@ -405,11 +464,14 @@ struct LQueue {
     int64_t C = 0, A = 0;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      P += chk[s];
-      if (e.need_C && dec[s]) C += cx[s];
-      if (e.need_A && chk[s]) A += (int64_t)chk[s] * cx[s] + (int64_t)chk[s] * (chk[s] + 1) / 2;
+      if (s < nrows) {
+        P += chk[s];
+        if (e.need_C && dec[s]) C += cx[s];
+        if (e.need_A && chk[s])
+          A += (int64_t)chk[s] * cx[s] + (int64_t)chk[s] * (chk[s] + 1) / 2;
+      }
     }
-    P = wave_sum32(P);
+    P = prefill_any ? wave_sum32(P) : 0;
     if (e.need_C) C = wave_sum64(C);
     if (e.need_A) A = wave_sum64(A);
     LStep o;
@@ -420,7 +482,10 @@ struct LQueue {
     bool ld = false, lf = false;
 #pragma unroll
     for (int s = 0; s < KS; ++s)
-      if (s * kWave + ln == lp) { ld = dec[s] != 0; lf = chk[s] > 0 && chk[s] == rp[s]; }
+      if (s == (lp >> 6) && ln == (lp & (kWave - 1))) {
+        ld = dec[s] != 0;
+        lf = chk[s] > 0 && chk[s] == rp[s];
+      }
     o.last_dec = ballot(ld) != 0;
     o.last_fill = ballot(lf) != 0;
     if constexpr (TRK) {
@@ -428,12 +493,15 @@ struct LQueue {
       int hit = 0;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
-        const bool first = tk->reading == 1 ? (chk[s] > 0 && chk[s] == rp[s]) : dec[s] != 0;
-        const int q = tg[s] - tk->tag0;
-        if (first && tg[s] >= 0 && q >= 0 && q < tk->N) {
-          tk->out[q] = end;
-          tg[s] = -1;
-          ++hit;
+        if (s < nrows) {
+          const bool first =
+              tk->reading == 1 ? (chk[s] > 0 && chk[s] == rp[s]) : dec[s] != 0;
+          const int q = tg[s] - tk->tag0;
+          if (first && tg[s] >= 0 && q >= 0 && q < tk->N) {
+            tk->out[q] = end;
+            tg[s] = -1;
+            ++hit;
+          }
         }
       }
       ntrk -= wave_sum32(hit);
@@ -443,10 +511,13 @@ struct LQueue {
     int nf = 0;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      if (dec[s]) { cx[s] += 1; rd[s] -= 1; }
-      if (chk[s]) { cx[s] += chk[s]; rp[s] -= chk[s]; }
-      fin[s] = dec[s] && rd[s] == 0;
-      nf += fin[s] ? 1 : 0;
+      fin[s] = false;
+      if (s < nrows) {
+        if (dec[s]) { cx[s] += 1; rd[s] -= 1; }
+        if (chk[s]) { cx[s] += chk[s]; rp[s] -= chk[s]; }
+        fin[s] = dec[s] && rd[s] == 0;
+        nf += fin[s] ? 1 : 0;
+      }
     }
     n_run += admitted;
     nf = wave_sum32(nf);
