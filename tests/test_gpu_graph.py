@@ -22,9 +22,12 @@ from paper_2607_18253_amd import context_for  # noqa: E402
 from workloads import make_workload  # noqa: E402
 
 
-@pytest.mark.parametrize("objective", ["lagrangian", "constrained"])
-def test_route_step_graph_replays(objective):
-    wl = make_workload("c2", n_q=400, n_inst=8)
+@pytest.mark.parametrize("objective,workload", [("lagrangian", "c2"), ("constrained", "c2"),
+                                                ("lagrangian", "c7")])
+def test_route_step_graph_replays(objective, workload):
+    """c7 runs the same step under scheduler limits (KV blocks, chunk cap, context
+    limit): what-if, route and commit of the limits engine in the graph."""
+    wl = make_workload(workload, n_q=400, n_inst=8)
     N, dev = wl.n_q, "cuda:0"
     tau = O.ttft_targets(wl.q_prefill, wl.tau_u_ms, wl.tau_v) if objective == "constrained" else None
     ref = O.trace(wl, tau=tau)

@@ -167,3 +167,30 @@ def test_limits_c7_prefix_reading_prefill_constrained():
     tau = O.ttft_targets(wl.q_prefill, wl.tau_u_ms, wl.tau_v)
     print("c7 prefix 1500 constrained reading 1", flush=True)
     _check(wl, _trace(wl, flags=1, tau=tau), reading=1, tau=tau)
+
+
+def test_limits_c7_full():
+    """The whole c7 trace (100k queries, 32 instances) in the launch configuration the
+    benchmark times, with realised TTFT: every choice, chosen TTFT, utility and
+    realised-TTFT bit and the final state equal the oracle's."""
+    wl = make_workload("c7")
+    print("c7 full", flush=True)
+    _check(wl, _trace(wl))
+
+
+def test_limits_c7_full_constrained_ontime():
+    """The whole c7 trace under Eq. 3 with the paper's targets; OnTimeUtility from the
+    realised TTFTs."""
+    wl = make_workload("c7")
+    tau = O.ttft_targets(wl.q_prefill, wl.tau_u_ms, wl.tau_v)
+    print("c7 full constrained", flush=True)
+    got = _trace(wl, tau=tau)
+    choice, real, ctx = got[0], got[3], got[4]
+    out = ctx.ontime_utility(T(choice, torch.int32), T(real, torch.float64),
+                             T(tau, torch.float64), T(wl.acc, torch.float64),
+                             T(wl.cost, torch.float64), T(wl.w_cost, torch.float64))
+    ctx.sync()
+    ref = O.trace(wl, tau=tau, max_iters=MAX_ITERS, final_state=False)
+    want = O.ontime_utility(ref.choice, ref.realized, tau, wl.acc, wl.cost, wl.col, wl.w_cost[0])
+    assert bits(out.cpu().numpy())[0] == bits(np.array([want]))[0]
+    _check(wl, got, tau=tau)
