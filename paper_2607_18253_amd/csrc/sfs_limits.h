@@ -98,7 +98,6 @@ struct LStep {
   double T;        // batch time
   bool last_dec;   // the last list entry received a decode token
   bool last_fill;  // the last list entry's prefill completed
-  bool preempted;
 };
 
 template <int KS>
@@ -475,7 +474,6 @@ struct LQueue {
     if (e.need_C) C = wave_sum64(C);
     if (e.need_A) A = wave_sum64(A);
     LStep o;
-    o.preempted = preempted;
     o.T = batch_time(e.k, P, D, C, A);
     // the last list entry (an estimate's query)
     const int lp = n_list - 1;

@@ -194,3 +194,71 @@ def test_limits_c7_full_constrained_ontime():
     want = O.ontime_utility(ref.choice, ref.realized, tau, wl.acc, wl.cost, wl.col, wl.w_cost[0])
     assert bits(out.cpu().numpy())[0] == bits(np.array([want]))[0]
     _check(wl, got, tau=tau)
+
+
+def test_limits_error_paths():
+    """Bad limits are rejected with nothing changed; calls between lar_set_scheduler and
+    the next load report LAR_E_STATE; a snapshot breaking the limits is LAR_E_STATE; a
+    query whose prompt does not fit the context limit sets the sticky LAR_E_ARG."""
+    from paper_2607_18253_amd.lar import LAR_E_ARG, LAR_E_STATE, LarError
+    wl = make_tiny_sched_workload(7, n_q=6, max_res=4)
+    ctx = context_for(wl, max_iters=MAX_ITERS)
+    bad = wl.sched.copy()
+    bad[0] = (0, 4, 3, 8)          # block size not a power of two
+    with pytest.raises(LarError) as e:
+        ctx.set_scheduler(bad)
+    assert e.value.code == LAR_E_ARG
+    bad[0] = (0, 2, 2, 8)          # 2 blocks of 2 tokens < context limit 8
+    with pytest.raises(LarError) as e:
+        ctx.set_scheduler(bad)
+    assert e.value.code == LAR_E_ARG
+    bad[0] = (0, 4, 2, 0)          # a KV cache without a context limit
+    with pytest.raises(LarError) as e:
+        ctx.set_scheduler(bad)
+    assert e.value.code == LAR_E_ARG
+    ctx.advance(float(wl.q_t_ms[0]))   # the context is unchanged: still loaded
+    ctx.sync()
+    ctx.set_scheduler(wl.sched)    # valid: the state must be loaded again
+    with pytest.raises(LarError) as e:
+        ctx.advance(float(wl.q_t_ms[0]))
+    assert e.value.code == LAR_E_STATE
+    tight = wl.sched.copy()
+    rp, rd, cx = wl.instance_requests(0)
+    tight[0, 3] = int((rp + cx).max())   # a resident at the context limit
+    tight[0, 1] = 0
+    if len(rp):
+        ctx.set_scheduler(tight)
+        with pytest.raises(LarError) as e:
+            ctx.load_workload(wl)
+        assert e.value.code == LAR_E_STATE
+    ctx.set_scheduler(wl.sched)
+    ctx.load_workload(wl)
+    ctx.advance(float(wl.q_t_ms[0]))
+    ctx.sync()
+    ctx.close()
+    # the prompt limit of the context and the context limit together: a trace whose
+    # query does not fit one instance's context limit
+    wl2 = make_tiny_sched_workload(8, n_q=6, max_res=4)
+    wl2.sched[:, 3] = np.maximum(wl2.sched[:, 3], 30)
+    wl2.sched[:, 1] = 0
+    wl2.sched[0, 3] = int(max((lambda r: (r[0] + r[2]).max() if len(r[0]) else 0)(
+        wl2.instance_requests(0)), 2)) + 1
+    wl2.q_prefill[:] = np.minimum(wl2.q_prefill, 12)
+    wl2.q_prefill[2] = wl2.sched[0, 3]            # does not fit instance 0
+    wl2.max_prompt = 40
+    ctx = context_for(wl2, max_iters=MAX_ITERS)
+    ctx.advance(float(wl2.q_t_ms[0]))
+    ctx.estimate(T(wl2.q_prefill[2:3], torch.int32), float(wl2.q_t_ms[0]))   # what-if
+    with pytest.raises(LarError) as e:
+        ctx.sync()
+    assert e.value.code == LAR_E_ARG
+    ctx.load_workload(wl2)   # clears the sticky error
+    ctx.advance(float(wl2.q_t_ms[0]))
+    with pytest.raises(LarError) as e:
+        ctx.route_trace(T(wl2.q_prefill, torch.int32), T(wl2.q_decode, torch.int32),
+                        T(wl2.q_t_ms, torch.float64), float(wl2.q_t_ms[-1]),
+                        T(wl2.acc, torch.float64), T(wl2.cost, torch.float64),
+                        T(wl2.w_cost, torch.float64), T(wl2.w_lat_ms, torch.float64))
+        ctx.sync()
+    assert e.value.code == LAR_E_ARG
+    ctx.close()
