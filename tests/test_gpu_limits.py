@@ -262,3 +262,26 @@ def test_limits_error_paths():
         ctx.sync()
     assert e.value.code == LAR_E_ARG
     ctx.close()
+
+
+def test_limits_reload_repeat():
+    """The benchmark's step under limits: reload the snapshot, replay to the first
+    arrival, trace; two steps give the oracle's results both times."""
+    wl = make_workload("c7", n_q=2000, n_inst=16)
+    ref = O.trace(wl, max_iters=MAX_ITERS)
+    ctx = context_for(wl, max_iters=MAX_ITERS)
+    N = wl.n_q
+    for rep in range(2):
+        ctx.reload_state()
+        ctx.advance(float(wl.q_t_ms[0]))
+        chosen = torch.full((1, N), -1.0, dtype=torch.float64, device=DEV)
+        choice = ctx.route_trace(T(wl.q_prefill, torch.int32), T(wl.q_decode, torch.int32),
+                                 T(wl.q_t_ms, torch.float64), float(wl.q_t_ms[-1]),
+                                 T(wl.acc, torch.float64), T(wl.cost, torch.float64),
+                                 T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64),
+                                 chosen_ttft=chosen)
+        ctx.sync()
+        np.testing.assert_array_equal(choice.cpu().numpy()[0], ref.choice, err_msg=f"step {rep}")
+        np.testing.assert_array_equal(bits(chosen.cpu().numpy()[0]), bits(ref.ttft_chosen))
+        assert_state_equal(ctx, 0, ref)
+    ctx.close()

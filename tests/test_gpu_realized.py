@@ -135,11 +135,13 @@ def test_realized_tracking_leaves_trace_unchanged():
     ctx1.close()
 
 
-def test_realized_split_calls():
+@pytest.mark.parametrize("name", ["c2", "c7"])
+def test_realized_split_calls(name):
     """One context, two trace calls: each call reports its own queries, and its end
     is the end of arrivals for the queries still waiting for a first token, so call
-    1 equals the oracle's trace of the prefix and call 2 the whole trace's tail."""
-    wl = make_workload("c2", n_q=1200, n_inst=8)
+    1 equals the oracle's trace of the prefix and call 2 the whole trace's tail (c7:
+    under scheduler limits)."""
+    wl = make_workload(name, n_q=1200, n_inst=8)
     N, N1 = wl.n_q, 500
     ctx = context_for(wl)
     ctx.advance(float(wl.q_t_ms[0]))
@@ -160,12 +162,13 @@ def test_realized_split_calls():
     ctx.close()
 
 
-def test_realized_tag_counter_wrap(monkeypatch):
+@pytest.mark.parametrize("name", ["c2", "c7"])
+def test_realized_tag_counter_wrap(monkeypatch, name):
     """The tag counter starts just below its end: the first call's tags run up to it,
     the second call wraps (every ring slot untagged, tags from 0 again); both calls
-    still report exactly the oracle's realised TTFTs."""
+    still report exactly the oracle's realised TTFTs (c7: under scheduler limits)."""
     monkeypatch.setenv("LAR_TEST_TAG_START", str(2 ** 31 - 1 - 1000))
-    wl = make_workload("c2", n_q=1200, n_inst=8)
+    wl = make_workload(name, n_q=1200, n_inst=8)
     N, N1 = wl.n_q, 500
     ctx = context_for(wl)
     monkeypatch.delenv("LAR_TEST_TAG_START")
