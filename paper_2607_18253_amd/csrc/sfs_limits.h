@@ -98,6 +98,7 @@ struct LStep {
   double T;        // batch time
   bool last_dec;   // the last list entry received a decode token
   bool last_fill;  // the last list entry's prefill completed
+  bool tail_ok;    // (TAIL steps) a new request at the tail could have been admitted
 };
 
 template <int KS>
@@ -370,8 +371,11 @@ struct LQueue {
   // One batch: compose, time, (TRK) first tokens at the batch end clk0 + T, apply.
   // Only the window rows that hold entries are visited (wave-uniform row count), the
   // chunk pass is skipped when no request has prefill left, and the admission pass
-  // when no request waits.
-  template <bool TRK>
+  // when no request waits.  TAIL: also report whether a request appended at the tail
+  // before this batch could have been admitted in it -- no preemption, every waiting
+  // request admitted, a sequence slot, budget and a KV block left -- which every
+  // admission needs, whatever the request's prompt.
+  template <bool TRK, bool TAIL = false>
   __device__ LStep step(const LEnv& e, const int32_t* tags, double clk0, const LTrack* tk) {
     const int ln = lane_id();
     const int sh = e.sh;
@@ -441,7 +445,7 @@ struct LQueue {
     } else if (waiting_any) {
       // admissions: a prefix of the waiting requests, cut where the budget, the
       // sequence cap or the blocks of a first chunk run out
-      int bcarry = 0, nadm = 0;
+      int bcarry = 0, nadm = 0, nblk = 0;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
         if (s < nrows && (s + 1) * kWave > n_run) {
@@ -454,9 +458,11 @@ struct LQueue {
           const bool ok = wait[s] && chk[s] > 0 && (!kv || cum <= room);
           if (wait[s] && !ok) chk[s] = 0;
           nadm += ok ? 1 : 0;
+          if constexpr (TAIL) nblk += ok ? need3 : 0;
         }
       }
       admitted = wave_sum32(nadm);
+      if constexpr (TAIL) room -= kv ? wave_sum32(nblk) : 0;
     }
     // features and time
     int P = 0;
@@ -475,6 +481,10 @@ struct LQueue {
     if (e.need_A) A = wave_sum64(A);
     LStep o;
     o.T = batch_time(e.k, P, D, C, A);
+    o.tail_ok = false;
+    if constexpr (TAIL)
+      o.tail_ok = !preempted && admitted == n_list - n_run && n_run + admitted < M &&
+                  L1 - P > 0 && (!kv || room >= 1);
     // the last list entry (an estimate's query)
     const int lp = n_list - 1;
     bool ld = false, lf = false;

@@ -59,6 +59,36 @@ __device__ __forceinline__ double lim_estimate(const LQueue<KS>& q, const LEnv& 
   return __dsub_rn(E, t);
 }
 
+// The state of a queue just before the first batch in which a request appended at
+// its tail could be admitted (whatever its prompt).  Batches before that one do not
+// depend on such a request -- it waits behind requests that are not all admitted, or
+// no slot, budget or KV block is left for it, or the batch preempts -- so an estimate
+// from the returned state F, whose clock is the left fold of those batches' times
+// from the queue's own clock, equals the estimate from the queue.  n receives their
+// number.  False (and the error set) when the batch cap is reached first.
+template <int KS>
+__device__ __forceinline__ bool lim_frontier(const LQueue<KS>& q, const LEnv& e, LQueue<KS>& F,
+                                             int64_t& n, int64_t max_iters, int32_t* err) {
+  LQueue<KS> g = q;
+  double E = g.clock;
+  n = 0;
+  while (g.n_list > 0) {
+    if (n == max_iters) {
+      if (lane_id() == 0) set_error(err, kErrIter);
+      return false;
+    }
+    LQueue<KS> h = g;
+    const LStep o = h.template step<false, true>(e, nullptr, 0.0, nullptr);
+    if (o.tail_ok) break;
+    E = __dadd_rn(E, o.T);
+    ++n;
+    g = h;
+  }
+  F = g;
+  F.clock = E;
+  return true;
+}
+
 // Append the query when this queue is the chosen one, then replay every batch that
 // starts before t; an idle queue's clock jumps to t.  TRK: the query is tracked
 // (tag) and first tokens of the replayed batches are recorded.
@@ -214,8 +244,10 @@ __global__ __launch_bounds__(NW * kWave) void k_ltrace(LAR_TRACE_PARAMS, DevLimi
 // in registers for the whole trace (the ring beyond it in HBM).  Per query i: the
 // workgroup's best candidate (LDS), the exchange with the other members, the outputs
 // from the wave holding the winner, then every wave commits i and replays its
-// instance to the next arrival and estimates query i + 1.  TRK: the replay reports
-// realised TTFT.
+// instance to the next arrival and estimates query i + 1 from the instance's cached
+// admission point (lim_frontier), which stays valid while the instance receives no
+// query and its replay has not passed that point.  TRK: the replay reports realised
+// TTFT.
 template <int KS, int W, bool TRK>
 __global__ __launch_bounds__(W * kWave) void k_ltrace_cl(LAR_TRACE_PARAMS, DevLimits lm, int G,
                                                         uint64_t* xslot, SyncCtl sc) {
@@ -248,6 +280,10 @@ __global__ __launch_bounds__(W * kWave) void k_ltrace_cl(LAR_TRACE_PARAMS, DevLi
   unsigned long long wbatch = 0;   // batches of this wave's estimates
   Cand c;
   c.j = -1; c.u = 0.0; c.ttft = 0.0; c.eq2 = 0.0;
+  LQueue<KS> F;             // cached admission point of the owned instance
+  bool f_ok = false;
+  bool f_skip = false;      // the last search found the point at once: estimate directly
+  int64_t f_iters = 0;      // the instance's replay count at F
   for (int i = -1; i < N; ++i) {
     const int l = i & (kWave - 1);
     const bool last_in_block = i >= 0 && l == kWave - 1;
@@ -285,9 +321,14 @@ __global__ __launch_bounds__(W * kWave) void k_ltrace_cl(LAR_TRACE_PARAMS, DevLi
         if (chosen_ttft) chosen_ttft[o] = c.ttft;
         if (utility && m >= 0) utility[o] = c.eq2;
       }
-      if (own)
+      if (own) {
         lim_commit_advance<KS, TRK>(Q, e, j == m, p, dq, tn, S.qcap, max_iters, err, tags,
                                     tag0 + i, tk);
+        // F stays the admission point while the replay has not run its batch
+        if (j == m || Q.iters > f_iters || (Q.iters == f_iters && Q.clock != F.clock))
+          f_ok = false;
+        if (j == m) f_skip = false;
+      }
     }
     c.j = -1; c.u = 0.0; c.ttft = 0.0; c.eq2 = 0.0;
     if (i + 1 < N) {
@@ -300,8 +341,26 @@ __global__ __launch_bounds__(W * kWave) void k_ltrace_cl(LAR_TRACE_PARAMS, DevLi
       if (!p1_ok && threadIdx.x == 0 && cid == 0) set_error(err, kErrArg);
       if (own) {
         int64_t it = 0;
-        const double ttft = p1_ok ? lim_estimate(Q, e, p1, d1, t1, reading, max_iters, err, &it)
-                                  : __builtin_nan("");
+        double ttft = __builtin_nan("");
+        if (p1_ok && Q.clock < t1) {
+          if (ln == 0) set_error(err, kErrState);
+        } else if (p1_ok) {
+          // a search that finds the point at once saves nothing and costs a batch: after
+          // one, the instance is estimated directly until it receives a query
+          if (!f_ok && !f_skip) {
+            int64_t nf = 0;
+            f_ok = lim_frontier(Q, e, F, nf, max_iters, err);
+            f_iters = Q.iters + nf;
+            if (f_ok && nf == 0) { f_ok = false; f_skip = true; }
+          }
+          if (f_ok) {
+            const int64_t pre = f_iters - Q.iters;   // batches before F, folded in F's clock
+            ttft = lim_estimate(F, e, p1, d1, t1, reading, max_iters - pre, err, &it);
+            it += pre;
+          } else {
+            ttft = lim_estimate(Q, e, p1, d1, t1, reading, max_iters, err, &it);
+          }
+        }
         wbatch += it;
         const double a = read_lane_f64(in_nxt ? nxt.acc[0] : cur.acc[0], l1);
         const double co = read_lane_f64(in_nxt ? nxt.cost[0] : cur.cost[0], l1);
