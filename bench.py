@@ -159,7 +159,7 @@ def oracle_sample(wl, budget_s, tau=None):
            "sample": f"scenario 0, first {n} of {wl.n_q} queries ({est} estimates + the "
                      f"replay; {dt:.2f} s single-threaded)",
            "routed_queries_per_s": n / dt}
-    return rec, n, batches
+    return rec, n, batches, r
 
 
 def whatif_oracle_sample(wl, budget_s):
@@ -167,18 +167,30 @@ def whatif_oracle_sample(wl, budget_s):
     rng = np.random.default_rng(1)
     n, t_used, batches = 0, 0.0, 0
     qs = {}
+    pairs = []
     t0 = time.perf_counter()
     while time.perf_counter() - t0 < budget_s:
         i, j = int(rng.integers(wl.n_q)), int(rng.integers(wl.n_inst))
         if j not in qs:
             qs[j] = orc.instance_queue(wl, j)
-        _, it = qs[j].estimate(int(wl.q_prefill[i]), 1, 0.0)
+        tt, it = qs[j].estimate(int(wl.q_prefill[i]), 1, 0.0)
+        pairs.append((i, j, tt))
         batches += it
         n += 1
     dt = time.perf_counter() - t0
     return {"value": n / dt, "unit": "TTFT estimates/s", "cores": 1, "kind": "oracle",
             "sample": f"{n} random (query, instance) pairs, literal per-pair SFS "
-                      f"({dt:.1f} s single-threaded)"}, batches / max(n, 1)
+                      f"({dt:.1f} s single-threaded)"}, batches / max(n, 1), pairs
+
+
+def parity_record(got, want, what):
+    """Bit-level comparison of GPU results with the oracle's on the same sample."""
+    got = np.ascontiguousarray(got, np.float64)
+    want = np.ascontiguousarray(want, np.float64)
+    rel = np.abs(got - want) / np.maximum(np.abs(want), 1e-300)
+    return {"compared": what, "n": int(got.size),
+            "ttft_bits_equal": bool(np.array_equal(got.view(np.int64), want.view(np.int64))),
+            "max_rel_ttft_err": float(rel.max()) if got.size else 0.0}
 
 
 import numpy as np  # noqa: E402
@@ -337,8 +349,12 @@ def main():
         line["batches_per_step"] = batches
     if not args.no_cpu_baseline:
         if whatif:
-            rec, batches_per_pair = whatif_oracle_sample(wl, args.cpu_seconds)
+            rec, batches_per_pair, pairs = whatif_oracle_sample(wl, args.cpu_seconds)
             line["cpu_baseline"] = rec
+            tt = ttft[0].cpu().numpy()
+            line["parity_vs_oracle"] = parity_record(
+                [tt[i, j] for i, j, _ in pairs], [x for _, _, x in pairs],
+                "TTFT of the oracle's sampled (query, instance) pairs, scenario 0")
             # HBM-bound output: the fp64 TTFT matrix written once, plus per-query and
             # per-instance inputs (negligible); algorithmic bytes per estimate = 8
             achieved = Z * N * I * 8 / (kernel_ms / 1000.0) / 1e9
@@ -348,11 +364,16 @@ def main():
                             f"a literal per-pair SFS would simulate {batches_per_pair:.0f} "
                             "batches per pair"}
         else:
-            rec, n, obatches = oracle_sample(
+            rec, n, obatches, ref = oracle_sample(
                 wl, args.cpu_seconds, tau=None if tau is None else tau.cpu().numpy())
             line["cpu_baseline"] = rec
             if n == N and Z == 1:
                 rec["oracle_batches"] = obatches
+            # the last timed step's results against the oracle's on the same prefix
+            par = parity_record(chosen[0, :n].cpu().numpy(), ref.ttft_chosen,
+                                f"chosen TTFT of queries 0..{n - 1}, scenario 0")
+            par["mismatched_choices"] = int((choice[0, :n].cpu().numpy() != ref.choice).sum())
+            line["parity_vs_oracle"] = par
     line["roofline"] = roof
     print(json.dumps(line), flush=True)
     ctx.close()
