@@ -285,3 +285,40 @@ def test_limits_reload_repeat():
         np.testing.assert_array_equal(bits(chosen.cpu().numpy()[0]), bits(ref.ttft_chosen))
         assert_state_equal(ctx, 0, ref)
     ctx.close()
+
+
+def test_limits_capacity_and_iteration_cap():
+    """Under limits, a full waiting queue is a sticky LAR_E_CAPACITY and an estimate or
+    replay past max_iters a sticky LAR_E_ITER, as the oracle reports them."""
+    from paper_2607_18253_amd.lar import LAR_E_CAPACITY, LAR_E_ITER, LarError
+    wl = make_workload("c7", n_q=300, n_inst=4)
+    ref_err = None
+    try:
+        O.trace(wl, queue_cap=130, max_iters=MAX_ITERS)
+    except O.OracleError as e:
+        ref_err = e.code
+    assert ref_err == O.E_CAPACITY
+    ctx = context_for(wl, max_iters=MAX_ITERS, queue_cap=130)
+    ctx.advance(float(wl.q_t_ms[0]))
+    with pytest.raises(LarError) as e:
+        ctx.route_trace(T(wl.q_prefill, torch.int32), T(wl.q_decode, torch.int32),
+                        T(wl.q_t_ms, torch.float64), float(wl.q_t_ms[-1]),
+                        T(wl.acc, torch.float64), T(wl.cost, torch.float64),
+                        T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64))
+        ctx.sync()
+    assert e.value.code == LAR_E_CAPACITY
+    ctx.close()
+    # an estimate of the first query needs more batches than the cap allows
+    with pytest.raises(O.OracleError) as oe:
+        O.trace(wl, n_q=1, max_iters=5)
+    assert oe.value.code == O.E_ITER
+    ctx = context_for(wl, max_iters=5)
+    ctx.advance(float(wl.q_t_ms[0]))
+    with pytest.raises(LarError) as e:
+        ctx.route_trace(T(wl.q_prefill[:1], torch.int32), T(wl.q_decode[:1], torch.int32),
+                        T(wl.q_t_ms[:1], torch.float64), float(wl.q_t_ms[0]),
+                        T(wl.acc[:1], torch.float64), T(wl.cost[:1], torch.float64),
+                        T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64))
+        ctx.sync()
+    assert e.value.code == LAR_E_ITER
+    ctx.close()
