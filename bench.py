@@ -183,6 +183,24 @@ def whatif_oracle_sample(wl, budget_s):
                       f"({dt:.1f} s single-threaded)"}, batches / max(n, 1), pairs
 
 
+def host_cpu():
+    """The host's CPU model and the threads available to this process."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        threads = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        threads = os.cpu_count() or 0
+    return model, threads
+
+
 def parity_record(got, want, what):
     """Bit-level comparison of GPU results with the oracle's on the same sample."""
     got = np.ascontiguousarray(got, np.float64)
@@ -348,8 +366,10 @@ def main():
                            "are not counted" if track else "")}
         line["batches_per_step"] = batches
     if not args.no_cpu_baseline:
+        model, threads = host_cpu()
         if whatif:
             rec, batches_per_pair, pairs = whatif_oracle_sample(wl, args.cpu_seconds)
+            rec["cpu_model"], rec["host_threads"] = model, threads
             line["cpu_baseline"] = rec
             tt = ttft[0].cpu().numpy()
             line["parity_vs_oracle"] = parity_record(
@@ -366,6 +386,7 @@ def main():
         else:
             rec, n, obatches, ref = oracle_sample(
                 wl, args.cpu_seconds, tau=None if tau is None else tau.cpu().numpy())
+            rec["cpu_model"], rec["host_threads"] = model, threads
             line["cpu_baseline"] = rec
             if n == N and Z == 1:
                 rec["oracle_batches"] = obatches
