@@ -379,7 +379,7 @@ def main():
             # per-instance inputs (negligible); algorithmic bytes per estimate = 8
             achieved = Z * N * I * 8 / (kernel_ms / 1000.0) / 1e9
             roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                    "frac": achieved / HBM_PEAK_GBS, "traffic": load_traffic(args.workload),
                     "note": "algorithmic bytes = 8 B of TTFT output per (query, instance); "
                             f"a literal per-pair SFS would simulate {batches_per_pair:.0f} "
                             "batches per pair"}
