@@ -316,9 +316,11 @@ def test_trace_c5_all_scenarios_prefix_and_stats():
     ctx.close()
 
 
-def test_checkpoint_resume_identical():
-    """read_state -> load_state into a fresh context, continue: same results."""
-    wl = make_workload("c2", n_q=600, n_inst=8)
+@pytest.mark.parametrize("name", ["c2", "c7"])
+def test_checkpoint_resume_identical(name):
+    """read_state -> load_state into a fresh context, continue: same results (c7: under
+    scheduler limits, the snapshot holding preempted requests and cut decodes)."""
+    wl = make_workload(name, n_q=600, n_inst=8)
     full_c, full_t, _, ctx = gpu_trace(wl)
     ctx.close()
     N1 = 250
@@ -333,6 +335,8 @@ def test_checkpoint_resume_identical():
     st = ctx1.read_state(0)
     ctx2 = LarContext(1, wl.n_inst, max_seqs_cap=int(wl.max_seqs.max()), queue_cap=wl.queue_cap,
                       max_prompt=wl.max_prompt)
+    if wl.sched is not None:
+        ctx2.set_scheduler(wl.sched)
     ctx2.load_state(a=wl.a, b=wl.b, c=wl.c, d=wl.d, e=wl.e, budget=wl.budget,
                     max_seqs=wl.max_seqs, col=wl.col, offsets=st["offsets"],
                     rem_prefill=st["rem_prefill"], rem_decode=st["rem_decode"],
