@@ -11,6 +11,7 @@ simulation follows and Sec. 2 on paged KV caches and chunked prefill.
 * invariants after every batch; error paths.
 """
 
+import itertools
 import json
 import os
 
@@ -227,3 +228,90 @@ def test_c7_limits_bind():
         for q in qs:
             q.advance(t_next)
     assert sum(q.preemptions() for q in qs) > 0
+
+
+# ------------------------------------------------------------------ exhaustive tiny states
+def _tiny_states(max_n=3):
+    dec = [[0, rd, cx] for rd in (1, 2) for cx in (1, 3)]
+    par = [[rp, rd, cx] for rp in (1, 3) for rd in (1, 2) for cx in (1, 3)]
+    wai = [[rp, rd, 0] for rp in (1, 3) for rd in (1, 2)]
+    run = dec + par
+    for n in range(0, max_n + 1):
+        for n_run in range(0, n + 1):
+            for rs in itertools.product(run, repeat=n_run):
+                for ws in itertools.product(wai, repeat=n - n_run):
+                    yield [list(x) for x in rs] + [list(x) for x in ws], n_run
+
+
+# (chunk cap, KV blocks, block size, context limit): none, context limit only, and KV
+# caches barely above one request's need at block sizes 1, 2 and 4
+_LIMITS = [(0, 0, 1, 0), (0, 0, 1, 9), (1, 7, 1, 7), (2, 4, 2, 8), (0, 3, 4, 10), (2, 0, 1, 0)]
+
+
+def _sched_cases(stride=1):
+    for idx, (reqs, n_run) in enumerate(_tiny_states()):
+        if idx % stride:
+            continue
+        for B, M in [(1, 1), (3, 2), (4, 3)]:
+            if n_run > M:
+                continue
+            for lim in _LIMITS:
+                H, K, S, X = lim
+                if X and any(r[0] + r[2] >= X for r in reqs):
+                    continue
+                if K and sum(-(-r[2] // S) for r in reqs if r[2] > 0) > K:
+                    continue
+                yield reqs, B, M, list(lim)
+
+
+def _pair(coef, B, M, reqs, lim):
+    c = coef
+    q = _queue(c, B, M, reqs, lim)
+    bf = BF.BFSchedInstance(c["a"], c["b"], c["c"], c["d"], c["e"], B, M, lim,
+                            *(zip(*reqs) if reqs else ((), (), ())))
+    return q, bf
+
+
+def test_sched_bruteforce_exhaustive_tiny_states():
+    """Every tiny state (<= 3 residents of every kind; one in three of the 3-resident
+    ones) under six limit settings against the token-at-a-time scheduler with numbered
+    KV blocks: iteration counts and TTFT bits, both readings."""
+    coef = dict(a=0.75, b=0.3, c=0.2, d=0.01, e=0.003)
+    n_checked = 0
+    preempting = 0
+    for reqs, B, M, lim in _sched_cases(stride=3):
+        q, bf = _pair(coef, B, M, reqs, lim)
+        for p in (1, 4):
+            if lim[3] and p >= lim[3]:
+                continue
+            for reading in (0, 1):
+                tt, it = q.estimate(p, 1, 0.0, reading)
+                w = bf.copy()
+                tb, ib = w.estimate(p, 1, 0.0, reading)
+                assert (it, tt) == (ib, tb), (reqs, B, M, lim, p, reading)
+                n_checked += 1
+        probe = bf.copy()
+        probe.append(4 if not lim[3] or lim[3] > 4 else 1, 1)
+        for _ in range(12):
+            if not probe.reqs:
+                break
+            probe.step()
+        preempting += probe.preemptions > 0
+    assert n_checked > 20000 and preempting > 500, (n_checked, preempting)
+
+
+def test_sched_bruteforce_steps_tiny_states():
+    """Three replayed batches per tiny state under every limit setting: features, batch
+    time and resulting state, against the token-at-a-time scheduler."""
+    coef = dict(a=0.75, b=0.3, c=0.2, d=0.01, e=0.003)
+    for reqs, B, M, lim in _sched_cases(stride=2):
+        q, bf = _pair(coef, B, M, reqs, lim)
+        for _ in range(3):
+            if not bf.reqs:
+                break
+            T, f = q.step()
+            Tb, fb = bf.step()
+            assert (T, f) == (Tb, fb), (reqs, B, M, lim)
+            rp, rd, cx, _, _ = q.state()
+            assert [list(x) for x in zip(rp, rd, cx)] == [list(x) for x in bf.state()], \
+                (reqs, B, M, lim)
