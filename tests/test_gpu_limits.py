@@ -322,3 +322,50 @@ def test_limits_capacity_and_iteration_cap():
         ctx.sync()
     assert e.value.code == LAR_E_ITER
     ctx.close()
+
+
+@pytest.mark.parametrize("reading", [0, 1])
+def test_limits_exhaustive_tiny_states(reading):
+    """Every tiny state of the CPU pins (up to 3 residents of every kind, three (B, M)
+    shapes, six limit settings: about 24k cases) as the instances of one context: the
+    what-if estimates of two prompts at every instance, then a replay of every instance
+    to t = 6 ms, against the oracle instance by instance."""
+    from paper_2607_18253_amd.lar import LarContext
+    import test_oracle_sched as TS
+    coef = dict(a=0.75, b=0.3, c=0.2, d=0.01, e=0.003)
+    cases = list(TS._sched_cases(stride=1))
+    I = len(cases)
+    offsets = np.zeros(I + 1, np.int32)
+    rp, rd, cx = [], [], []
+    for j, (reqs, B, M, lim) in enumerate(cases):
+        offsets[j + 1] = offsets[j] + len(reqs)
+        for r in reqs:
+            rp.append(r[0]); rd.append(r[1]); cx.append(r[2])
+    ctx = LarContext(1, I, max_seqs_cap=3, queue_cap=8, max_prompt=4, flags=reading,
+                     max_iters=MAX_ITERS)
+    ctx.set_scheduler(np.array([lim for _, _, _, lim in cases], np.int32))
+    ctx.load_state(a=[coef["a"]] * I, b=[coef["b"]] * I, c=[coef["c"]] * I,
+                   d=[coef["d"]] * I, e=[coef["e"]] * I,
+                   budget=[B for _, B, _, _ in cases], max_seqs=[M for _, _, M, _ in cases],
+                   col=[0] * I, offsets=offsets, rem_prefill=np.array(rp, np.int32),
+                   rem_decode=np.array(rd, np.int32), context=np.array(cx, np.int32),
+                   clock_ms=np.zeros(I))
+    ps = [1, 4]
+    tt, it = ctx.estimate(T(np.array(ps), torch.int32), 0.0)
+    ctx.advance(6.0)
+    ctx.sync()
+    tt, it = tt.cpu().numpy()[0], it.cpu().numpy()[0]
+    st = ctx.read_state(0)
+    ctx.close()
+    for j, (reqs, B, M, lim) in enumerate(cases):
+        q = TS._queue(coef, B, M, reqs, lim)
+        for a, p in enumerate(ps):
+            want, wit = q.estimate(p, 1, 0.0, reading)
+            assert bits(tt[a, j]) == bits(want) and it[a, j] == wit, (reqs, B, M, lim, p)
+        q.advance(6.0)
+        grp, grd, gcx, gclk, gits = q.state()
+        lo, hi = st["offsets"][j], st["offsets"][j + 1]
+        assert list(st["rem_prefill"][lo:hi]) == list(grp), (reqs, B, M, lim)
+        assert list(st["rem_decode"][lo:hi]) == list(grd), (reqs, B, M, lim)
+        assert list(st["context"][lo:hi]) == list(gcx), (reqs, B, M, lim)
+        assert bits(st["clock_ms"][j]) == bits(gclk) and st["iterations"][j] == gits
