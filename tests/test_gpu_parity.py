@@ -523,3 +523,48 @@ def test_trace_fast_walk_tiny_pools(seed, flags):
         np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
         assert_state_equal(ctx, z, ref)
     ctx.close()
+
+
+@pytest.mark.parametrize("reading", [0, 1])
+def test_exhaustive_tiny_states_one_context(reading):
+    """Every tiny state of the oracle's exhaustive pins (up to 3 residents of every
+    kind, six (B, M) shapes) as the instances of one context: the what-if estimates
+    (shared trajectory, k_traj + k_est) of three prompts at every instance, then a
+    replay of every instance to t = 6 ms, against the oracle instance by instance."""
+    from paper_2607_18253_amd.lar import LarContext
+    import test_oracle_pins as TP
+    coef = dict(a=0.75, b=0.3, c=0.2, d=0.01, e=0.003)
+    cases = [(reqs, B, M) for reqs, n_run in TP._tiny_states()
+             for B, M in [(1, 1), (2, 1), (2, 2), (3, 2), (4, 3), (4, 1)] if n_run <= M]
+    I = len(cases)
+    offsets = np.zeros(I + 1, np.int32)
+    rp, rd, cx = [], [], []
+    for j, (reqs, B, M) in enumerate(cases):
+        offsets[j + 1] = offsets[j] + len(reqs)
+        for r in reqs:
+            rp.append(r[0]); rd.append(r[1]); cx.append(r[2])
+    ctx = LarContext(1, I, max_seqs_cap=3, queue_cap=8, max_prompt=5, flags=reading)
+    ctx.load_state(a=[coef["a"]] * I, b=[coef["b"]] * I, c=[coef["c"]] * I,
+                   d=[coef["d"]] * I, e=[coef["e"]] * I, budget=[B for _, B, _ in cases],
+                   max_seqs=[M for _, _, M in cases], col=[0] * I, offsets=offsets,
+                   rem_prefill=np.array(rp, np.int32), rem_decode=np.array(rd, np.int32),
+                   context=np.array(cx, np.int32), clock_ms=np.zeros(I))
+    ps = [1, 2, 5]
+    tt, it = ctx.estimate(T(np.array(ps), torch.int32), 0.0)
+    ctx.advance(6.0)
+    ctx.sync()
+    tt, it = tt.cpu().numpy()[0], it.cpu().numpy()[0]
+    st = ctx.read_state(0)
+    ctx.close()
+    for j, (reqs, B, M) in enumerate(cases):
+        q = TP._queue(coef, B, M, reqs)
+        for a, p in enumerate(ps):
+            want, wit = q.estimate(p, 1, 0.0, reading)
+            assert bits(tt[a, j]) == bits(want) and it[a, j] == wit, (reqs, B, M, p)
+        q.advance(6.0)
+        grp, grd, gcx, gclk, gits = q.state()
+        lo, hi = st["offsets"][j], st["offsets"][j + 1]
+        assert list(st["rem_prefill"][lo:hi]) == list(grp), (reqs, B, M)
+        assert list(st["rem_decode"][lo:hi]) == list(grd), (reqs, B, M)
+        assert list(st["context"][lo:hi]) == list(gcx), (reqs, B, M)
+        assert bits(st["clock_ms"][j]) == bits(gclk) and st["iterations"][j] == gits
