@@ -179,6 +179,8 @@ lar_status lar_reload_state(lar_ctx *ctx);
  * tokens, 1..max_prompt) arriving at time t_ms at every instance of every
  * scenario.  Pure: the state is not modified.  Every instance clock must be
  * >= t_ms (advance with lar_commit first), else the sticky LAR_E_STATE is set.
+ * Under scheduler limits a prompt must also be below the instance's context limit
+ * (else NaN there and the sticky LAR_E_ARG).
  *   q_prefill dev [Q]
  *   ttft_ms   dev [Z][Q][I]  float64, TTFT = (clock + T_1 + ... + T_l) - t_ms
  *   iters     dev [Z][Q][I]  int32, l = number of batches simulated; may be NULL
@@ -237,7 +239,9 @@ lar_status lar_ttft_targets(lar_ctx *ctx, int32_t n, const int32_t *q_prefill,
  * raised to 1) joins the FCFS tail of instance choice[z] as a waiting request
  * (choice == NULL or choice[z] < 0: nothing is appended); then on every instance
  * every batch that starts before t_next_ms runs, and an idle instance's clock
- * jumps to t_next_ms.  A full waiting queue sets the sticky LAR_E_CAPACITY.
+ * jumps to t_next_ms.  A full waiting queue sets the sticky LAR_E_CAPACITY.  Under
+ * scheduler limits the predicted decode is cut to what the context limit leaves,
+ * and a prompt at or above that limit is not appended (sticky LAR_E_ARG).
  *   choice dev [Z] or NULL
  */
 lar_status lar_commit(lar_ctx *ctx, const int32_t *choice, int32_t q_prefill, int32_t q_decode,
@@ -342,7 +346,9 @@ lar_status lar_ontime_utility(lar_ctx *ctx, int32_t n_q, const int32_t *choice,
 /*
  * Copy scenario `scen`'s state out (synchronises): resident requests of every
  * instance in FCFS order as in lar_load_state, the clocks and the number of
- * batches replayed per instance since the load.  out_cap = capacity of the
+ * batches replayed per instance since the load.  Under scheduler limits the
+ * predicted decodes are the ones cut to the context limit, and a preempted request
+ * is a waiting one (context 0) with its whole context to prefill again.  out_cap = capacity of the
  * request arrays; LAR_E_CAPACITY if they are too small (*n_total still set).
  *   offsets host [I+1]; rem_prefill, rem_decode, context host [out_cap]
  *   clock_ms host [I]; iterations_run host [I]
