@@ -2,7 +2,8 @@
 // (chunk cap, context limit, KV-cache blocks with recompute preemption; the system
 // appendix lists them among what the simulation follows), on the explicit-list
 // wave engine of sfs_limits.h.  Every estimate simulates its (query, instance) pair
-// from the instance state.
+// batch by batch: from the instance state, or in the clustered trace from the
+// instance's cached admission point (lim_frontier), which gives the same result.
 //
 //   k_lest     one wave per (scenario, query, instance): what-if estimate.
 //   k_lcommit  one wave per (scenario, instance): append the routed query, replay
