@@ -369,3 +369,26 @@ def test_limits_exhaustive_tiny_states(reading):
         assert list(st["rem_decode"][lo:hi]) == list(grd), (reqs, B, M, lim)
         assert list(st["context"][lo:hi]) == list(gcx), (reqs, B, M, lim)
         assert bits(st["clock_ms"][j]) == bits(gclk) and st["iterations"][j] == gits
+
+
+def test_limits_prompt_at_the_context_boundary():
+    """A prompt of X - 1 tokens fits an instance with context limit X (its decode is cut
+    to 1): estimated at every instance as the oracle does, under both readings."""
+    for reading in (0, 1):
+        wl = make_tiny_sched_workload(9, n_q=4, max_res=4)
+        wl.sched[:, 3] = np.maximum(wl.sched[:, 3], 14)
+        K, S, Xs = wl.sched[:, 1], wl.sched[:, 2], wl.sched[:, 3]
+        wl.sched[:, 1] = np.where(K > 0, np.maximum(K, -(-Xs // S)), 0)   # K*S >= X
+        X = int(wl.sched[:, 3].min())
+        wl.max_prompt = X
+        ctx = context_for(wl, flags=reading, max_iters=MAX_ITERS)
+        ps = np.array([X - 1, 1], np.int32)
+        tt, it = ctx.estimate(T(ps, torch.int32), 0.0)
+        ctx.sync()
+        tt, it = tt.cpu().numpy()[0], it.cpu().numpy()[0]
+        ctx.close()
+        for j in range(wl.n_inst):
+            q = O.instance_queue(wl, j)
+            for a, p in enumerate(ps):
+                want, wit = q.estimate(int(p), 1, 0.0, reading)
+                assert bits(tt[a, j]) == bits(want) and it[a, j] == wit, (reading, j, p)
