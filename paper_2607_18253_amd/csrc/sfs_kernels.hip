@@ -1071,6 +1071,10 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
       if (j < I) {
         const QEnv& e = env[r];
         Queue<KS> wk;
+        // with several waves per SIMD, the chosen instance's commit, walk and next
+        // estimate are the longest link of the query chain: let its wave issue first
+        const bool hot = (W > 4) && i >= 0 && j == m;
+        if (hot) __builtin_amdgcn_s_setprio(3);
         wk.template from_lds<TRK>(sst[wid][r], &stags[TRK ? wid : 0][r]);
         const VisitOut vo = visit<KS, TRK>(wk, fc[r], e, i >= 0 && j == m, p, dq, tn, S.qcap,
                                            kmax, max_iters, err, sst[wid][r],
@@ -1092,6 +1096,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
           const double u = cand_value(eq2, ttft, wl, tau, tq, j, &k);
           cand_take(c, u, k, ttft, eq2);
         }
+        if (hot) __builtin_amdgcn_s_setprio(0);
       }
     }
     if (last_in_block) {
