@@ -531,7 +531,64 @@ struct Queue {
     // prefill chunks in FCFS order over the window (and further windows)
     int64_t P = 0, A = 0;
     int free_slots = k.M - (int)o.D - n_part;   // slots for waiting admissions
-    while (n_pre > 0 && left > 0 && (n_part > 0 || free_slots > 0)) {
+    bool more = true;
+    // The usual batch: only the window's first entry can take tokens (it is the one
+    // eligible entry, or it takes the whole budget).  Its chunk, and its move to a
+    // decode slot when it completes, need no scan and no staging; the result is that
+    // of the loop below.
+    if (n_pre > 0 && left > 0 && (n_part > 0 || free_slots > 0) && nwin > 0 && n_part <= 1) {
+      const int r0 = lane_read(wrp, woff);
+      const int n_elig = n_part + max(0, min(free_slots, nwin - n_part));
+      if (r0 >= left || n_elig == 1) {
+        const int nw0 = nwin;
+        const int cx0 = lane_read(wcx, woff);
+        const int ch = min(r0, left);
+        P += ch;
+        left -= ch;
+        pre_sum -= ch;
+        if (need_A) A += (int64_t)ch * cx0 + (int64_t)ch * (ch + 1) / 2;
+        if (ln == woff) {
+          wrp -= ch;
+          wcx += ch;
+        }
+        if (n_part == 0) free_slots -= 1;   // a waiting entry was admitted
+        const bool full = ch == r0;
+        if (full) {
+          // completed prefill: decoding from the next batch, last = g + 1 + rd
+          const int nl = gn + lane_read(wrd, woff);
+          const int nc = cx0 + ch - gn;
+          const int sq = lane_read(wseq, woff);
+          if (need_C) c0sum += nc;
+          if constexpr (TRK) {
+            const int tg = lane_read(wtag, woff);
+            if (ln == nd) pt_new = tg;
+          }
+          bool placed = false;
+#pragma unroll
+          for (int s = 0; s < KS; ++s) {
+            const uint64_t fm = ballot(dl[s] <= gn);
+            if (!placed && fm) {
+              if (ln == __builtin_ctzll(fm)) { dl[s] = nl; dc[s] = nc; ds[s] = sq; }
+              placed = true;
+            }
+          }
+          n_dec += 1;
+          if constexpr (TRK) nd += 1;
+          woff += 1;
+          nwin -= 1;
+          head += 1;
+          if (head >= e.rcap) head -= e.rcap;
+          n_pre -= 1;
+          if (n_part == 1) n_part = 0;
+        } else if (n_part == 0) {
+          n_part = 1;   // the waiting entry got a chunk and stays partial
+        }
+        // the loop below goes on only when the whole window was served
+        more = full && nw0 == 1;
+        if (more) refill<TRK>(e, tags);
+      }
+    }
+    while (more && n_pre > 0 && left > 0 && (n_part > 0 || free_slots > 0)) {
       if (nwin == 0) refill<TRK>(e, tags);
       const int nw0 = nwin;
       const int idx = ln - woff;
