@@ -36,6 +36,10 @@
  *    (queue overflow, iteration cap, instance not advanced, prompt too long) set a
  *    sticky device flag, reported by lar_sync / lar_read_state; once observed it is
  *    returned by every later call until lar_load_state resets it.
+ *  - A batch of zero queries (n_q == 0, n == 0) is valid: the call returns LAR_OK,
+ *    enqueues nothing and leaves the state as it was (a trace of zero queries does
+ *    not advance the instances either).  A negative count is LAR_E_ARG.
+ *    lar_stats and lar_ontime_utility average over the queries and need n_q >= 1.
  *  - A context is not thread-safe.
  *
  * Time unit: milliseconds.  Layouts are row-major.

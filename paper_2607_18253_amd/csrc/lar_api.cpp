@@ -526,7 +526,6 @@ lar_status lar_route(lar_ctx* ctx, int32_t n_q, const double* ttft_ms, const dou
                      const double* cost, int32_t n_cols, const double* w_cost,
                      const double* w_lat, int32_t* choice, double* chosen_ttft,
                      double* utility) {
-  if (ctx && !w_lat) return fail(ctx, LAR_E_ARG, "null argument");
   return route_rows(ctx, n_q, ttft_ms, nullptr, acc, cost, n_cols, w_cost, w_lat, choice,
                     chosen_ttft, utility);
 }
@@ -535,7 +534,6 @@ lar_status lar_route_constrained(lar_ctx* ctx, int32_t n_q, const double* ttft_m
                                  const double* tau_ms, const double* acc, const double* cost,
                                  int32_t n_cols, const double* w_cost, int32_t* choice,
                                  double* chosen_ttft, double* utility) {
-  if (ctx && !tau_ms) return fail(ctx, LAR_E_ARG, "null argument");
   return route_rows(ctx, n_q, ttft_ms, tau_ms, acc, cost, n_cols, w_cost, nullptr, choice,
                     chosen_ttft, utility);
 }
@@ -638,7 +636,6 @@ lar_status lar_route_trace(lar_ctx* ctx, int32_t n_q, const int32_t* q_prefill,
                            const double* acc, const double* cost, int32_t n_cols,
                            const double* w_cost, const double* w_lat, int32_t* choice,
                            double* chosen_ttft, double* utility, double* realized_ttft) {
-  if (ctx && !w_lat) return fail(ctx, LAR_E_ARG, "null argument");
   return trace_rows(ctx, n_q, q_prefill, q_decode, q_t_ms, t_after_ms, nullptr, acc, cost, n_cols,
                     w_cost, w_lat, choice, chosen_ttft, utility, realized_ttft);
 }
@@ -649,7 +646,6 @@ lar_status lar_route_trace_constrained(lar_ctx* ctx, int32_t n_q, const int32_t*
                                        const double* cost, int32_t n_cols, const double* w_cost,
                                        int32_t* choice, double* chosen_ttft, double* utility,
                                        double* realized_ttft) {
-  if (ctx && !tau_ms) return fail(ctx, LAR_E_ARG, "null argument");
   return trace_rows(ctx, n_q, q_prefill, q_decode, q_t_ms, t_after_ms, tau_ms, acc, cost, n_cols,
                     w_cost, nullptr, choice, chosen_ttft, utility, realized_ttft);
 }

@@ -366,6 +366,41 @@ def test_empty_pool_and_single_slot():
     ctx.close()
 
 
+def test_empty_batches_are_noops():
+    """A batch of zero queries is valid and does nothing: estimate, route (both
+    objectives), targets and traces (both objectives) with n = 0 return OK, enqueue
+    nothing and leave every instance as it was; negative counts are argument errors."""
+    wl = make_tiny_workload(3, n_inst=3, n_q=4)
+    ctx = context_for(wl)
+    ctx.advance(float(wl.q_t_ms[0]))
+    ctx.sync()
+    before = ctx.read_state(0)
+    I = wl.n_inst
+    e_i = torch.empty(0, dtype=torch.int32, device=DEV)
+    e_d = torch.empty(0, dtype=torch.float64, device=DEV)
+    e_rows = torch.empty((0, int(wl.acc.shape[1])), dtype=torch.float64, device=DEV)
+    wc, wlat = T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64)
+    tt, it = ctx.estimate(e_i, float(wl.q_t_ms[0]))
+    assert tt.shape == (1, 0, I) and it.shape == (1, 0, I)
+    ch = ctx.route(torch.empty((1, 0, I), dtype=torch.float64, device=DEV), e_rows, e_rows,
+                   wc, wlat)
+    assert ch.shape == (1, 0)
+    ctx.route_constrained(torch.empty((1, 0, I), dtype=torch.float64, device=DEV), e_d,
+                          e_rows, e_rows, wc)
+    assert ctx.ttft_targets(e_i, e_d, e_d).shape == (0,)
+    ctx.route_trace(e_i, e_i, e_d, float(wl.q_t_ms[-1]) + 1e6, e_rows, e_rows, wc, wlat)
+    ctx.route_trace_constrained(e_i, e_i, e_d, float(wl.q_t_ms[-1]) + 1e6, e_d, e_rows,
+                                e_rows, wc)
+    ctx.sync()
+    after = ctx.read_state(0)
+    for k in ("offsets", "rem_prefill", "rem_decode", "context", "iterations"):
+        np.testing.assert_array_equal(after[k], before[k], err_msg=k)
+    np.testing.assert_array_equal(bits(after["clock_ms"]), bits(before["clock_ms"]))
+    assert ctx._L.lar_estimate_ttft(ctx._h, -1, None, 0.0, None, None) == L.LAR_E_ARG
+    assert ctx._L.lar_ttft_targets(ctx._h, -1, None, None, None, None) == L.LAR_E_ARG
+    ctx.close()
+
+
 def test_sticky_errors():
     coef = dict(a=1.0, b=0.5, c=0.25, d=0.0, e=0.0)
     # prompt above max_prompt -> LAR_E_ARG from the kernel, sticky until reload
