@@ -209,6 +209,24 @@ def test_trace_tiny_pools_long_prompts(seed, prompt_max, path):
     ctx.close()
 
 
+@pytest.mark.parametrize("n_q", [1, 63, 64, 65, 128, 129])
+def test_trace_query_block_boundaries(n_q):
+    """The clustered trace reads the queries in blocks of 64, one lane each, with the
+    next block fetched ahead: traces one query long, one short of a block, exactly one
+    block, one past it, two blocks and one past two, over three workgroups per
+    scenario (9 instances, 4 waves each) and two scenarios."""
+    wl = make_tiny_workload(200 + n_q, n_inst=9, max_res=5, n_q=n_q, n_scen=2)
+    assert _tail_k(wl) <= 64   # the clustered kernel
+    choice, chosen, util, ctx = gpu_trace(wl, queue_cap=10 ** 4)
+    for z in range(wl.n_scen):
+        ref = O.trace(wl, scenario=z, queue_cap=10 ** 4)
+        np.testing.assert_array_equal(choice[z], ref.choice)
+        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen))
+        np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
+        assert_state_equal(ctx, z, ref)
+    ctx.close()
+
+
 def test_trace_c1_full():
     wl = make_workload("c1")
     choice, chosen, util, ctx = gpu_trace(wl)
