@@ -77,6 +77,16 @@ def test_limits_tiny_pools(seed):
     _check(wl, _trace(wl, flags=reading), reading=reading)
 
 
+@pytest.mark.parametrize("n_q", [1, 63, 64, 65, 128, 129])
+def test_limits_trace_query_block_boundaries(n_q):
+    """The clustered limits trace reads the queries in blocks of 64 as the default
+    one does: traces at and around one and two blocks, 9 instances (three
+    workgroups per scenario), two scenarios, realised TTFT tracked and untracked."""
+    wl = make_tiny_sched_workload(300 + n_q, n_inst=9, n_q=n_q, max_res=5, n_scen=2)
+    print(f"limits block boundary n_q {n_q}", flush=True)
+    _check(wl, _trace(wl, realized=n_q % 2 == 1), scenarios=(0, 1), state=(0, 1))
+
+
 @pytest.mark.parametrize("seed", range(8))
 def test_limits_tiny_pools_constrained(seed):
     wl = make_tiny_sched_workload(100 + seed, n_q=25, max_res=5)
