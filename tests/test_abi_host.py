@@ -3,6 +3,7 @@
 import ctypes
 import os
 import re
+import sys
 
 import numpy as np
 import pytest
@@ -148,3 +149,25 @@ def test_c5_weight_grid():
 def test_tiny_generator_states_valid(seed):
     from workloads import make_tiny_workload
     _check_state(make_tiny_workload(seed))
+
+
+def test_missing_library_fails_loudly():
+    """The binding raises when the HIP library is absent: there is no CPU fallback."""
+    import subprocess
+    code = ("import paper_2607_18253_amd.lar as L\n"
+            "try:\n    L.load_library('/nonexistent/liblar.so')\n"
+            "except RuntimeError as e:\n    print('RAISED', e)\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
+                       timeout=300)
+    assert "RAISED" in r.stdout and "not built" in r.stdout, r.stdout + r.stderr
+
+
+def test_product_package_never_touches_the_oracle():
+    """No module of the package (binding, build, C/HIP sources) imports, links or names
+    the oracle: the oracle is test infrastructure only."""
+    pkg = os.path.join(ROOT, "paper_2607_18253_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in text.lower(), os.path.join(dirpath, f)
