@@ -459,6 +459,23 @@ lar_status lar_set_scheduler(lar_ctx* ctx, const lar_sched_limits* limits) {
   return LAR_OK;
 }
 
+// Z copies of one scenario's array of n 32-bit words, dst[z * n + i] = src[i]: the
+// snapshot re-installed for every scenario in one launch per array.
+__global__ void k_replicate(uint32_t* dst, const uint32_t* src, int64_t n, int64_t total) {
+  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < total;
+       x += (int64_t)gridDim.x * blockDim.x)
+    dst[x] = src[x % n];
+}
+
+static hipError_t replicate(void* dst, const void* src, size_t bytes, int Z, hipStream_t s) {
+  const int64_t n = (int64_t)(bytes / 4), total = n * Z;
+  if (total == 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(k_replicate, dim3((unsigned)blocks), dim3(256), 0, s, (uint32_t*)dst,
+                     (const uint32_t*)src, n, total);
+  return hipGetLastError();
+}
+
 lar_status lar_reload_state(lar_ctx* ctx) {
   if (!ctx) return LAR_E_ARG;
   if (!ctx->loaded) return fail(ctx, LAR_E_STATE, "no state loaded (call lar_load_state)");
@@ -466,19 +483,17 @@ lar_status lar_reload_state(lar_ctx* ctx) {
   const lar::DevState& sn = ctx->snap;
   const lar::DevState& S = ctx->S;
   hipStream_t s = ctx->stream;
-  const hipMemcpyKind k = hipMemcpyDeviceToDevice;
-  for (int z = 0; z < ctx->Z; ++z) {
-    const size_t o = (size_t)z * I;
-    HIP_TRY(ctx, hipMemcpyAsync(S.sc + o, sn.sc, I * sizeof(lar::QScal), k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.d_last + o * mcap, sn.d_last, I * mcap * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.d_cx0 + o * mcap, sn.d_cx0, I * mcap * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.d_seq + o * mcap, sn.d_seq, I * mcap * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.r_rp + o * rcap, sn.r_rp, I * rcap * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.r_rd + o * rcap, sn.r_rd, I * rcap * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.r_cx + o * rcap, sn.r_cx, I * rcap * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.r_seq + o * rcap, sn.r_seq, I * rcap * 4, k, s));
-    HIP_TRY(ctx, hipMemcpyAsync(S.r_tag + o * rcap, sn.r_tag, I * rcap * 4, k, s));
-  }
+  const int Z = ctx->Z;
+  static_assert(sizeof(lar::QScal) % 4 == 0, "QScal is copied in 32-bit words");
+  HIP_TRY(ctx, replicate(S.sc, sn.sc, I * sizeof(lar::QScal), Z, s));
+  HIP_TRY(ctx, replicate(S.d_last, sn.d_last, I * mcap * 4, Z, s));
+  HIP_TRY(ctx, replicate(S.d_cx0, sn.d_cx0, I * mcap * 4, Z, s));
+  HIP_TRY(ctx, replicate(S.d_seq, sn.d_seq, I * mcap * 4, Z, s));
+  HIP_TRY(ctx, replicate(S.r_rp, sn.r_rp, I * rcap * 4, Z, s));
+  HIP_TRY(ctx, replicate(S.r_rd, sn.r_rd, I * rcap * 4, Z, s));
+  HIP_TRY(ctx, replicate(S.r_cx, sn.r_cx, I * rcap * 4, Z, s));
+  HIP_TRY(ctx, replicate(S.r_seq, sn.r_seq, I * rcap * 4, Z, s));
+  HIP_TRY(ctx, replicate(S.r_tag, sn.r_tag, I * rcap * 4, Z, s));
   ctx->tag_next = ctx->tag_start;   // every ring entry is untracked again
   HIP_TRY(ctx, lar::launch_clear_error(env_of(ctx)));
   ctx->sticky = LAR_OK;
