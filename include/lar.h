@@ -75,7 +75,7 @@ enum {
 /* Per-instance batch-time coefficients (ms) and scheduler limits (Sec. 4.1). */
 typedef struct {
   double a, b, c, d, e;   /* T = a + b*P + c*D + d*C + e*A, all finite             */
-  int32_t token_budget;   /* B: tokens per batch, max_seqs <= B <= 2^30            */
+  int32_t token_budget;   /* B: tokens per batch, max_seqs <= B <= 2^30 - 1        */
   int32_t max_seqs;       /* M: running sequences, 1 <= M <= lar_config.max_seqs_cap */
   int32_t col;            /* column of this instance in the acc / cost arrays, >= 0 */
   int32_t reserved;       /* must be 0                                              */
@@ -238,7 +238,11 @@ lar_status lar_ttft_targets(lar_ctx *ctx, int32_t n, const int32_t *q_prefill,
                             const double *u_ms, const double *v, double *tau_ms);
 
 /*
- * Commit one routed query and replay the instances to t_next_ms: in scenario z,
+ * Commit one routed query and replay the instances to t_next_ms.  The paper's
+ * router takes a fresh snapshot of every instance after each engine iteration
+ * (appendix on the system, query workload snapshots); here the instances are
+ * instead replayed by the same token-batch simulation (Sec. 4.1) between
+ * arrivals, which stands in for those snapshots.  In scenario z,
  * the query (q_prefill >= 1 prompt tokens, q_decode predicted decode tokens,
  * raised to 1) joins the FCFS tail of instance choice[z] as a waiting request
  * (choice == NULL or choice[z] < 0: nothing is appended); then on every instance

@@ -6,6 +6,13 @@ of the benchmark use it.  The product path never imports this module.
 ``build()`` compiles the oracle with gcc (-O2 -ffp-contract=off: binary64
 round-to-nearest-even, no fused multiply-add); ``lib()`` loads it, building it
 first if it is missing.
+
+Threads: ``set_threads(n)`` lets the oracle run the independent estimates of one
+query (one per instance), the replays of the instances and the pairs of a what-if
+matrix on n threads; ``trace_scenarios`` runs independent scenarios on threads of
+their own.  Each thread runs the same sequential code on its own instance or
+scenario and results are gathered in order, so threaded runs are bit-identical to
+single-threaded ones (a CPU test checks it).  The default is one thread.
 """
 
 from __future__ import annotations
@@ -13,6 +20,7 @@ from __future__ import annotations
 import ctypes as C
 import os
 import subprocess
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass
 
 import numpy as np
@@ -41,7 +49,8 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp"
         subprocess.run(["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math",
-                        "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, _SRC], check=True)
+                        "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, _SRC],
+                       check=True)
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -115,11 +124,27 @@ def lib():
     L.orc_ontime_utility.restype = C.c_int
     L.orc_ontime_utility.argtypes = [C.c_int32, _i32p, _f64p, _f64p, _f64p, _f64p, C.c_int32,
                                      _i32p, C.c_double, C.POINTER(C.c_double)]
+    L.orc_set_threads.restype = None
+    L.orc_set_threads.argtypes = [C.c_int]
+    L.orc_get_threads.restype = C.c_int
+    L.orc_get_threads.argtypes = []
+    L.orc_estimate_matrix.restype = C.c_int
+    L.orc_estimate_matrix.argtypes = [C.c_int32, C.POINTER(C.c_void_p), C.c_int32, _i32p, _i32p,
+                                      C.c_double, C.c_int32, C.c_int64, _f64p, _i32p]
     L.orc_stats.restype = C.c_int
     L.orc_stats.argtypes = [C.c_int32, _i32p, _f64p, _f64p, _f64p, C.c_int32, _i32p, C.c_double,
                             _f64p]
     _lib = L
     return L
+
+
+def set_threads(n: int) -> None:
+    """Threads for the independent per-instance work of one query (default 1)."""
+    lib().orc_set_threads(int(n))
+
+
+def get_threads() -> int:
+    return int(lib().orc_get_threads())
 
 
 def make_params(a, b, c, d, e, budget, max_seqs) -> Params:
@@ -351,3 +376,37 @@ def estimate_matrix(wl, queries, instances, t_ms=0.0, reading=READING_DECODE_BAT
                                                        int(wl.q_decode[i]), t_ms, reading,
                                                        max_iters)
     return out, its
+
+
+def estimate_matrix_all(wl, t_ms=0.0, *, queries=None, reading=READING_DECODE_BATCH,
+                        max_iters=10_000_000):
+    """The literal what-if matrix: TTFT and batch count of every query (all, or the
+    given indices) at every instance of ``wl``, each pair simulated on its own copy
+    of the instance (runs on ``set_threads`` threads).  Returns (ttft, iters), both
+    [Q][I]."""
+    qidx = np.arange(wl.n_q) if queries is None else np.asarray(queries, np.int64)
+    qs = [instance_queue(wl, j) for j in range(wl.n_inst)]
+    for q in qs:
+        if q._L is None or q._q is None:
+            raise OracleError(E_ARG, "queue")
+    ptrs = (C.c_void_p * wl.n_inst)(*[q._q for q in qs])
+    p = _i32(np.asarray(wl.q_prefill)[qidx])
+    d = _i32(np.asarray(wl.q_decode)[qidx])
+    ttft = np.zeros((len(qidx), wl.n_inst))
+    iters = np.zeros((len(qidx), wl.n_inst), np.int32)
+    st = lib().orc_estimate_matrix(wl.n_inst, ptrs, len(qidx), p, d, float(t_ms), int(reading),
+                                   int(max_iters), ttft, iters)
+    if st != OK:
+        raise OracleError(st, "estimate_matrix")
+    del qs
+    return ttft, iters
+
+
+def trace_scenarios(wl, scenarios, n_threads: int, **kw):
+    """``trace(wl, z, **kw)`` for each z in ``scenarios``, the scenarios on up to
+    n_threads threads at once (each trace single-threaded inside).  Returns the
+    results in the order of ``scenarios``."""
+    if n_threads <= 1:
+        return [trace(wl, scenario=z, **kw) for z in scenarios]
+    with ThreadPoolExecutor(max_workers=n_threads) as ex:
+        return list(ex.map(lambda z: trace(wl, scenario=z, **kw), scenarios))

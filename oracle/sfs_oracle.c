@@ -97,6 +97,20 @@
 #include <stdlib.h>
 #include <string.h>
 
+/*
+ * Threads.  The estimates of one query at the different instances are
+ * independent (each works on its own copy of one instance), and so is the replay
+ * of each instance between two arrivals; the loops over instances below, and the
+ * (query, instance) pairs of orc_estimate_matrix, may therefore run on several
+ * threads.  Every thread runs exactly the same sequential code on its own
+ * instance, and the results are combined in instance order afterwards, so a
+ * threaded run is bit-identical to a single-threaded one.  Default: 1 thread.
+ */
+static int g_threads = 1;
+
+void orc_set_threads(int n) { g_threads = n < 1 ? 1 : n; }
+int orc_get_threads(void) { return g_threads; }
+
 #define ORC_OK 0
 #define ORC_E_ARG (-1)
 #define ORC_E_STATE (-2)
@@ -587,6 +601,47 @@ void orc_ttft_targets(int32_t n, const int32_t *p, const double *u_ms, const dou
 
 /* ---------------------------------------------------------------- trace */
 
+/* The lowest-indexed error of a loop over instances (what a sequential loop that
+   stops at its first error returns), or ORC_OK. */
+static int first_error(const int *jst, int32_t n) {
+  for (int32_t j = 0; j < n; ++j)
+    if (jst[j] != ORC_OK) return jst[j];
+  return ORC_OK;
+}
+
+/* Replay every instance to t; the instances are independent. */
+static int advance_all(orc_queue **qs, int32_t n_inst, double t, int64_t max_iters, int *jst) {
+#pragma omp parallel for num_threads(g_threads) schedule(dynamic, 1)
+  for (int32_t j = 0; j < n_inst; ++j) jst[j] = orc_queue_advance(qs[j], t, max_iters);
+  return first_error(jst, n_inst);
+}
+
+/*
+ * What-if matrix (the SFS estimate of Sec. 4.1 for many queries at once): for
+ * every query i < n_q and instance j < n_inst, the literal estimate of a query of
+ * p[i] prompt tokens (predicted decode d[i]) arriving at t at instance j, into
+ * ttft[i*n_inst + j] and iters[i*n_inst + j].  The instances must already be
+ * advanced to t.  Returns the error of the lowest (i, j) in row-major order that
+ * fails, or ORC_OK.
+ */
+int orc_estimate_matrix(int32_t n_inst, orc_queue *const *qs, int32_t n_q, const int32_t *p,
+                        const int32_t *d, double t, int32_t reading, int64_t max_iters,
+                        double *ttft, int32_t *iters) {
+  if (n_inst < 1 || n_q < 0) return ORC_E_ARG;
+  int64_t n = (int64_t)n_q * n_inst;
+  int *pst = (int *)malloc((size_t)(n > 0 ? n : 1) * sizeof(int));
+  if (!pst) return ORC_E_ARG;
+#pragma omp parallel for num_threads(g_threads) schedule(dynamic, 16)
+  for (int64_t k = 0; k < n; ++k) {
+    int64_t i = k / n_inst, j = k % n_inst;
+    pst[k] = orc_queue_estimate(qs[j], p[i], d[i], t, reading, max_iters, &ttft[k], &iters[k]);
+  }
+  int st = ORC_OK;
+  for (int64_t k = 0; k < n && st == ORC_OK; ++k) st = pst[k];
+  free(pst);
+  return st;
+}
+
 /*
  * Sequential routing trace of one scenario:
  *   advance every instance to t_0;
@@ -618,7 +673,8 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
     if (col[j] < 0 || col[j] >= n_cols) return ORC_E_ARG;
   orc_queue **qs = (orc_queue **)calloc((size_t)n_inst, sizeof(orc_queue *));
   double *row = (double *)malloc((size_t)n_inst * sizeof(double));
-  if (!qs || !row) { free(qs); free(row); return ORC_E_ARG; }
+  int *jst = (int *)malloc((size_t)n_inst * sizeof(int));
+  if (!qs || !row || !jst) { free(qs); free(row); free(jst); return ORC_E_ARG; }
   for (int32_t j = 0; j < n_inst && st == ORC_OK; ++j) {
     int64_t lo = offsets[j], hi = offsets[j + 1];
     qs[j] = orc_queue_new(&params[j], hi - lo, rp + lo, rd + lo, cx + lo, clock[j], &st);
@@ -632,16 +688,17 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
   }
   if (realized)
     for (int32_t i = 0; i < n_q; ++i) realized[i] = NAN;
-  if (st == ORC_OK && n_q > 0)
-    for (int32_t j = 0; j < n_inst && st == ORC_OK; ++j)
-      st = orc_queue_advance(qs[j], q_t[0], max_iters);
+  if (st == ORC_OK && n_q > 0) st = advance_all(qs, n_inst, q_t[0], max_iters, jst);
   for (int32_t i = 0; i < n_q && st == ORC_OK; ++i) {
-    int32_t it = 0;
-    for (int32_t j = 0; j < n_inst && st == ORC_OK; ++j) {
-      st = orc_queue_estimate(qs[j], q_p[i], q_d[i], q_t[i], reading, max_iters, &row[j], &it);
+#pragma omp parallel for num_threads(g_threads) schedule(dynamic, 1)
+    for (int32_t j = 0; j < n_inst; ++j) {
+      int32_t it = 0;
+      jst[j] = orc_queue_estimate(qs[j], q_p[i], q_d[i], q_t[i], reading, max_iters, &row[j],
+                                  &it);
       if (ttft_all) ttft_all[(int64_t)i * n_inst + j] = row[j];
       if (iters_all) iters_all[(int64_t)i * n_inst + j] = it;
     }
+    st = first_error(jst, n_inst);
     if (st != ORC_OK) { *failed_query = i; break; }
     const double *arow = acc + (int64_t)i * n_cols;
     const double *crow = cost + (int64_t)i * n_cols;
@@ -655,8 +712,7 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
     }
     st = append_tagged(qs[m], q_p[i], q_d[i], queue_cap, i);
     double t_next = (i + 1 < n_q) ? q_t[i + 1] : q_t[i];
-    for (int32_t j = 0; j < n_inst && st == ORC_OK; ++j)
-      st = orc_queue_advance(qs[j], t_next, max_iters);
+    if (st == ORC_OK) st = advance_all(qs, n_inst, t_next, max_iters, jst);
     if (st != ORC_OK) *failed_query = i;
   }
   /* queries without their first token at the end: run a copy of each instance on,
@@ -685,6 +741,7 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
   for (int32_t j = 0; j < n_inst; ++j) orc_queue_free(qs[j]);
   free(qs);
   free(row);
+  free(jst);
   return st;
 }
 

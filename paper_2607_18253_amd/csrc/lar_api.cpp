@@ -126,7 +126,9 @@ lar_status ready(lar_ctx* ctx) {
   return LAR_OK;
 }
 
-const int64_t kMaxBudget = int64_t(1) << 30;
+// Largest token budget: the saturating prefix sums of the batch composition add two
+// values of at most B each in 32-bit lanes, so 2B must stay below 2^31.
+const int64_t kMaxBudget = (int64_t(1) << 30) - 1;
 
 }  // namespace
 
@@ -251,7 +253,7 @@ lar_status lar_load_state(lar_ctx* ctx, const lar_instance_params* params, const
     if (p.max_seqs < 1 || p.max_seqs > mcap)
       return fail(ctx, LAR_E_ARG, "instance %d: max_seqs %d outside [1, %d]", j, p.max_seqs, mcap);
     if (p.token_budget < p.max_seqs || p.token_budget > kMaxBudget)
-      return fail(ctx, LAR_E_ARG, "instance %d: token_budget %d outside [max_seqs, 2^30]", j,
+      return fail(ctx, LAR_E_ARG, "instance %d: token_budget %d outside [max_seqs, 2^30 - 1]", j,
                   p.token_budget);
     if (p.col < 0 || p.reserved != 0)
       return fail(ctx, LAR_E_ARG, "instance %d: bad col/reserved", j);

@@ -119,7 +119,8 @@ __device__ __forceinline__ int mbcnt(uint64_t m) {
 
 // Inclusive prefix sum over the wave, saturating at cap, with DPP lane moves
 // (row_shr within 16-lane rows, then row_bcast:15 / row_bcast:31 across rows).
-// Inputs in [0, cap] with cap <= 2^30, so no intermediate overflows;
+// Inputs in [0, cap] with cap < 2^30 (the token budget's bound), so a sum of two
+// saturated values stays below 2^31: no intermediate overflows;
 // min(sat(x), L) == min(x, L) for every L <= cap.
 __device__ __forceinline__ int scan_sat(int x, int cap) {
   x = min(x + __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true), cap);  // row_shr:1

@@ -479,7 +479,8 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
       wbatch += it;
       double eq2;
       int k;
-      const double u = utility_lane(q, v, wc, wl, tau, ttft, j, &k, &eq2);
+      const double u = utility_lane(q, v, wc, wl, tau, ttft, j, &k, &eq2, i, acc, cost,
+                                      n_cols, v < kWave ? 0 : pr.col[j]);
       if (better(u, k, bu, bj)) { bu = u; bj = k; bt = ttft; bq = eq2; }
     }
     const int m = trace_pick<NW>(bu, bj, bt, bq, i, z, N, choice, chosen_ttft, utility, s_u,
@@ -1253,7 +1254,6 @@ __global__ __launch_bounds__(256) void k_stats(int N, int I, const int32_t* choi
   }
 }
 
-// A one-thread kernel instead of a memset node, so the clear can sit in a captured graph.
 // ------------------------------------------------------------------ targets, OnTimeUtility
 // TTFT target of each query (appendix on TTFT latency assignment), in the written
 // order: lin = 155 + 3.5e-3*p, raw = u + lin*v, clipped to [150, 1120] ms.
@@ -1308,6 +1308,7 @@ __global__ __launch_bounds__(256) void k_ontime(int N, int I, const int32_t* cho
   if (threadIdx.x == 0) out[z] = __ddiv_rn(s, (double)N);
 }
 
+// A one-thread kernel instead of a memset node, so the clear can sit in a captured graph.
 __global__ void k_clear_error(int32_t* err) { *err = 0; }
 
 // ------------------------------------------------------------------ launchers
@@ -1332,7 +1333,6 @@ static hipError_t launch_commit_ks(const LaunchEnv& env, const int32_t* choice,
 template <int KS, int NW>
 static hipError_t launch_trace_mem(const LaunchEnv& env, const TraceArgs& a) {
   const int nw = env.I < NW ? env.I : NW;
-  if ((env.I + nw - 1) / nw > kWave) return hipErrorInvalidValue;   // 64 instances per wave
   if (a.realized)
     hipLaunchKernelGGL((k_trace_mem<KS, NW, true>), dim3(env.Z), dim3(nw * kWave), 0,
                        env.stream, LAR_TRACE_ARGS);
@@ -1349,19 +1349,19 @@ static hipError_t launch_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
   if (G > kMaxCluster) return hipErrorInvalidValue;
   if ((uint64_t)a.N >= (1ull << 31)) return hipErrorInvalidValue;  // 32-bit post tags
   const int w_used = G == 1 ? (env.I + IPW - 1) / IPW : W;
-  if (!co_resident(k_trace_cl<KS, W, IPW, TRK>, w_used * kWave, env.Z, G))
-    return hipErrorInvalidConfiguration;
-  if (G > 1) {
-    const int64_t n = (int64_t)env.Z * 2 * kMaxCluster * 4;
-    hipLaunchKernelGGL(k_clear_exchange, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
-                       env.stream, env.xslot, n);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
   const int blocks = env.Z * G;
-  hipLaunchKernelGGL((k_trace_cl<KS, W, IPW, TRK>), dim3(blocks), dim3(w_used * kWave), 0,
-                     env.stream, LAR_TRACE_ARGS, G, env.xslot, env.T.K, env.sync);
-  return hipGetLastError();
+  if (G == 1) {   // no exchange: the workgroups never wait for each other
+    hipLaunchKernelGGL((k_trace_cl<KS, W, IPW, TRK>), dim3(blocks), dim3(w_used * kWave), 0,
+                       env.stream, LAR_TRACE_ARGS, G, env.xslot, env.T.K, env.sync);
+    return hipGetLastError();
+  }
+  const int64_t n = (int64_t)env.Z * 2 * kMaxCluster * 4;
+  hipLaunchKernelGGL(k_clear_exchange, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                     env.stream, env.xslot, n);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_together(k_trace_cl<KS, W, IPW, TRK>, dim3(blocks), dim3(w_used * kWave),
+                         env.stream, LAR_TRACE_ARGS, G, env.xslot, env.T.K, env.sync);
 }
 
 // The clustered trace with (realised TTFT requested) or without first-token tracking.
@@ -1373,7 +1373,8 @@ static hipError_t launch_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
 
 template <int KS>
 static hipError_t launch_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
-  // One instance per wave.  The whole grid must be resident at once: up to 1024
+  // One instance per wave.  The whole grid must be resident at once (a cooperative
+  // launch when a scenario spans several workgroups): up to 1024
   // queues get one wave per SIMD (4 per workgroup; the per-query chain is issue
   // latency bound, so a wave runs fastest alone on its SIMD), up to 4096 get 16-wave
   // workgroups (4 waves per SIMD, 128 VGPRs each).  N must fit the 31-bit post tags
@@ -1384,8 +1385,9 @@ static hipError_t launch_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
     return G <= kMaxCluster && (uint64_t)a.N < (1ull << 31) && env.T.K >= 1 &&
            env.T.K <= kWave;
   };
-  // A shape whose workgroups cannot all be resident together reports
-  // hipErrorInvalidConfiguration without launching; the next one is tried.
+  // A shape whose workgroups the runtime cannot make resident together reports
+  // hipErrorInvalidConfiguration without running; the next one is tried, and the
+  // HBM-state kernel, whose workgroups never wait for each other, takes any size.
   hipError_t e = hipErrorInvalidConfiguration;
   if constexpr (KS <= 4) {
     if (queues <= 1024 && fits(4)) e = launch_trace_cl<KS, 4, 1>(env, a);

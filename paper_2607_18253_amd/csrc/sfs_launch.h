@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <tuple>
+
 #include "sfs_device.h"
 #include "sfs_limits.h"
 
@@ -85,19 +87,30 @@ hipError_t launch_stats(const LaunchEnv& env, int N, const int32_t* choice,
                         const double* chosen_ttft, const double* acc, const double* cost,
                         int n_cols, const double* w_cost, double* out);
 
-// Every workgroup of a clustered trace must be resident at once (members wait for
-// each other): with the blocks dealt to the 8 XCDs in turn, ceil(Z * G / 8) per XCD
-// must fit its compute units at the kernel's occupancy.
-template <class K>
-inline bool co_resident(K kernel, int threads, int Z, int G) {
-  int dev = 0, n_cu = 0, per_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return false;
-  if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-    return false;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess)
-    return false;
-  const int64_t per_xcd = ((int64_t)Z * G + 7) / 8;
-  return per_cu > 0 && per_xcd <= (int64_t)(n_cu / 8) * per_cu;
+// Launch a grid whose workgroups wait for each other (the clustered traces: the
+// members of a scenario exchange candidates every query) as a cooperative launch,
+// so that the runtime either makes every workgroup resident at once or refuses the
+// launch.  A refusal is reported as hipErrorInvalidConfiguration, on which the
+// callers fall through to a launch shape that needs no co-residency.  The kernel's
+// bounded wait stays as a backstop.
+template <typename... KArgs, typename... Args>
+inline hipError_t launch_together(void (*kernel)(KArgs...), dim3 grid, dim3 block,
+                                  hipStream_t stream, Args... args) {
+  static_assert(sizeof...(KArgs) == sizeof...(Args), "one value per kernel parameter");
+  std::tuple<KArgs...> vals(static_cast<KArgs>(args)...);
+  void* ptrs[sizeof...(KArgs)];
+  std::apply([&ptrs](auto&... v) {
+    int k = 0;
+    ((ptrs[k++] = static_cast<void*>(&v)), ...);
+  }, vals);
+  const hipError_t e =
+      hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kernel), grid, block, ptrs, 0,
+                                 stream);
+  if (e == hipErrorCooperativeLaunchTooLarge) {
+    (void)hipGetLastError();   // clear it: the caller tries another shape
+    return hipErrorInvalidConfiguration;
+  }
+  return e;
 }
 
 }  // namespace lar

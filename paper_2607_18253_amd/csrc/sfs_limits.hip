@@ -222,7 +222,8 @@ __global__ __launch_bounds__(NW * kWave) void k_ltrace(LAR_TRACE_PARAMS, DevLimi
       wbatch += it;
       double eq2;
       int k;
-      const double u = utility_lane(q, v, wc, wl, tau, ttft, j, &k, &eq2);
+      const double u = utility_lane(q, v, wc, wl, tau, ttft, j, &k, &eq2, i, acc, cost,
+                                      n_cols, v < kWave ? 0 : pr.col[j]);
       if (better(u, k, bu, bj)) { bu = u; bj = k; bt = ttft; bq = eq2; }
     }
     const int m = trace_pick<NW>(bu, bj, bt, bq, i, z, N, choice, chosen_ttft, utility, s_u,
@@ -453,7 +454,6 @@ template <int KS>
 static hipError_t launch_lim_trace_ks(const LaunchEnv& env, const TraceArgs& a) {
   constexpr int NW = lim_trace_waves<KS>();
   const int nw = env.I < NW ? env.I : NW;
-  if ((env.I + nw - 1) / nw > kWave) return hipErrorInvalidValue;   // 64 instances per wave
   if (a.realized)
     hipLaunchKernelGGL((k_ltrace<KS, NW, true>), dim3(env.Z), dim3(nw * kWave), 0, env.stream,
                        LAR_TRACE_ARGS, env.L);
@@ -463,24 +463,25 @@ static hipError_t launch_lim_trace_ks(const LaunchEnv& env, const TraceArgs& a) 
   return hipGetLastError();
 }
 
-// The clustered trace under limits (4 waves per workgroup, one per SIMD); reports
-// hipErrorInvalidConfiguration without launching when its workgroups cannot all be
-// resident at once.
+// The clustered trace under limits (4 waves per workgroup, one per SIMD), a
+// cooperative launch when a scenario spans several workgroups; reports
+// hipErrorInvalidConfiguration without running when the runtime cannot make its
+// workgroups resident at once.
 template <int KS, bool TRK>
 static hipError_t launch_lim_trace_cl(const LaunchEnv& env, const TraceArgs& a) {
   constexpr int W = 4;
   const int G = (env.I + W - 1) / W;
   if (G > kMaxCluster || (uint64_t)a.N >= (1ull << 31)) return hipErrorInvalidConfiguration;
   const int w_used = G == 1 ? env.I : W;
-  if (!co_resident(k_ltrace_cl<KS, W, TRK>, w_used * kWave, env.Z, G))
-    return hipErrorInvalidConfiguration;
-  if (G > 1) {
-    const hipError_t e = launch_clear_exchange(env);
-    if (e != hipSuccess) return e;
+  if (G == 1) {   // no exchange: the workgroups never wait for each other
+    hipLaunchKernelGGL((k_ltrace_cl<KS, W, TRK>), dim3(env.Z * G), dim3(w_used * kWave), 0,
+                       env.stream, LAR_TRACE_ARGS, env.L, G, env.xslot, env.sync);
+    return hipGetLastError();
   }
-  hipLaunchKernelGGL((k_ltrace_cl<KS, W, TRK>), dim3(env.Z * G), dim3(w_used * kWave), 0,
-                     env.stream, LAR_TRACE_ARGS, env.L, G, env.xslot, env.sync);
-  return hipGetLastError();
+  const hipError_t e = launch_clear_exchange(env);
+  if (e != hipSuccess) return e;
+  return launch_together(k_ltrace_cl<KS, W, TRK>, dim3(env.Z * G), dim3(w_used * kWave),
+                         env.stream, LAR_TRACE_ARGS, env.L, G, env.xslot, env.sync);
 }
 
 template <int KS>

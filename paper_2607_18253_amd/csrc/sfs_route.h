@@ -132,11 +132,21 @@ __device__ __forceinline__ double read_lane_f64(double v, int l) {
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
+// Candidate of the wave's l-th owned instance j for query i: lane l holds its acc /
+// cost for l < 64; an instance beyond the wave's 64th reads them from memory.
 __device__ __forceinline__ double utility_lane(const QueryIn& q, int l, double wc, double wl,
                                                const double* tau, double ttft, int j, int* key,
-                                               double* eq2) {
-  const double a = read_lane_f64(q.acc_l, l);
-  const double c = read_lane_f64(q.cost_l, l);
+                                               double* eq2, int i, const double* acc,
+                                               const double* cost, int n_cols, int col_j) {
+  double a, c;
+  if (l < kWave) {
+    a = read_lane_f64(q.acc_l, l);
+    c = read_lane_f64(q.cost_l, l);
+  } else {
+    const int64_t o = (int64_t)i * n_cols + col_j;
+    a = acc[o];
+    c = cost[o];
+  }
   const double u = __dsub_rn(a, __dmul_rn(wc, c));
   *eq2 = u;
   return cand_value(u, ttft, wl, tau, q.tau, j, key);

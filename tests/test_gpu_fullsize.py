@@ -1,20 +1,26 @@
-"""GPU parity at full size, in the launch configurations bench.py times.
+"""GPU parity at full size, in the launch configurations bench.py times, against
+expected values the oracle wrote (``tests/golden/make_fullsize.py``, oracle only):
 
-* c5: all 64 scenarios x 100k queries x 64 instances routed together; four scenarios
-  checked in full against the oracle (every choice and chosen-TTFT bit, the
-  per-scenario stats, final states).
-* c4: 256 instances x 50k queries; the oracle cannot replay the whole trace in a
-  test (each estimate walks a backlog of ~10^3 batches of 512 sequences), so the GPU
-  routes the first 49,992 queries, the oracle takes the GPU's state at that point
-  (validated on load: every resident list invariant) and routes the last 8 queries
-  from it, and the GPU's last 8 choices, chosen TTFTs and final state must be the
-  oracle's.
-* c6 in full, and c2 in full under Eq. 3 with realised-TTFT tracking.
+* c3: every entry of the 4096 x 1024 what-if matrix (TTFT bits and batch counts, in
+  blocks of 16 rows) and the route of every row (choices, Eq. 2 utility at the
+  choice).
+* c4: the 256-instance trace from the original snapshot over every query block the
+  oracle has covered (blocks of 1000 queries; all 50,000 when complete): choices,
+  chosen-TTFT and utility bits per block, the batches behind the estimates, and the
+  state of every instance after the last covered block.
+* c5: all 64 scenarios x 100k queries routed together: per scenario every choice,
+  chosen-TTFT and utility bit, the stats, the final state and the batches behind
+  the estimates.
+* c6 in full, and c2 in full under Eq. 3 with realised-TTFT tracking, against the
+  oracle run in the test.
+
+A mismatch names the first differing block or scenario; the oracle can then be run
+on that part alone.
 """
 
 from __future__ import annotations
 
-import dataclasses
+import json
 import os
 import sys
 
@@ -24,70 +30,109 @@ import pytest
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
-sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, HERE)
+sys.path.insert(0, os.path.join(HERE, "golden"))
+from digests import digest, state_digest  # noqa: E402
 from gpu_util import T, assert_state_equal, bits, gpu_trace  # noqa: E402
 from oracle import oracle as O  # noqa: E402
 from paper_2607_18253_amd import context_for  # noqa: E402
 from workloads import make_workload  # noqa: E402
 
 
-def test_c5_full_size_four_scenarios():
+def _golden(name):
+    path = os.path.join(HERE, "golden", f"fullsize_{name}.json")
+    if not os.path.exists(path):
+        pytest.fail(f"missing {path}: run tests/golden/make_fullsize.py {name}")
+    with open(path) as f:
+        return json.load(f)
+
+
+def _state_digest(ctx, z):
+    s = ctx.read_state(z)
+    return state_digest(s["offsets"], s["rem_prefill"], s["rem_decode"], s["context"],
+                        s["clock_ms"], s["iterations"])
+
+
+def test_c3_full_matrix_every_entry():
+    g = _golden("c3")
+    wl = make_workload("c3")
+    assert (g["rows"], g["instances"]) == (wl.n_q, wl.n_inst)
+    ctx = context_for(wl)
+    tt, it = ctx.estimate(T(wl.q_prefill, torch.int32), 0.0)
+    util = torch.empty((1, wl.n_q), dtype=torch.float64, device="cuda:0")
+    chosen = torch.empty((1, wl.n_q), dtype=torch.float64, device="cuda:0")
+    ch = ctx.route(tt, T(wl.acc, torch.float64), T(wl.cost, torch.float64),
+                   T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64),
+                   chosen_ttft=chosen, utility=util)
+    ctx.sync()
+    tt = tt.cpu().numpy()[0]
+    it = it.cpu().numpy()[0].astype(np.int32)
+    ch = ch.cpu().numpy()[0].astype(np.int32)
+    B = g["block_rows"]
+    bad_t = [b for b, d in enumerate(g["ttft_blocks"]) if digest(tt[b * B:(b + 1) * B]) != d]
+    bad_i = [b for b, d in enumerate(g["iters_blocks"]) if digest(it[b * B:(b + 1) * B]) != d]
+    assert not bad_t, f"TTFT differs in row blocks {bad_t[:8]} (rows of {B})"
+    assert not bad_i, f"batch counts differ in row blocks {bad_i[:8]} (rows of {B})"
+    assert int(it.sum(dtype=np.int64)) == g["iters_total"]
+    assert digest(ch) == g["choice"], "route choices differ"
+    assert digest(util.cpu().numpy()[0]) == g["utility"], "utility at the choice differs"
+    np.testing.assert_array_equal(bits(chosen.cpu().numpy()[0]),
+                                  bits(tt[np.arange(wl.n_q), ch]))
+    ctx.close()
+
+
+def test_c4_full_size_from_original_snapshot():
+    g = _golden("c4")
+    blocks = g["blocks"]
+    assert blocks, "no c4 block written yet"
+    wl = make_workload("c4")
+    N = blocks[-1]["end"]
+    assert all(b["first"] == k * g["block_queries"] for k, b in enumerate(blocks))
+    ctx = context_for(wl)
+    ctx.advance(float(wl.q_t_ms[0]))
+    chosen = torch.full((1, N), -1.0, dtype=torch.float64, device="cuda:0")
+    util = torch.full((1, N), -1.0, dtype=torch.float64, device="cuda:0")
+    ch = ctx.route_trace(T(wl.q_prefill[:N], torch.int32), T(wl.q_decode[:N], torch.int32),
+                         T(wl.q_t_ms[:N], torch.float64), float(wl.q_t_ms[N - 1]),
+                         T(wl.acc[:N], torch.float64), T(wl.cost[:N], torch.float64),
+                         T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64),
+                         chosen_ttft=chosen, utility=util)
+    assert ctx.status() == 0
+    ch = ch.cpu().numpy()[0].astype(np.int32)
+    chosen = chosen.cpu().numpy()[0]
+    util = util.cpu().numpy()[0]
+    for k, b in enumerate(blocks):
+        sl = slice(b["first"], b["end"])
+        assert digest(ch[sl]) == b["choice"], f"choices differ in block {k} ({sl})"
+        assert digest(chosen[sl]) == b["ttft"], f"chosen TTFT differs in block {k}"
+        assert digest(util[sl]) == b["utility"], f"utility differs in block {k}"
+    assert int(ctx.trace_work()[0]) == sum(b["estimate_batches"] for b in blocks)
+    assert _state_digest(ctx, 0) == blocks[-1]["state"], f"state after {N} queries differs"
+    ctx.close()
+
+
+def test_c5_all_scenarios_full_size():
+    g = _golden("c5")
     wl = make_workload("c5")
+    assert (g["scenarios"], g["queries"]) == (wl.n_scen, wl.n_q)
     choice, chosen, util, ctx = gpu_trace(wl)
+    assert ctx.status() == 0
     st = ctx.stats(T(choice, torch.int32), T(chosen, torch.float64), T(wl.acc, torch.float64),
                    T(wl.cost, torch.float64), T(wl.w_cost, torch.float64))
     ctx.sync()
     st = st.cpu().numpy()
-    for z in (0, 21, 42, 63):
-        ref = O.trace(wl, scenario=z)
-        np.testing.assert_array_equal(choice[z], ref.choice, err_msg=f"scenario {z}")
-        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen))
-        np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
-        assert_state_equal(ctx, z, ref)
-        want = O.stats(ref.choice, ref.ttft_chosen, wl.acc, wl.cost, wl.col, wl.w_cost[z])
-        np.testing.assert_array_equal(bits(st[z]), bits(want), err_msg=f"stats {z}")
-    ctx.close()
-
-
-def test_c4_full_size_last_queries():
-    wl = make_workload("c4")
-    N, tail = wl.n_q, 8
-    N1 = N - tail
-    ctx = context_for(wl)
-    ctx.advance(float(wl.q_t_ms[0]))
-
-    def run(lo, hi, t_after):
-        chosen = torch.full((1, hi - lo), -1.0, dtype=torch.float64, device="cuda:0")
-        util = torch.full((1, hi - lo), -1.0, dtype=torch.float64, device="cuda:0")
-        ch = ctx.route_trace(T(wl.q_prefill[lo:hi], torch.int32), T(wl.q_decode[lo:hi], torch.int32),
-                             T(wl.q_t_ms[lo:hi], torch.float64), t_after,
-                             T(wl.acc[lo:hi], torch.float64), T(wl.cost[lo:hi], torch.float64),
-                             T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64),
-                             chosen_ttft=chosen, utility=util)
-        ctx.sync()
-        return ch.cpu().numpy()[0], chosen.cpu().numpy()[0], util.cpu().numpy()[0]
-
-    run(0, N1, float(wl.q_t_ms[N1]))
-    s = ctx.read_state(0)
-    c2, t2, u2 = run(N1, N, float(wl.q_t_ms[-1]))
-    # the oracle from the GPU's state after the first N1 queries (the oracle checks every
-    # resident-list invariant when it loads the state)
-    rest = dataclasses.replace(
-        wl, offsets=s["offsets"], rem_prefill=s["rem_prefill"], rem_decode=s["rem_decode"],
-        context=s["context"], clock_ms=s["clock_ms"], q_prefill=wl.q_prefill[N1:],
-        q_decode=wl.q_decode[N1:], q_t_ms=wl.q_t_ms[N1:], acc=wl.acc[N1:], cost=wl.cost[N1:],
-        tau_u_ms=wl.tau_u_ms[N1:], tau_v=wl.tau_v[N1:])
-    ref = O.trace(rest, queue_cap=10 ** 6)
-    np.testing.assert_array_equal(c2, ref.choice)
-    np.testing.assert_array_equal(bits(t2), bits(ref.ttft_chosen))
-    np.testing.assert_array_equal(bits(u2), bits(ref.util_chosen))
-    fin = ctx.read_state(0)
-    np.testing.assert_array_equal(fin["offsets"], ref.offsets)
-    np.testing.assert_array_equal(fin["rem_prefill"], ref.rem_prefill)
-    np.testing.assert_array_equal(fin["rem_decode"], ref.rem_decode)
-    np.testing.assert_array_equal(fin["context"], ref.context)
-    np.testing.assert_array_equal(bits(fin["clock_ms"]), bits(ref.clock_ms))
-    np.testing.assert_array_equal(fin["iterations"] - s["iterations"], ref.iterations)
+    work = ctx.trace_work()
+    bad = []
+    for z, want in enumerate(g["per_scenario"]):
+        got = dict(choice=digest(choice[z].astype(np.int32)), ttft=digest(chosen[z]),
+                   utility=digest(util[z]),
+                   stats_bits=[format(int(v), "016x") for v in st[z].view(np.uint64)],
+                   state=_state_digest(ctx, z), estimate_batches=int(work[z]))
+        diff = [k for k in got if got[k] != want[k]]
+        if diff:
+            bad.append((z, diff))
+    assert not bad, f"scenarios differing from the oracle: {bad[:8]}"
     ctx.close()
 
 

@@ -130,39 +130,35 @@ def test_estimate_many_slots_and_ragged():
     ctx.close()
 
 
-def test_estimate_c3_full_matrix_sampled():
-    """Config 3 at full size: 1024 instances x 512 residents, 4096 queries in one
-    call.  Every iteration count and TTFT bit is checked on two whole rows and a
-    random sample of pairs; the row argmax is checked on every row."""
-    wl = make_workload("c3")
-    ctx = context_for(wl)
-    qp = T(wl.q_prefill, torch.int32)
-    tt, it = ctx.estimate(qp, 0.0)
-    acc, cost = T(wl.acc, torch.float64), T(wl.cost, torch.float64)
-    util = torch.empty((1, wl.n_q), dtype=torch.float64, device=DEV)
-    chosen = torch.empty((1, wl.n_q), dtype=torch.float64, device=DEV)
-    ch = ctx.route(tt, acc, cost, T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64),
-                   chosen_ttft=chosen, utility=util)
+@pytest.mark.parametrize("flags", [0, 1])
+def test_max_budget_adjacent_large_waiting(flags):
+    """The largest token budget, 2^30 - 1, with four waiting entries of nearly that
+    many tokens behind a smaller first one: the saturating prefix sum that composes
+    the batch adds two saturated partial sums (2B - 2 < 2^31).  Estimates at several
+    prompts and a replay, against the oracle."""
+    B = (1 << 30) - 1
+    M = 8
+    coef = dict(a=1.0, b=2.0 ** -20, c=0.5, d=0.0, e=2.0 ** -40)
+    reqs = [(5, 3, 0), (B - 1, 2, 0), (B - 2, 4, 0), (B - 3, 1, 0), (B - 4, 2, 0)]
+    ctx = _single(coef, B, M, reqs, flags=flags, max_prompt=B)
+    ps = [1, 3, 1000, B - 7, B]
+    tt, it = ctx.estimate(T(ps, torch.int32), 0.0)
     ctx.sync()
-    tt, it, ch = tt.cpu().numpy()[0], it.cpu().numpy()[0], ch.cpu().numpy()[0]
-    rng = np.random.default_rng(0)
-    rows = [0, int(np.argmax(wl.q_prefill))]
-    ref, ref_it = O.estimate_matrix(wl, rows, range(wl.n_inst), 0.0)
-    np.testing.assert_array_equal(it[rows], ref_it)
-    np.testing.assert_array_equal(bits(tt[rows]), bits(ref))
-    for r, i in enumerate(rows):
-        m, _ = O.route_row(ref[r], wl.acc[i], wl.cost[i], wl.col, wl.w_cost[0], wl.w_lat_ms[0])
-        assert ch[i] == m
-    qs = rng.integers(0, wl.n_q, 300)
-    js = rng.integers(0, wl.n_inst, 300)
-    for q, j in zip(qs, js):
-        want, wit = O.instance_queue(wl, int(j)).estimate(int(wl.q_prefill[q]), 1, 0.0)
-        assert it[q, j] == wit and bits(tt[q, j]) == bits(want), (q, j)
-    # every row: choice is the oracle's route of the GPU's (oracle-identical) TTFT row
-    for i in range(wl.n_q):
-        m, _ = O.route_row(tt[i], wl.acc[i], wl.cost[i], wl.col, wl.w_cost[0], wl.w_lat_ms[0])
-        assert ch[i] == m, i
-    assert np.array_equal(bits(chosen.cpu().numpy()[0]), bits(tt[np.arange(wl.n_q), ch]))
+    tt, it = tt.cpu().numpy()[0, :, 0], it.cpu().numpy()[0, :, 0]
+    par = O.make_params(coef["a"], coef["b"], coef["c"], coef["d"], coef["e"], B, M)
+    q = O.Queue(par, [r[0] for r in reqs], [r[1] for r in reqs], [r[2] for r in reqs])
+    for k, p in enumerate(ps):
+        want, wit = q.estimate(p, 1, 0.0, reading=flags)
+        assert it[k] == wit and bits(tt[k]) == bits(want), (p, tt[k], want, it[k], wit)
+    t_next = float(tt[2]) * 0.75
+    ctx.advance(t_next)
+    q.advance(t_next)
+    s = ctx.read_state(0)
+    rp, rd, cx, clk, its = q.state()
+    np.testing.assert_array_equal(s["rem_prefill"], rp)
+    np.testing.assert_array_equal(s["rem_decode"], rd)
+    np.testing.assert_array_equal(s["context"], cx)
+    assert bits(s["clock_ms"][0]) == bits(clk) and s["iterations"][0] == its
     ctx.close()
 
 
@@ -312,6 +308,28 @@ def test_trace_c4_instances_shared(n_inst, n_q):
     np.testing.assert_array_equal(bits(chosen[0]), bits(ref.ttft_chosen))
     np.testing.assert_array_equal(bits(util[0]), bits(ref.util_chosen))
     assert_state_equal(ctx, 0, ref)
+    ctx.close()
+
+
+@pytest.mark.parametrize("limits", [False, True])
+def test_trace_large_pool_hbm_kernel(limits):
+    """600 instances in 8 scenarios (4800 queues, more than the clustered shapes
+    take): the HBM-state trace, each of 8 waves owning 75 instances, so the
+    instances past a wave's 64th read their accuracy and cost from memory; under
+    scheduler limits 1100 instances over 16 waves (69 each).  Three scenarios
+    against the oracle."""
+    n_inst = 1100 if limits else 600
+    wl = make_tiny_workload(11, n_inst=n_inst, n_scen=8, n_q=12, max_res=6, budget=(4, 16),
+                            max_seqs=(2, 6), prompt=(1, 20))
+    if limits:
+        wl.sched = np.tile(np.array([[3, 0, 0, 64]], np.int32), (wl.n_inst, 1))
+    choice, chosen, util, ctx = gpu_trace(wl)
+    for z in (0, 3, 7):
+        ref = O.trace(wl, scenario=z)
+        np.testing.assert_array_equal(choice[z], ref.choice, err_msg=f"scenario {z}")
+        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen))
+        np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
+        assert_state_equal(ctx, z, ref)
     ctx.close()
 
 

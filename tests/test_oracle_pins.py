@@ -542,3 +542,56 @@ def test_realized_properties_tiny(seed):
                             n_scen=1)
     for reading in (0, 1):
         _realized_properties(wl, O.trace(wl, reading=reading, queue_cap=10 ** 6))
+
+
+# ------------------------------------------------------------------ threads
+def _same_trace(a, b):
+    for f in ("choice", "ttft_chosen", "util_chosen", "ttft_all", "iters_all", "offsets",
+              "rem_prefill", "rem_decode", "context", "clock_ms", "iterations", "realized"):
+        x, y = getattr(a, f), getattr(b, f)
+        if x is None:
+            assert y is None
+            continue
+        x, y = np.asarray(x), np.asarray(y)
+        if x.dtype == np.float64:
+            x, y = x.view(np.int64), y.view(np.int64)
+        np.testing.assert_array_equal(x, y, err_msg=f)
+
+
+def test_threaded_oracle_is_bit_identical():
+    """The oracle's loops over independent instances (estimates of one query, the
+    replays) and over the pairs of a what-if matrix, and scenarios run on threads of
+    their own, give exactly the single-threaded results: c1 and c7 in full, c2 and
+    c4 prefixes with every TTFT row, c3 what-if rows, c5 scenarios."""
+    from workloads import make_workload
+    cases = [("c1", None, {}), ("c7", 1500, {}), ("c2", 1500, {}), ("c4", 3, {}),
+             ("c2", 400, {"tau": "targets"})]
+    try:
+        for name, n_q, kw in cases:
+            wl = make_workload(name)
+            if kw.get("tau") == "targets":
+                kw = {"tau": O.ttft_targets(wl.q_prefill, wl.tau_u_ms, wl.tau_v)}
+            O.set_threads(1)
+            one = O.trace(wl, n_q=n_q, full_rows=True, **kw)
+            O.set_threads(4)
+            four = O.trace(wl, n_q=n_q, full_rows=True, **kw)
+            _same_trace(one, four)
+        wl = make_workload("c3")
+        rows = [0, 1, int(np.argmax(wl.q_prefill))]
+        O.set_threads(1)
+        t1, i1 = O.estimate_matrix_all(wl, queries=rows)
+        O.set_threads(4)
+        t4, i4 = O.estimate_matrix_all(wl, queries=rows)
+        np.testing.assert_array_equal(t1.view(np.int64), t4.view(np.int64))
+        np.testing.assert_array_equal(i1, i4)
+        # the literal per-pair estimate of the Python loop gives the same values
+        ref, ref_it = O.estimate_matrix(wl, rows[:1], range(0, wl.n_inst, 97))
+        np.testing.assert_array_equal(ref.view(np.int64), t1[:1, ::97].view(np.int64))
+        np.testing.assert_array_equal(ref_it, i1[:1, ::97])
+    finally:
+        O.set_threads(1)
+    wl = make_workload("c5", n_q=150)
+    seq = O.trace_scenarios(wl, [0, 9, 63], 1)
+    par = O.trace_scenarios(wl, [0, 9, 63], 3)
+    for a, b in zip(seq, par):
+        _same_trace(a, b)
