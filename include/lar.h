@@ -409,6 +409,65 @@ lar_status lar_board_collect(lar_board *board, int32_t *offsets, int32_t *rem_pr
  */
 lar_status lar_trace_work(lar_ctx *ctx, int64_t *estimate_batches);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): lar_estimate_ttft followed
+ * by lar_route for one scenario, with no context.  Same results bit for bit.  The
+ * snapshot is read from device memory and laid out on the device; every
+ * intermediate buffer lives in one 32 MiB device array in the library, of which
+ * each GPU holds its own copy, set up on the first call on that GPU (the stream's
+ * device must be current) and kept until the process ends.  The call allocates
+ * nothing and does not synchronise.  Calls that overlap on one GPU (other threads,
+ * other streams) share that array and race: serialise them.
+ *   cfg  host: n_inst I >= 1; max_seqs_cap (bound on every M, 1..1024); max_resident
+ *        (bound on the requests of any one instance in the snapshot, >= 0);
+ *        max_prompt (>= every q_prefill, >= 1); n_cols (columns of acc / cost);
+ *        flags (LAR_FIRST_TOKEN_*); max_iters (>= 1); stream (hipStream_t, NULL =
+ *        null stream).  The working memory, about
+ *          I * (936 + 12 * max_seqs_cap + 16 * (max_resident + max_seqs_cap))
+ *        bytes (each of its 21 arrays rounded up to 256 bytes), must fit the 32 MiB
+ *        (else LAR_E_CAPACITY, nothing enqueued).
+ *   params   dev [I] instance coefficients and limits, as for lar_load_state
+ *   offsets  dev [I+1]; rem_prefill, rem_decode, context dev [offsets[I]]:
+ *            the resident requests of every instance in FCFS order (lar_load_state's
+ *            layout); the offsets must index these arrays
+ *   clock_ms dev [I];  q_prefill dev [Q];  t_ms the arrival time (every clock >= t_ms)
+ *   acc, cost dev [Q][n_cols];  w_cost, w_lat dev [1] (as lar_route)
+ *   ttft_ms dev [Q][I];  iters dev [Q][I] or NULL;  choice dev [Q];
+ *   chosen_ttft, utility dev [Q] or NULL
+ *   status   dev [1] int32: set to 0 first, then to the first error found on the
+ *            device -- LAR_E_ARG (bad coefficients or limits, a column >= n_cols,
+ *            a prompt outside 1..max_prompt, or a prompt bound needing more than 64
+ *            decode-only batches after its admission batch), LAR_E_STATE (an
+ *            instance's requests break lar_load_state's rules, more than
+ *            max_resident of them, or a clock behind t_ms), LAR_E_ITER.  An instance
+ *            found invalid is treated as empty; the outputs are meaningful only when
+ *            status is 0 after the stream completes.
+ * Errors found on the host return at once with nothing enqueued;
+ * lar_noalloc_error_string() gives this thread's last detail.  n_q == 0: LAR_OK,
+ * nothing enqueued, status not written.
+ */
+typedef struct {
+  int32_t n_inst;
+  int32_t max_seqs_cap;
+  int32_t max_resident;
+  int32_t max_prompt;
+  int32_t n_cols;
+  int32_t flags;
+  int64_t max_iters;
+  void *stream;
+} lar_whatif_config;
+
+lar_status lar_whatif_noalloc(const lar_whatif_config *cfg, const lar_instance_params *params,
+                              const int32_t *offsets, const int32_t *rem_prefill,
+                              const int32_t *rem_decode, const int32_t *context,
+                              const double *clock_ms, int32_t n_q, const int32_t *q_prefill,
+                              double t_ms, const double *acc, const double *cost,
+                              const double *w_cost, const double *w_lat, double *ttft_ms,
+                              int32_t *iters, int32_t *choice, double *chosen_ttft,
+                              double *utility, int32_t *status);
+const char *lar_noalloc_error_string(void);
+
 /* Synchronise the stream; return the sticky device error, if any. */
 lar_status lar_sync(lar_ctx *ctx);
 

@@ -74,7 +74,10 @@ struct DevTraj {
   int32_t* tailD;       // [K][ZI] decode tokens of the k-th batch after admission
   int64_t* tailC;       // [K][ZI] their context sum
   int32_t K;
+  const int32_t* Kdev;  // when set, K is read from device memory (worked out there)
 };
+
+__device__ __forceinline__ int tail_count(const DevTraj& tr) { return tr.Kdev ? *tr.Kdev : tr.K; }
 
 struct Coef {
   double a, b, c, d, e;

@@ -87,7 +87,8 @@ __global__ __launch_bounds__(kWave) void k_traj(DevState S, DevParams pr, DevTra
     else w.step(e);   // the admission batch itself (background only)
   }
   const int ZI = Z * I;
-  for (int kk = 0; kk < tr.K; ++kk) {
+  const int K = tail_count(tr);
+  for (int kk = 0; kk < K; ++kk) {
     int64_t D = 0, C = 0;
     if (ok) {
       if (readonly) {
@@ -148,8 +149,9 @@ __global__ __launch_bounds__(256) void k_est(DevParams pr, DevTraj tr, int Z, in
   int64_t cxq = ch;
   bool done = reading == 1 && rem == 0;
   int kk = 0;
+  const int K = tail_count(tr);
   while (!done) {
-    if (kk >= tr.K) {   // cannot happen for p <= max_prompt; guard the tail bounds
+    if (kk >= K) {   // cannot happen for p <= max_prompt; guard the tail bounds
       set_error(err, kErrIter);
       E = __builtin_nan("");
       break;

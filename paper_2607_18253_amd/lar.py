@@ -23,7 +23,8 @@ EXPORTED = ("lar_create", "lar_destroy", "lar_error_string", "lar_load_state", "
             "lar_commit", "lar_route_step", "lar_route_trace", "lar_route_trace_constrained",
             "lar_stats", "lar_set_scheduler",
             "lar_ontime_utility", "lar_read_state", "lar_sync", "lar_trace_work", "lar_board_create",
-            "lar_board_destroy", "lar_board_publish", "lar_board_collect")
+            "lar_board_destroy", "lar_board_publish", "lar_board_collect",
+            "lar_whatif_noalloc", "lar_noalloc_error_string")
 
 
 class LarError(RuntimeError):
@@ -41,6 +42,12 @@ class Config(C.Structure):
 class SchedLimits(C.Structure):
     _fields_ = [("chunk_cap", C.c_int32), ("kv_blocks", C.c_int32), ("block_size", C.c_int32),
                 ("max_ctx", C.c_int32)]
+
+
+class WhatifConfig(C.Structure):
+    _fields_ = [("n_inst", C.c_int32), ("max_seqs_cap", C.c_int32), ("max_resident", C.c_int32),
+                ("max_prompt", C.c_int32), ("n_cols", C.c_int32), ("flags", C.c_int32),
+                ("max_iters", C.c_int64), ("stream", C.c_void_p)]
 
 
 class InstanceParams(C.Structure):
@@ -110,6 +117,11 @@ def load_library(path: str = LIB_PATH):
     L.lar_read_state.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, i64, C.POINTER(i64)]
     L.lar_sync.restype = i32
     L.lar_sync.argtypes = [vp]
+    L.lar_whatif_noalloc.restype = i32
+    L.lar_whatif_noalloc.argtypes = [C.POINTER(WhatifConfig), vp, vp, vp, vp, vp, vp, i32, vp, dbl,
+                                     vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.lar_noalloc_error_string.restype = C.c_char_p
+    L.lar_noalloc_error_string.argtypes = []
     _lib = L
     return L
 
@@ -476,3 +488,53 @@ class SnapshotBoard:
             self.close()
         except Exception:
             pass
+
+
+def params_array(a, b, c, d, e, budget, max_seqs, col):
+    """Instance parameters as a numpy array of lar_instance_params records (to copy
+    into device memory for lar_whatif_noalloc)."""
+    I = len(a)
+    rec = np.zeros(I, dtype=np.dtype([("a", "<f8"), ("b", "<f8"), ("c", "<f8"), ("d", "<f8"),
+                                      ("e", "<f8"), ("token_budget", "<i4"),
+                                      ("max_seqs", "<i4"), ("col", "<i4"), ("reserved", "<i4")]))
+    rec["a"], rec["b"], rec["c"], rec["d"], rec["e"] = a, b, c, d, e
+    rec["token_budget"], rec["max_seqs"], rec["col"] = budget, max_seqs, col
+    assert rec.dtype.itemsize == C.sizeof(InstanceParams)
+    return rec
+
+
+def whatif_noalloc(params, offsets, rem_prefill, rem_decode, context, clock_ms, q_prefill,
+                   t_ms, acc, cost, w_cost, w_lat, ttft, choice, status, *, max_seqs_cap,
+                   max_resident, max_prompt, flags=FIRST_TOKEN_DECODE_BATCH,
+                   max_iters=10_000_000, iters=None, chosen_ttft=None, utility=None,
+                   stream=None):
+    """lar_whatif_noalloc: every argument array is a GPU tensor the caller allocated
+    (params: uint8 tensor holding lar_instance_params records, see params_array);
+    writes ttft [Q][I], choice [Q], status [1] (and iters, chosen_ttft, utility
+    when given).  Enqueues on the current stream (or ``stream``) and returns."""
+    import torch
+    L = load_library()
+    I = int(offsets.numel()) - 1
+    Q = int(q_prefill.numel())
+    n_cols = int(acc.shape[1]) if acc.dim() == 2 else 1
+    if stream is None:
+        stream = torch.cuda.current_stream().cuda_stream
+    cfg = WhatifConfig(I, int(max_seqs_cap), int(max_resident), int(max_prompt), n_cols,
+                       int(flags), int(max_iters), C.c_void_p(stream))
+    if params.dtype != torch.uint8 or params.numel() != I * C.sizeof(InstanceParams):
+        raise ValueError("params must hold one lar_instance_params record per instance")
+    st = L.lar_whatif_noalloc(
+        C.byref(cfg), _dev(params, torch.uint8, "params"), _dev(offsets, torch.int32, "offsets"),
+        _dev(rem_prefill, torch.int32, "rem_prefill"), _dev(rem_decode, torch.int32, "rem_decode"),
+        _dev(context, torch.int32, "context"), _dev(clock_ms, torch.float64, "clock_ms", I), Q,
+        _dev(q_prefill, torch.int32, "q_prefill"), float(t_ms),
+        _dev(acc, torch.float64, "acc", Q * n_cols), _dev(cost, torch.float64, "cost", Q * n_cols),
+        _dev(w_cost, torch.float64, "w_cost", 1), _dev(w_lat, torch.float64, "w_lat", 1),
+        _dev(ttft, torch.float64, "ttft", Q * I),
+        _dev(iters, torch.int32, "iters", Q * I) if iters is not None else None,
+        _dev(choice, torch.int32, "choice", Q),
+        _dev(chosen_ttft, torch.float64, "chosen_ttft", Q) if chosen_ttft is not None else None,
+        _dev(utility, torch.float64, "utility", Q) if utility is not None else None,
+        _dev(status, torch.int32, "status", 1))
+    if st != LAR_OK:
+        raise LarError(st, L.lar_noalloc_error_string().decode())
