@@ -131,6 +131,15 @@ def lib():
     L.orc_estimate_matrix.restype = C.c_int
     L.orc_estimate_matrix.argtypes = [C.c_int32, C.POINTER(C.c_void_p), C.c_int32, _i32p, _i32p,
                                       C.c_double, C.c_int32, C.c_int64, _f64p, _i32p]
+    L.orc_lps_wait.restype = C.c_double
+    L.orc_lps_wait.argtypes = [C.c_double, C.c_double, C.c_int32, C.c_int32, C.c_double,
+                               C.c_double]
+    L.orc_lps_ttft.restype = C.c_double
+    L.orc_lps_ttft.argtypes = [C.c_double, C.c_double, C.c_int32, C.c_int32, C.c_double,
+                               C.c_double, C.c_double, C.c_double, C.c_int32]
+    L.orc_lps_matrix.restype = None
+    L.orc_lps_matrix.argtypes = [C.c_int32, _f64p, _f64p, _i32p, _f64p, _f64p, _f64p, _f64p,
+                                 C.c_int32, C.c_int32, _i32p, _f64p]
     L.orc_stats.restype = C.c_int
     L.orc_stats.argtypes = [C.c_int32, _i32p, _f64p, _f64p, _f64p, C.c_int32, _i32p, C.c_double,
                             _f64p]
@@ -410,3 +419,31 @@ def trace_scenarios(wl, scenarios, n_threads: int, **kw):
         return [trace(wl, scenario=z, **kw) for z in scenarios]
     with ThreadPoolExecutor(max_workers=n_threads) as ex:
         return list(ex.map(lambda z: trace(wl, scenario=z, **kw), scenarios))
+
+
+LPS_POISSON = 0        # Eqs. 10 and 12
+LPS_VARIABILITY = 1    # Eq. 13
+
+
+def lps_wait(alpha, mu, k, mode=LPS_POISSON, ca2=1.0, cs2=1.0):
+    """Expected LPS queueing delay (ms) of an instance; NaN outside the model."""
+    return float(lib().orc_lps_wait(float(alpha), float(mu), int(k), int(mode), float(ca2),
+                                    float(cs2)))
+
+
+def lps_ttft(alpha, mu, k, theta, t_dec, p, mode=LPS_POISSON, ca2=1.0, cs2=1.0):
+    """Average-case TTFT estimate (Eq. 11), ms."""
+    return float(lib().orc_lps_ttft(float(alpha), float(mu), int(k), int(mode), float(ca2),
+                                    float(cs2), float(theta), float(t_dec), int(p)))
+
+
+def lps_matrix(prm, p, mode=LPS_POISSON):
+    """LPS TTFT of every query (prompts p) at every instance; prm holds per-instance
+    arrays alpha, mu, k, ca2, cs2, theta, t_dec.  Returns [Q][I]."""
+    f = lambda k: np.ascontiguousarray(prm[k], np.float64)  # noqa: E731
+    I = len(prm["alpha"])
+    p = _i32(p)
+    out = np.zeros((len(p), I))
+    lib().orc_lps_matrix(I, f("alpha"), f("mu"), _i32(prm["k"]), f("ca2"), f("cs2"),
+                         f("theta"), f("t_dec"), int(mode), len(p), p, out)
+    return out

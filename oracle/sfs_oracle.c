@@ -745,6 +745,73 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
   return st;
 }
 
+/* ---------------------------------------------------------------- LPS */
+
+/*
+ * Average-case TTFT without real-time workload information (Sec. 4.2, Eqs. 10 and
+ * 11; the appendix on the limited-processor-sharing abstraction, Eqs. 12 and 13).
+ * An instance is one server of aggregate capacity mu (queries per ms) shared
+ * equally by at most k active queries; further queries wait in FCFS order.  Queries
+ * arrive at rate alpha (queries per ms); the model needs alpha < mu.
+ *
+ *   mode 0, Poisson arrivals and memoryless work (Eqs. 10 and 12):
+ *       rho = alpha / mu,   W = rho^k / (mu - alpha)
+ *   mode 1, the variability-corrected approximation (Eq. 13), with the mean work
+ *   E[Q] = 1/mu and squared coefficients of variation ca2 (inter-arrival times) and
+ *   cs2 (work):
+ *       E[Q] = 1 / mu,  rho = alpha * E[Q],
+ *       W = ((ca2 + cs2) / 2) * ((rho^k * E[Q]) / (1 - rho))
+ *   and the TTFT estimate (Eq. 11) of a query of p prompt tokens, with prefill
+ *   throughput theta (tokens per ms) and mean decode batch time t_dec (ms):
+ *       L = (W + p / theta) + t_dec.
+ * rho^k is the product of k factors rho taken left to right.  Each operation is one
+ * binary64 round-to-nearest-even operation in the order written.  Parameters outside
+ * the model (k < 1, alpha < 0, alpha >= mu, rho >= 1, theta <= 0, t_dec < 0, negative
+ * variation coefficients, non-finite values) and p < 1 give NaN.
+ */
+static double pow_left(double r, int32_t k) {
+  double x = r;
+  for (int32_t m = 1; m < k; ++m) x = x * r;
+  return x;
+}
+
+double orc_lps_wait(double alpha, double mu, int32_t k, int32_t mode, double ca2, double cs2) {
+  if (!(isfinite(alpha) && isfinite(mu) && alpha >= 0.0 && alpha < mu && k >= 1)) return NAN;
+  if (mode == 0) {
+    const double rho = alpha / mu;
+    return pow_left(rho, k) / (mu - alpha);
+  }
+  if (mode != 1 || !(isfinite(ca2) && isfinite(cs2) && ca2 >= 0.0 && cs2 >= 0.0)) return NAN;
+  const double eq = 1.0 / mu;
+  const double rho = alpha * eq;
+  if (!(rho < 1.0)) return NAN;
+  const double h = (ca2 + cs2) / 2.0;
+  double t = pow_left(rho, k) * eq;
+  t = t / (1.0 - rho);
+  return h * t;
+}
+
+double orc_lps_ttft(double alpha, double mu, int32_t k, int32_t mode, double ca2, double cs2,
+                    double theta, double t_dec, int32_t p) {
+  const double w = orc_lps_wait(alpha, mu, k, mode, ca2, cs2);
+  if (isnan(w) || p < 1 || !(isfinite(theta) && theta > 0.0) ||
+      !(isfinite(t_dec) && t_dec >= 0.0))
+    return NAN;
+  return (w + (double)p / theta) + t_dec;
+}
+
+/* The LPS estimate of every query i < n_q at every instance j < n_inst (parameters
+   per instance), into out[i*n_inst + j]. */
+void orc_lps_matrix(int32_t n_inst, const double *alpha, const double *mu, const int32_t *k,
+                    const double *ca2, const double *cs2, const double *theta,
+                    const double *t_dec, int32_t mode, int32_t n_q, const int32_t *p,
+                    double *out) {
+  for (int32_t i = 0; i < n_q; ++i)
+    for (int32_t j = 0; j < n_inst; ++j)
+      out[(int64_t)i * n_inst + j] = orc_lps_ttft(alpha[j], mu[j], k[j], mode, ca2[j], cs2[j],
+                                                  theta[j], t_dec[j], p[i]);
+}
+
 /* ---------------------------------------------------------------- stats */
 
 static int cmp_double(const void *x, const void *y) {
