@@ -767,7 +767,9 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
  * rho^k is the product of k factors rho taken left to right.  Each operation is one
  * binary64 round-to-nearest-even operation in the order written.  Parameters outside
  * the model (k < 1, alpha < 0, alpha >= mu, rho >= 1, theta <= 0, t_dec < 0, negative
- * variation coefficients, non-finite values) and p < 1 give NaN.
+ * variation coefficients, non-finite values) and p < 1 give NaN, and so does
+ * k > 65536 (a concurrency cap far beyond any serving engine's, which bounds the work
+ * of the product).
  */
 static double pow_left(double r, int32_t k) {
   double x = r;
@@ -776,7 +778,8 @@ static double pow_left(double r, int32_t k) {
 }
 
 double orc_lps_wait(double alpha, double mu, int32_t k, int32_t mode, double ca2, double cs2) {
-  if (!(isfinite(alpha) && isfinite(mu) && alpha >= 0.0 && alpha < mu && k >= 1)) return NAN;
+  if (!(isfinite(alpha) && isfinite(mu) && alpha >= 0.0 && alpha < mu && k >= 1 && k <= 65536))
+    return NAN;
   if (mode == 0) {
     const double rho = alpha / mu;
     return pow_left(rho, k) / (mu - alpha);

@@ -57,7 +57,8 @@ def test_limits_and_monotonicity():
     assert all(a > b for a, b in zip(ws, ws[1:]))     # geometric decay in k
     ws = [O.lps_wait(a, 1.0, 4) for a in np.linspace(0.05, 0.95, 30)]
     assert all(a < b for a, b in zip(ws, ws[1:]))     # grows with the load
-    for bad in [(1.0, 1.0, 2), (1.5, 1.0, 2), (-0.1, 1.0, 2), (0.5, 1.0, 0),
+    assert O.lps_wait(0.5, 1.0, 65536) == 0.0
+    for bad in [(1.0, 1.0, 2), (1.5, 1.0, 2), (-0.1, 1.0, 2), (0.5, 1.0, 0), (0.5, 1.0, 65537),
                 (np.nan, 1.0, 2), (0.5, np.inf, 2)]:
         assert np.isnan(O.lps_wait(*bad)), bad
     assert np.isnan(O.lps_wait(0.5, 1.0, 2, O.LPS_VARIABILITY, -1.0, 1.0))
