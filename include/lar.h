@@ -468,6 +468,44 @@ lar_status lar_whatif_noalloc(const lar_whatif_config *cfg, const lar_instance_p
                               double *utility, int32_t *status);
 const char *lar_noalloc_error_string(void);
 
+/*
+ * Average-case TTFT estimate for routing without real-time workload information
+ * (Sec. 4.2, Eqs. 10 and 11; the appendix on the limited-processor-sharing
+ * abstraction, Eqs. 12 and 13).  Instance j of scenario z is a server of aggregate
+ * capacity mu (service_rate) shared equally by at most k active queries, the others
+ * waiting in FCFS order, with queries arriving at rate alpha (arrival_rate):
+ *   LAR_LPS_POISSON (Poisson arrivals, memoryless work; Eqs. 10, 12):
+ *       rho = alpha / mu,  W = rho^k / (mu - alpha);
+ *   LAR_LPS_VARIABILITY (Eq. 13, squared coefficients of variation ca2 of the
+ *   inter-arrival times and cs2 of the work):
+ *       E[Q] = 1 / mu,  rho = alpha * E[Q],  W = ((ca2 + cs2) / 2) * ((rho^k * E[Q]) / (1 - rho));
+ *   and for query q of p = q_prefill[q] prompt tokens (Eq. 11):
+ *       ttft_ms[z][q][j] = (W + p / prefill_rate) + decode_ms.
+ * rho^k is the product of k factors taken left to right; every operation is one
+ * binary64 round-to-nearest-even operation in the order written.  Rates are per ms,
+ * times in ms.  The model needs 0 <= alpha < mu, 1 <= k <= 65536, prefill_rate > 0,
+ * decode_ms >= 0 (and ca2, cs2 >= 0, rho < 1 under LAR_LPS_VARIABILITY), all finite,
+ * reserved == 0, and p >= 1: otherwise NaN there and the sticky LAR_E_ARG.  Needs no
+ * loaded snapshot (route the result with lar_route / lar_route_constrained, which
+ * take the instances' columns from lar_load_state: an empty snapshot will do).
+ *   params    dev [Z][I]
+ *   q_prefill dev [Q];  ttft_ms dev [Z][Q][I]
+ */
+typedef struct {
+  double arrival_rate;   /* alpha, queries per ms                               */
+  double service_rate;   /* mu, queries per ms at full load                      */
+  double prefill_rate;   /* theta, prompt tokens per ms                           */
+  double decode_ms;      /* mean time of a decode token batch, ms                 */
+  double ca2, cs2;       /* squared coefficients of variation (Eq. 13 only)       */
+  int32_t k;             /* queries served at once                                */
+  int32_t reserved;      /* must be 0                                             */
+} lar_lps_params;
+
+enum { LAR_LPS_POISSON = 0, LAR_LPS_VARIABILITY = 1 };
+
+lar_status lar_estimate_lps(lar_ctx *ctx, const lar_lps_params *params, int32_t mode,
+                            int32_t n_q, const int32_t *q_prefill, double *ttft_ms);
+
 /* Synchronise the stream; return the sticky device error, if any. */
 lar_status lar_sync(lar_ctx *ctx);
 

@@ -16,6 +16,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "liblar.so")
 SOURCES = [os.path.join(CSRC, "sfs_kernels.hip"), os.path.join(CSRC, "sfs_limits.hip"),
+           os.path.join(CSRC, "sfs_lps.hip"),
            os.path.join(CSRC, "lar_api.cpp"), os.path.join(CSRC, "lar_noalloc.hip"),
            os.path.join(CSRC, "lar_board.cpp")]
 HEADERS = [os.path.join(CSRC, "sfs_device.h"), os.path.join(CSRC, "sfs_launch.h"),

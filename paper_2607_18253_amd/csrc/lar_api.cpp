@@ -33,6 +33,7 @@ struct lar_ctx {
   uint64_t* xslot = nullptr;   // [Z][2][kMaxCluster][4] candidate posts of the clustered trace
   lar::SyncCtl sync{1000000000ull, -1, -1};   // 10 s wait bound; no post left out
   unsigned long long* work = nullptr;          // [Z] estimate batches of the last trace
+  double* lps_wait = nullptr;                  // [Z][I] LPS queueing delays (lar_estimate_lps)
   int32_t tag_next = 0;        // ring tag of the next query tracked for its realised TTFT
   int32_t tag_start = 0;       // tag_next after a (re)load
   lar::DevState snap{};        // one scenario's copy of the last loaded snapshot
@@ -207,6 +208,9 @@ lar_status lar_create(lar_ctx** out, const lar_config* cfg) {
   chk(dev_alloc(ctx, &ctx->xslot, (size_t)ctx->Z * 2 * lar::kMaxCluster * 4));
   chk(dev_alloc(ctx, &ctx->work, (size_t)ctx->Z));
   chk(dev_alloc(ctx, &ctx->plim, 4 * (size_t)ctx->I));
+  chk(dev_alloc(ctx, &ctx->lps_wait, ZI));
+  if (st == LAR_OK && hipMemset(ctx->err, 0, sizeof(int32_t)) != hipSuccess)
+    st = fail(ctx, LAR_E_HIP, "hipMemset of the error word failed");
   if (st == LAR_OK && hipMemset(ctx->work, 0, sizeof(unsigned long long) * ctx->Z) != hipSuccess)
     st = fail(ctx, LAR_E_HIP, "hipMemset of the work counters failed");
   if (st != LAR_OK) {
@@ -699,6 +703,21 @@ lar_status lar_ontime_utility(lar_ctx* ctx, int32_t n_q, const int32_t* choice,
   return LAR_OK;
 }
 
+lar_status lar_estimate_lps(lar_ctx* ctx, const lar_lps_params* params, int32_t mode,
+                            int32_t n_q, const int32_t* q_prefill, double* ttft_ms) {
+  if (!ctx) return LAR_E_ARG;
+  if (ctx->sticky != LAR_OK) return ctx->sticky;
+  if (n_q < 0) return fail(ctx, LAR_E_ARG, "n_q < 0");
+  if (mode != LAR_LPS_POISSON && mode != LAR_LPS_VARIABILITY)
+    return fail(ctx, LAR_E_ARG, "unknown LPS mode %d", mode);
+  if (n_q == 0) return LAR_OK;
+  if (!params || !q_prefill || !ttft_ms) return fail(ctx, LAR_E_ARG, "null argument");
+  if ((int64_t)ctx->Z * n_q * ((ctx->I + 255) / 256) > 0x7fffffff)
+    return fail(ctx, LAR_E_ARG, "output too large");
+  HIP_TRY(ctx, lar::launch_lps(env_of(ctx), params, mode, ctx->lps_wait, n_q, q_prefill, ttft_ms));
+  return LAR_OK;
+}
+
 lar_status lar_trace_work(lar_ctx* ctx, int64_t* estimate_batches) {
   if (!ctx || !estimate_batches) return LAR_E_ARG;
   HIP_TRY(ctx, hipStreamSynchronize(ctx->stream));
@@ -710,7 +729,7 @@ lar_status lar_trace_work(lar_ctx* ctx, int64_t* estimate_batches) {
 lar_status lar_sync(lar_ctx* ctx) {
   if (!ctx) return LAR_E_ARG;
   HIP_TRY(ctx, hipStreamSynchronize(ctx->stream));
-  if (ctx->loaded && ctx->sticky == LAR_OK) {
+  if (ctx->sticky == LAR_OK) {
     int32_t e = 0;
     HIP_TRY(ctx, hipMemcpy(&e, ctx->err, sizeof e, hipMemcpyDeviceToHost));
     if (e != 0) {

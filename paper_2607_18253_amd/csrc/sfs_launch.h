@@ -6,6 +6,7 @@
 
 #include <tuple>
 
+#include "../../include/lar.h"
 #include "sfs_device.h"
 #include "sfs_limits.h"
 
@@ -83,6 +84,8 @@ hipError_t launch_lim_commit(const LaunchEnv& env, const int32_t* choice, int64_
                              const double* t_ptr, double t_val);
 hipError_t launch_lim_trace(const LaunchEnv& env, const TraceArgs& a);
 hipError_t launch_untag(const LaunchEnv& env);
+hipError_t launch_lps(const LaunchEnv& env, const lar_lps_params* prm, int mode, double* wait,
+                      int Q, const int32_t* q_prefill, double* ttft);
 hipError_t launch_stats(const LaunchEnv& env, int N, const int32_t* choice,
                         const double* chosen_ttft, const double* acc, const double* cost,
                         int n_cols, const double* w_cost, double* out);

@@ -24,7 +24,8 @@ EXPORTED = ("lar_create", "lar_destroy", "lar_error_string", "lar_load_state", "
             "lar_stats", "lar_set_scheduler",
             "lar_ontime_utility", "lar_read_state", "lar_sync", "lar_trace_work", "lar_board_create",
             "lar_board_destroy", "lar_board_publish", "lar_board_collect",
-            "lar_whatif_noalloc", "lar_noalloc_error_string")
+            "lar_whatif_noalloc", "lar_noalloc_error_string", "lar_estimate_lps")
+LPS_POISSON, LPS_VARIABILITY = 0, 1
 
 
 class LarError(RuntimeError):
@@ -48,6 +49,17 @@ class WhatifConfig(C.Structure):
     _fields_ = [("n_inst", C.c_int32), ("max_seqs_cap", C.c_int32), ("max_resident", C.c_int32),
                 ("max_prompt", C.c_int32), ("n_cols", C.c_int32), ("flags", C.c_int32),
                 ("max_iters", C.c_int64), ("stream", C.c_void_p)]
+
+
+class LpsParams(C.Structure):
+    _fields_ = [("arrival_rate", C.c_double), ("service_rate", C.c_double),
+                ("prefill_rate", C.c_double), ("decode_ms", C.c_double), ("ca2", C.c_double),
+                ("cs2", C.c_double), ("k", C.c_int32), ("reserved", C.c_int32)]
+
+
+LPS_DTYPE = np.dtype([("arrival_rate", "<f8"), ("service_rate", "<f8"), ("prefill_rate", "<f8"),
+                      ("decode_ms", "<f8"), ("ca2", "<f8"), ("cs2", "<f8"), ("k", "<i4"),
+                      ("reserved", "<i4")])
 
 
 class InstanceParams(C.Structure):
@@ -117,6 +129,8 @@ def load_library(path: str = LIB_PATH):
     L.lar_read_state.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, i64, C.POINTER(i64)]
     L.lar_sync.restype = i32
     L.lar_sync.argtypes = [vp]
+    L.lar_estimate_lps.restype = i32
+    L.lar_estimate_lps.argtypes = [vp, vp, i32, i32, vp, vp]
     L.lar_whatif_noalloc.restype = i32
     L.lar_whatif_noalloc.argtypes = [C.POINTER(WhatifConfig), vp, vp, vp, vp, vp, vp, i32, vp, dbl,
                                      vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -244,6 +258,23 @@ class LarContext:
             self._h, Q, _dev(q_prefill, torch.int32, "q_prefill"), float(t_ms),
             _dev(ttft, torch.float64, "ttft", n), _dev(iters, torch.int32, "iters", n)))
         return ttft, iters
+
+    def estimate_lps(self, params, q_prefill, mode=LPS_POISSON, ttft=None):
+        """Average-case LPS TTFT (lar_estimate_lps): params is a GPU uint8 tensor of
+        Z*I lar_lps_params records (see lps_params_array), scenario-major; returns
+        ttft [Z][Q][I]."""
+        torch = self._torch
+        Q = int(q_prefill.numel())
+        if params.dtype != torch.uint8 or params.numel() != self.Z * self.I * LPS_DTYPE.itemsize:
+            raise ValueError("params must hold Z*I lar_lps_params records")
+        if ttft is None:
+            ttft = torch.empty((self.Z, Q, self.I), dtype=torch.float64,
+                               device=q_prefill.device)
+        self._check(self._L.lar_estimate_lps(
+            self._h, _dev(params, torch.uint8, "params"), int(mode), Q,
+            _dev(q_prefill, torch.int32, "q_prefill"),
+            _dev(ttft, torch.float64, "ttft", self.Z * Q * self.I)))
+        return ttft
 
     def route(self, ttft, acc, cost, w_cost, w_lat, choice=None, chosen_ttft=None,
               utility=None):
@@ -538,3 +569,16 @@ def whatif_noalloc(params, offsets, rem_prefill, rem_decode, context, clock_ms, 
         _dev(status, torch.int32, "status", 1))
     if st != LAR_OK:
         raise LarError(st, L.lar_noalloc_error_string().decode())
+
+
+def lps_params_array(arrival_rate, service_rate, prefill_rate, decode_ms, k, ca2=None, cs2=None):
+    """LPS parameters as a numpy array of lar_lps_params records (rates per ms, times
+    in ms); copy its bytes to the GPU for LarContext.estimate_lps."""
+    n = len(arrival_rate)
+    rec = np.zeros(n, dtype=LPS_DTYPE)
+    rec["arrival_rate"], rec["service_rate"] = arrival_rate, service_rate
+    rec["prefill_rate"], rec["decode_ms"], rec["k"] = prefill_rate, decode_ms, k
+    rec["ca2"] = 1.0 if ca2 is None else ca2
+    rec["cs2"] = 1.0 if cs2 is None else cs2
+    assert rec.dtype.itemsize == C.sizeof(LpsParams)
+    return rec

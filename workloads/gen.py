@@ -349,3 +349,29 @@ def make_tiny_sched_workload(seed: int, **kw) -> Workload:
     wl.sched = sched
     wl.name = f"tinysched{seed}"
     return wl
+
+
+def lps_params(wl: Workload, seed: int = 0) -> dict:
+    """Per-instance parameters of the average-case LPS estimator (Sec. 4.2), derived
+    from each instance's batch-time model and drawn from a stream of their own (rates
+    per ms, times in ms):
+      prefill throughput theta = B / (a + b B), a batch that is all prefill;
+      mean decode batch time  t_dec = a + c M/2, half the sequence cap decoding;
+      capacity mu = M / ((a + c M) * mean decode length), queries per ms completed
+        by full decode batches;
+      load rho ~ U(0.05, 0.98), arrival rate alpha = rho * mu;
+      parallelism k ~ U{1..64} (the paper observes about 25 on its engine);
+      squared coefficients of variation ca2 ~ U(0.5, 2), cs2 ~ U(0.5, 3)."""
+    rng = np.random.default_rng([seed, 0x1F5])
+    I = wl.n_inst
+    a, b, c = (np.asarray(x, np.float64) for x in (wl.a, wl.b, wl.c))
+    B = np.asarray(wl.budget, np.float64)
+    M = np.asarray(wl.max_seqs, np.float64)
+    dbar = float(wl.meta.get("decode_mean", 256))
+    theta = B / (a + b * B)
+    t_dec = a + c * (M / 2.0)
+    mu = M / ((a + c * M) * dbar)
+    rho = rng.uniform(0.05, 0.98, I)
+    return dict(alpha=rho * mu, mu=mu, k=rng.integers(1, 65, I).astype(np.int32),
+                ca2=rng.uniform(0.5, 2.0, I), cs2=rng.uniform(0.5, 3.0, I), theta=theta,
+                t_dec=t_dec)
