@@ -51,8 +51,8 @@ GOLDEN = os.path.join(ROOT, "tests", "golden")
 METRIC = "TTFT estimates/sec (query x instance) and routed queries/sec on 1 MI355X"
 HBM_PEAK_GBS = 8000.0
 VALU_PEAK_GINSTR = 256 * 4 * 2.4 / 4        # G wave64 VALU instructions per second
-SUITE = ("c1", "c2", "c3", "c4")            # sub-records of the default run
-SUB_STEPS = {"c1": 20, "c2": 5, "c3": 20, "c4": 5, "c5": 5, "c6": 5, "c7": 3}
+SUITE = ("c1", "c2", "c3", "c3_lps", "c4")  # sub-records of the default run
+SUB_STEPS = {"c1": 20, "c2": 5, "c3": 20, "c3_lps": 20, "c4": 5, "c5": 5, "c6": 5, "c7": 3}
 
 # Algorithmic work per query step, per scenario (the shared-trajectory method):
 #  bytes: every instance's running slots (M requests x 12 B: remaining prefill,
@@ -71,8 +71,9 @@ def _parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default=None,
-                    choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7"],
-                    help="one workload alone (default: c5 with sub-records c1-c4)")
+                    choices=["c1", "c2", "c3", "c3_lps", "c4", "c5", "c6", "c7"],
+                    help="one workload alone (default: c5 with sub-records c1-c4); c3_lps "
+                         "is c3's what-if with the average-case LPS estimator (Sec. 4.2)")
     ap.add_argument("--n-q", type=int, default=None, help="shorten the trace (testing only)")
     ap.add_argument("--objective", default="lagrangian", choices=["lagrangian", "constrained"],
                     help="route by the Lagrangian objective or by Eq. 3 with the paper's "
@@ -101,6 +102,7 @@ COPY_PROBE_BYTES = 256 << 20
 _CSRC = "paper_2607_18253_amd/csrc/"
 KERNEL_SOURCES = tuple(_CSRC + f for f in ("sfs_kernels.hip", "sfs_device.h", "sfs_route.h",
                                            "sfs_launch.h"))
+LPS_KERNEL_SOURCES = tuple(_CSRC + f for f in ("sfs_lps.hip", "sfs_kernels.hip", "sfs_route.h"))
 LIMIT_KERNEL_SOURCES = tuple(_CSRC + f for f in ("sfs_limits.hip", "sfs_limits.h", "sfs_device.h",
                                                  "sfs_route.h", "sfs_launch.h"))
 
@@ -109,7 +111,8 @@ def kernel_source_hash(workload=None):
     """Hash of the sources of the workload's kernels (a counter record is reported
     only while they are unchanged)."""
     h = hashlib.sha256()
-    for f in (LIMIT_KERNEL_SOURCES if workload == "c7" else KERNEL_SOURCES):
+    srcs = {"c7": LIMIT_KERNEL_SOURCES, "c3_lps": LPS_KERNEL_SOURCES}.get(workload, KERNEL_SOURCES)
+    for f in srcs:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -119,6 +122,8 @@ def dominant_kernels(workload):
     """Kernel-name fragments of the timed region's dominant kernel(s)."""
     if workload == "c3":
         return ("k_traj", "k_est", "k_route")
+    if workload == "c3_lps":
+        return ("k_lps_wait", "k_lps_est", "k_route")
     return ("k_ltrace",) if workload == "c7" else ("k_trace_cl",)
 
 
@@ -201,6 +206,11 @@ def algorithmic_work(name, wl):
     """(bytes, wave64 VALU instructions) the method must move / issue per step."""
     Z, I, N = wl.n_scen, wl.n_inst, wl.n_q
     M = int(np.max(wl.max_seqs))
+    if name == "c3_lps":
+        # parameters per instance (56 B), prompts, acc + cost, TTFT written and read back
+        # by the route; the wait per instance and one division, two adds per pair
+        nbytes = I * 56 + N * 4 + 2 * N * wl.n_cols * 8 + 2 * N * I * 8
+        return nbytes, N * I / 64 * 20
     if name == "c3":
         R = int(np.max(np.diff(wl.offsets)))
         nbytes = I * R * 12 + 2 * N * wl.n_cols * 8 + N * I * 8   # state, acc + cost, TTFT
@@ -275,6 +285,21 @@ def cpu_baselines(name, wl, budget_s, threads, tau=None):
     the workload.  Returns (record, single-thread trace result or what-if pairs)."""
     from oracle import oracle as orc
     model, _ = host_cpu()
+    if name == "c3_lps":
+        from workloads.gen import lps_params
+        prm = lps_params(wl)
+        rows = np.random.default_rng(1).permutation(wl.n_q)
+        n1, dt1, _ = _grow(lambda k: orc.lps_matrix(prm, wl.q_prefill[rows[:k]]), budget_s,
+                           wl.n_q, n0=8)
+        n, dt, _ = _grow(lambda k: orc.lps_matrix(prm, wl.q_prefill[rows[:k]], n_threads=threads),
+                         budget_s, wl.n_q, n0=8)
+        one = {"value": n1 * wl.n_inst / dt1, "cores": 1,
+               "sample": f"{n1} random whole rows (x {wl.n_inst} instances) ({dt1:.2f} s)"}
+        allc = {"value": n * wl.n_inst / dt, "cores": threads,
+                "sample": f"{n} random whole rows (x {wl.n_inst} instances), rows split over "
+                          f"{threads} threads ({dt:.2f} s)"}
+        return _baseline(allc, one, model, threads), orc.lps_matrix(prm, wl.q_prefill,
+                                                                    n_threads=threads)
     if name == "c3":
         rng = np.random.default_rng(1)
         qs, pairs = {}, []
@@ -388,6 +413,11 @@ def golden_parity(name, wl, ctx, out):
 
 
 def sample_parity(name, out, sample):
+    if name == "c3_lps":   # the whole matrix, computed by the oracle
+        got, want = out["ttft"][0], sample
+        return {"compared": f"every TTFT bit of the {got.shape[0]} x {got.shape[1]} LPS matrix",
+                "n": int(got.size),
+                "ttft_bits_equal": bool(np.array_equal(got.view(np.int64), want.view(np.int64)))}
     if name == "c3":
         tt = out["ttft"][0]
         got = np.array([tt[i, j] for i, j, _ in sample])
@@ -416,7 +446,8 @@ def run_workload(name, args, steps, warmup, want_cpu):
     from workloads import make_workload
 
     dev = torch.device("cuda:0")
-    wl = make_workload(name, n_q=args.n_q)
+    lps = name == "c3_lps"
+    wl = make_workload("c3" if lps else name, n_q=args.n_q)
     Z, I, N = wl.n_scen, wl.n_inst, wl.n_q
 
     def T(a, dt):
@@ -431,7 +462,15 @@ def run_workload(name, args, steps, warmup, want_cpu):
     stats = torch.empty((Z, 5), dtype=torch.float64, device=dev)
     ctx = context_for(wl)
     stream = ctx.stream
-    whatif = name == "c3"
+    whatif = name in ("c3", "c3_lps")
+    if lps:
+        from paper_2607_18253_amd import lar as L
+        from workloads.gen import lps_params
+        prm = lps_params(wl)
+        lps_dev = torch.as_tensor(L.lps_params_array(prm["alpha"], prm["mu"], prm["theta"],
+                                                     prm["t_dec"], prm["k"], prm["ca2"],
+                                                     prm["cs2"]).view(np.uint8).copy(),
+                                  device=dev)
     constrained = args.objective == "constrained" and not whatif
     t_first, t_last = float(wl.q_t_ms[0]), float(wl.q_t_ms[-1])
     tau = None
@@ -451,7 +490,10 @@ def run_workload(name, args, steps, warmup, want_cpu):
         if whatif:
             if record:
                 e0.record(stream)
-            ctx.estimate(qp, 0.0, ttft=ttft, want_iters=False)
+            if lps:
+                ctx.estimate_lps(lps_dev, qp, L.LPS_POISSON, ttft=ttft)
+            else:
+                ctx.estimate(qp, 0.0, ttft=ttft, want_iters=False)
             ctx.route(ttft, acc, cost, wc, wlat, choice=choice, chosen_ttft=chosen, utility=util)
             if record:
                 e1.record(stream)
@@ -499,13 +541,16 @@ def run_workload(name, args, steps, warmup, want_cpu):
     rec = {
         "metric": METRIC, "value": Z * N * I / (ms_per_step / 1000.0), "unit": "TTFT estimates/s",
         "steps": steps, "warmup": warmup, "ms_per_step": ms_per_step,
-        "config": {"workload": f"{name}: {wl.meta['title']}", "scenarios": Z, "instances": I,
+        "config": {"workload": (f"{name}: {wl.meta['title']} with the average-case LPS "
+                                "estimator (Sec. 4.2)") if lps else f"{name}: {wl.meta['title']}",
+                   "scenarios": Z, "instances": I,
                    "queries": N, "resident_per_instance": wl.meta["resident"],
                    "token_budget": int(wl.budget[0]), "max_seqs": int(wl.max_seqs[0]),
                    "objective": "eq3-constrained" if constrained else
                    ("what-if" if whatif else "lagrangian")},
         "routed_queries_per_s": Z * N / (ms_per_step / 1000.0),
-        "kernel": ("k_traj + k_est + k_route (lar_estimate_ttft + lar_route)" if whatif else
+        "kernel": ("k_lps_wait + k_lps_est + k_route (lar_estimate_lps + lar_route)" if lps else
+                   "k_traj + k_est + k_route (lar_estimate_ttft + lar_route)" if whatif else
                    ("k_ltrace (lar_route_trace under scheduler limits)" if wl.sched is not None
                     else "k_trace_cl (lar_route_trace, one launch per step)")),
         "kernel_ms": kernel_ms,

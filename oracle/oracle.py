@@ -437,13 +437,28 @@ def lps_ttft(alpha, mu, k, theta, t_dec, p, mode=LPS_POISSON, ca2=1.0, cs2=1.0):
                                     float(cs2), float(theta), float(t_dec), int(p)))
 
 
-def lps_matrix(prm, p, mode=LPS_POISSON):
+def lps_matrix(prm, p, mode=LPS_POISSON, n_threads=1):
     """LPS TTFT of every query (prompts p) at every instance; prm holds per-instance
-    arrays alpha, mu, k, ca2, cs2, theta, t_dec.  Returns [Q][I]."""
+    arrays alpha, mu, k, ca2, cs2, theta, t_dec.  Returns [Q][I].  With n_threads > 1
+    the rows are split into chunks computed on threads of their own (each row is
+    independent; the same code runs per chunk)."""
     f = lambda k: np.ascontiguousarray(prm[k], np.float64)  # noqa: E731
     I = len(prm["alpha"])
     p = _i32(p)
     out = np.zeros((len(p), I))
-    lib().orc_lps_matrix(I, f("alpha"), f("mu"), _i32(prm["k"]), f("ca2"), f("cs2"),
-                         f("theta"), f("t_dec"), int(mode), len(p), p, out)
+    args = (f("alpha"), f("mu"), _i32(prm["k"]), f("ca2"), f("cs2"), f("theta"), f("t_dec"))
+
+    def rows(lo, hi):
+        if hi > lo:
+            blk = np.zeros((hi - lo, I))
+            lib().orc_lps_matrix(I, *args, int(mode), hi - lo, np.ascontiguousarray(p[lo:hi]),
+                                 blk)
+            out[lo:hi] = blk
+
+    if n_threads <= 1:
+        rows(0, len(p))
+    else:
+        cuts = np.linspace(0, len(p), n_threads + 1).astype(int)
+        with ThreadPoolExecutor(max_workers=n_threads) as ex:
+            list(ex.map(lambda t: rows(cuts[t], cuts[t + 1]), range(n_threads)))
     return out
