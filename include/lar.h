@@ -136,8 +136,11 @@ lar_status lar_load_state(lar_ctx *ctx, const lar_instance_params *params,
  *   chunk_cap   a request receives at most this many prefill tokens per batch;
  *   max_ctx     context limit: a request's context (prompt + generated tokens) never
  *               exceeds it.  A request entering with cx + rp tokens has its predicted
- *               decode cut to max_ctx - (cx + rp); cx + rp < max_ctx is required (a
- *               query with prompt >= max_ctx is an error);
+ *               decode cut to max_ctx - (cx + rp); cx + rp < max_ctx is required.  An
+ *               instance cannot take a query whose prompt is >= its max_ctx: its
+ *               estimate is +infinity and the routes never choose it (a pool may mix
+ *               small and large limits); a query that no instance can take is routed
+ *               nowhere (choice -1) with the sticky LAR_E_ARG;
  *   kv_blocks   KV cache of kv_blocks blocks of block_size tokens (block_size a power
  *               of two, 1 .. 65536): a running request holds ceil(cx / block_size)
  *               blocks.  Requires max_ctx > 0 and kv_blocks * block_size >= max_ctx.
@@ -183,8 +186,8 @@ lar_status lar_reload_state(lar_ctx *ctx);
  * tokens, 1..max_prompt) arriving at time t_ms at every instance of every
  * scenario.  Pure: the state is not modified.  Every instance clock must be
  * >= t_ms (advance with lar_commit first), else the sticky LAR_E_STATE is set.
- * Under scheduler limits a prompt must also be below the instance's context limit
- * (else NaN there and the sticky LAR_E_ARG).
+ * Under scheduler limits an instance whose context limit is at or below the prompt
+ * cannot take the query: +infinity there (iters 0), no error.
  *   q_prefill dev [Q]
  *   ttft_ms   dev [Z][Q][I]  float64, TTFT = (clock + T_1 + ... + T_l) - t_ms
  *   iters     dev [Z][Q][I]  int32, l = number of batches simulated; may be NULL
@@ -203,7 +206,9 @@ lar_status lar_estimate_ttft(lar_ctx *ctx, int32_t n_q, const int32_t *q_prefill
  *   choice      dev [Z][Q] int32
  *   chosen_ttft dev [Z][Q] TTFT at the choice; may be NULL
  *   utility     dev [Z][Q] acc - w_cost*cost at the choice (Eq. 2); may be NULL
- * NaN utilities are not supported.
+ * An instance whose TTFT is +infinity (it cannot take the query) is no candidate, and
+ * neither is a NaN utility; a row without any candidate gets choice -1 and sets the
+ * sticky LAR_E_ARG.
  */
 lar_status lar_route(lar_ctx *ctx, int32_t n_q, const double *ttft_ms, const double *acc,
                      const double *cost, int32_t n_cols, const double *w_cost,
@@ -219,7 +224,8 @@ lar_status lar_route(lar_ctx *ctx, int32_t n_q, const double *ttft_ms, const dou
  *   acc, cost dev [Q][n_cols];  w_cost dev [Z] (lambda of Eq. 2)
  *   choice dev [Z][Q];  chosen_ttft, utility dev [Z][Q] as in lar_route (may be NULL)
  * Errors: LAR_E_ARG for a null required pointer or n_cols not covering every
- * instance's column.  NaN TTFTs are not supported.
+ * instance's column.  An instance whose TTFT is +infinity is no candidate in either
+ * branch; a row without any candidate gets choice -1 and sets the sticky LAR_E_ARG.
  */
 lar_status lar_route_constrained(lar_ctx *ctx, int32_t n_q, const double *ttft_ms,
                                  const double *tau_ms, const double *acc, const double *cost,

@@ -42,7 +42,10 @@
  *
  *   * Route (Eq. for the Lagrangian routing objective with the utility of Eq. 2):
  *       u_j = (acc_j - w_cost*cost_j) - w_lat*TTFT_j,
- *     choice = the lowest j attaining the maximum.
+ *     choice = the lowest j attaining the maximum.  Under scheduler limits an
+ *     instance whose context limit cannot hold the query's prompt cannot serve it:
+ *     its estimate is +infinity and it is no candidate; a query no instance can
+ *     take is an error.
  *
  *   * Commit / advance (replay of the instances between snapshots, App. E on
  *     workload snapshots): append the routed query as a waiting request of the
@@ -517,8 +520,13 @@ int orc_queue_append(orc_queue *q, int32_t p, int32_t dhat, int64_t queue_cap) {
    already be advanced to t).  Pure: the queue is not modified. */
 int orc_queue_estimate(const orc_queue *q, int32_t p, int32_t dhat, double t, int32_t reading,
                        int64_t max_iters, double *ttft, int32_t *iters) {
-  if (p < 1 || decode_of(q, p, dhat) < 1) return ORC_E_ARG;
+  if (p < 1) return ORC_E_ARG;
   if (q->clock < t) return ORC_E_STATE;
+  if (decode_of(q, p, dhat) < 1) {   /* the context limit cannot hold the prompt */
+    *ttft = INFINITY;
+    *iters = 0;
+    return ORC_OK;
+  }
   orc_queue *w = q_clone(q);
   if (!w) return ORC_E_ARG;
   w->rp[w->n] = p;
@@ -555,6 +563,7 @@ int32_t orc_route_row(int32_t n_inst, const double *ttft, const double *acc_row,
   int32_t best = -1;
   double bu = 0.0;
   for (int32_t j = 0; j < n_inst; ++j) {
+    if (ttft[j] == INFINITY) continue;   /* the instance cannot take the query */
     double pen = w_cost * cost_row[col[j]];
     double u = acc_row[col[j]] - pen;
     double lat = w_lat * ttft[j];
@@ -580,8 +589,10 @@ int32_t orc_route_row_constrained(int32_t n_inst, const double *ttft, double tau
   }
   if (best >= 0) return best;
   double bt = 0.0;
-  for (int32_t j = 0; j < n_inst; ++j)
+  for (int32_t j = 0; j < n_inst; ++j) {
+    if (ttft[j] == INFINITY) continue;   /* the instance cannot take the query */
     if (best < 0 || ttft[j] < bt) { best = j; bt = ttft[j]; }
+  }
   return best;
 }
 
@@ -705,6 +716,11 @@ int orc_trace(int32_t n_inst, const orc_params *params, const int32_t *col,
     int32_t m = tau ? orc_route_row_constrained(n_inst, row, tau[i], arow, crow, col, w_cost)
                     : orc_route_row(n_inst, row, arow, crow, col, w_cost, w_lat, NULL);
     choice[i] = m;
+    if (m < 0) {   /* no instance's context limit holds the prompt */
+      st = ORC_E_ARG;
+      *failed_query = i;
+      break;
+    }
     if (ttft_chosen) ttft_chosen[i] = row[m];
     if (util_chosen) {
       double pen = w_cost * crow[col[m]];

@@ -184,7 +184,7 @@ __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double
                                               const double* w_cost, const double* w_lat,
                                               const double* tau, int32_t* choice,
                                               double* chosen_ttft, double* utility,
-                                              int64_t out_zstride, int out_q0) {
+                                              int64_t out_zstride, int out_q0, int32_t* err) {
   __shared__ double s_u[256 / kWave];
   __shared__ int s_j[256 / kWave];
   const int row = blockIdx.x;   // z * Q + q
@@ -219,6 +219,7 @@ __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double
       if (better(s_u[w], s_j[w], bu, bj)) { bu = s_u[w]; bj = s_j[w]; }
     const int64_t o = (int64_t)z * out_zstride + out_q0 + q;
     bj = bj >= 0 ? key_index(bj) : -1;
+    if (bj < 0) set_error(err, kErrArg);   // no instance can take the query
     choice[o] = bj;
     if (bj >= 0) {
       if (chosen_ttft) chosen_ttft[o] = trow[bj];
@@ -487,6 +488,7 @@ __global__ __launch_bounds__(NW * kWave) void k_trace_mem(LAR_TRACE_PARAMS) {
     }
     const int m = trace_pick<NW>(bu, bj, bt, bq, i, z, N, choice, chosen_ttft, utility, s_u,
                                  s_t, s_q, s_j);
+    if (m < 0 && threadIdx.x == 0) set_error(err, kErrArg);   // no candidate
     for (int j = wid; j < I; j += nw) {
       const QEnv e = make_env(S, pr, z * I + j, j, stage[wid]);
       Queue<KS> w;
@@ -1042,6 +1044,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
         if (bj == -2) break;
       }
       m = bj >= 0 ? key_index(bj) : -1;
+      if (m < 0 && cid == 0 && threadIdx.x == 0) set_error(err, kErrArg);   // no candidate
       // the wave holding the winner (its own best) writes the outputs
       const bool mine = m >= 0 ? c.j == bj : (cid == 0 && wid == 0);
       if (mine && ln == 0) {
@@ -1503,7 +1506,7 @@ hipError_t launch_route(const LaunchEnv& env, int Q, const double* ttft, int64_t
                         double* chosen_ttft, double* utility, int64_t out_zstride, int out_q0) {
   hipLaunchKernelGGL(k_route, dim3(env.Z * Q), dim3(256), 0, env.stream, env.Z, Q, env.I, ttft,
                      ttft_zstride, acc, cost, n_cols, env.P.col, w_cost, w_lat, tau, choice,
-                     chosen_ttft, utility, out_zstride, out_q0);
+                     chosen_ttft, utility, out_zstride, out_q0, env.err);
   return hipGetLastError();
 }
 

@@ -24,8 +24,9 @@ namespace lar {
 
 // SFS estimate under limits: a private copy of the queue with the query appended at
 // the tail, stepped until the query's first decode (reading 1: its prefill
-// completes).  NaN with an error when the state is behind t, the prompt does not fit
-// the context limit or the batch cap is reached.
+// completes).  +infinity when the instance's context limit cannot hold the prompt
+// (it cannot take the query); NaN with an error when the state is behind t or the
+// batch cap is reached.
 template <int KS>
 __device__ __forceinline__ double lim_estimate(const LQueue<KS>& q, const LEnv& e, int p, int d,
                                                double t, int reading, int64_t max_iters,
@@ -36,11 +37,12 @@ __device__ __forceinline__ double lim_estimate(const LQueue<KS>& q, const LEnv& 
     if (ln == 0) set_error(err, kErrState);
     return __builtin_nan("");
   }
-  const int dq = entry_decode(e, p, d);
-  if (p < 1 || dq < 1) {
+  if (p < 1) {
     if (ln == 0) set_error(err, kErrArg);
     return __builtin_nan("");
   }
+  const int dq = entry_decode(e, p, d);
+  if (dq < 1) return __builtin_inf();   // the context limit cannot hold the prompt
   LQueue<KS> w = q;
   w.template append<false>(e, p, dq, false, nullptr, -1);
   double E = w.clock;
@@ -228,6 +230,7 @@ __global__ __launch_bounds__(NW * kWave) void k_ltrace(LAR_TRACE_PARAMS, DevLimi
     }
     const int m = trace_pick<NW>(bu, bj, bt, bq, i, z, N, choice, chosen_ttft, utility, s_u,
                                  s_t, s_q, s_j);
+    if (m < 0 && threadIdx.x == 0) set_error(err, kErrArg);   // no instance can take it
     for (int j = wid; j < I; j += nw) {
       const LEnv e = make_lenv(S, pr, lm, z * I + j, j, lds[wid]);
       int32_t* tags = TRK ? S.r_tag + (int64_t)(z * I + j) * S.rcap : nullptr;
@@ -315,6 +318,7 @@ __global__ __launch_bounds__(W * kWave) void k_ltrace_cl(LAR_TRACE_PARAMS, DevLi
         if (bj == -2) break;
       }
       const int m = bj >= 0 ? key_index(bj) : -1;
+      if (m < 0 && cid == 0 && threadIdx.x == 0) set_error(err, kErrArg);   // no instance can take it
       // the wave holding the winner writes the outputs
       const bool mine = m >= 0 ? c.j == bj : (cid == 0 && wid == 0);
       if (mine && ln == 0) {

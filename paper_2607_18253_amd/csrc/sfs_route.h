@@ -15,14 +15,16 @@ namespace lar {
 // then the lower index.  Under the Lagrangian objective every key is the bare
 // index and the value is the Lagrangian utility; under Eq. 3 the value is the
 // utility of Eq. 2 for a candidate meeting its target and -TTFT otherwise (so the
-// empty feasible set falls back to the least estimated TTFT).  Written without
-// branches so a lane-wise use stays a few selects.
+// empty feasible set falls back to the least estimated TTFT).  An instance whose
+// estimate is +infinity (its context limit cannot hold the prompt) is no candidate,
+// and neither is a NaN value.  Written without branches so a lane-wise use stays a
+// few selects.
 constexpr int kLateBit = 1 << 30;
 __device__ __forceinline__ int key_index(int k) { return k & (kLateBit - 1); }
 
 __device__ __forceinline__ bool better(double u1, int k1, double u2, int k2) {
   const int c1 = k1 >> 30, c2 = k2 >> 30;
-  return (k1 >= 0) &
+  return (k1 >= 0) & (u1 == u1) &   // a NaN value is never a candidate
          ((k2 < 0) | (c1 < c2) | ((c1 == c2) & ((u1 > u2) | ((u1 == u2) & (k1 < k2)))));
 }
 
@@ -31,6 +33,10 @@ __device__ __forceinline__ bool better(double u1, int k1, double u2, int k2) {
 // query's target *tau.
 __device__ __forceinline__ double cand_value(double eq2, double ttft, double wl,
                                              const double* tau, double tq, int j, int* key) {
+  if (ttft == __builtin_inf()) {   // the instance cannot take the query: no candidate
+    *key = -1;
+    return 0.0;
+  }
   if (!tau) {
     *key = j;
     return __dsub_rn(eq2, __dmul_rn(wl, ttft));

@@ -246,31 +246,53 @@ def test_limits_error_paths():
     ctx.advance(float(wl.q_t_ms[0]))
     ctx.sync()
     ctx.close()
-    # the prompt limit of the context and the context limit together: a trace whose
-    # query does not fit one instance's context limit
-    wl2 = make_tiny_sched_workload(8, n_q=6, max_res=4)
-    wl2.sched[:, 3] = np.maximum(wl2.sched[:, 3], 30)
-    wl2.sched[:, 1] = 0
-    wl2.sched[0, 3] = int(max((lambda r: (r[0] + r[2]).max() if len(r[0]) else 0)(
-        wl2.instance_requests(0)), 2)) + 1
-    wl2.q_prefill[:] = np.minimum(wl2.q_prefill, 12)
-    wl2.q_prefill[2] = wl2.sched[0, 3]            # does not fit instance 0
-    wl2.max_prompt = 40
-    ctx = context_for(wl2, max_iters=MAX_ITERS)
-    ctx.advance(float(wl2.q_t_ms[0]))
-    ctx.estimate(T(wl2.q_prefill[2:3], torch.int32), float(wl2.q_t_ms[0]))   # what-if
-    with pytest.raises(LarError) as e:
-        ctx.sync()
-    assert e.value.code == LAR_E_ARG
-    ctx.load_workload(wl2)   # clears the sticky error
-    ctx.advance(float(wl2.q_t_ms[0]))
-    with pytest.raises(LarError) as e:
-        ctx.route_trace(T(wl2.q_prefill, torch.int32), T(wl2.q_decode, torch.int32),
-                        T(wl2.q_t_ms, torch.float64), float(wl2.q_t_ms[-1]),
-                        T(wl2.acc, torch.float64), T(wl2.cost, torch.float64),
-                        T(wl2.w_cost, torch.float64), T(wl2.w_lat_ms, torch.float64))
-        ctx.sync()
-    assert e.value.code == LAR_E_ARG
+
+
+def test_mixed_context_limits():
+    """A pool mixing a small context limit (instance 0, the best choice whenever it
+    can take a query) with larger ones: the what-if estimate is +inf exactly where
+    the limit cannot hold the prompt, the route skips those instances, and the trace
+    (both objectives) is the oracle's; a query that no instance can take is routed
+    nowhere with the sticky LAR_E_ARG, the queries before it as the oracle routes
+    them."""
+    from paper_2607_18253_amd.lar import LAR_E_ARG
+    from test_oracle_sched import _mixed_limit_pool
+    wl = _mixed_limit_pool()
+    ctx = context_for(wl, max_iters=MAX_ITERS)
+    assert (wl.clock_ms == 0.0).all()
+    tt, it = ctx.estimate(T(wl.q_prefill, torch.int32), 0.0)
+    ch = ctx.route(tt, T(wl.acc, torch.float64), T(wl.cost, torch.float64),
+                   T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64))
+    assert ctx.status() == 0
+    tt, it, ch = tt.cpu().numpy()[0], it.cpu().numpy()[0], ch.cpu().numpy()[0]
+    ref = O.estimate_matrix(wl, range(wl.n_q), range(wl.n_inst), 0.0)
+    np.testing.assert_array_equal(bits(tt), bits(ref[0]))
+    np.testing.assert_array_equal(it, ref[1])
+    assert np.isinf(tt[:, 0]).sum() > 5
+    for i in range(wl.n_q):
+        m, _ = O.route_row(ref[0][i], wl.acc[i], wl.cost[i], wl.col, wl.w_cost[0],
+                           wl.w_lat_ms[0])
+        assert ch[i] == m, i
+    ctx.close()
+    tau = O.ttft_targets(wl.q_prefill, wl.tau_u_ms, wl.tau_v)
+    for t in (None, tau):
+        _check(wl, _trace(wl, tau=t), tau=t)
+    # a query at every instance's limit
+    wl.q_prefill[4] = 64
+    ctx = context_for(wl, max_iters=MAX_ITERS)
+    ctx.advance(float(wl.q_t_ms[0]))
+    chosen = torch.full((1, wl.n_q), -1.0, dtype=torch.float64, device=DEV)
+    choice = ctx.route_trace(T(wl.q_prefill, torch.int32), T(wl.q_decode, torch.int32),
+                             T(wl.q_t_ms, torch.float64), float(wl.q_t_ms[-1]),
+                             T(wl.acc, torch.float64), T(wl.cost, torch.float64),
+                             T(wl.w_cost, torch.float64), T(wl.w_lat_ms, torch.float64),
+                             chosen_ttft=chosen)
+    assert ctx.status() == LAR_E_ARG
+    choice, chosen = choice.cpu().numpy(), chosen.cpu().numpy()
+    ref = O.trace(wl, n_q=4)
+    np.testing.assert_array_equal(choice[0, :4], ref.choice)
+    np.testing.assert_array_equal(bits(chosen[0, :4]), bits(ref.ttft_chosen))
+    assert choice[0, 4] == -1
     ctx.close()
 
 

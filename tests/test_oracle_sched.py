@@ -208,8 +208,55 @@ def test_sched_errors():
     with pytest.raises(O.OracleError) as e:
         q.append(6, 1)                                      # no room for a decode
     assert e.value.code == O.E_ARG
+    # an instance whose context limit cannot hold the prompt cannot take the query
+    assert q.estimate(6, 1, 0.0) == (np.inf, 0)
     with pytest.raises(O.OracleError):
-        q.estimate(6, 1, 0.0)
+        q.estimate(0, 1, 0.0)                               # a prompt has a token
+
+
+def _mixed_limit_pool(n_q=40, seed=5):
+    """A pool mixing a small context limit (instance 0, the cheapest and most
+    accurate) with larger ones; prompts that only the larger instances can hold."""
+    wl = make_tiny_sched_workload(seed, n_inst=4, n_q=n_q, max_res=3)
+    wl.sched[:, 1] = 0                     # no KV cache (the limit then needs no blocks)
+    wl.sched[:, 3] = 64
+    wl.sched[0, 3] = 24
+    for j in range(4):                    # every resident fits its instance's limit
+        rp, rd, cx = wl.instance_requests(j)
+        assert len(rp) == 0 or (rp + cx).max() < wl.sched[j, 3]
+    wl.acc[:, :] = 0.1
+    wl.acc[:, wl.col[0]] = 0.9            # instance 0 wins whenever it can take a query
+    rng = np.random.default_rng(seed)
+    wl.q_prefill[:] = rng.integers(1, 40, n_q)   # many do not fit instance 0's limit
+    wl.max_prompt = 64
+    return wl
+
+
+def test_mixed_context_limits_route():
+    """Routing over instances with different context limits: a prompt at or above an
+    instance's limit gives it TTFT +inf there and it is never chosen; the choice is
+    the argmax over the instances that can take the query (a restatement of Eq. 5
+    over the feasible instances, numpy's argmax)."""
+    wl = _mixed_limit_pool()
+    r = O.trace(wl, full_rows=True)
+    assert np.isinf(r.ttft_all[:, 0]).sum() > 5 and np.isfinite(r.ttft_all[:, 1:]).all()
+    for i in range(wl.n_q):
+        row = r.ttft_all[i]
+        u = (wl.acc[i, wl.col] - wl.w_cost[0] * wl.cost[i, wl.col]) - wl.w_lat_ms[0] * row
+        u[np.isinf(row)] = -np.inf
+        assert r.choice[i] == int(np.argmax(u)), i
+        assert np.isfinite(row[r.choice[i]])
+    assert (r.choice == 0).sum() > 0 and (r.choice != 0).sum() > 0
+
+
+def test_query_no_instance_can_take():
+    wl = _mixed_limit_pool(n_q=10)
+    wl.q_prefill[4] = 64                  # at every instance's context limit
+    r = O.trace(wl, n_q=4)
+    assert len(r.choice) == 4
+    with pytest.raises(O.OracleError) as e:
+        O.trace(wl)
+    assert e.value.code == O.E_ARG and "query 4" in str(e.value)
 
 
 def test_c7_limits_bind():
