@@ -525,6 +525,13 @@ __global__ void k_clear_exchange(uint64_t* xs, int64_t n) {
 // next admission point (again exact by the FCFS argument).
 struct FCache {
   bool valid;
+  // Summary of the instance state when it admits a tail query in its very next
+  // batch (no frontier needed): its batch counter and clock in g and E, the
+  // admission batch's background in aP .. aA, and the decode batch after it (every
+  // request left decodes there) in sD1 / sC1.  Valid while the state is unchanged.
+  bool summ;
+  int sD1;
+  int64_t sC1;
   int g;           // batch counter of F
   double E;        // clock folded up to F
   int aP, aD, left;
@@ -956,6 +963,42 @@ __device__ __forceinline__ double estimate_visit(const FCache& fc, const Queue<K
   return __dsub_rn(E, t);
 }
 
+// The summary of a state that admits a tail query in its next batch (FCache.summ),
+// taken from the state itself: what the direct estimate reads of it for a query
+// whose prefill fits the admission batch.
+template <int KS>
+__device__ __forceinline__ void take_summary(FCache& fc, const Queue<KS>& S, const QEnv& e) {
+  const Coef& k = e.k;
+  fc.summ = true;
+  fc.g = S.g;
+  fc.E = S.clock;
+  fc.aP = (int)S.pre_sum;
+  fc.aD = S.n_dec;
+  fc.left = k.B - fc.aD - fc.aP;
+  fc.aC = e.need_C ? S.c0sum + (int64_t)fc.aD * S.g : 0;
+  fc.aA = e.need_A ? S.pre_attention_all(e) : 0;
+  const typename Queue<KS>::Tail tl = S.tail_begin(e);
+  fc.sD1 = (int)tl.D;
+  fc.sC1 = e.need_C ? tl.c0 + tl.D * (int64_t)(S.g + 1) : 0;
+}
+
+// The direct estimate of a query of p <= left prompt tokens (its prefill completes in
+// the admission batch) from the summary: the same batches, in the same order, as
+// estimate_visit's direct path.
+__device__ __forceinline__ double estimate_summary(const FCache& fc, const QEnv& e, int p,
+                                                   double t, int reading, int64_t* it_out) {
+  const Coef& k = e.k;
+  double E = __dadd_rn(fc.E, batch_time(k, fc.aP + p, fc.aD, fc.aC,
+                                         fc.aA + (int64_t)p * (p + 1) / 2));
+  int64_t it = 1;
+  if (reading != 1) {   // the decode batch after the admission batch
+    E = __dadd_rn(E, batch_time(k, 0, fc.sD1 + 1, fc.sC1 + p, 0));
+    ++it;
+  }
+  *it_out = it;
+  return __dsub_rn(E, t);
+}
+
 // The whole sequential trace with each wave owning IPW instances whose states stay
 // in LDS for the whole trace (one working copy in VGPRs per visit).  A scenario spans
 // G workgroups of W waves; block b serves scenario z = b / G as cluster member b % G
@@ -992,11 +1035,14 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
   int cols[IPW];
   FCache fc[IPW];
   QEnv env[IPW];   // per owned instance: coefficients, ring, staging (loop invariant)
+  int sg[IPW];        // per owned instance: the batch counter and clock of its state
+  double sclk[IPW];
 #pragma unroll
   for (int r = 0; r < IPW; ++r) {
     const int j = jbase + r;
     cols[r] = j < I ? pr.col[j] : -1;
     fc[r].valid = false;
+    fc[r].summ = false;
     fc[r].tD = 0;
     fc[r].tC = 0;
     if (j < I) {
@@ -1005,6 +1051,8 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
       q.template load<TRK>(S, env[r], z * I + j,
                            TRK ? S.r_tag + (int64_t)(z * I + j) * S.rcap : nullptr);
       q.template to_lds<TRK>(sst[wid][r], &stags[TRK ? wid : 0][r]);
+      sg[r] = q.g;
+      sclk[r] = q.clock;
     }
   }
   QueryBlock<IPW> cur = fetch_block<IPW>(0, N, qp, qd, qt, tau, acc, cost, n_cols, cols);
@@ -1081,18 +1129,47 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
         // estimate are the longest link of the query chain: let its wave issue first
         const bool hot = (W > 4) && i >= 0 && j == m;
         if (hot) __builtin_amdgcn_s_setprio(3);
-        wk.template from_lds<TRK>(sst[wid][r], &stags[TRK ? wid : 0][r]);
-        const VisitOut vo = visit<KS, TRK>(wk, fc[r], e, i >= 0 && j == m, p, dq, tn, S.qcap,
-                                           kmax, max_iters, err, sst[wid][r],
-                                           &stags[TRK ? wid : 0][r], fst[wid][r],
-                                           TRK ? S.r_tag + (int64_t)(z * I + j) * S.rcap
-                                               : nullptr,
-                                           tag0 + i, tk);
+        // Nothing to commit and no batch starting before tn: the visit would leave
+        // the state as it is, so it is skipped while a cache or summary of that
+        // state answers the estimate.
+        // (not for the wide-slot shape of long-context pools, whose chosen instance's
+        // walk is the chain and whose register budget the extra state would strain:
+        // measured 1-2 % slower there)
+        const bool idle = KS <= 4 && !(i >= 0 && j == m) && sclk[r] >= tn &&
+                          (fc[r].valid || fc[r].summ);
+        VisitOut vo;
+        vo.direct = false;
+        if (!idle) {
+          wk.template from_lds<TRK>(sst[wid][r], &stags[TRK ? wid : 0][r]);
+          vo = visit<KS, TRK>(wk, fc[r], e, i >= 0 && j == m, p, dq, tn, S.qcap, kmax,
+                              max_iters, err, sst[wid][r], &stags[TRK ? wid : 0][r],
+                              fst[wid][r],
+                              TRK ? S.r_tag + (int64_t)(z * I + j) * S.rcap : nullptr,
+                              tag0 + i, tk);
+          sg[r] = vo.g;
+          sclk[r] = vo.clock;
+          fc[r].summ = false;
+          if constexpr (KS <= 4)
+            if (vo.direct) take_summary(fc[r], wk, e);
+        } else {
+          vo.g = sg[r];
+          vo.clock = sclk[r];
+        }
         if (more) {
           int64_t it = 0;
-          const double ttft = p1_ok ? estimate_visit(fc[r], wk, vo, e, p1, t1, reading, kmax,
-                                                     max_iters, err, &it)
-                                    : __builtin_nan("");
+          double ttft;
+          if (!p1_ok) {
+            ttft = __builtin_nan("");
+          } else if (fc[r].summ && p1 <= fc[r].left && sclk[r] >= t1) {
+            ttft = estimate_summary(fc[r], e, p1, t1, reading, &it);
+          } else {
+            if (idle && fc[r].summ) {   // a prompt beyond the admission batch: the state
+              wk.template from_lds<TRK>(sst[wid][r], &stags[TRK ? wid : 0][r]);
+              wk.refill(e);   // the whole prefill list in the window, as the visit left it
+              vo.direct = true;
+            }
+            ttft = estimate_visit(fc[r], wk, vo, e, p1, t1, reading, kmax, max_iters, err, &it);
+          }
           wbatch += it;
           const double a = read_lane_f64(in_nxt ? nxt.acc[r] : cur.acc[r], l1);
           const double co = read_lane_f64(in_nxt ? nxt.cost[r] : cur.cost[r], l1);
