@@ -532,6 +532,7 @@ struct FCache {
   bool summ;
   int sD1;
   int64_t sC1;
+  int snf;         // summary: the next batch in which a decoding request finishes
   int g;           // batch counter of F
   double E;        // clock folded up to F
   int aP, aD, left;
@@ -980,6 +981,53 @@ __device__ __forceinline__ void take_summary(FCache& fc, const Queue<KS>& S, con
   const typename Queue<KS>::Tail tl = S.tail_begin(e);
   fc.sD1 = (int)tl.D;
   fc.sC1 = e.need_C ? tl.c0 + tl.D * (int64_t)(S.g + 1) : 0;
+  fc.snf = S.next_finish();
+}
+
+// The replay of a summarised state with an empty prefill list up to t, when it only
+// folds quiet batches (nothing to prefill, no decode finishing: with lazy decoders
+// such a batch changes only the batch counter and the clock) and stops before the
+// next decode finish -- the batches Queue::quiet_run folds, with the same times in
+// the same order -- or, for an empty instance, the idle jump of the clock to t.
+// Returns false, changing nothing, when the replay would need more (a stepped batch,
+// a new summary, the batch cap); otherwise brings the summary, the instance's scalars
+// in LDS (batch counter, clock, batches replayed) and g, clk to the new state.
+template <int KS>
+__device__ __forceinline__ bool replay_summary(FCache& fc, const QEnv& e, LdsQueue<KS>& SL,
+                                               int& g, double& clk, double t,
+                                               int64_t max_iters) {
+  if (fc.aD == 0) {   // nothing resident (the list is empty too): the clock jumps to t
+    clk = t;
+    fc.E = t;
+    if (lane_id() == 0) SL.clock = t;
+    __builtin_amdgcn_wave_barrier();
+    return true;
+  }
+  const int D = fc.aD;
+  double c = clk;
+  int gg = g;
+  int64_t n = 0;
+  int64_t C = fc.aC;   // decode context sum of the next batch
+  while (gg + 1 < fc.snf && c < t && n < max_iters) {
+    c = __dadd_rn(c, e.need_C ? batch_time(e.k, 0, D, C, 0) : batch_time(e.k, 0, D, 0, 0));
+    C += D;
+    ++gg;
+    ++n;
+  }
+  if (c < t || gg + 1 >= fc.snf) return false;
+  g = gg;
+  clk = c;
+  fc.g = gg;
+  fc.E = c;
+  fc.aC = e.need_C ? C : 0;
+  if (e.need_C) fc.sC1 += (int64_t)fc.sD1 * n;
+  if (lane_id() == 0) {
+    SL.g = gg;
+    SL.clock = c;
+    SL.iters += n;
+  }
+  __builtin_amdgcn_wave_barrier();
+  return true;
 }
 
 // The direct estimate of a query of p <= left prompt tokens (its prefill completes in
@@ -1139,7 +1187,20 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
                           (fc[r].valid || fc[r].summ);
         VisitOut vo;
         vo.direct = false;
-        if (!idle) {
+        bool fold = false;
+        if constexpr (KS <= 4 && !TRK && W > 4) {
+          // a replay that only folds quiet batches, on the summary (with several waves
+          // per SIMD, where the waves it relieves share the issue slots; with one, the
+          // code it adds measured slower)
+          if (!idle && !(i >= 0 && j == m) && fc[r].summ && fc[r].aP == 0) {
+            fold = replay_summary(fc[r], e, sst[wid][r], sg[r], sclk[r], tn, max_iters);
+            if (fold) {
+              vo.g = sg[r];
+              vo.clock = sclk[r];
+            }
+          }
+        }
+        if (!idle && !fold) {
           wk.template from_lds<TRK>(sst[wid][r], &stags[TRK ? wid : 0][r]);
           vo = visit<KS, TRK>(wk, fc[r], e, i >= 0 && j == m, p, dq, tn, S.qcap, kmax,
                               max_iters, err, sst[wid][r], &stags[TRK ? wid : 0][r],
@@ -1163,7 +1224,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
           } else if (fc[r].summ && p1 <= fc[r].left && sclk[r] >= t1) {
             ttft = estimate_summary(fc[r], e, p1, t1, reading, &it);
           } else {
-            if (idle && fc[r].summ) {   // a prompt beyond the admission batch: the state
+            if ((idle || fold) && fc[r].summ) {   // a prompt beyond the admission batch: the state
               wk.template from_lds<TRK>(sst[wid][r], &stags[TRK ? wid : 0][r]);
               wk.refill(e);   // the whole prefill list in the window, as the visit left it
               vo.direct = true;
