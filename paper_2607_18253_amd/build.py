@@ -20,7 +20,7 @@ SOURCES = [os.path.join(CSRC, "sfs_kernels.hip"), os.path.join(CSRC, "sfs_limits
            os.path.join(CSRC, "lar_api.cpp"), os.path.join(CSRC, "lar_noalloc.hip"),
            os.path.join(CSRC, "lar_board.cpp")]
 HEADERS = [os.path.join(CSRC, "sfs_device.h"), os.path.join(CSRC, "sfs_launch.h"),
-           os.path.join(CSRC, "sfs_limits.h"), os.path.join(CSRC, "sfs_route.h"),
+           os.path.join(CSRC, "sfs_limits.h"), os.path.join(CSRC, "sfs_route.h"), os.path.join(CSRC, "sfs_walk.h"),
            os.path.join(ROOT, "include", "lar.h")]
 ARCH = "gfx950"
 

@@ -46,6 +46,7 @@ struct lar_ctx {
   size_t tail_elems = 0;  // allocated K * Z * I
   bool loaded = false;
   int max_col = 0;
+  bool no_ctx_term = false;   // every instance of the loaded pool has d == 0
   lar_status sticky = LAR_OK;
   std::string msg;
   std::vector<void*> allocs;
@@ -106,6 +107,7 @@ LaunchEnv env_of(const lar_ctx* ctx) {
   e.ks = ctx->ks;
   e.max_iters = ctx->cfg.max_iters;
   e.max_prompt = ctx->cfg.max_prompt;
+  e.no_ctx_term = ctx->no_ctx_term;
   e.reading = ctx->cfg.flags & 1;
   e.err = ctx->err;
   e.stream = ctx->stream;
@@ -404,6 +406,9 @@ lar_status lar_load_state(lar_ctx* ctx, const lar_instance_params* params, const
     pi[I + j] = params[j].max_seqs;
     pi[2 * I + j] = params[j].col;
   }
+  ctx->no_ctx_term = true;
+  for (int j = 0; j < I; ++j)
+    if (params[j].d != 0.0) ctx->no_ctx_term = false;
   hipStream_t s = ctx->stream;
   HIP_TRY(ctx, hipStreamSynchronize(s));
   HIP_TRY(ctx, hipMemcpy(ctx->pa, pa.data(), pa.size() * sizeof(double), hipMemcpyHostToDevice));

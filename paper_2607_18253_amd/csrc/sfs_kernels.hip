@@ -26,11 +26,14 @@
 #include "sfs_device.h"
 #include "sfs_launch.h"
 #include "sfs_route.h"
+#include "sfs_walk.h"
 
 namespace lar {
 
 // ------------------------------------------------------------------ k_traj
-template <int KS>
+// NC: some instance has d != 0, so the walk keeps context sums per batch; without
+// them an instance with d != 0 runs the engine.
+template <int KS, bool NC>
 __global__ __launch_bounds__(kWave) void k_traj(DevState S, DevParams pr, DevTraj tr, int Z, int I,
                                                const double* t_ptr, double t_val,
                                                int64_t max_iters, int32_t* err) {
@@ -40,7 +43,25 @@ __global__ __launch_bounds__(kWave) void k_traj(DevState S, DevParams pr, DevTra
   const double t = t_ptr ? *t_ptr : t_val;
   const int ln = lane_id();
   __shared__ alignas(16) int stage[stage_words<false>()];
+  __shared__ WalkLds<NC> walk_lds;
   const QEnv e = make_env(S, pr, qid, j, stage);
+  bool walked;
+  if (e.need_C) {
+    if constexpr (NC)
+      walked = e.need_A ? walk_traj<KS, NC, true, true>(S, e, qid, tr, Z * I, t, max_iters, err,
+                                                        walk_lds)
+                        : walk_traj<KS, NC, true, false>(S, e, qid, tr, Z * I, t, max_iters, err,
+                                                         walk_lds);
+    else
+      walked = false;
+  } else {
+    walked = e.need_A ? walk_traj<KS, NC, false, true>(S, e, qid, tr, Z * I, t, max_iters, err,
+                                                       walk_lds)
+                      : walk_traj<KS, NC, false, false>(S, e, qid, tr, Z * I, t, max_iters, err,
+                                                        walk_lds);
+  }
+  if (walked) return;
+  // the engine, for queues outside what the walk covers
   Queue<KS> w;
   w.load(S, e, qid);
   double E = w.clock;
@@ -1457,8 +1478,12 @@ __global__ void k_clear_error(int32_t* err) { *err = 0; }
 // ------------------------------------------------------------------ launchers
 template <int KS>
 static hipError_t launch_traj_ks(const LaunchEnv& env, const double* t_ptr, double t_val) {
-  hipLaunchKernelGGL(k_traj<KS>, dim3(env.Z * env.I), dim3(kWave), 0, env.stream, env.S,
-                     env.P, env.T, env.Z, env.I, t_ptr, t_val, env.max_iters, env.err);
+  if (env.no_ctx_term)
+    hipLaunchKernelGGL((k_traj<KS, false>), dim3(env.Z * env.I), dim3(kWave), 0, env.stream,
+                       env.S, env.P, env.T, env.Z, env.I, t_ptr, t_val, env.max_iters, env.err);
+  else
+    hipLaunchKernelGGL((k_traj<KS, true>), dim3(env.Z * env.I), dim3(kWave), 0, env.stream,
+                       env.S, env.P, env.T, env.Z, env.I, t_ptr, t_val, env.max_iters, env.err);
   return hipGetLastError();
 }
 

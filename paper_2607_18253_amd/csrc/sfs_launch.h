@@ -28,6 +28,7 @@ struct LaunchEnv {
   int ks;             // running slots per lane (1, 2, 4, 8, 16)
   int64_t max_iters;
   int max_prompt;
+  bool no_ctx_term;   // every instance has d == 0 (the trajectory walk keeps no context sums)
   int reading;        // 0: first decode batch, 1: batch completing the prefill
   int32_t* err;       // sticky device error
   hipStream_t stream;
