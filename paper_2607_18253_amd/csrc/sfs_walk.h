@@ -56,7 +56,8 @@ __device__ __forceinline__ int64_t lane_read64(int64_t v, int l) {
 // walked, so the read may go through the scalar cache (constant address space).
 typedef const __attribute__((address_space(4))) int32_t walk_cint;
 __device__ __forceinline__ int ring_s(const int32_t* base, int pos) {
-  return ((walk_cint*)base)[pos];
+  const uint32_t off = (uint32_t)pos * 4u;   // pos < rcap: a 32-bit byte offset
+  return *(walk_cint*)((const char*)base + off);
 }
 
 // Decoding requests of one queue as per-batch counts (see the top of this file).
@@ -75,18 +76,18 @@ struct WalkBins {
   // takes them in at far_update(), which must come before batch nl - kWalkNear.
   __device__ __forceinline__ void place(int nl, int nc, int near) {
     const int ln = lane_id();
-    if (near) {
-      const int x = nl - hb;
-      if (x < kWave) {
-        hv += ln == x ? 1 : 0;
-        if constexpr (QC) hvc += ln == x ? (int64_t)nc : 0;
-      } else if (ln == 0) {
-        atomicAdd(&L.cnt[nl & (kWalkBins - 1)], 1);
-        if constexpr (QC)
-          atomicAdd((unsigned long long*)&L.c0[nl & (kWalkBins - 1)],
-                    (unsigned long long)(int64_t)nc);
-      }
-    } else {
+    const int x = nl - hb;
+    // in the window: that lane's bin (no lane matches a bin past the window)
+    hv += ln == x ? 1 : 0;
+    if constexpr (QC) hvc += ln == x ? (int64_t)nc : 0;
+    // past the window: the ring bin
+    if (ln == 0 && x >= kWave && near) {
+      atomicAdd(&L.cnt[nl & (kWalkBins - 1)], 1);
+      if constexpr (QC)
+        atomicAdd((unsigned long long*)&L.c0[nl & (kWalkBins - 1)],
+                  (unsigned long long)(int64_t)nc);
+    }
+    if (!near) {
       if (ln == 0 && n_far < kWalkFar) { L.flast[n_far] = nl; L.fc0[n_far] = nc; }
       n_far += 1;
     }
@@ -327,20 +328,21 @@ __device__ bool walk_traj(const DevState& S, const QEnv& e, int qid, const DevTr
           if (need_C) c0sum += nc;
           n_part = 0;
           n_pre -= 1;
-          if (n_pre > 0) {   // entries after the head are waiting: context 0
-            pos = pos + 1 == rcap ? 0 : pos + 1;
-            h_rp = ring_s(e.r_rp, pos);
-            h_rd = ring_s(e.r_rd, pos);
-            h_cx = 0;
-          }
+          // entries after the head are waiting: context 0 (past the list's end the
+          // slot holds an unused value)
+          pos = pos + 1 == rcap ? 0 : pos + 1;
+          h_rp = ring_s(e.r_rp, pos);
+          h_rd = ring_s(e.r_rd, pos);
+          h_cx = 0;
         }
       }
       if (n_part == 0) {
-        while (n_pre > 0 && left > 0 && free_slots > 0) {
+        // waiting entries that may be admitted: one slot each, while budget lasts
+        int adm = min(n_pre, free_slots);
+        while (adm > 0 && left > 0) {
           const int ch = min(h_rp, left);
           P += ch;
           left -= ch;
-          free_slots -= 1;
           if (need_A) A += (int64_t)ch * (ch + 1) / 2;
           if (ch < h_rp) {   // admitted, served in part
             h_rp -= ch;
@@ -353,11 +355,11 @@ __device__ bool walk_traj(const DevState& S, const QEnv& e, int qid, const DevTr
           n_dec += 1;
           if (need_C) c0sum += nc;
           n_pre -= 1;
-          if (n_pre > 0) {
-            pos = pos + 1 == rcap ? 0 : pos + 1;
-            h_rp = ring_s(e.r_rp, pos);
-            h_rd = ring_s(e.r_rd, pos);
-          }
+          adm -= 1;
+          // the next entry (past the list's end the slot holds an unused value)
+          pos = pos + 1 == rcap ? 0 : pos + 1;
+          h_rp = ring_s(e.r_rp, pos);
+          h_rd = ring_s(e.r_rd, pos);
         }
       }
       ps -= P;
@@ -365,7 +367,25 @@ __device__ bool walk_traj(const DevState& S, const QEnv& e, int qid, const DevTr
       E = __dadd_rn(E, batch_time(k, P, D, C, A));
       if (g >= g_stop) break;
       if (n_dec + n_pre < M && ps < B - n_dec) break;
-      if (!(n_pre > 0 && n_dec < B && (n_part > 0 || n_dec + n_part < M))) break;
+      if (!(n_pre > 0 && n_dec < B && (n_part > 0 || n_dec + n_part < M))) {
+        // quiet until the next decode finish: folded here when that finish is in
+        // the window and before the stop (else the outer loop folds)
+        const uint64_t m = ballot(w.hv != 0 && w.hb + ln > g);
+        const int nf = m ? w.hb + __builtin_ctzll(m) : 0x7fffffff;
+        if (nf > g_stop) break;
+        const int n = nf - 1 - g;
+        if constexpr (!QC) {
+          const double T = batch_time(k, 0, n_dec, 0, 0);
+          for (int i = 0; i < n; ++i) E = __dadd_rn(E, T);
+        } else {
+          int64_t C2 = c0sum + (int64_t)n_dec * g;
+          for (int i = 0; i < n; ++i) {
+            E = __dadd_rn(E, batch_time(k, 0, n_dec, C2, 0));
+            C2 += n_dec;
+          }
+        }
+        g = nf - 1;
+      }
       fin = lane_read(w.hv, g + 1 - w.hb);
       if constexpr (QC) finc = lane_read64(w.hvc, g + 1 - w.hb);
     }
