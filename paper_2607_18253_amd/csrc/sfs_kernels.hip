@@ -6,9 +6,9 @@
 //            is last in FCFS order and only takes budget and slots the background
 //            leaves, so all batches before its admission batch are the same with or
 //            without it, and after that batch the background only decodes.
-//   k_est    one thread per (scenario, query, instance), instance fastest: the
-//            query's own continuation from the shared trajectory (Sec. 4.1, the
-//            first-output-token batch and the TTFT sum).
+//   k_est    one thread per (scenario, instance, chunk of queries), instance
+//            fastest: each query's own continuation from the shared trajectory
+//            (Sec. 4.1, the first-output-token batch and the TTFT sum).
 //   k_route  one block per (scenario, query) row: Lagrangian utility and argmax
 //            with ties to the lowest instance (Sec. 3, Eq. 2).
 //   k_commit one wave per (scenario, instance): append the routed query, then
@@ -130,72 +130,110 @@ __global__ __launch_bounds__(kWave) void k_traj(DevState S, DevParams pr, DevTra
 }
 
 // ------------------------------------------------------------------ k_est
+// One block per (scenario, chunk of kEstChunk queries, 256 instances), one thread
+// per instance: the thread keeps its instance's trajectory in registers and walks
+// the chunk's queries (their prompt lengths staged in LDS), so each wave writes 64
+// consecutive estimates per query.
+constexpr int kEstChunk = 16;
+
 __global__ __launch_bounds__(256) void k_est(DevParams pr, DevTraj tr, int Z, int Q, int I,
                                             const int32_t* q_prefill, const double* t_ptr,
                                             double t_val, int max_prompt,
                                             int reading, int64_t max_iters, double* ttft,
                                             int32_t* iters, int32_t* err) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t total = (int64_t)Z * Q * I;
-  if (idx >= total) return;
-  const int j = (int)(idx % I);
-  const int64_t zq = idx / I;
-  const int q = (int)(zq % Q);
-  const int z = (int)(zq / Q);
+  __shared__ int s_p[kEstChunk];
+  const int n_chunks = (Q + kEstChunk - 1) / kEstChunk;
+  const int col_blocks = (I + 255) / 256;
+  const int cb = (int)(blockIdx.x % (unsigned)col_blocks);
+  const int zc = (int)(blockIdx.x / (unsigned)col_blocks);
+  const int c = zc % n_chunks;
+  const int z = zc / n_chunks;
+  const int q0 = c * kEstChunk;
+  const int q1 = Q - q0 < kEstChunk ? Q : q0 + kEstChunk;
+  if ((int)threadIdx.x < q1 - q0) s_p[threadIdx.x] = q_prefill[q0 + threadIdx.x];
+  __syncthreads();
+  const int j = cb * 256 + (int)threadIdx.x;
+  if (j >= I) return;
   const int qid = z * I + j;
   const int ZI = Z * I;
-  const int p = q_prefill[q];
   const double t = t_ptr ? *t_ptr : t_val;
-  if (p < 1 || p > max_prompt) {
-    set_error(err, kErrArg);
-    ttft[idx] = __builtin_nan("");
-    if (iters) iters[idx] = -1;
-    return;
-  }
-  if (!tr.ok[qid]) {
-    set_error(err, kErrIter);   // a clock behind t was already reported as a state error
-    ttft[idx] = __builtin_nan("");
-    if (iters) iters[idx] = -1;
-    return;
-  }
   const Coef k = load_coef(pr, j);
-  double E = tr.E[qid];
-  int64_t it = (int64_t)tr.pre[qid] + 1;
-  // admission batch: background features plus the query's first chunk (context 0)
+  const int ok = tr.ok[qid];
+  const double E0 = tr.E[qid];
+  const int64_t it0 = (int64_t)tr.pre[qid] + 1;
   const int lft = tr.left[qid];
-  const int64_t ch = p < lft ? p : lft;
-  E = __dadd_rn(E, batch_time(k, tr.P[qid] + ch, tr.D[qid], tr.C[qid],
-                              tr.A[qid] + ch * (ch + 1) / 2));
-  int64_t rem = p - ch;
-  int64_t cxq = ch;
-  bool done = reading == 1 && rem == 0;
-  int kk = 0;
+  // P <= B and D <= M fit in 32 bits
+  const int P0 = (int)tr.P[qid], D0 = (int)tr.D[qid];
+  const int64_t C0 = tr.C[qid], A0 = tr.A[qid];
   const int K = tail_count(tr);
-  while (!done) {
-    if (kk >= K) {   // cannot happen for p <= max_prompt; guard the tail bounds
-      set_error(err, kErrIter);
-      E = __builtin_nan("");
-      break;
+  // the first decode-tail batch, which nearly every query reaches
+  const int D1 = K > 0 ? tr.tailD[qid] : 0;
+  const int64_t C1 = K > 0 ? tr.tailC[qid] : 0;
+  // Batch time of Sec. 4.1 with batch_time's operations: the context and attention
+  // terms are converted only where their coefficient is non-zero (lanes whose
+  // instances all have d = 0 or e = 0 skip them); otherwise the term is coef * 0.0.
+  const bool need_C = k.d != 0.0, need_A = k.e != 0.0;
+  const double dz = __dmul_rn(k.d, 0.0), ez = __dmul_rn(k.e, 0.0);
+  auto bt_pd = [&](int P, int D) {
+    return __dadd_rn(__dadd_rn(k.a, __dmul_rn(k.b, (double)P)), __dmul_rn(k.c, (double)D));
+  };
+  auto bt_ca = [&](double t, int64_t C, int64_t A) {
+    double td = dz, te = ez;
+    if (need_C) td = __dmul_rn(k.d, (double)C);
+    if (need_A) te = __dmul_rn(k.e, (double)A);
+    return __dadd_rn(__dadd_rn(t, td), te);
+  };
+  for (int q = q0; q < q1; ++q) {
+    const int64_t o = ((int64_t)z * Q + q) * I + j;
+    const int p = s_p[q - q0];
+    if (p < 1 || p > max_prompt) {
+      set_error(err, kErrArg);
+      ttft[o] = __builtin_nan("");
+      if (iters) iters[o] = -1;
+      continue;
     }
-    const int64_t Dk = tr.tailD[(int64_t)kk * ZI + qid];
-    const int64_t Ck = tr.tailC[(int64_t)kk * ZI + qid];
-    if (rem > 0) {
-      const int64_t room = (int64_t)k.B - Dk;
-      const int64_t c2 = rem < room ? rem : room;
-      E = __dadd_rn(E, batch_time(k, c2, Dk, Ck, c2 * cxq + c2 * (c2 + 1) / 2));
-      rem -= c2;
-      cxq += c2;
-      done = reading == 1 && rem == 0;
-    } else {
-      E = __dadd_rn(E, batch_time(k, 0, Dk + 1, Ck + cxq, 0));
-      done = true;
+    if (!ok) {
+      set_error(err, kErrIter);   // a clock behind t was already reported as a state error
+      ttft[o] = __builtin_nan("");
+      if (iters) iters[o] = -1;
+      continue;
     }
-    ++kk;
-    ++it;
+    int64_t it = it0;
+    // admission batch: background features plus the query's first chunk (context 0)
+    const int ch = p < lft ? p : lft;
+    double E = __dadd_rn(
+        E0, bt_ca(bt_pd(P0 + ch, D0), C0, need_A ? A0 + (int64_t)ch * (ch + 1) / 2 : 0));
+    int rem = p - ch;
+    int cxq = ch;
+    bool done = reading == 1 && rem == 0;
+    int kk = 0;
+    while (!done) {
+      if (kk >= K) {   // cannot happen for p <= max_prompt; guard the tail bounds
+        set_error(err, kErrIter);
+        E = __builtin_nan("");
+        break;
+      }
+      const int Dk = kk == 0 ? D1 : tr.tailD[(int64_t)kk * ZI + qid];
+      const int64_t Ck = kk == 0 ? C1 : tr.tailC[(int64_t)kk * ZI + qid];
+      if (rem > 0) {
+        const int room = k.B - Dk;
+        const int c2 = rem < room ? rem : room;
+        E = __dadd_rn(E, bt_ca(bt_pd(c2, Dk), Ck,
+                               need_A ? (int64_t)c2 * cxq + (int64_t)c2 * (c2 + 1) / 2 : 0));
+        rem -= c2;
+        cxq += c2;
+        done = reading == 1 && rem == 0;
+      } else {
+        E = __dadd_rn(E, bt_ca(bt_pd(0, Dk + 1), Ck + cxq, 0));
+        done = true;
+      }
+      ++kk;
+      ++it;
+    }
+    if (it > max_iters) set_error(err, kErrIter);
+    ttft[o] = __dsub_rn(E, t);
+    if (iters) iters[o] = (int32_t)it;
   }
-  if (it > max_iters) set_error(err, kErrIter);
-  ttft[idx] = __dsub_rn(E, t);
-  if (iters) iters[idx] = (int32_t)it;
 }
 
 // ------------------------------------------------------------------ k_route
@@ -226,12 +264,9 @@ __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double
     const double u = cand_value(eq2, trow[j], wl, tau, tq, j, &k);
     if (better(u, k, bu, bj)) { bu = u; bj = k; }
   }
-#pragma unroll
-  for (int o = kWave / 2; o > 0; o >>= 1) {
-    const double u2 = __shfl_xor(bu, o, kWave);
-    const int j2 = __shfl_xor(bj, o, kWave);
-    if (better(u2, j2, bu, bj)) { bu = u2; bj = j2; }
-  }
+  // the wave's best (DPP; `better` is a total order, so the combining order does not
+  // matter), then the block's over its waves
+  lane_best(bu, bj, kWave);
   const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
   if (lane_id() == 0) { s_u[wid] = bu; s_j[wid] = bj; }
   __syncthreads();
@@ -1654,8 +1689,10 @@ hipError_t launch_commit(const LaunchEnv& env, const int32_t* choice, int64_t ch
 hipError_t launch_est(const LaunchEnv& env, int Q, const int32_t* q_prefill, const double* t_ptr,
                       double t_val, double* ttft, int32_t* iters) {
   if (env.limited) return launch_lim_est(env, Q, q_prefill, t_ptr, t_val, ttft, iters);
-  const int64_t total = (int64_t)env.Z * Q * env.I;
-  const int64_t blocks = (total + 255) / 256;
+  const int64_t blocks =
+      (int64_t)env.Z * ((Q + kEstChunk - 1) / kEstChunk) * ((env.I + 255) / 256);
+  if (blocks == 0) return hipSuccess;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_est, dim3((unsigned)blocks), dim3(256), 0, env.stream, env.P, env.T,
                      env.Z, Q, env.I, q_prefill, t_ptr, t_val, env.max_prompt, env.reading,
                      env.max_iters,
@@ -1667,7 +1704,9 @@ hipError_t launch_route(const LaunchEnv& env, int Q, const double* ttft, int64_t
                         const double* acc, const double* cost, int n_cols, const double* w_cost,
                         const double* w_lat, const double* tau, int32_t* choice,
                         double* chosen_ttft, double* utility, int64_t out_zstride, int out_q0) {
-  hipLaunchKernelGGL(k_route, dim3(env.Z * Q), dim3(256), 0, env.stream, env.Z, Q, env.I, ttft,
+  // one block per row; as many waves as the row needs, up to four
+  const int waves = env.I <= kWave ? 1 : env.I >= 4 * kWave ? 4 : (env.I + kWave - 1) / kWave;
+  hipLaunchKernelGGL(k_route, dim3(env.Z * Q), dim3(waves * kWave), 0, env.stream, env.Z, Q, env.I, ttft,
                      ttft_zstride, acc, cost, n_cols, env.P.col, w_cost, w_lat, tau, choice,
                      chosen_ttft, utility, out_zstride, out_q0, env.err);
   return hipGetLastError();
