@@ -101,7 +101,7 @@ def _parse():
 COPY_PROBE_BYTES = 256 << 20
 _CSRC = "paper_2607_18253_amd/csrc/"
 KERNEL_SOURCES = tuple(_CSRC + f for f in ("sfs_kernels.hip", "sfs_device.h", "sfs_route.h",
-                                           "sfs_launch.h"))
+                                           "sfs_launch.h", "sfs_walk.h"))
 LPS_KERNEL_SOURCES = tuple(_CSRC + f for f in ("sfs_lps.hip", "sfs_kernels.hip", "sfs_route.h"))
 LIMIT_KERNEL_SOURCES = tuple(_CSRC + f for f in ("sfs_limits.hip", "sfs_limits.h", "sfs_device.h",
                                                  "sfs_route.h", "sfs_launch.h"))
