@@ -1230,7 +1230,9 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
         const QEnv& e = env[r];
         Queue<KS> wk;
         // with several waves per SIMD, the chosen instance's commit, walk and next
-        // estimate are the longest link of the query chain: let its wave issue first
+        // estimate are the longest link of the query chain: let its wave issue first,
+        // then the waves whose instances replay batches, then quiet replays, then the
+        // rest (which only estimate)
         const bool hot = (W > 4) && i >= 0 && j == m;
         if (hot) __builtin_amdgcn_s_setprio(3);
         // Nothing to commit and no batch starting before tn: the visit would leave
@@ -1249,6 +1251,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
           // per SIMD, where the waves it relieves share the issue slots; with one, the
           // code it adds measured slower)
           if (!idle && !(i >= 0 && j == m) && fc[r].summ && fc[r].aP == 0) {
+            __builtin_amdgcn_s_setprio(1);
             fold = replay_summary(fc[r], e, sst[wid][r], sg[r], sclk[r], tn, max_iters);
             if (fold) {
               vo.g = sg[r];
@@ -1256,6 +1259,8 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
             }
           }
         }
+        // the other visits that replay batches are the next longest links
+        if ((W > 4) && !hot && !idle && !fold) __builtin_amdgcn_s_setprio(2);
         if (!idle && !fold) {
           wk.template from_lds<TRK>(sst[wid][r], &stags[TRK ? wid : 0][r]);
           vo = visit<KS, TRK>(wk, fc[r], e, i >= 0 && j == m, p, dq, tn, S.qcap, kmax,
@@ -1296,7 +1301,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
           const double u = cand_value(eq2, ttft, wl, tau, tq, j, &k);
           cand_take(c, u, k, ttft, eq2);
         }
-        if (hot) __builtin_amdgcn_s_setprio(0);
+        if (W > 4) __builtin_amdgcn_s_setprio(0);
       }
     }
     if (last_in_block) {
