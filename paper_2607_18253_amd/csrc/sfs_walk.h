@@ -52,6 +52,20 @@ __device__ __forceinline__ int64_t lane_read64(int64_t v, int l) {
   return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
 }
 
+// One lane's add to an LDS word (32 or 64 bits), issued as a single ds_add: the
+// compiler's atomic lowering would first count the active lanes, and here exactly one
+// lane is active.  A wave's LDS operations complete in order, so a later read by any
+// lane sees the sum; the memory clobber keeps the compiler from moving LDS accesses
+// across it.
+__device__ __forceinline__ void lds_add_one(int* p, int v) {
+  const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int*)p;
+  asm volatile("ds_add_u32 %0, %1" : : "v"(a), "v"(v) : "memory");
+}
+__device__ __forceinline__ void lds_add_one(int64_t* p, int64_t v) {
+  const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int64_t*)p;
+  asm volatile("ds_add_u64 %0, %1" : : "v"(a), "v"(v) : "memory");
+}
+
 // Wave-uniform read of a ring field.  Nothing writes the rings while a trajectory is
 // walked, so the read may go through the scalar cache (constant address space).
 typedef const __attribute__((address_space(4))) int32_t walk_cint;
@@ -80,16 +94,12 @@ struct WalkBins {
     // in the window: that lane's bin (no lane matches a bin past the window)
     hv += ln == x ? 1 : 0;
     if constexpr (QC) hvc += ln == x ? (int64_t)nc : 0;
-    // past the window: the ring bin
-    if (ln == 0 && x >= kWave && near) {
-      atomicAdd(&L.cnt[nl & (kWalkBins - 1)], 1);
-      if constexpr (QC)
-        atomicAdd((unsigned long long*)&L.c0[nl & (kWalkBins - 1)],
-                  (unsigned long long)(int64_t)nc);
-    }
-    if (!near) {
+    if (__builtin_expect(!near, 0)) {   // far: the list
       if (ln == 0 && n_far < kWalkFar) { L.flast[n_far] = nl; L.fc0[n_far] = nc; }
       n_far += 1;
+    } else if (ln == 0 && x >= kWave) {   // past the window: the ring bin
+      lds_add_one(&L.cnt[nl & (kWalkBins - 1)], 1);
+      if constexpr (QC) lds_add_one(&L.c0[nl & (kWalkBins - 1)], (int64_t)nc);
     }
   }
 
@@ -337,19 +347,14 @@ __device__ bool walk_traj(const DevState& S, const QEnv& e, int qid, const DevTr
         }
       }
       if (n_part == 0) {
-        // waiting entries that may be admitted: one slot each, while budget lasts
+        // waiting entries that may be admitted (one slot each): those whose whole
+        // prompt fits the budget left complete here ...
         int adm = min(n_pre, free_slots);
-        while (adm > 0 && left > 0) {
-          const int ch = min(h_rp, left);
+        while (adm > 0 && h_rp <= left) {
+          const int ch = h_rp;
           P += ch;
           left -= ch;
           if (need_A) A += (int64_t)ch * (ch + 1) / 2;
-          if (ch < h_rp) {   // admitted, served in part
-            h_rp -= ch;
-            h_cx = ch;
-            n_part = 1;
-            break;
-          }
           const int nc = ch - gn;
           w.place(gn + h_rd, nc, h_rd <= kWalkNear);
           n_dec += 1;
@@ -360,6 +365,16 @@ __device__ bool walk_traj(const DevState& S, const QEnv& e, int qid, const DevTr
           pos = pos + 1 == rcap ? 0 : pos + 1;
           h_rp = ring_s(e.r_rp, pos);
           h_rd = ring_s(e.r_rd, pos);
+        }
+        // ... and the next one, if admitted, takes the rest of the budget in part
+        if (adm > 0 && left > 0) {
+          const int ch = left;
+          P += ch;
+          left = 0;
+          if (need_A) A += (int64_t)ch * (ch + 1) / 2;
+          h_rp -= ch;
+          h_cx = ch;
+          n_part = 1;
         }
       }
       ps -= P;
