@@ -1117,8 +1117,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
                                                         int tail_k, SyncCtl sc) {
   __shared__ double s_u[2][W];
   __shared__ int s_j[2][W];
-  __shared__ double s_mu[2];
-  __shared__ int s_mj[2];
+  __shared__ int s_abort;
   __shared__ alignas(16) int stage[W][stage_words<TRK>()];
   __shared__ LdsQueue<KS> sst[W][IPW];   // instance states
   __shared__ LdsQueue<KS> fst[W][IPW];   // frontier states
@@ -1136,6 +1135,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
   const int jbase = (cid * W + wid) * IPW;
   const int kmax = tail_k;   // <= 64, checked at launch
   const Track tk{TRK ? realized + (int64_t)z * N : nullptr, tag0, N, reading};
+  if (threadIdx.x == 0) s_abort = 0;   // read after the first query's barrier
   int cols[IPW];
   FCache fc[IPW];
   QEnv env[IPW];   // per owned instance: coefficients, ring, staging (loop invariant)
@@ -1179,31 +1179,40 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
       const int buf = i & 1;
       if (ln == 0) { s_u[buf][wid] = c.u; s_j[buf][wid] = c.j; }
       __syncthreads();
+      if (s_abort) break;   // an exchange failed on the previous query
       // lane v reads wave v's candidate; log2(nw) shuffle steps apply the total order
       double bu = 0.0;
       int bj = -1;
       if (ln < nw) { bu = s_u[buf][ln]; bj = s_j[buf][ln]; }
       lane_best(bu, bj, nw);
+      // Only the wave holding the workgroup's best (wave 0 when the workgroup has no
+      // candidate) can hold the query's winner.  With several workgroups that wave
+      // alone exchanges with the others and learns the winner; the other waves are
+      // not chosen and go on to their visits while the exchange runs.
+      int holder = 1, xok = 1;
       if (G > 1) {
-        // wave 0 exchanges with the other workgroups, then broadcasts the winner
-        if (wid == 0) {
-          const bool ok = cluster_exchange(bu, bj, i, G, cid, xs, err, sc);
-          if (ln == 0) { s_mu[buf] = bu; s_mj[buf] = ok ? bj : -2; }
+        holder = bj >= 0 ? (c.j == bj ? 1 : 0) : (wid == 0 ? 1 : 0);
+        if (holder) {
+          __builtin_amdgcn_s_setprio(3);   // the chain waits on this wave
+          if (!cluster_exchange(bu, bj, i, G, cid, xs, err, sc)) {
+            xok = 0;   // every wave leaves after the next workgroup barrier
+            if (ln == 0) s_abort = 1;
+          }
+          __builtin_amdgcn_s_setprio(0);
         }
-        __syncthreads();
-        bu = s_mu[buf];
-        bj = s_mj[buf];
-        if (bj == -2) break;
       }
-      m = bj >= 0 ? key_index(bj) : -1;
-      if (m < 0 && cid == 0 && threadIdx.x == 0) set_error(err, kErrArg);   // no candidate
-      // the wave holding the winner (its own best) writes the outputs
-      const bool mine = m >= 0 ? c.j == bj : (cid == 0 && wid == 0);
-      if (mine && ln == 0) {
-        const int64_t o = (int64_t)z * N + i;
-        choice[o] = m;
-        if (chosen_ttft) chosen_ttft[o] = c.ttft;
-        if (utility && m >= 0) utility[o] = c.eq2;
+      m = holder && xok && bj >= 0 ? key_index(bj) : -1;
+      if (holder && xok) {
+        if (m < 0 && cid == 0 && (G > 1 || wid == 0) && ln == 0)
+          set_error(err, kErrArg);   // no candidate
+        // the wave holding the winner (its own best) writes the outputs
+        const bool mine = m >= 0 ? c.j == bj : (cid == 0 && wid == 0);
+        if (mine && ln == 0) {
+          const int64_t o = (int64_t)z * N + i;
+          choice[o] = m;
+          if (chosen_ttft) chosen_ttft[o] = c.ttft;
+          if (utility && m >= 0) utility[o] = c.eq2;
+        }
       }
     }
     const bool more = i + 1 < N;
