@@ -258,8 +258,7 @@ __global__ __launch_bounds__(W * kWave) void k_ltrace_cl(LAR_TRACE_PARAMS, DevLi
                                                         uint64_t* xslot, SyncCtl sc) {
   __shared__ double s_u[2][W];
   __shared__ int s_j[2][W];
-  __shared__ double s_mu[2];
-  __shared__ int s_mj[2];
+  __shared__ int s_abort;
   __shared__ alignas(16) int lds[W][lim_lds_words<KS>()];
   const int b = blockIdx.x;
   const int z = b / G;
@@ -275,6 +274,7 @@ __global__ __launch_bounds__(W * kWave) void k_ltrace_cl(LAR_TRACE_PARAMS, DevLi
   const bool own = j < I;
   const int qid = z * I + (own ? j : 0);
   const LTrack tk{TRK ? realized + (int64_t)z * N : nullptr, tag0, N, reading};
+  if (threadIdx.x == 0) s_abort = 0;   // read after the first query's barrier
   int cols[1] = {own ? pr.col[j] : -1};
   int32_t* tags = (TRK && own) ? S.r_tag + (int64_t)qid * S.rcap : nullptr;
   const LEnv e = make_lenv(S, pr, lm, qid, own ? j : 0, lds[wid]);
@@ -302,30 +302,34 @@ __global__ __launch_bounds__(W * kWave) void k_ltrace_cl(LAR_TRACE_PARAMS, DevLi
       const int buf = i & 1;
       if (ln == 0) { s_u[buf][wid] = c.u; s_j[buf][wid] = c.j; }
       __syncthreads();
+      if (s_abort) break;   // an exchange failed on the previous query
       double bu = 0.0;
       int bj = -1;
       if (ln < nw) { bu = s_u[buf][ln]; bj = s_j[buf][ln]; }
       lane_best(bu, bj, nw);
+      // Only the wave holding the workgroup's best (wave 0 when the workgroup has no
+      // candidate) can hold the query's winner: with several workgroups it alone
+      // exchanges with the others, while the other waves (not chosen) go on.
+      int holder = 1, xok = 1;
       if (G > 1) {
-        // wave 0 exchanges with the other workgroups, then broadcasts the winner
-        if (wid == 0) {
-          const bool ok = cluster_exchange(bu, bj, i, G, cid, xs, err, sc);
-          if (ln == 0) { s_mu[buf] = bu; s_mj[buf] = ok ? bj : -2; }
+        holder = bj >= 0 ? (c.j == bj ? 1 : 0) : (wid == 0 ? 1 : 0);
+        if (holder && !cluster_exchange(bu, bj, i, G, cid, xs, err, sc)) {
+          xok = 0;   // every wave leaves after the next workgroup barrier
+          if (ln == 0) s_abort = 1;
         }
-        __syncthreads();
-        bu = s_mu[buf];
-        bj = s_mj[buf];
-        if (bj == -2) break;
       }
-      const int m = bj >= 0 ? key_index(bj) : -1;
-      if (m < 0 && cid == 0 && threadIdx.x == 0) set_error(err, kErrArg);   // no instance can take it
-      // the wave holding the winner writes the outputs
-      const bool mine = m >= 0 ? c.j == bj : (cid == 0 && wid == 0);
-      if (mine && ln == 0) {
-        const int64_t o = (int64_t)z * N + i;
-        choice[o] = m;
-        if (chosen_ttft) chosen_ttft[o] = c.ttft;
-        if (utility && m >= 0) utility[o] = c.eq2;
+      const int m = holder && xok && bj >= 0 ? key_index(bj) : -1;
+      if (holder && xok) {
+        if (m < 0 && cid == 0 && (G > 1 || wid == 0) && ln == 0)
+          set_error(err, kErrArg);   // no instance can take it
+        // the wave holding the winner writes the outputs
+        const bool mine = m >= 0 ? c.j == bj : (cid == 0 && wid == 0);
+        if (mine && ln == 0) {
+          const int64_t o = (int64_t)z * N + i;
+          choice[o] = m;
+          if (chosen_ttft) chosen_ttft[o] = c.ttft;
+          if (utility && m >= 0) utility[o] = c.eq2;
+        }
       }
       if (own) {
         lim_commit_advance<KS, TRK>(Q, e, j == m, p, dq, tn, S.qcap, max_iters, err, tags,
