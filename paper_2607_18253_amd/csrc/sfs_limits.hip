@@ -303,16 +303,21 @@ __global__ __launch_bounds__(W * kWave) void k_ltrace_cl(LAR_TRACE_PARAMS, DevLi
       if (ln == 0) { s_u[buf][wid] = c.u; s_j[buf][wid] = c.j; }
       __syncthreads();
       if (s_abort) break;   // an exchange failed on the previous query
-      double bu = 0.0;
-      int bj = -1;
-      if (ln < nw) { bu = s_u[buf][ln]; bj = s_j[buf][ln]; }
-      lane_best(bu, bj, nw);
-      // Only the wave holding the workgroup's best (wave 0 when the workgroup has no
-      // candidate) can hold the query's winner: with several workgroups it alone
-      // exchanges with the others, while the other waves (not chosen) go on.
-      int holder = 1, xok = 1;
+      // Lane v reads wave v's candidate.  The order is total, so the wave whose
+      // candidate no other beats holds the workgroup's best (wave 0 when the workgroup
+      // has no candidate); only it can hold the query's winner: with several
+      // workgroups it alone exchanges with the others, while the other waves (not
+      // chosen) go on.
+      double vu = 0.0;
+      int vj = -1;
+      if (ln < nw) { vu = s_u[buf][ln]; vj = s_j[buf][ln]; }
+      const bool any = ballot(vj >= 0) != 0;
+      const bool beaten = ballot(better(vu, vj, c.u, c.j)) != 0;
+      const int holder = any ? (c.j >= 0 && !beaten ? 1 : 0) : (wid == 0 ? 1 : 0);
+      double bu = holder && any ? c.u : 0.0;
+      int bj = holder && any ? c.j : -1;
+      int xok = 1;
       if (G > 1) {
-        holder = bj >= 0 ? (c.j == bj ? 1 : 0) : (wid == 0 ? 1 : 0);
         if (holder && !cluster_exchange(bu, bj, i, G, cid, xs, err, sc)) {
           xok = 0;   // every wave leaves after the next workgroup barrier
           if (ln == 0) s_abort = 1;
@@ -320,10 +325,10 @@ __global__ __launch_bounds__(W * kWave) void k_ltrace_cl(LAR_TRACE_PARAMS, DevLi
       }
       const int m = holder && xok && bj >= 0 ? key_index(bj) : -1;
       if (holder && xok) {
-        if (m < 0 && cid == 0 && (G > 1 || wid == 0) && ln == 0)
+        if (bj == -1 && cid == 0 && wid == 0 && ln == 0)
           set_error(err, kErrArg);   // no instance can take it
         // the wave holding the winner writes the outputs
-        const bool mine = m >= 0 ? c.j == bj : (cid == 0 && wid == 0);
+        const bool mine = m >= 0 || (bj == -1 && cid == 0 && wid == 0);
         if (mine && ln == 0) {
           const int64_t o = (int64_t)z * N + i;
           choice[o] = m;

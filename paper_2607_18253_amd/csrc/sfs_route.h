@@ -246,7 +246,10 @@ __device__ __forceinline__ void cand_take(Cand& c, double u, int k, double ttft,
 // unless the host sets another bound): a member that never posts, or an error
 // raised by another member, ends the trace with kErrSync instead of a hang.  Two slot
 // sets suffice: a member posts query i + 2 only after every member has posted i + 1,
-// i.e. has finished reading the posts of i.
+// i.e. has finished reading the posts of i.  On return j is the caller's own key if
+// its post is the scenario's best, -1 if no member has a candidate, and kOtherBest
+// otherwise (u is left as posted).
+constexpr int kOtherBest = -2;
 __device__ __forceinline__ bool cluster_exchange(double& u, int& j, int i, int G, int cid,
                                                  uint64_t* xs, int32_t* err, SyncCtl sc) {
   const int ln = lane_id();
@@ -298,15 +301,17 @@ __device__ __forceinline__ bool cluster_exchange(double& u, int& j, int i, int G
       }
     }
   }
-  double bu = 0.0;
-  int bj = -1;
+  // The order is total: the caller's post is the scenario's best when no other post
+  // beats it.
+  double pu = 0.0;
+  int pj = -1;
   if (ln < G) {
-    bu = __longlong_as_double((long long)((w0 & 0xffffffffull) | (w1 << 32)));
-    bj = (int)(uint32_t)w2;
+    pu = __longlong_as_double((long long)((w0 & 0xffffffffull) | (w1 << 32)));
+    pj = (int)(uint32_t)w2;
   }
-  lane_best(bu, bj, G);
-  u = bu;
-  j = bj;
+  const bool any = ballot(pj >= 0) != 0;
+  const bool beaten = ballot(better(pu, pj, u, j)) != 0;
+  j = !any ? -1 : (j >= 0 && !beaten ? j : kOtherBest);
   return true;
 }
 
