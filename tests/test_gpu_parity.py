@@ -223,6 +223,40 @@ def test_trace_query_block_boundaries(n_q):
     ctx.close()
 
 
+def _identical_empty_pool(seed, n_inst, n_q, n_scen):
+    """A tiny workload whose instances are identical and empty and share one
+    accuracy / cost column: the utilities of instances in the same state tie exactly."""
+    import dataclasses
+    wl = make_tiny_workload(seed, n_inst=n_inst, max_res=1, n_q=n_q, n_scen=n_scen,
+                            dyadic=True, budget=(6, 6), max_seqs=(2, 2))
+    same = {f: np.full_like(getattr(wl, f), getattr(wl, f)[0])
+            for f in ("a", "b", "c", "d", "e", "budget", "max_seqs")}
+    return dataclasses.replace(
+        wl, **same, col=np.zeros(n_inst, np.int32), offsets=np.zeros(n_inst + 1, np.int32),
+        rem_prefill=np.zeros(0, np.int32), rem_decode=np.zeros(0, np.int32),
+        context=np.zeros(0, np.int32), clock_ms=np.zeros(n_inst))
+
+
+@pytest.mark.parametrize("n_inst", [13, 40])
+def test_trace_ties_across_workgroups(n_inst):
+    """Every query's best utility is shared by all instances in the same state, so the
+    lowest index among them must win: within a workgroup (one comparison and a ballot
+    over its waves) and across workgroups (one over the posts) -- 13 instances are 4
+    workgroups of 4 waves, 40 are 10; two scenarios."""
+    wl = _identical_empty_pool(31 + n_inst, n_inst, 120, 2)
+    assert _tail_k(wl) <= 64   # the clustered kernel
+    choice, chosen, util, ctx = gpu_trace(wl, queue_cap=10 ** 4)
+    for z in range(wl.n_scen):
+        ref = O.trace(wl, scenario=z, queue_cap=10 ** 4)
+        np.testing.assert_array_equal(choice[z], ref.choice)
+        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen))
+        np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
+        assert_state_equal(ctx, z, ref)
+        # ties did decide: some query went to a non-zero index while a lower one tied
+        assert len(set(ref.choice.tolist())) > 1
+    ctx.close()
+
+
 def test_trace_c1_full():
     wl = make_workload("c1")
     choice, chosen, util, ctx = gpu_trace(wl)
