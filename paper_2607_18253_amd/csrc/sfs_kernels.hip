@@ -20,7 +20,7 @@
 //   k_trace_mem the same trace with the states in HBM, for pools too large for LDS.
 //   k_drain, k_track_begin, k_track_end  first-token tracking around a trace
 //            (realised TTFT of each query in the replay).
-//   k_stats  one block per scenario: means in query order, nearest-rank p50/p99.
+//   k_stats  two blocks per scenario: means in query order; nearest-rank p50/p99.
 //   k_targets, k_ontime  TTFT targets per query; OnTimeUtility (Eq. 4).
 // Under scheduler limits the same calls dispatch to sfs_limits.hip.
 #include "sfs_device.h"
@@ -1387,83 +1387,114 @@ __device__ __forceinline__ double key_value(uint64_t k) {
   return __longlong_as_double((long long)b);
 }
 
-// k-th smallest key (0-based) of x[0..n) by 8-bit radix select, block-wide.
-__device__ uint64_t block_select(const double* x, int n, int kth, unsigned* hist) {
-  uint64_t prefix = 0, mask = 0;
-  int rank = kth;
-  for (int shift = 56; shift >= 0; shift -= 8) {
-    for (int b = threadIdx.x; b < 256; b += blockDim.x) hist[b] = 0;
-    __syncthreads();
-    for (int i = threadIdx.x; i < n; i += blockDim.x) {
-      const uint64_t key = okey(x[i]);
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 0xff], 1u);
-    }
-    __syncthreads();
-    __shared__ int s_digit, s_rank;
-    if (threadIdx.x == 0) {
-      int r = rank, dgt = 0;
-      for (; dgt < 256; ++dgt) {
-        if (r < (int)hist[dgt]) break;
-        r -= (int)hist[dgt];
-      }
-      s_digit = dgt;
-      s_rank = r;
-    }
-    __syncthreads();
-    prefix |= (uint64_t)s_digit << shift;
-    mask |= (uint64_t)0xff << shift;
-    rank = s_rank;
-    __syncthreads();
+// Adds 1 to hist[d] for every lane of the wave with `on`, one atomic per wave when
+// all of them carry the same digit (the usual case in the high digits of values of
+// one magnitude, where per-lane atomics would all hit one counter).
+__device__ __forceinline__ void hist_add(unsigned* hist, int d, bool on) {
+  const uint64_t act = ballot(on);
+  if (act == 0) return;
+  const int l0 = __builtin_ctzll(act);
+  const int d0 = __builtin_amdgcn_readlane(d, l0);
+  if (ballot(on && d == d0) == act) {
+    if (lane_id() == l0) atomicAdd(&hist[d0], (unsigned)popc(act));
+  } else if (on) {
+    atomicAdd(&hist[d], 1u);
   }
-  return prefix;
 }
 
-__global__ __launch_bounds__(256) void k_stats(int N, int I, const int32_t* choice,
-                                              const double* chosen_ttft, const double* acc,
-                                              const double* cost, int n_cols,
-                                              const int32_t* col, const double* w_cost,
-                                              double* out) {
-  __shared__ unsigned hist[256];
-  const int z = blockIdx.x;
+// The k0-th and k1-th smallest keys (0-based) of x[0..n) by 8-bit radix select,
+// block-wide: both selections share each pass over x (one histogram each).
+__device__ void block_select2(const double* x, int n, int k0, int k1, unsigned* h0,
+                              unsigned* h1, uint64_t& r0, uint64_t& r1) {
+  __shared__ int s_dig[2], s_rank[2];
+  uint64_t p0 = 0, p1 = 0, mask = 0;
+  int q0 = k0, q1 = k1;
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    for (int b = threadIdx.x; b < 256; b += blockDim.x) { h0[b] = 0; h1[b] = 0; }
+    __syncthreads();
+    for (int base = 0; base < n; base += blockDim.x) {
+      const int i = base + (int)threadIdx.x;
+      uint64_t key = 0;
+      if (i < n) key = okey(x[i]);
+      const int d = (int)((key >> shift) & 0xff);
+      hist_add(h0, d, i < n && (key & mask) == p0);
+      hist_add(h1, d, i < n && (key & mask) == p1);
+    }
+    __syncthreads();
+    if (threadIdx.x < 2) {   // thread 0 walks h0, thread 1 h1
+      const unsigned* h = threadIdx.x == 0 ? h0 : h1;
+      int r = threadIdx.x == 0 ? q0 : q1, dgt = 0;
+      for (; dgt < 256; ++dgt) {
+        if (r < (int)h[dgt]) break;
+        r -= (int)h[dgt];
+      }
+      s_dig[threadIdx.x] = dgt;
+      s_rank[threadIdx.x] = r;
+    }
+    __syncthreads();
+    p0 |= (uint64_t)s_dig[0] << shift;
+    p1 |= (uint64_t)s_dig[1] << shift;
+    mask |= (uint64_t)0xff << shift;
+    q0 = s_rank[0];
+    q1 = s_rank[1];
+    __syncthreads();
+  }
+  r0 = p0;
+  r1 = p1;
+}
+
+// Per scenario z, two blocks: block 2z folds the means in query order (thread 0, the
+// values staged in LDS by all threads), block 2z + 1 selects the nearest-rank p50 and
+// p99 of the chosen TTFTs; the two run side by side.
+__global__ __launch_bounds__(1024) void k_stats(int N, int I, const int32_t* choice,
+                                               const double* chosen_ttft, const double* acc,
+                                               const double* cost, int n_cols,
+                                               const int32_t* col, const double* w_cost,
+                                               double* out) {
+  const int z = blockIdx.x >> 1;
   const int32_t* ch = choice + (int64_t)z * N;
   const double* tt = chosen_ttft + (int64_t)z * N;
-  __shared__ double s_a[256], s_c[256];
-  const double wc = w_cost[z];
-  double sa = 0.0, sc = 0.0, su = 0.0;
-  for (int base = 0; base < N; base += 256) {
-    const int i = base + (int)threadIdx.x;
-    if (i < N) {
-      const int cj = ch[i];
-      if (cj >= 0 && cj < I) {
-        const int c = col[cj];
-        s_a[threadIdx.x] = acc[(int64_t)i * n_cols + c];
-        s_c[threadIdx.x] = cost[(int64_t)i * n_cols + c];
-      } else {   // not a routed instance: poison the means
-        s_a[threadIdx.x] = __builtin_nan("");
-        s_c[threadIdx.x] = __builtin_nan("");
+  if ((blockIdx.x & 1) == 0) {
+    __shared__ double s_a[1024], s_c[1024];
+    const double wc = w_cost[z];
+    double sa = 0.0, sc = 0.0, su = 0.0;
+    for (int base = 0; base < N; base += blockDim.x) {
+      const int i = base + (int)threadIdx.x;
+      if (i < N) {
+        const int cj = ch[i];
+        if (cj >= 0 && cj < I) {
+          const int c = col[cj];
+          s_a[threadIdx.x] = acc[(int64_t)i * n_cols + c];
+          s_c[threadIdx.x] = cost[(int64_t)i * n_cols + c];
+        } else {   // not a routed instance: poison the means
+          s_a[threadIdx.x] = __builtin_nan("");
+          s_c[threadIdx.x] = __builtin_nan("");
+        }
       }
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {   // left folds in query order
-      const int m = N - base < 256 ? N - base : 256;
-      for (int r = 0; r < m; ++r) {
-        const double a = s_a[r], co = s_c[r];
-        sa = __dadd_rn(sa, a);
-        sc = __dadd_rn(sc, co);
-        su = __dadd_rn(su, __dsub_rn(a, __dmul_rn(wc, co)));
+      __syncthreads();
+      if (threadIdx.x == 0) {   // left folds in query order
+        const int m = N - base < (int)blockDim.x ? N - base : (int)blockDim.x;
+        for (int r = 0; r < m; ++r) {
+          const double a = s_a[r], co = s_c[r];
+          sa = __dadd_rn(sa, a);
+          sc = __dadd_rn(sc, co);
+          su = __dadd_rn(su, __dsub_rn(a, __dmul_rn(wc, co)));
+        }
       }
+      __syncthreads();
     }
-    __syncthreads();
+    if (threadIdx.x == 0) {
+      out[z * 5 + 0] = __ddiv_rn(sa, (double)N);
+      out[z * 5 + 1] = __ddiv_rn(sc, (double)N);
+      out[z * 5 + 2] = __ddiv_rn(su, (double)N);
+    }
+    return;
   }
-  if (threadIdx.x == 0) {
-    out[z * 5 + 0] = __ddiv_rn(sa, (double)N);
-    out[z * 5 + 1] = __ddiv_rn(sc, (double)N);
-    out[z * 5 + 2] = __ddiv_rn(su, (double)N);
-  }
+  __shared__ unsigned h50[256], h99[256];
   const int k50 = (int)(((int64_t)50 * N + 99) / 100 - 1);
   const int k99 = (int)(((int64_t)99 * N + 99) / 100 - 1);
-  const uint64_t v50 = block_select(tt, N, k50, hist);
-  const uint64_t v99 = block_select(tt, N, k99, hist);
+  uint64_t v50, v99;
+  block_select2(tt, N, k50, k99, h50, h99, v50, v99);
   if (threadIdx.x == 0) {
     out[z * 5 + 3] = key_value(v50);
     out[z * 5 + 4] = key_value(v99);
@@ -1765,7 +1796,7 @@ hipError_t launch_clear_error(const LaunchEnv& env) {
 hipError_t launch_stats(const LaunchEnv& env, int N, const int32_t* choice,
                         const double* chosen_ttft, const double* acc, const double* cost,
                         int n_cols, const double* w_cost, double* out) {
-  hipLaunchKernelGGL(k_stats, dim3(env.Z), dim3(256), 0, env.stream, N, env.I, choice, chosen_ttft,
+  hipLaunchKernelGGL(k_stats, dim3(2 * env.Z), dim3(1024), 0, env.stream, N, env.I, choice, chosen_ttft,
                      acc, cost, n_cols, env.P.col, w_cost, out);
   return hipGetLastError();
 }
