@@ -9,7 +9,7 @@
 //   k_est    one thread per (scenario, instance, chunk of queries), instance
 //            fastest: each query's own continuation from the shared trajectory
 //            (Sec. 4.1, the first-output-token batch and the TTFT sum).
-//   k_route  one block per (scenario, query) row: Lagrangian utility and argmax
+//   k_route  one wave per (scenario, query) row: Lagrangian utility and argmax
 //            with ties to the lowest instance (Sec. 3, Eq. 2).
 //   k_commit one wave per (scenario, instance): append the routed query, then
 //            replay batches until the clock reaches the next arrival.
@@ -244,9 +244,9 @@ __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double
                                               const double* tau, int32_t* choice,
                                               double* chosen_ttft, double* utility,
                                               int64_t out_zstride, int out_q0, int32_t* err) {
-  __shared__ double s_u[256 / kWave];
-  __shared__ int s_j[256 / kWave];
-  const int row = blockIdx.x;   // z * Q + q
+  const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
+  const int row = (int)blockIdx.x * (int)(blockDim.x / kWave) + wid;   // z * Q + q
+  if ((int64_t)row >= (int64_t)Z * Q) return;   // (no barrier below: a whole wave leaves)
   const int z = row / Q;
   const int q = row % Q;
   const double wc = w_cost[z];
@@ -257,22 +257,17 @@ __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double
   const double tq = tau ? tau[q] : 0.0;
   double bu = 0.0;
   int bj = -1;
-  for (int j = threadIdx.x; j < I; j += blockDim.x) {
+  for (int j = lane_id(); j < I; j += kWave) {
     const int c = col[j];
     const double eq2 = __dsub_rn(arow[c], __dmul_rn(wc, crow[c]));
     int k;
     const double u = cand_value(eq2, trow[j], wl, tau, tq, j, &k);
     if (better(u, k, bu, bj)) { bu = u; bj = k; }
   }
-  // the wave's best (DPP; `better` is a total order, so the combining order does not
-  // matter), then the block's over its waves
+  // the row's best over the lanes (DPP; `better` is a total order, so the combining
+  // order does not matter)
   lane_best(bu, bj, kWave);
-  const int wid = uni((int)(threadIdx.x / kWave));   // wave-uniform: keeps per-wave data in SGPRs
-  if (lane_id() == 0) { s_u[wid] = bu; s_j[wid] = bj; }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int w = 1; w < (int)(blockDim.x / kWave); ++w)
-      if (better(s_u[w], s_j[w], bu, bj)) { bu = s_u[w]; bj = s_j[w]; }
+  if (lane_id() == 0) {
     const int64_t o = (int64_t)z * out_zstride + out_q0 + q;
     bj = bj >= 0 ? key_index(bj) : -1;
     if (bj < 0) set_error(err, kErrArg);   // no instance can take the query
@@ -1752,9 +1747,12 @@ hipError_t launch_route(const LaunchEnv& env, int Q, const double* ttft, int64_t
                         const double* acc, const double* cost, int n_cols, const double* w_cost,
                         const double* w_lat, const double* tau, int32_t* choice,
                         double* chosen_ttft, double* utility, int64_t out_zstride, int out_q0) {
-  // one block per row; as many waves as the row needs, up to four
-  const int waves = env.I <= kWave ? 1 : env.I >= 4 * kWave ? 4 : (env.I + kWave - 1) / kWave;
-  hipLaunchKernelGGL(k_route, dim3(env.Z * Q), dim3(waves * kWave), 0, env.stream, env.Z, Q, env.I, ttft,
+  // one wave per row, four rows per block
+  const int64_t rows = (int64_t)env.Z * Q;
+  if (rows == 0) return hipSuccess;
+  const int waves = rows < 4 ? (int)rows : 4;
+  hipLaunchKernelGGL(k_route, dim3((unsigned)((rows + waves - 1) / waves)), dim3(waves * kWave), 0,
+                     env.stream, env.Z, Q, env.I, ttft,
                      ttft_zstride, acc, cost, n_cols, env.P.col, w_cost, w_lat, tau, choice,
                      chosen_ttft, utility, out_zstride, out_q0, env.err);
   return hipGetLastError();
