@@ -257,12 +257,26 @@ __global__ __launch_bounds__(256) void k_route(int Z, int Q, int I, const double
   const double tq = tau ? tau[q] : 0.0;
   double bu = 0.0;
   int bj = -1;
-  for (int j = lane_id(); j < I; j += kWave) {
-    const int c = col[j];
-    const double eq2 = __dsub_rn(arow[c], __dmul_rn(wc, crow[c]));
-    int k;
-    const double u = cand_value(eq2, trow[j], wl, tau, tq, j, &k);
-    if (better(u, k, bu, bj)) { bu = u; bj = k; }
+  // four instances per lane and pass, their loads issued before any is used
+  for (int j0 = lane_id(); j0 < I; j0 += 4 * kWave) {
+    int cc[4];
+    double tt[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int j = j0 + u * kWave;
+      cc[u] = j < I ? col[j] : 0;
+      tt[u] = j < I ? trow[j] : 0.0;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int j = j0 + u * kWave;
+      if (j < I) {
+        const double eq2 = __dsub_rn(arow[cc[u]], __dmul_rn(wc, crow[cc[u]]));
+        int k;
+        const double v = cand_value(eq2, tt[u], wl, tau, tq, j, &k);
+        if (better(v, k, bu, bj)) { bu = v; bj = k; }
+      }
+    }
   }
   // the row's best over the lanes (DPP; `better` is a total order, so the combining
   // order does not matter)
