@@ -386,6 +386,39 @@ def test_trace_c5_all_scenarios_prefix_and_stats():
     ctx.close()
 
 
+@pytest.mark.parametrize("n", [1, 2, 3, 100, 1023, 1024, 1025, 4097])
+def test_stats_ragged_lengths_and_ties(n):
+    """The statistics kernel (means folded in query order by one block, p50 / p99 by
+    radix passes in another) on trace lengths around its 1024-query chunks, with TTFTs
+    that all tie (scenario 0), take a few values (1), or differ only in their low bits
+    over several magnitudes (2), against the oracle bit for bit."""
+    rng = np.random.default_rng(n)
+    I, Z, n_cols = 5, 3, 3
+    col = np.array([0, 1, 2, 0, 1], np.int32)
+    ctx = LarContext(Z, I, max_seqs_cap=4, queue_cap=4, max_prompt=16)
+    ones = np.ones(I)
+    ctx.load_state(a=ones, b=ones, c=ones, d=0 * ones, e=0 * ones, budget=np.full(I, 8, np.int32),
+                   max_seqs=np.full(I, 4, np.int32), col=col, offsets=np.zeros(I + 1, np.int32),
+                   rem_prefill=np.zeros(0, np.int32), rem_decode=np.zeros(0, np.int32),
+                   context=np.zeros(0, np.int32), clock_ms=np.zeros(I))
+    choice = rng.integers(0, I, size=(Z, n)).astype(np.int32)
+    ttft = np.empty((Z, n))
+    ttft[0] = 157.25
+    ttft[1] = rng.choice([3.5, 40.0, 40.0, 1200.125], size=n)
+    base = rng.choice([0.75, 12.0, 480.0, 9000.0], size=n)
+    ttft[2] = base + rng.integers(0, 64, size=n) * np.spacing(base)
+    acc, cost = rng.random((n, n_cols)), rng.random((n, n_cols))
+    w_cost = np.array([0.0, 0.5, 2.0])
+    st = ctx.stats(T(choice, torch.int32), T(ttft, torch.float64), T(acc, torch.float64),
+                   T(cost, torch.float64), T(w_cost, torch.float64))
+    ctx.sync()
+    st = st.cpu().numpy()
+    for z in range(Z):
+        want = O.stats(choice[z], ttft[z], acc, cost, col, w_cost[z])
+        np.testing.assert_array_equal(bits(st[z]), bits(want), err_msg=f"scenario {z}")
+    ctx.close()
+
+
 @pytest.mark.parametrize("name", ["c2", "c7"])
 def test_checkpoint_resume_identical(name):
     """read_state -> load_state into a fresh context, continue: same results (c7: under
