@@ -302,15 +302,15 @@ __global__ __launch_bounds__(W * kWave) void k_ltrace_cl(LAR_TRACE_PARAMS, DevLi
       const int buf = i & 1;
       if (ln == 0) { s_u[buf][wid] = c.u; s_j[buf][wid] = c.j; }
       __syncthreads();
+      double vu = 0.0;   // (read together with the abort flag: one LDS round trip)
+      int vj = -1;
+      if (ln < nw) { vu = s_u[buf][ln]; vj = s_j[buf][ln]; }
       if (s_abort) break;   // an exchange failed on the previous query
-      // Lane v reads wave v's candidate.  The order is total, so the wave whose
+      // Lane v holds wave v's candidate.  The order is total, so the wave whose
       // candidate no other beats holds the workgroup's best (wave 0 when the workgroup
       // has no candidate); only it can hold the query's winner: with several
       // workgroups it alone exchanges with the others, while the other waves (not
       // chosen) go on.
-      double vu = 0.0;
-      int vj = -1;
-      if (ln < nw) { vu = s_u[buf][ln]; vj = s_j[buf][ln]; }
       const bool any = ballot(vj >= 0) != 0;
       const bool beaten = ballot(better(vu, vj, c.u, c.j)) != 0;
       const int holder = any ? (c.j >= 0 && !beaten ? 1 : 0) : (wid == 0 ? 1 : 0);
