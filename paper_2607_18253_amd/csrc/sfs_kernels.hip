@@ -598,6 +598,7 @@ struct FCache {
   int sD1;
   int64_t sC1;
   int snf;         // summary: the next batch in which a decoding request finishes
+                   // (-1: not taken yet; replay_summary takes it from the state in LDS)
   int g;           // batch counter of F
   double E;        // clock folded up to F
   int aP, aD, left;
@@ -1046,7 +1047,7 @@ __device__ __forceinline__ void take_summary(FCache& fc, const Queue<KS>& S, con
   const typename Queue<KS>::Tail tl = S.tail_begin(e);
   fc.sD1 = (int)tl.D;
   fc.sC1 = e.need_C ? tl.c0 + tl.D * (int64_t)(S.g + 1) : 0;
-  fc.snf = S.next_finish();
+  fc.snf = -1;   // taken when a replay on the summary first needs it
 }
 
 // The replay of a summarised state with an empty prefill list up to t, when it only
@@ -1067,6 +1068,15 @@ __device__ __forceinline__ bool replay_summary(FCache& fc, const QEnv& e, LdsQue
     if (lane_id() == 0) SL.clock = t;
     __builtin_amdgcn_wave_barrier();
     return true;
+  }
+  if (fc.snf < 0) {   // the next decode finish of the summarised state, from its slots in LDS
+    int m = 0x7fffffff;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int dl = SL.dl[s * kWave + lane_id()];
+      if (dl > fc.g) m = min(m, dl);
+    }
+    fc.snf = wave_min(m);
   }
   const int D = fc.aD;
   double c = clk;
