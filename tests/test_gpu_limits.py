@@ -296,6 +296,35 @@ def test_mixed_context_limits():
     ctx.close()
 
 
+def test_mixed_context_limits_whole_workgroup():
+    """Twelve instances, three workgroups of four: the first workgroup's instances
+    have a small context limit and the best accuracy, so for prompts beyond it that
+    whole workgroup has no candidate and posts none while the others do; for shorter
+    prompts it usually holds the winner.  Trace under both objectives against the
+    oracle."""
+    rng = np.random.default_rng(17)
+    for seed in range(40, 80):
+        wl = make_tiny_sched_workload(seed, n_inst=12, n_q=60, max_res=3)
+        wl.sched[:, 1] = 0                 # no KV cache (the limit then needs no blocks)
+        wl.sched[:, 3] = 64
+        wl.sched[:4, 3] = 24
+        if all(len(rp) == 0 or (rp + cx).max() < wl.sched[j, 3]
+               for j, (rp, _, cx) in ((j, wl.instance_requests(j)) for j in range(12))):
+            break
+    else:
+        pytest.fail("no seed whose residents fit the limits")
+    wl.col[:] = np.arange(12) % wl.acc.shape[1]
+    wl.acc[:, :] = 0.1
+    wl.acc[:, wl.col[0]] = 0.9
+    wl.col[4:] = (wl.col[0] + 1) % wl.acc.shape[1]   # the first workgroup alone has the best column
+    wl.q_prefill[:] = rng.integers(1, 40, wl.n_q)    # many do not fit the first workgroup's limit
+    wl.max_prompt = 64
+    assert (wl.q_prefill >= 24).sum() > 10 and (wl.q_prefill < 24).sum() > 10
+    tau = O.ttft_targets(wl.q_prefill, wl.tau_u_ms, wl.tau_v)
+    for t in (None, tau):
+        _check(wl, _trace(wl, tau=t), tau=t)
+
+
 def test_limits_reload_repeat():
     """The benchmark's step under limits: reload the snapshot, replay to the first
     arrival, trace; two steps give the oracle's results both times."""
