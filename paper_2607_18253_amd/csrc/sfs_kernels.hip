@@ -663,29 +663,57 @@ __device__ __forceinline__ void tail_readonly(FCache& fc, const Queue<KS>& w, co
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   int far_n = 0;
   int64_t far_c = 0;
-#pragma unroll
-  for (int s = 0; s < KS; ++s) {
-    const int kl = w.dl[s] - g1;   // >= 1: survives the admission batch
-    if (kl >= kmax) {
-      ++far_n;
-      far_c += w.dc[s];
-    } else if (kl >= 1) {
-      atomicAdd(&cnt[kl - 1], 1);
-      if (need_C) atomicAdd(&csum[kl - 1], (unsigned long long)(int64_t)w.dc[s]);
-    }
-  }
   const int idx = ln - w.woff;
-  if (idx >= 0 && idx < w.nwin) {   // rd >= 1
-    const int64_t c0 = (int64_t)(w.wcx + w.wrp) - g1;
-    if (w.wrd >= kmax) {
-      ++far_n;
-      far_c += c0;
-    } else {
-      atomicAdd(&cnt[w.wrd - 1], 1);
-      if (need_C) atomicAdd(&csum[w.wrd - 1], (unsigned long long)c0);
+  if constexpr (KS >= 8) {
+    // wide queues (the tail is taken on most chosen visits): the far requests are
+    // counted by ballots and their cx0 summed per lane with selects; only the near
+    // ones branch, to their bins
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int kl = w.dl[s] - g1;   // >= 1: survives the admission batch
+      const bool far = kl >= kmax;
+      far_n += popc(ballot(far));
+      if (need_C) far_c += far ? (int64_t)w.dc[s] : 0;
+      if (kl >= 1 && !far) {
+        atomicAdd(&cnt[kl - 1], 1);
+        if (need_C) atomicAdd(&csum[kl - 1], (unsigned long long)(int64_t)w.dc[s]);
+      }
     }
+    const bool ent = idx >= 0 && idx < w.nwin;   // rd >= 1
+    const bool efar = ent && w.wrd >= kmax;
+    far_n += popc(ballot(efar));
+    if (need_C) far_c += efar ? (int64_t)(w.wcx + w.wrp) - g1 : 0;
+    if (ent && !efar) {
+      atomicAdd(&cnt[w.wrd - 1], 1);
+      if (need_C) atomicAdd(&csum[w.wrd - 1], (unsigned long long)((int64_t)(w.wcx + w.wrp) - g1));
+    }
+    far_n = uni(far_n);
+  } else {
+    // narrow queues take the tail rarely; this form keeps their kernels' register
+    // allocation (the form above measured slower there through it)
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int kl = w.dl[s] - g1;
+      if (kl >= kmax) {
+        ++far_n;
+        far_c += w.dc[s];
+      } else if (kl >= 1) {
+        atomicAdd(&cnt[kl - 1], 1);
+        if (need_C) atomicAdd(&csum[kl - 1], (unsigned long long)(int64_t)w.dc[s]);
+      }
+    }
+    if (idx >= 0 && idx < w.nwin) {
+      const int64_t c0 = (int64_t)(w.wcx + w.wrp) - g1;
+      if (w.wrd >= kmax) {
+        ++far_n;
+        far_c += c0;
+      } else {
+        atomicAdd(&cnt[w.wrd - 1], 1);
+        if (need_C) atomicAdd(&csum[w.wrd - 1], (unsigned long long)c0);
+      }
+    }
+    far_n = wave_sum32(far_n);
   }
-  far_n = wave_sum32(far_n);
   if (need_C) far_c = wave_sum64(far_c);
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -713,6 +741,70 @@ struct VisitOut {
   bool direct;
 };
 
+// F's admission batch stepped from the cache, for F + query (the list's last entry,
+// p prompt tokens) with the whole list in the window: the batch serves every entry
+// of F in full and gives the query min(p, left) tokens, so its features are the
+// summary's plus the query's chunk, and the decoders alive after it are those of
+// tail batch 1 (lane 0), plus the query when its prefill completes.  The completed
+// entries take free decode slots in the order Queue::step gives them (staged in
+// LDS), and the window and list move as there.  The result is step()'s.
+template <int KS>
+__device__ __forceinline__ void admission_step(Queue<KS>& wk, const FCache& fc, const QEnv& e,
+                                               int p, double& clk) {
+  const int ln = lane_id();
+  const int g1 = wk.g + 1;
+  const int ch = min(p, fc.left);
+  clk = __dadd_rn(clk, batch_time(e.k, fc.aP + ch, fc.aD, fc.aC,
+                                  e.need_A ? fc.aA + (int64_t)ch * (ch + 1) / 2 : 0));
+  const bool qfull = ch == p;
+  const int n_full = wk.n_pre - (qfull ? 0 : 1);
+  int* stg = e.stg;
+  const int idx = ln - wk.woff;
+  if (idx >= 0 && idx < n_full) {
+    stg[idx] = g1 + wk.wrd;
+    stg[kWave + idx] = wk.wcx + wk.wrp - g1;
+    stg[2 * kWave + idx] = wk.wseq;
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  int placed = 0;
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    if (placed < n_full) {
+      const bool fr = wk.dl[s] <= g1;
+      const uint64_t fm = ballot(fr);
+      const int r = placed + mbcnt(fm);
+      if (fr && r < n_full) {
+        wk.dl[s] = stg[r]; wk.dc[s] = stg[kWave + r]; wk.ds[s] = stg[2 * kWave + r];
+      }
+      placed += popc(fm);
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  const int D1 = __builtin_amdgcn_readlane(fc.tD, 0);
+  wk.n_dec = D1 + (qfull ? 1 : 0);
+  if (e.need_C)
+    wk.c0sum = read_lane_i64(fc.tC, 0) - (int64_t)D1 * g1 + (qfull ? (int64_t)(p - g1) : 0);
+  wk.woff += n_full;
+  wk.nwin -= n_full;
+  wk.head += n_full;
+  if (wk.head >= e.rcap) wk.head -= e.rcap;
+  wk.n_pre -= n_full;
+  if (qfull) {
+    wk.n_part = 0;
+    wk.pre_sum = 0;
+  } else {
+    if (ln == wk.woff) {
+      wk.wrp -= ch;
+      wk.wcx += ch;
+    }
+    wk.n_part = 1;
+    wk.pre_sum = p - ch;
+  }
+  wk.g = g1;
+}
+
 // F + query (p prompt tokens, rdq >= 1 decodes) walked towards its next admission
 // point without stepping the background batch by batch.  F's admission batch is
 // stepped: it serves every list entry of F in full and gives the query its first
@@ -733,11 +825,14 @@ __device__ __forceinline__ void walk_fast(Queue<KS>& wk, const FCache& fc, const
   const Coef& kc = e.k;
   const int ln = lane_id();
   if (wk.tail_admitted_next(e) || n >= max_iters) return;
-  {
-    const StepOut o = wk.step(e);   // F's admission batch, with the query's first chunk
+  // F's admission batch, with the query's first chunk
+  if (wk.nwin == wk.n_pre) {
+    admission_step(wk, fc, e, p, clk);
+  } else {
+    const StepOut o = wk.step(e);
     clk = __dadd_rn(clk, batch_time(kc, o.P, o.D, o.C, o.A));
-    ++n;
   }
+  ++n;
   if (wk.tail_admitted_next(e)) return;
   const int gA = wk.g;
   // the query: the list's only entry, or decoding since the admission batch
