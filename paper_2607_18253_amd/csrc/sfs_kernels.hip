@@ -605,6 +605,7 @@ struct FCache {
   int64_t aC, aA;  // admission-batch background features
   int tD;          // lane k: decode tokens of tail batch k + 1
   int64_t tC;      // lane k: their context sum
+  int depth;       // tail batches held (lanes 0 .. depth - 1; at least the tail depth K)
 };
 
 __device__ __forceinline__ int64_t read_lane_i64(int64_t v, int l) {
@@ -729,6 +730,53 @@ __device__ __forceinline__ void tail_readonly(FCache& fc, const Queue<KS>& w, co
   if (need_C) c0 = suffix_sum64(c0);
   fc.tD = ln < kmax ? D : 0;
   fc.tC = need_C && ln < kmax ? c0 + (int64_t)D * (w.g + ln + 1) : 0;
+}
+
+// The tail of F' (F + query walked to its next admission point, g' = w.g) from F's
+// tail: F' holds F's background -- the same requests, decode-only after F's admission
+// batch -- plus the query, so its tail batch k is F's tail batch k + sh (sh = g' - g_F
+// batches between the two admission batches) plus the query's own term.  The query is
+// the list's last entry (all of its prefill in the admission batch, then rd decodes) or
+// a decoding request (its slot found by its sequence number).  F's tail must hold
+// sh + K batches; F' then holds sh fewer.
+template <int KS>
+__device__ __forceinline__ void tail_shift(FCache& fc, const Queue<KS>& w, const QEnv& e, int sh,
+                                           int seqq) {
+  const int ln = lane_id();
+  const int depth = fc.depth - sh;
+  const int src = min(ln + sh, kWave - 1);
+  int D = __shfl(fc.tD, src, kWave);
+  int64_t C = 0;
+  if (e.need_C) {
+    const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)(uint64_t)fc.tC, src, kWave);
+    const uint32_t hi = (uint32_t)__shfl((int)(uint32_t)((uint64_t)fc.tC >> 32), src, kWave);
+    C = (int64_t)(((uint64_t)hi << 32) | lo);
+  }
+  const int g1 = w.g + 1;   // the admission batch
+  int kl = 0;               // the query decodes in tail batches 1 .. kl
+  int64_t c0 = 0;           // its context in batch b is c0 + b - 1
+  if (w.n_pre > 0) {
+    const int q = w.woff + w.n_pre - 1;
+    kl = __builtin_amdgcn_readlane(w.wrd, q);
+    c0 = (int64_t)(__builtin_amdgcn_readlane(w.wcx, q) + __builtin_amdgcn_readlane(w.wrp, q)) - g1;
+  } else {
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const uint64_t m = ballot(w.ds[s] == seqq && w.dl[s] > w.g);
+      if (m) {
+        const int l = __builtin_ctzll(m);
+        kl = __builtin_amdgcn_readlane(w.dl[s], l) - g1;
+        c0 = __builtin_amdgcn_readlane(w.dc[s], l);
+      }
+    }
+  }
+  if (ln < kl) {
+    D += 1;
+    if (e.need_C) C += c0 + (int64_t)(w.g + ln + 1);
+  }
+  fc.tD = ln < depth ? D : 0;
+  fc.tC = e.need_C && ln < depth ? C : 0;
+  fc.depth = depth;
 }
 
 // What the estimate needs of the instance after a visit: its batch counter and
@@ -960,6 +1008,8 @@ __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv&
   double stop_t = tn;
   int64_t n = 0;
   int kk = -1;
+  int shift_g = -1;   // (wide queues) g of F when the walk starts from it, for the tail shift
+  int seqq = 0;
   for (;;) {
     bool stop;
     if (phase == kReplay) {
@@ -986,6 +1036,10 @@ __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv&
         const bool from_f = joined && fc.valid;
         if (from_f) {
           wk.from_lds(F);
+          if constexpr (KS >= 8) {
+            shift_g = fc.g;
+            seqq = wk.next_seq;
+          }
           wk.append(e, p, d);   // F shares the instance's ring: same slot, entry and tag
           clk = fc.E;
         } else if (!fc.valid) {
@@ -1017,9 +1071,21 @@ __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv&
         fc.valid = true;
         wk.to_lds(F);
         if (wk.nwin == wk.n_pre) {
-          tail_readonly(fc, wk, e, kmax);
+          if constexpr (KS >= 8) {
+            // (wide queues walk on most chosen visits: F's tail is shifted while it
+            // holds enough batches, else taken afresh to the full lane width)
+            if (shift_g >= 0 && fc.depth - (wk.g - shift_g) >= kmax) {
+              tail_shift(fc, wk, e, wk.g - shift_g, seqq);
+            } else {
+              tail_readonly(fc, wk, e, kWave);
+              fc.depth = kWave;
+            }
+          } else {
+            tail_readonly(fc, wk, e, kmax);
+          }
           break;
         }
+        if constexpr (KS >= 8) fc.depth = kmax;
         phase = kTail;   // step the admission batch, then record kmax decode-only batches
         kk = -1;
         continue;
@@ -1263,6 +1329,7 @@ __global__ __launch_bounds__(W * kWave) void k_trace_cl(LAR_TRACE_PARAMS, int G,
     fc[r].summ = false;
     fc[r].tD = 0;
     fc[r].tC = 0;
+    fc[r].depth = 0;
     if (j < I) {
       env[r] = make_env(S, pr, z * I + j, j, stage[wid]);
       Queue<KS> q;

@@ -663,6 +663,32 @@ def test_trace_fast_walk_tiny_pools(seed, flags):
     ctx.close()
 
 
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("flags", [0, 1])
+def test_trace_fast_walk_shifted_tails(seed, flags):
+    """Queues of 8 decode slots per lane, with a decode-only tail of only a few batches
+    (short prompts against budgets of 6..8 tokens): the tail of the admission point a
+    query is walked to is then taken from the previous one by a shift while the 64
+    held batches last, and afresh when they run out (every couple of dozen walks).
+    Long traces on two instances with 1..3-token decodes, so queries are still in the
+    list, decoding, or done at the new admission point; arrivals every 0.4 ms (a
+    growing backlog), 1.5 ms or 3 ms (the query often admitted at once, a shift of
+    zero batches); against the oracle, both first-token readings."""
+    wl = make_tiny_workload(900 + seed, n_inst=2, max_res=8, n_q=400, prompt=(1, 8),
+                            decode=(1, 3), budget=(6, 8), max_seqs=(1, 3),
+                            mean_gap_ms=(0.4, 1.5, 3.0)[seed % 3], n_scen=2,
+                            dyadic=(seed % 2 == 0))
+    assert _tail_k(wl) <= 4
+    choice, chosen, util, ctx = gpu_trace(wl, flags=flags, queue_cap=10 ** 4, max_seqs_cap=300)
+    for z in range(wl.n_scen):
+        ref = O.trace(wl, scenario=z, reading=flags, queue_cap=10 ** 4)
+        np.testing.assert_array_equal(choice[z], ref.choice)
+        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen))
+        np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
+        assert_state_equal(ctx, z, ref)
+    ctx.close()
+
+
 @pytest.mark.parametrize("reading", [0, 1])
 def test_exhaustive_tiny_states_one_context(reading):
     """Every tiny state of the oracle's exhaustive pins (up to 3 residents of every
