@@ -789,16 +789,18 @@ struct VisitOut {
   bool direct;
 };
 
-// F's admission batch stepped from the cache, for F + query (the list's last entry,
+// The admission batch of a summarised state (F, or the instance's own state under a
+// summary) stepped from the summary, for that state + query (the list's last entry,
 // p prompt tokens) with the whole list in the window: the batch serves every entry
-// of F in full and gives the query min(p, left) tokens, so its features are the
+// in full and gives the query min(p, left) tokens, so its features are the
 // summary's plus the query's chunk, and the decoders alive after it are those of
-// tail batch 1 (lane 0), plus the query when its prefill completes.  The completed
-// entries take free decode slots in the order Queue::step gives them (staged in
-// LDS), and the window and list move as there.  The result is step()'s.
+// the first decode batch after it (D1 of them, context sum C1), plus the query when
+// its prefill completes.  The completed entries take free decode slots in the order
+// Queue::step gives them (staged in LDS), and the window and list move as there.
+// The result is step()'s.
 template <int KS>
 __device__ __forceinline__ void admission_step(Queue<KS>& wk, const FCache& fc, const QEnv& e,
-                                               int p, double& clk) {
+                                               int p, double& clk, int D1, int64_t C1) {
   const int ln = lane_id();
   const int g1 = wk.g + 1;
   const int ch = min(p, fc.left);
@@ -830,10 +832,8 @@ __device__ __forceinline__ void admission_step(Queue<KS>& wk, const FCache& fc, 
     }
   }
   __builtin_amdgcn_wave_barrier();
-  const int D1 = __builtin_amdgcn_readlane(fc.tD, 0);
   wk.n_dec = D1 + (qfull ? 1 : 0);
-  if (e.need_C)
-    wk.c0sum = read_lane_i64(fc.tC, 0) - (int64_t)D1 * g1 + (qfull ? (int64_t)(p - g1) : 0);
+  if (e.need_C) wk.c0sum = C1 - (int64_t)D1 * g1 + (qfull ? (int64_t)(p - g1) : 0);
   wk.woff += n_full;
   wk.nwin -= n_full;
   wk.head += n_full;
@@ -875,7 +875,7 @@ __device__ __forceinline__ void walk_fast(Queue<KS>& wk, const FCache& fc, const
   if (wk.tail_admitted_next(e) || n >= max_iters) return;
   // F's admission batch, with the query's first chunk
   if (wk.nwin == wk.n_pre) {
-    admission_step(wk, fc, e, p, clk);
+    admission_step(wk, fc, e, p, clk, __builtin_amdgcn_readlane(fc.tD, 0), read_lane_i64(fc.tC, 0));
   } else {
     const StepOut o = wk.step(e);
     clk = __dadd_rn(clk, batch_time(kc, o.P, o.D, o.C, o.A));
@@ -1010,6 +1010,11 @@ __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv&
   int kk = -1;
   int shift_g = -1;   // (wide queues) g of F when the walk starts from it, for the tail shift
   int seqq = 0;
+  // (narrow queues, untracked) the query joined a state under a current summary: the
+  // replay's first batch is that state's admission batch
+  bool summ_step = false;
+  if constexpr (KS <= 4 && !TRK)
+    summ_step = joined && fc.summ && fc.g == wk.g && fc.E == clk0 && wk.nwin == wk.n_pre;
   for (;;) {
     bool stop;
     if (phase == kReplay) {
@@ -1091,6 +1096,14 @@ __device__ __forceinline__ VisitOut visit(Queue<KS>& wk, FCache& fc, const QEnv&
         continue;
       }
       break;
+    }
+    if constexpr (KS <= 4 && !TRK) {
+      if (summ_step && phase == kReplay) {   // the replay steps its first batch
+        summ_step = false;
+        admission_step(wk, fc, e, p, clk, fc.sD1, fc.sC1);
+        ++n;
+        continue;
+      }
     }
     if (phase != kTail && wk.quiet(e)) {
       // a quiet run ends before the batch in which a decode finishes (or at the stop
