@@ -306,6 +306,27 @@ def test_trace_c5_two_scenarios_1000():
     ctx.close()
 
 
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("flags", [0, 1])
+def test_trace_tiny_pools_sixteen_waves(seed, flags):
+    """Tiny random pools with every coefficient term (d and e too), 256 scenarios of 5
+    instances: 1280 queues take the 16-wave workgroups, whose replays of summarised
+    instances fold quiet batches on the summary (keeping its first decode batch's
+    context sum current) and whose chosen instances step their admission batch from
+    it. Every 17th scenario against the oracle, states included, both readings."""
+    wl = make_tiny_workload(1100 + seed, n_inst=5, max_res=6, n_q=40, n_scen=256,
+                            dyadic=(seed % 2 == 0))
+    assert (wl.d != 0).any() and (wl.e != 0).any()
+    choice, chosen, util, ctx = gpu_trace(wl, flags=flags, queue_cap=10 ** 4)
+    for z in range(0, wl.n_scen, 17):
+        ref = O.trace(wl, scenario=z, reading=flags, queue_cap=10 ** 4)
+        np.testing.assert_array_equal(choice[z], ref.choice, err_msg=f"scenario {z}")
+        np.testing.assert_array_equal(bits(chosen[z]), bits(ref.ttft_chosen))
+        np.testing.assert_array_equal(bits(util[z]), bits(ref.util_chosen))
+        assert_state_equal(ctx, z, ref)
+    ctx.close()
+
+
 def test_trace_c6_bursty_prefix():
     """Config 6: the medium pool under MMPP-2 arrivals (bursts at 6x the low rate),
     first 5000 queries."""
